@@ -1,0 +1,227 @@
+/*
+ * minima_kv.h — C ABI of the MI355X (gfx950) Minima-KV hot path.
+ *
+ * Minima-KV (arXiv 2608.23834) keeps every logical KV page of a live request
+ * in one of two physical formats: FP8 for Recent and Anchor pages and a 3-bit
+ * rotated, norm-corrected format ("TQ3") for Stale pages (Sec. 3.1).  Decode
+ * attention reads both formats, dequantizes in registers and merges all
+ * partial results under one softmax (Sec. 3.3, Eq. softmax-merge), with no
+ * cache-sized dense copy (Sec. 4.1).
+ *
+ * Conventions shared by every call
+ *  - All pointers marked "device" are device memory owned by the caller; the
+ *    library never allocates device memory that grows with the number of
+ *    tokens.  Pointers marked "host" are read during the call only.
+ *  - Work is enqueued on the caller's HIP stream and the call returns without
+ *    waiting; results are ordered by stream order (the copy-before-publish and
+ *    release-after-readers rules of Alg. 1 follow from it on one stream).
+ *  - Page size is 16 tokens.  head_dim is 128 or 256.  Query head hq uses KV
+ *    head hq / (n_q_heads / n_kv_heads).
+ *  - Block table: int32 [n_req][max_pages], entry = physical page id in the
+ *    pool named by the tag, -1 = unmapped.  It is shared by all layers (Sec.
+ *    4.1: entries are logical blocks, not layers or K/V roles).
+ *  - Tags: uint8 [n_req][max_pages]: 0 = Recent (FP8), 1 = Anchor (FP8),
+ *    2 = Stale (TQ3), 0xFF = unmapped (Sec. 3.1 tiers z in {R, A, S}).
+ *  - bf16 tensors are passed as raw 16-bit patterns (uint16_t).
+ *  - Every call checks its host-visible arguments before enqueuing anything,
+ *    so a call that returns an error has changed nothing.  Conditions that only
+ *    the device can see (a free list running dry, a page in the wrong state)
+ *    make the kernels skip all writes of that call and set a bit of the pool's
+ *    device error word, read with kv_pool_check_errors().
+ */
+#ifndef MINIMA_KV_H
+#define MINIMA_KV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MKV_OK = 0,
+  MKV_EINVAL = 1, /* bad argument (null pointer, negative size, bad geometry) */
+  MKV_EUNSUP = 2, /* head_dim, page size or GQA group not compiled */
+  MKV_ENOMEM = 3, /* a caller buffer is smaller than the call needs */
+  MKV_ERANGE = 4, /* an index or length is out of range */
+  MKV_ESTATE = 5, /* the pool is in a state that does not allow the call */
+  MKV_EHIP = 6    /* a HIP runtime call or kernel launch failed */
+} mkv_status;
+
+/* Device error word bits (sticky until cleared). */
+#define MKV_DEVERR_FP8_EXHAUSTED 0x1u /* append: FP8 free list too short */
+#define MKV_DEVERR_TQ3_EXHAUSTED 0x2u /* migrate: TQ3 free list too short */
+#define MKV_DEVERR_NOT_RECENT 0x4u    /* append: tokens land in a mapped non-Recent page */
+#define MKV_DEVERR_RANGE 0x8u         /* a sequence length or page index is out of range */
+#define MKV_DEVERR_BAD_TAG 0x10u      /* attention found an unmapped page below seq_len */
+
+#define MKV_PAGE_SIZE 16
+#define MKV_ALL_LAYERS (-1)
+
+typedef struct mkv_pool mkv_pool; /* opaque host handle */
+
+/* Pool geometry and caller-owned storage.  Sizes of the four device buffers
+ * come from kv_pool_bytes(). */
+typedef struct mkv_pool_desc {
+  int32_t n_layers;      /* full-attention layers held by the pool */
+  int32_t n_q_heads;     /* query heads; a multiple of n_kv_heads, group <= 16 */
+  int32_t n_kv_heads;
+  int32_t head_dim;      /* 128 or 256 */
+  int32_t page_size;     /* must be 16 */
+  int32_t n_fp8_pages;   /* physical FP8 pages (each holds all layers and heads) */
+  int32_t n_tq3_pages;   /* physical TQ3 pages */
+  int32_t recent_tokens; /* Recent window W >= 1 (Sec. 3.1) */
+  const int8_t* rot_signs;  /* host [head_dim], each +1 or -1: R = d^-1/2 H diag(s) */
+  const int32_t* fp8_order; /* host [n_fp8_pages] permutation: order in which FP8
+                               ids are handed out; NULL = 0, 1, 2, ... */
+  const int32_t* tq3_order; /* host [n_tq3_pages] permutation or NULL */
+  void* fp8_data;        /* device: [n_layers][n_fp8_pages][n_kv_heads][2*16*d] bytes */
+  size_t fp8_data_bytes;
+  void* fp8_scales;      /* device: fp32 [n_layers][n_fp8_pages][n_kv_heads][2] (K, V) */
+  size_t fp8_scales_bytes;
+  void* tq3_data;        /* device: [n_layers][n_tq3_pages][n_kv_heads][16*d+32] bytes */
+  size_t tq3_data_bytes;
+  void* ctrl;            /* device: free lists, counters, work lists, error word */
+  size_t ctrl_bytes;
+} mkv_pool_desc;
+
+/* Cheap instrumentation (Sec. 3.3 / Sec. 6.3 route, fallback and dense-shadow
+ * counters).  This library has no fallback path and never builds a dense
+ * shadow, so those two counters are always zero. */
+typedef struct mkv_counters {
+  uint64_t decode_routes;     /* paged_attn_decode layer calls served */
+  uint64_t chunk_routes;      /* paged_attn_chunk layer calls served */
+  uint64_t fallbacks;         /* always 0 */
+  uint64_t dense_shadow_bytes;/* always 0 */
+  uint64_t fp8_pages_live;    /* FP8 pages currently allocated (synchronizes) */
+  uint64_t tq3_pages_live;    /* TQ3 pages currently allocated (synchronizes) */
+  uint64_t fp8_bytes_live;    /* physical bytes of live FP8 pages, all layers */
+  uint64_t tq3_bytes_live;    /* physical bytes of live TQ3 pages, all layers */
+} mkv_counters;
+
+/* Byte sizes of the four caller-owned device buffers for a geometry.
+ * Only the geometry fields of desc are read.  Returns MKV_EUNSUP for an
+ * uncompiled head_dim/page size/group, MKV_EINVAL for non-positive sizes. */
+mkv_status kv_pool_bytes(const mkv_pool_desc* desc, size_t* fp8_data_bytes,
+                         size_t* fp8_scales_bytes, size_t* tq3_data_bytes, size_t* ctrl_bytes);
+
+/* Create a pool over caller-owned buffers (Sec. 4.4: separate per-format pools
+ * with per-kind free lists).  Initialises the free lists and error word in
+ * ctrl synchronously; pool contents are left as they are.  The handle owns
+ * only host metadata.  Errors: EINVAL, EUNSUP, ENOMEM (a buffer smaller than
+ * kv_pool_bytes() reports), EHIP. */
+mkv_status kv_pool_create(const mkv_pool_desc* desc, mkv_pool** out);
+mkv_status kv_pool_destroy(mkv_pool* pool);
+
+/* Append(q, p) of Alg. 1 / Recent tier of Sec. 3.1: quantize new bf16 K/V to
+ * FP8 E4M3 (round to nearest even, saturating at 448) with one fp32 scale per
+ * (layer, page, KV head, K or V), s = amax / 448.
+ *  - Request r receives tokens at positions seq_lens_before[r] ..
+ *    seq_lens_before[r] + n_r - 1, n_r = cu_new_tokens[r+1] - cu_new_tokens[r];
+ *    its rows in k/v are cu_new_tokens[r] .. cu_new_tokens[r+1]-1.
+ *  - Every logical page that receives tokens and is unmapped gets a new FP8 id
+ *    from the free list (ascending (request, page) order) and tag Recent; the
+ *    mapping is written to block_table/tags in place.  A mapped page must be
+ *    Recent; a partly filled page keeps its scale unless the new tokens exceed
+ *    448 * scale, in which case its scale grows and earlier codes are
+ *    re-rounded; unused slots of a new page are zero.
+ *  - layer = MKV_ALL_LAYERS writes every layer and k/v are
+ *    [n_layers][n_new_total][n_kv_heads][head_dim]; else only that layer and
+ *    k/v are [n_new_total][n_kv_heads][head_dim].
+ *  - seq_lens_before, cu_new_tokens ([n_req+1], cu[0] = 0, cu[n_req] =
+ *    n_new_total) are device int32.  seq_lens are not updated.
+ * Device-side failures (free list too short, page not Recent, page index
+ * beyond max_pages) set the error word and leave everything unchanged. */
+mkv_status kv_append_fp8(mkv_pool* pool, int32_t layer, int32_t n_req, int32_t* block_table,
+                         uint8_t* tags, int32_t max_pages, const int32_t* seq_lens_before,
+                         const int32_t* cu_new_tokens, int32_t n_new_total, const uint16_t* k,
+                         const uint16_t* v, hipStream_t stream);
+
+/* Retier(p, TQ3) of Alg. 1 for every page that has left the Recent window
+ * (Sec. 3.1): page p of request r is Recent while (p+1)*16 > seq_len - W.  A
+ * Recent page outside the window becomes Anchor (tag only, stays FP8) when
+ * anchor_mask[r][p] != 0, else it is encoded FP8 -> TQ3 for all layers and
+ * heads ("normalize-rotate-pack", Sec. 4.3) into a newly allocated TQ3 page;
+ * only then are (tag Stale, new id) published and the FP8 page released to its
+ * free list (Alg. 1 copy-before-publish).  TQ3 ids are handed out and FP8 ids
+ * released in ascending (request, page) order.  anchor_mask: device uint8
+ * [n_req][max_pages] or NULL; seq_lens: device int32 [n_req].  If the TQ3 free
+ * list is too short nothing changes and the error word is set. */
+mkv_status kv_migrate_to_tq3(mkv_pool* pool, int32_t n_req, int32_t* block_table, uint8_t* tags,
+                             int32_t max_pages, const uint8_t* anchor_mask,
+                             const int32_t* seq_lens, hipStream_t stream);
+
+/* Workspace bytes for paged_attn_decode (n_q_total = 0) or paged_attn_chunk
+ * (n_q_total = total chunk queries) at this batch shape. */
+mkv_status paged_attn_workspace_bytes(const mkv_pool* pool, int32_t n_req, int32_t max_pages,
+                                      int32_t n_q_total, size_t* bytes);
+
+/* Zero the part of a workspace that must start at zero (the split counters).
+ * A workspace from torch.zeros/hipMemset needs no call; every completed
+ * attention call leaves that part zero again. */
+mkv_status paged_attn_workspace_init(void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Mixed-format decode attention (Sec. 3.3; Sec. 4.1 direct fused decode).
+ * The query of request r sits at position seq_lens[r]-1 and attends to every
+ * logical token t < seq_lens[r] (1 <= seq_lens[r] <= 16*max_pages), read from
+ * its FP8 (Recent/Anchor) and TQ3 (Stale) pages:
+ *     out[r][hq] = sum_t softmax_t(q . k_hat_t / sqrt(d)) v_hat_t,
+ * k_hat/v_hat being the pages' dequantized values.  Each split of either format
+ * produces (m_j, l_j, normalized O_j); all splits are merged by Eq.
+ * (softmax-merge).  q: device bf16 [n_req][n_q_heads][d]; out: device fp32
+ * [n_req][n_q_heads][d]; lse: device fp32 [n_req][n_q_heads] (natural log of
+ * the softmax denominator, scores in units of q.k/sqrt(d)) or NULL.
+ * ws: device, >= paged_attn_workspace_bytes(pool, n_req, max_pages, 0), whose
+ * counter part is zero (see paged_attn_workspace_init).  An invalid seq_len
+ * or an unmapped page below seq_len sets the error word; such requests get
+ * zero outputs. */
+mkv_status paged_attn_decode(mkv_pool* pool, int32_t layer, int32_t n_req, const uint16_t* q,
+                             const int32_t* block_table, const uint8_t* tags, int32_t max_pages,
+                             const int32_t* seq_lens, float* out, float* lse, void* ws,
+                             size_t ws_bytes, hipStream_t stream);
+
+/* Causal chunked-prefill attention over the same mixed pages.  Request r has
+ * n_r = cu_q[r+1]-cu_q[r] queries; query i sits at position
+ * seq_lens[r] - n_r + i and attends to keys t <= that position (the chunk's
+ * own KV must already be appended as FP8).  q: device bf16
+ * [n_q_total][n_q_heads][d]; cu_q: device int32 [n_req+1]; out: device fp32
+ * [n_q_total][n_q_heads][d]; ws >= paged_attn_workspace_bytes(..., n_q_total).
+ * (The paper runs prefill on a generic dense path, Sec. 4.1; this variant
+ * keeps the mixed pages and uses MFMA for the dense contraction.) */
+mkv_status paged_attn_chunk(mkv_pool* pool, int32_t layer, int32_t n_req, const uint16_t* q,
+                            const int32_t* cu_q, int32_t n_q_total, const int32_t* block_table,
+                            const uint8_t* tags, int32_t max_pages, const int32_t* seq_lens,
+                            float* out, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Compact per-format page lists (Sec. 4.1): the stable partition of logical
+ * pages [0, ceil(seq_len/16)) into FP8 (tags R, A) and TQ3 (tag S), logical
+ * order kept.  list8/list3: device int32 [n_req][max_pages][2] =
+ * (logical page, physical id); counts: device int32 [n_req][2] = (n_fp8,
+ * n_tq3).  Entries past the counts are left untouched. */
+mkv_status kv_partition_pages(int32_t n_req, const int32_t* block_table, const uint8_t* tags,
+                              int32_t max_pages, const int32_t* seq_lens, int32_t* list8,
+                              int32_t* list3, int32_t* counts, hipStream_t stream);
+
+/* Free-list state (synchronizes with the device). */
+mkv_status kv_pool_free_counts(mkv_pool* pool, int32_t* n_fp8_free, int32_t* n_tq3_free);
+
+/* Copy the free stacks to host memory (synchronizes): ids in [0, top) from the
+ * bottom; the next id handed out is the last one. */
+mkv_status kv_pool_read_free_lists(mkv_pool* pool, int32_t* fp8_ids, int32_t* n_fp8,
+                                   int32_t* tq3_ids, int32_t* n_tq3);
+
+/* Route / fallback / dense-shadow / physical-byte counters (synchronizes). */
+mkv_status kv_pool_counters(mkv_pool* pool, mkv_counters* out);
+
+/* Read (and optionally clear) the device error word; synchronizes. */
+mkv_status kv_pool_check_errors(mkv_pool* pool, uint32_t* err_word, int32_t clear);
+
+const char* mkv_status_string(mkv_status s);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MINIMA_KV_H */

@@ -122,7 +122,7 @@ def anchor_mask(w: Workload, max_pages: int, seq_lens=None) -> np.ndarray:
     ``anchor_frac`` of the remaining old pages (count rounded half to even);
     "remaining" excludes the first pages and the pages of the Recent window."""
     lens = w.ctx if seq_lens is None else seq_lens
-    m = np.zeros((w.n_req, max_pages), np.uint8)
+    m = np.zeros((len(lens), max_pages), np.uint8)
     for r, L in enumerate(lens):
         npg = n_pages_of(L)
         first = min(w.first_anchor_pages, npg)

@@ -63,59 +63,43 @@ double orc_e4m3_to_f64(uint8_t b) {
 /* Round an fp32 to E4M3 by the definition: among the finite E4M3 values pick
  * the nearest; on a tie pick the one with an even mantissa; magnitudes beyond
  * the largest finite value (448) saturate to +-448; NaN maps to 0x7F|sign.
- * Written as a search over the 127 non-negative finite codes, in fp64 where
- * every E4M3 value and every midpoint is exact. */
-uint8_t orc_e4m3_from_f32(float xf) {
-  double x = (double)xf;
-  uint8_t sign = 0;
-  if (isnan(x)) return signbit(x) ? 0xFF : 0x7F;
-  if (signbit(x)) { sign = 0x80; x = -x; }
-  if (x >= 448.0) return sign | 0x7E;
-  int best = 0;
-  for (int c = 1; c <= 0x7E; ++c) {
-    double vc = orc_e4m3_to_f64((uint8_t)c);
-    if (vc <= x) best = c; /* codes are monotone in value */
+ * The non-negative finite codes 0x00..0x7E are increasing in value, so the
+ * neighbours of |x| are found by bisection over their value table (fp64,
+ * where every E4M3 value and every midpoint is exact). */
+static double E4M3_VALS[127];
+static int e4m3_table_ready = 0;
+static void e4m3_table(void) {
+  if (!e4m3_table_ready) {
+    for (int c = 0; c < 127; ++c) E4M3_VALS[c] = orc_e4m3_to_f64((uint8_t)c);
+    e4m3_table_ready = 1;
   }
-  /* x lies in [v(best), v(best+1)) */
-  double lo = orc_e4m3_to_f64((uint8_t)best);
-  if (best == 0x7E) return sign | 0x7E;
-  double hi = orc_e4m3_to_f64((uint8_t)(best + 1));
-  double mid = 0.5 * (lo + hi);
-  int pick;
-  if (x < mid) pick = best;
-  else if (x > mid) pick = best + 1;
+}
+static uint8_t e4m3_round(double v) {
+  uint8_t sign = 0;
+  if (isnan(v)) return signbit(v) ? 0xFF : 0x7F;
+  if (signbit(v)) { sign = 0x80; v = -v; }
+  if (v >= 448.0) return sign | 0x7E;
+  int lo = 0, hi = 126; /* largest c with value(c) <= v */
+  while (lo < hi) {
+    int mid = (lo + hi + 1) >> 1;
+    if (E4M3_VALS[mid] <= v) lo = mid; else hi = mid - 1;
+  }
+  int best = lo, pick;
+  double m = 0.5 * (E4M3_VALS[best] + E4M3_VALS[best + 1]);
+  if (v < m) pick = best;
+  else if (v > m) pick = best + 1;
   else pick = (best & 1) ? best + 1 : best; /* tie: even mantissa bit */
   return sign | (uint8_t)pick;
 }
+uint8_t orc_e4m3_from_f32(float xf) {
+  e4m3_table();
+  return e4m3_round((double)xf);
+}
 
 void orc_e4m3_from_f32_array(const float* x, uint8_t* out, int64_t n) {
-  /* fast path for the exhaustive sweeps: same definition via a sorted table */
-  static double vals[127];
-  static int init = 0;
-  if (!init) {
-    for (int c = 0; c < 127; ++c) vals[c] = orc_e4m3_to_f64((uint8_t)c);
-    init = 1;
-  }
+  e4m3_table();
 #pragma omp parallel for schedule(static)
-  for (int64_t i = 0; i < n; ++i) {
-    double v = (double)x[i];
-    uint8_t sign = 0;
-    if (isnan(v)) { out[i] = signbit(v) ? 0xFF : 0x7F; continue; }
-    if (signbit(v)) { sign = 0x80; v = -v; }
-    if (v >= 448.0) { out[i] = sign | 0x7E; continue; }
-    int lo = 0, hi = 126; /* largest c with vals[c] <= v */
-    while (lo < hi) {
-      int mid = (lo + hi + 1) >> 1;
-      if (vals[mid] <= v) lo = mid; else hi = mid - 1;
-    }
-    int best = lo, pick;
-    if (best == 126) { out[i] = sign | 0x7E; continue; }
-    double m = 0.5 * (vals[best] + vals[best + 1]);
-    if (v < m) pick = best;
-    else if (v > m) pick = best + 1;
-    else pick = (best & 1) ? best + 1 : best;
-    out[i] = sign | (uint8_t)pick;
-  }
+  for (int64_t i = 0; i < n; ++i) out[i] = e4m3_round((double)x[i]);
 }
 
 /* ------------------------------------------------------------------------ */
@@ -202,15 +186,29 @@ static float bf16_to_f32(uint16_t b) {
 /* Rotation (Sec. 3.1 "rotated scalar quantizer"; Sec. 4.3 "rotate").         */
 /* Sylvester Hadamard H_ij = (-1)^popcount(i & j), applied by definition.     */
 /* ------------------------------------------------------------------------ */
-static int hsign(int i, int j) { return (__builtin_popcount((unsigned)(i & j)) & 1) ? -1 : 1; }
-
-/* y = H * x over int64 (exact). */
+/* y = H * x over int64 (exact), H Sylvester of order n (a power of two),
+ * H_ij = (-1)^popcount(i & j).  Computed with the standard radix-2 butterflies
+ * (a, b) -> (a + b, a - b), which factor the Sylvester matrix exactly. */
 void orc_hadamard_i64(const int64_t* x, int64_t* y, int n) {
-  for (int i = 0; i < n; ++i) {
-    int64_t acc = 0;
-    for (int j = 0; j < n; ++j) acc += hsign(i, j) * x[j];
-    y[i] = acc;
-  }
+  for (int i = 0; i < n; ++i) y[i] = x[i];
+  for (int s = 1; s < n; s <<= 1)
+    for (int i = 0; i < n; i += 2 * s)
+      for (int j = i; j < i + s; ++j) {
+        int64_t a = y[j], b = y[j + s];
+        y[j] = a + b;
+        y[j + s] = a - b;
+      }
+}
+/* Same transform over fp64 (used on sums of codebook levels, which are
+ * multiples of 1/8 and therefore exact). */
+static void hadamard_f64(double* y, int n) {
+  for (int s = 1; s < n; s <<= 1)
+    for (int i = 0; i < n; i += 2 * s)
+      for (int j = i; j < i + s; ++j) {
+        double a = y[j], b = y[j + s];
+        y[j] = a + b;
+        y[j + s] = a - b;
+      }
 }
 
 /* ------------------------------------------------------------------------ */
@@ -315,16 +313,17 @@ void orc_tq3_dequant(int d, const uint8_t* kcode, const uint16_t* gamma, const u
                      const uint16_t* vscale, const uint16_t* vzero, const int8_t* sigma,
                      double* khat, double* vhat) {
   double inv = 1.0 / sqrt((double)d);
+  double* w = (double*)malloc(sizeof(double) * d);
   for (int t = 0; t < ORC_PAGE; ++t) {
     double g = orc_f16_to_f64(gamma[t]);
-    for (int i = 0; i < d; ++i) {
-      double acc = 0.0;
-      for (int j = 0; j < d; ++j) acc += hsign(i, j) * MU[kcode[t * d + j]];
-      khat[t * d + i] = g * sigma[i] * inv * acc;
-    }
+    /* R^T mu_c = d^-1/2 diag(sigma) H mu_c  (H symmetric) */
+    for (int j = 0; j < d; ++j) w[j] = MU[kcode[t * d + j]];
+    hadamard_f64(w, d);
+    for (int i = 0; i < d; ++i) khat[t * d + i] = g * sigma[i] * inv * w[i];
     for (int c = 0; c < d; ++c)
       vhat[t * d + c] = orc_f16_to_f64(vzero[c]) + orc_f16_to_f64(vscale[c]) * vcode[t * d + c];
   }
+  free(w);
 }
 
 /* ------------------------------------------------------------------------ */

@@ -1,0 +1,253 @@
+"""Python binding of libminimakv (MI355X / gfx950 Minima-KV hot path).
+
+Argument marshalling only: every step of the path runs in the HIP kernels of
+``libminimakv.so``.  torch supplies device memory and streams.  The functions
+keep the C ABI's names (include/minima_kv.h).  There is no CPU fallback: if the
+built library is missing, loading fails loudly.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "_lib", "libminimakv.so")
+
+MKV_ALL_LAYERS = -1
+PAGE = 16
+TAG_R, TAG_A, TAG_S, TAG_NONE = 0, 1, 2, 0xFF
+STATUS = {0: "MKV_OK", 1: "MKV_EINVAL", 2: "MKV_EUNSUP", 3: "MKV_ENOMEM", 4: "MKV_ERANGE",
+          5: "MKV_ESTATE", 6: "MKV_EHIP"}
+DEVERR = {"FP8_EXHAUSTED": 0x1, "TQ3_EXHAUSTED": 0x2, "NOT_RECENT": 0x4, "RANGE": 0x8,
+          "BAD_TAG": 0x10}
+EXPORTS = ["kv_pool_bytes", "kv_pool_create", "kv_pool_destroy", "kv_append_fp8",
+           "kv_migrate_to_tq3", "paged_attn_workspace_bytes", "paged_attn_workspace_init",
+           "paged_attn_decode", "paged_attn_chunk", "kv_partition_pages", "kv_pool_free_counts",
+           "kv_pool_read_free_lists", "kv_pool_counters", "kv_pool_check_errors",
+           "mkv_status_string"]
+
+_lib = None
+
+
+class MkvError(RuntimeError):
+    def __init__(self, fn, code):
+        super().__init__(f"{fn} failed: {STATUS.get(code, code)}")
+        self.code = code
+
+
+class PoolDesc(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("n_q_heads", ctypes.c_int32),
+                ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
+                ("page_size", ctypes.c_int32), ("n_fp8_pages", ctypes.c_int32),
+                ("n_tq3_pages", ctypes.c_int32), ("recent_tokens", ctypes.c_int32),
+                ("rot_signs", ctypes.c_void_p), ("fp8_order", ctypes.c_void_p),
+                ("tq3_order", ctypes.c_void_p),
+                ("fp8_data", ctypes.c_void_p), ("fp8_data_bytes", ctypes.c_size_t),
+                ("fp8_scales", ctypes.c_void_p), ("fp8_scales_bytes", ctypes.c_size_t),
+                ("tq3_data", ctypes.c_void_p), ("tq3_data_bytes", ctypes.c_size_t),
+                ("ctrl", ctypes.c_void_p), ("ctrl_bytes", ctypes.c_size_t)]
+
+
+class Counters(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_uint64) for n in (
+        "decode_routes", "chunk_routes", "fallbacks", "dense_shadow_bytes", "fp8_pages_live",
+        "tq3_pages_live", "fp8_bytes_live", "tq3_bytes_live")]
+
+
+def lib() -> ctypes.CDLL:
+    """Load the built library (build it with ``python -m paper_2608_23834_amd.build``)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"libminimakv.so is not built ({LIB_PATH}); run "
+                               "`python -m paper_2608_23834_amd.build` first")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+        for name in EXPORTS:
+            getattr(L, name).restype = ctypes.c_int
+        L.mkv_status_string.restype = ctypes.c_char_p
+        L.kv_pool_bytes.argtypes = [vp, vp, vp, vp, vp]
+        L.kv_pool_create.argtypes = [vp, vp]
+        L.kv_pool_destroy.argtypes = [vp]
+        L.kv_append_fp8.argtypes = [vp, i32, i32, vp, vp, i32, vp, vp, i32, vp, vp, vp]
+        L.kv_migrate_to_tq3.argtypes = [vp, i32, vp, vp, i32, vp, vp, vp]
+        L.paged_attn_workspace_bytes.argtypes = [vp, i32, i32, i32, vp]
+        L.paged_attn_workspace_init.argtypes = [vp, sz, vp]
+        L.paged_attn_decode.argtypes = [vp, i32, i32, vp, vp, vp, i32, vp, vp, vp, vp, sz, vp]
+        L.paged_attn_chunk.argtypes = [vp, i32, i32, vp, vp, i32, vp, vp, i32, vp, vp, vp, sz, vp]
+        L.kv_partition_pages.argtypes = [i32, vp, vp, i32, vp, vp, vp, vp, vp]
+        L.kv_pool_free_counts.argtypes = [vp, vp, vp]
+        L.kv_pool_read_free_lists.argtypes = [vp, vp, vp, vp, vp]
+        L.kv_pool_counters.argtypes = [vp, vp]
+        L.kv_pool_check_errors.argtypes = [vp, vp, i32]
+        L.mkv_status_string.argtypes = [ctypes.c_int]
+        _lib = L
+    return _lib
+
+
+def _check(fn, code):
+    if code != 0:
+        raise MkvError(fn, code)
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def pool_bytes(n_layers, n_q_heads, n_kv_heads, head_dim, n_fp8_pages, n_tq3_pages, recent_tokens):
+    d = PoolDesc(n_layers, n_q_heads, n_kv_heads, head_dim, PAGE, n_fp8_pages, n_tq3_pages,
+                 recent_tokens)
+    out = (ctypes.c_size_t * 4)()
+    _check("kv_pool_bytes", lib().kv_pool_bytes(ctypes.byref(d), ctypes.byref(out, 0),
+                                                ctypes.byref(out, 8), ctypes.byref(out, 16),
+                                                ctypes.byref(out, 24)))
+    return tuple(out)
+
+
+class Pool:
+    """A pool over torch-allocated device buffers (the caller owns memory)."""
+
+    def __init__(self, n_layers, n_q_heads, n_kv_heads, head_dim, n_fp8_pages, n_tq3_pages,
+                 recent_tokens, rot_signs, fp8_order=None, tq3_order=None, device="cuda"):
+        import torch
+        self.n_layers, self.n_q_heads, self.n_kv_heads, self.d = n_layers, n_q_heads, n_kv_heads, head_dim
+        self.n_fp8, self.n_tq3, self.recent = n_fp8_pages, n_tq3_pages, recent_tokens
+        b8, bs, b3, bc = pool_bytes(n_layers, n_q_heads, n_kv_heads, head_dim, n_fp8_pages,
+                                    n_tq3_pages, recent_tokens)
+        self.fp8 = torch.zeros(b8, dtype=torch.uint8, device=device)
+        self.fp8_scales = torch.zeros(bs // 4, dtype=torch.float32, device=device)
+        self.tq3 = torch.zeros(max(b3, 16), dtype=torch.uint8, device=device)
+        self.ctrl = torch.zeros(bc // 4, dtype=torch.int32, device=device)
+        sig = np.ascontiguousarray(rot_signs, dtype=np.int8)
+        o8 = None if fp8_order is None else np.ascontiguousarray(fp8_order, dtype=np.int32)
+        o3 = None if tq3_order is None else np.ascontiguousarray(tq3_order, dtype=np.int32)
+        desc = PoolDesc(n_layers, n_q_heads, n_kv_heads, head_dim, PAGE, n_fp8_pages, n_tq3_pages,
+                        recent_tokens, sig.ctypes.data,
+                        None if o8 is None else o8.ctypes.data,
+                        None if o3 is None else o3.ctypes.data,
+                        self.fp8.data_ptr(), b8, self.fp8_scales.data_ptr(), bs,
+                        self.tq3.data_ptr(), b3, self.ctrl.data_ptr(), bc)
+        h = ctypes.c_void_p()
+        torch.cuda.synchronize()
+        _check("kv_pool_create", lib().kv_pool_create(ctypes.byref(desc), ctypes.byref(h)))
+        self.handle = h
+
+    # views in the documented layouts
+    def fp8_view(self):
+        return self.fp8.view(self.n_layers, self.n_fp8, self.n_kv_heads, 2 * PAGE * self.d)
+
+    def fp8_scales_view(self):
+        return self.fp8_scales.view(self.n_layers, self.n_fp8, self.n_kv_heads, 2)
+
+    def tq3_view(self):
+        return self.tq3[: self.n_layers * self.n_tq3 * self.n_kv_heads * (16 * self.d + 32)].view(
+            self.n_layers, self.n_tq3, self.n_kv_heads, 16 * self.d + 32)
+
+    def close(self):
+        if getattr(self, "handle", None):
+            lib().kv_pool_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def kv_append_fp8(pool: Pool, layer, block_table, tags, seq_lens_before, cu_new_tokens, k, v,
+                  stream=None):
+    n_req, max_pages = block_table.shape
+    n_new = int(k.shape[-3]) if k is not None else 0
+    _check("kv_append_fp8", lib().kv_append_fp8(
+        pool.handle, layer, n_req, _ptr(block_table), _ptr(tags), max_pages, _ptr(seq_lens_before),
+        _ptr(cu_new_tokens), n_new, _ptr(k), _ptr(v), _stream(stream)))
+
+
+def kv_migrate_to_tq3(pool: Pool, block_table, tags, anchor_mask, seq_lens, stream=None):
+    n_req, max_pages = block_table.shape
+    _check("kv_migrate_to_tq3", lib().kv_migrate_to_tq3(
+        pool.handle, n_req, _ptr(block_table), _ptr(tags), max_pages, _ptr(anchor_mask),
+        _ptr(seq_lens), _stream(stream)))
+
+
+def paged_attn_workspace_bytes(pool: Pool, n_req, max_pages, n_q_total=0):
+    out = ctypes.c_size_t()
+    _check("paged_attn_workspace_bytes", lib().paged_attn_workspace_bytes(
+        pool.handle, n_req, max_pages, n_q_total, ctypes.byref(out)))
+    return out.value
+
+
+def workspace(pool: Pool, n_req, max_pages, n_q_total=0, device="cuda"):
+    import torch
+    return torch.zeros(paged_attn_workspace_bytes(pool, n_req, max_pages, n_q_total),
+                       dtype=torch.uint8, device=device)
+
+
+def paged_attn_workspace_init(ws, stream=None):
+    _check("paged_attn_workspace_init", lib().paged_attn_workspace_init(
+        _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def paged_attn_decode(pool: Pool, layer, q, block_table, tags, seq_lens, out, lse, ws,
+                      stream=None):
+    n_req, max_pages = block_table.shape
+    _check("paged_attn_decode", lib().paged_attn_decode(
+        pool.handle, layer, n_req, _ptr(q), _ptr(block_table), _ptr(tags), max_pages,
+        _ptr(seq_lens), _ptr(out), _ptr(lse), _ptr(ws), ws.numel() * ws.element_size(),
+        _stream(stream)))
+
+
+def paged_attn_chunk(pool: Pool, layer, q, cu_q, block_table, tags, seq_lens, out, ws,
+                     stream=None):
+    n_req, max_pages = block_table.shape
+    _check("paged_attn_chunk", lib().paged_attn_chunk(
+        pool.handle, layer, n_req, _ptr(q), _ptr(cu_q), int(q.shape[0]), _ptr(block_table),
+        _ptr(tags), max_pages, _ptr(seq_lens), _ptr(out), _ptr(ws), ws.numel() * ws.element_size(),
+        _stream(stream)))
+
+
+def kv_partition_pages(block_table, tags, seq_lens, list8, list3, counts, stream=None):
+    n_req, max_pages = block_table.shape
+    _check("kv_partition_pages", lib().kv_partition_pages(
+        n_req, _ptr(block_table), _ptr(tags), max_pages, _ptr(seq_lens), _ptr(list8), _ptr(list3),
+        _ptr(counts), _stream(stream)))
+
+
+def kv_pool_free_counts(pool: Pool):
+    a, b = ctypes.c_int32(), ctypes.c_int32()
+    _check("kv_pool_free_counts", lib().kv_pool_free_counts(pool.handle, ctypes.byref(a),
+                                                             ctypes.byref(b)))
+    return a.value, b.value
+
+
+def kv_pool_read_free_lists(pool: Pool):
+    f8 = np.zeros(pool.n_fp8, np.int32)
+    f3 = np.zeros(max(pool.n_tq3, 1), np.int32)
+    n8, n3 = ctypes.c_int32(), ctypes.c_int32()
+    _check("kv_pool_read_free_lists", lib().kv_pool_read_free_lists(
+        pool.handle, f8.ctypes.data, ctypes.byref(n8), f3.ctypes.data, ctypes.byref(n3)))
+    return f8[: n8.value].copy(), f3[: n3.value].copy()
+
+
+def kv_pool_counters(pool: Pool) -> dict:
+    c = Counters()
+    _check("kv_pool_counters", lib().kv_pool_counters(pool.handle, ctypes.byref(c)))
+    return {n: getattr(c, n) for n, _ in Counters._fields_}
+
+
+def kv_pool_check_errors(pool: Pool, clear=False) -> int:
+    e = ctypes.c_uint32()
+    _check("kv_pool_check_errors", lib().kv_pool_check_errors(pool.handle, ctypes.byref(e),
+                                                               int(bool(clear))))
+    return e.value

@@ -1,0 +1,83 @@
+// Host-side pool handle and the launchers each kernel translation unit
+// exports to the C ABI layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "mkv_device.h"
+
+struct mkv_pool {
+  int n_layers, n_q_heads, n_kv_heads, d, group, n_fp8, n_tq3, recent;
+  uint8_t* fp8;       // device
+  float* fp8_scales;  // device
+  uint8_t* tq3;       // device
+  int32_t* ctrl;      // device
+  mkv::CtrlLayout cl;
+  uint64_t decode_routes, chunk_routes;
+};
+
+namespace mkv {
+
+struct PoolView {
+  uint8_t* fp8;
+  float* fp8_scales;
+  uint8_t* tq3;
+  int32_t* ctrl;
+  const int8_t* sigma;
+  int32_t* fp8_stack;
+  int32_t* tq3_stack;
+  int32_t* list;
+  int n_layers, n_kv_heads, d, group, n_fp8, n_tq3, recent;
+};
+
+inline PoolView view_of(const mkv_pool* p) {
+  PoolView v;
+  v.fp8 = p->fp8;
+  v.fp8_scales = p->fp8_scales;
+  v.tq3 = p->tq3;
+  v.ctrl = p->ctrl;
+  v.sigma = reinterpret_cast<const int8_t*>(reinterpret_cast<const uint8_t*>(p->ctrl) + p->cl.sigma_bytes);
+  v.fp8_stack = p->ctrl + p->cl.fp8_stack;
+  v.tq3_stack = p->ctrl + p->cl.tq3_stack;
+  v.list = p->ctrl + p->cl.list;
+  v.n_layers = p->n_layers;
+  v.n_kv_heads = p->n_kv_heads;
+  v.d = p->d;
+  v.group = p->group;
+  v.n_fp8 = p->n_fp8;
+  v.n_tq3 = p->n_tq3;
+  v.recent = p->recent;
+  return v;
+}
+
+// mkv_pool_kernels.hip
+hipError_t launch_append(const PoolView& P, int layer, int n_req, int32_t* bt, uint8_t* tags,
+                         int max_pages, const int32_t* seq_before, const int32_t* cu_new,
+                         int n_new_total, const uint16_t* k, const uint16_t* v, hipStream_t s);
+hipError_t launch_migrate(const PoolView& P, int n_req, int32_t* bt, uint8_t* tags, int max_pages,
+                          const uint8_t* anchor, const int32_t* seq_lens, hipStream_t s);
+hipError_t launch_partition(int n_req, const int32_t* bt, const uint8_t* tags, int max_pages,
+                            const int32_t* seq_lens, int32_t* list8, int32_t* list3,
+                            int32_t* counts, int32_t* err, hipStream_t s);
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
+
+// mkv_decode.hip
+struct DecodeShape {
+  int c3, c8, max_chunks;
+};
+DecodeShape decode_shape(int n_req, int max_pages, int n_kv_heads);
+size_t decode_ws_bytes(int n_req, int max_pages, int n_kv_heads, int group, int d);
+hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t* q,
+                         const int32_t* bt, const uint8_t* tags, int max_pages,
+                         const int32_t* seq_lens, float* out, float* lse, void* ws,
+                         hipStream_t s);
+
+// mkv_chunk.hip
+size_t chunk_ws_bytes(int n_req, int max_pages, int n_q_total, int n_kv_heads, int group, int d);
+hipError_t launch_chunk(const PoolView& P, int layer, int n_req, const uint16_t* q,
+                        const int32_t* cu_q, int n_q_total, const int32_t* bt,
+                        const uint8_t* tags, int max_pages, const int32_t* seq_lens, float* out,
+                        void* ws, hipStream_t s);
+
+}  // namespace mkv

@@ -1,0 +1,534 @@
+// Pool-state kernels: FP8 append (Alg. 1 Append; Sec. 3.1 Recent tier), FP8 ->
+// TQ3 migration (Alg. 1 Retier; Sec. 4.3 normalize-rotate-pack), the compact
+// per-format page lists (Sec. 4.1) and a zero-fill helper.
+//
+// Every result that the CPU oracle fixes bit for bit (page ids, tags, free
+// lists, FP8 codes and scales, TQ3 codes, gamma, V scale/zero) is produced by
+// integer arithmetic or by single IEEE operations in a fixed order; this file
+// is compiled with -ffp-contract=off.
+#include <hip/hip_runtime.h>
+
+#include "mkv_internal.h"
+#include "../../include/minima_kv.h"
+
+namespace mkv {
+
+// ===========================================================================
+// Append
+// ===========================================================================
+
+// One workgroup: validate the whole call, then hand out FP8 ids in ascending
+// (request, page) order and list every page that receives tokens.
+__global__ __launch_bounds__(1024) void append_plan_kernel(int n_req, int32_t* bt, uint8_t* tags,
+                                                           int max_pages, const int32_t* sb,
+                                                           const int32_t* cu, int32_t* ctrl,
+                                                           const int32_t* fp8_stack, int32_t* list,
+                                                           int n_fp8, int n_new_total) {
+  __shared__ int scratch[32];
+  __shared__ int s_err, s_need, s_touch;
+  const int tid = threadIdx.x;
+  if (tid == 0) {
+    s_err = 0; s_need = 0; s_touch = 0;
+    // rows of request r are cu[r] .. cu[r+1]-1 of an n_new_total-row input
+    if (cu[0] != 0 || cu[n_req] != n_new_total) s_err = MKV_DEVERR_RANGE;
+  }
+  __syncthreads();
+  for (int r = 0; r < n_req; ++r) {
+    const int n = cu[r + 1] - cu[r], s0 = sb[r];
+    if (n < 0 || s0 < 0) {
+      if (tid == 0) atomicOr(&s_err, (int)MKV_DEVERR_RANGE);
+      continue;
+    }
+    if (n == 0) continue;
+    const int p0 = s0 / PAGE, p1 = (s0 + n - 1) / PAGE;
+    if (p1 >= max_pages) {
+      if (tid == 0) atomicOr(&s_err, (int)MKV_DEVERR_RANGE);
+      continue;
+    }
+    int need = 0, bad = 0;
+    for (int p = p0 + tid; p <= p1; p += blockDim.x) {
+      const int64_t i = (int64_t)r * max_pages + p;
+      if (bt[i] < 0) need++;
+      else if (tags[i] != TAG_R) bad |= MKV_DEVERR_NOT_RECENT;
+      else if (bt[i] >= n_fp8) bad |= MKV_DEVERR_RANGE;
+    }
+    if (need) atomicAdd(&s_need, need);
+    if (bad) atomicOr(&s_err, bad);
+    if (tid == 0) s_touch += p1 - p0 + 1;
+  }
+  __syncthreads();
+  const int top = ctrl[CTRL_FP8_TOP];
+  if (tid == 0) {
+    if (s_err == 0 && s_need > top) s_err |= MKV_DEVERR_FP8_EXHAUSTED;
+    if (s_err == 0 && s_touch > n_fp8) s_err |= MKV_DEVERR_RANGE;
+  }
+  __syncthreads();
+  if (s_err) {
+    if (tid == 0) {
+      atomicOr(&ctrl[CTRL_ERR], s_err);
+      ctrl[CTRL_ABORT] = 1;
+      ctrl[CTRL_NLIST] = 0;
+    }
+    return;
+  }
+  int base_alloc = 0, base_list = 0;
+  for (int r = 0; r < n_req; ++r) {
+    const int n = cu[r + 1] - cu[r], s0 = sb[r];
+    if (n <= 0) continue;
+    const int p0 = s0 / PAGE, p1 = (s0 + n - 1) / PAGE;
+    for (int c0 = p0; c0 <= p1; c0 += blockDim.x) {
+      const int p = c0 + tid;
+      const bool in = p <= p1;
+      const int64_t i = (int64_t)r * max_pages + p;
+      const int unm = (in && bt[i] < 0) ? 1 : 0;
+      int tot;
+      const int rank = block_excl_scan(unm, scratch, &tot);
+      if (in) {
+        int id;
+        if (unm) {
+          id = fp8_stack[top - 1 - (base_alloc + rank)];
+          bt[i] = id;
+          tags[i] = TAG_R;
+        } else {
+          id = bt[i];
+        }
+        int32_t* e = list + 4LL * (base_list + (p - p0));
+        e[0] = r;
+        e[1] = p;
+        e[2] = id;
+        e[3] = 0;
+      }
+      base_alloc += tot;
+    }
+    base_list += p1 - p0 + 1;
+  }
+  if (tid == 0) {
+    ctrl[CTRL_FP8_TOP] = top - base_alloc;
+    ctrl[CTRL_NLIST] = base_list;
+    ctrl[CTRL_ABORT] = 0;
+  }
+}
+
+__device__ __forceinline__ float block_max_f(float v, float* red) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  const int wid = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) red[wid] = v;
+  __syncthreads();
+  float m = red[0];
+  for (int w = 1; w < (int)(blockDim.x >> 6); ++w) m = fmaxf(m, red[w]);
+  __syncthreads();
+  return m;
+}
+
+template <int D>
+__device__ __forceinline__ int fp8_off(int kv, int t, int c) {
+  if (!kv) return t * D + c;
+  constexpr int CL = D / 16;
+  const int r = c / CL, m = c % CL, g = t >> 2, u = t & 3;
+  return PAGE * D + ((r * 4 + g) * CL + m) * 4 + u;
+}
+
+// Quantize every listed page-head of every requested layer (grid-stride).
+template <int D>
+__global__ __launch_bounds__(256) void append_quant_kernel(PoolView P, int layer_sel, int n_lcall,
+                                                           const int32_t* sb, const int32_t* cu,
+                                                           int n_new_total, const uint16_t* k,
+                                                           const uint16_t* v) {
+  if (P.ctrl[CTRL_ABORT]) return;
+  __shared__ float red[8];
+  const int H = P.n_kv_heads;
+  const int64_t n_items = (int64_t)P.ctrl[CTRL_NLIST] * n_lcall * H;
+  const int tid = threadIdx.x;
+  for (int64_t item = blockIdx.x; item < n_items; item += gridDim.x) {
+    const int e = (int)(item / (n_lcall * H));
+    const int lh = (int)(item % (n_lcall * H));
+    const int li = lh / H, h = lh % H;
+    const int r = P.list[4 * e], p = P.list[4 * e + 1], id = P.list[4 * e + 2];
+    const int layer = layer_sel < 0 ? li : layer_sel;
+    const int s0 = sb[r], n = cu[r + 1] - cu[r];
+    const int t0 = max(0, s0 - p * PAGE), t1 = min(PAGE, s0 + n - p * PAGE);
+    const int64_t ph = ((int64_t)layer * P.n_fp8 + id) * H + h;
+    uint8_t* reg = P.fp8 + ph * fp8_region_bytes(D);
+    float* sc = P.fp8_scales + ph * 2;
+    const int64_t row0 = (int64_t)cu[r] + p * PAGE - s0;  // input row of slot t is row0 + t
+    for (int kv = 0; kv < 2; ++kv) {
+      const uint16_t* src = (kv ? v : k) + (int64_t)li * n_new_total * H * D;
+      float amax = 0.0f;
+      for (int idx = tid; idx < (t1 - t0) * D; idx += blockDim.x) {
+        const int t = t0 + idx / D, c = idx % D;
+        amax = fmaxf(amax, fabsf(bf16_to_f32(src[((row0 + t) * H + h) * D + c])));
+      }
+      amax = block_max_f(amax, red);
+      const float s_old = t0 > 0 ? sc[kv] : 0.0f;
+      float s_new = s_old;
+      bool requant = false;
+      if (t0 == 0) {
+        s_new = amax / 448.0f;
+      } else if (!(amax <= 448.0f * s_old)) {
+        s_new = amax / 448.0f;
+        requant = true;
+      }
+      __syncthreads();
+      if (requant) {
+        for (int idx = tid; idx < t0 * D; idx += blockDim.x) {
+          const int t = idx / D, c = idx % D;
+          const int off = fp8_off<D>(kv, t, c);
+          const float deq = e4m3_to_f32(reg[off]) * s_old;
+          reg[off] = (uint8_t)f32_to_e4m3(deq / s_new);
+        }
+      }
+      for (int idx = tid; idx < (t1 - t0) * D; idx += blockDim.x) {
+        const int t = t0 + idx / D, c = idx % D;
+        const float x = bf16_to_f32(src[((row0 + t) * H + h) * D + c]);
+        reg[fp8_off<D>(kv, t, c)] = s_new > 0.0f ? (uint8_t)f32_to_e4m3(x / s_new) : (uint8_t)0;
+      }
+      if (t0 == 0) {
+        for (int idx = tid; idx < (PAGE - t1) * D; idx += blockDim.x) {
+          const int t = t1 + idx / D, c = idx % D;
+          reg[fp8_off<D>(kv, t, c)] = 0;
+        }
+      }
+      if (tid == 0) sc[kv] = s_new;
+      __syncthreads();
+    }
+  }
+}
+
+// ===========================================================================
+// Migrate (Retier to TQ3)
+// ===========================================================================
+
+__global__ __launch_bounds__(1024) void migrate_plan_kernel(int n_req, const int32_t* bt,
+                                                            uint8_t* tags, int max_pages,
+                                                            const uint8_t* anchor,
+                                                            const int32_t* seq_lens, int W,
+                                                            int32_t* ctrl, const int32_t* tq3_stack,
+                                                            int32_t* list, int n_fp8) {
+  __shared__ int scratch[32];
+  __shared__ int s_err, s_cnt;
+  const int tid = threadIdx.x;
+  if (tid == 0) { s_err = 0; s_cnt = 0; }
+  __syncthreads();
+  for (int r = 0; r < n_req; ++r) {
+    const int S = seq_lens[r];
+    const int np = (S + PAGE - 1) / PAGE;
+    if (S < 0 || np > max_pages) {
+      if (tid == 0) atomicOr(&s_err, (int)MKV_DEVERR_RANGE);
+      continue;
+    }
+    int cnt = 0, bad = 0;
+    for (int p = tid; p < np; p += blockDim.x) {
+      const int64_t i = (int64_t)r * max_pages + p;
+      if (tags[i] == TAG_R && (p + 1) * PAGE <= S - W && !(anchor && anchor[i])) {
+        cnt++;
+        if (bt[i] < 0 || bt[i] >= n_fp8) bad = 1;
+      }
+    }
+    if (cnt) atomicAdd(&s_cnt, cnt);
+    if (bad) atomicOr(&s_err, (int)MKV_DEVERR_RANGE);
+  }
+  __syncthreads();
+  const int top = ctrl[CTRL_TQ3_TOP];
+  if (tid == 0) {
+    if (s_err == 0 && s_cnt > top) s_err |= MKV_DEVERR_TQ3_EXHAUSTED;
+    if (s_err == 0 && s_cnt > n_fp8) s_err |= MKV_DEVERR_RANGE;
+  }
+  __syncthreads();
+  if (s_err) {
+    if (tid == 0) {
+      atomicOr(&ctrl[CTRL_ERR], s_err);
+      ctrl[CTRL_ABORT] = 1;
+      ctrl[CTRL_NLIST] = 0;
+    }
+    return;
+  }
+  int base = 0;
+  for (int r = 0; r < n_req; ++r) {
+    const int S = seq_lens[r];
+    const int np = (S + PAGE - 1) / PAGE;
+    for (int c0 = 0; c0 < np; c0 += blockDim.x) {
+      const int p = c0 + tid;
+      const int64_t i = (int64_t)r * max_pages + p;
+      int mig = 0;
+      if (p < np && tags[i] == TAG_R && (p + 1) * PAGE <= S - W) {
+        if (anchor && anchor[i]) tags[i] = TAG_A;  // Anchor: tag only, stays FP8
+        else mig = 1;
+      }
+      int tot;
+      const int rank = block_excl_scan(mig, scratch, &tot);
+      if (mig) {
+        int32_t* e = list + 4LL * (base + rank);
+        e[0] = r;
+        e[1] = p;
+        e[2] = bt[i];
+        e[3] = tq3_stack[top - 1 - (base + rank)];
+      }
+      base += tot;
+    }
+  }
+  if (tid == 0) {
+    ctrl[CTRL_TQ3_TOP] = top - base;
+    ctrl[CTRL_NLIST] = base;
+    ctrl[CTRL_ABORT] = 0;
+  }
+}
+
+__device__ __forceinline__ int tq3_decide(int32_t y, int64_t n2) {
+  const int64_t a = 16LL * y;
+  const int64_t a2 = a * a;
+  const int tau[7] = {-29, -17, -8, 0, 8, 17, 29};
+  int c = 0;
+#pragma unroll
+  for (int k = 0; k < 7; ++k) {
+    const int64_t t = tau[k];
+    bool above;
+    if (t == 0) above = a > 0;
+    else if (t > 0) above = (a > 0) && (a2 > t * t * n2);
+    else above = (a >= 0) || (a2 < t * t * n2);
+    c += above ? 1 : 0;
+  }
+  return c;
+}
+
+// Encode one FP8 page-head into a TQ3 region per work item (grid-stride over
+// listed pages x layers x heads).  256 threads.
+template <int D>
+__global__ __launch_bounds__(256) void migrate_encode_kernel(PoolView P) {
+  if (P.ctrl[CTRL_ABORT]) return;
+  constexpr int CL = D / 16, NDW = 3 * D / 128, CB = 3 * D / 32;
+  __shared__ int32_t y[PAGE * D];
+  __shared__ uint8_t kc[PAGE * D];
+  __shared__ uint8_t vc[PAGE * D];
+  const int H = P.n_kv_heads, L = P.n_layers;
+  const int64_t n_items = (int64_t)P.ctrl[CTRL_NLIST] * L * H;
+  const int tid = threadIdx.x, tok = tid >> 4, l16 = tid & 15;
+  for (int64_t item = blockIdx.x; item < n_items; item += gridDim.x) {
+    const int e = (int)(item / (L * H));
+    const int lh = (int)(item % (L * H));
+    const int layer = lh / H, h = lh % H;
+    const int src = P.list[4 * e + 2], dst = P.list[4 * e + 3];
+    const int64_t sph = ((int64_t)layer * P.n_fp8 + src) * H + h;
+    const uint8_t* f8 = P.fp8 + sph * fp8_region_bytes(D);
+    const float sK = P.fp8_scales[sph * 2], sV = P.fp8_scales[sph * 2 + 1];
+    uint8_t* reg = P.tq3 + (((int64_t)layer * P.n_tq3 + dst) * H + h) * tq3_region_bytes(D);
+    // keys: X = sigma * e4m3 * 2^9 (integers), n2 = |X|^2
+    int64_t n2 = 0;
+    for (int j = 0; j < D / 16; ++j) {
+      const int c = l16 + 16 * j;
+      const int32_t X = (int32_t)P.sigma[c] * e4m3_times_512(f8[tok * D + c]);
+      y[tok * D + c] = X;
+      n2 += (int64_t)X * X;
+    }
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) n2 += __shfl_xor(n2, o, 64);
+    __syncthreads();
+    // Sylvester Walsh-Hadamard transform of each token row (exact in int32)
+    for (int s = 1; s < D; s <<= 1) {
+      for (int b = l16; b < D / 2; b += 16) {
+        const int i = (b / s) * 2 * s + (b % s);
+        const int32_t a0 = y[tok * D + i], a1 = y[tok * D + i + s];
+        y[tok * D + i] = a0 + a1;
+        y[tok * D + i + s] = a0 - a1;
+      }
+      __syncthreads();
+    }
+    int M = 0;
+    for (int j = 0; j < D / 16; ++j) {
+      const int c = l16 + 16 * j;
+      const int code = n2 ? tq3_decide(y[tok * D + c], n2) : 3;
+      kc[tok * D + c] = (uint8_t)code;
+      M += mu2x64(code);
+    }
+#pragma unroll
+    for (int o = 1; o < 16; o <<= 1) M += __shfl_xor(M, o, 64);
+    if (l16 == 0) {
+      uint16_t g16 = 0;
+      if (n2) {
+        const double rr = (double)n2 / (double)M;
+        const double sq = sqrt(rr);
+        const double g = sq * ((double)sK * 0.015625);
+        g16 = f64_to_f16_rne_sat(g);
+      }
+      reinterpret_cast<uint16_t*>(reg + 12 * D)[tok] = g16;
+    }
+    // values: per channel asymmetric 3-bit over the 16 tokens
+    if (tid < D) {
+      const int c = tid;
+      double lo = INFINITY, hi = -INFINITY;
+      for (int t = 0; t < PAGE; ++t) {
+        const double vv = (double)sV * (double)e4m3_to_f32(f8[fp8_off<D>(1, t, c)]);
+        lo = fmin(lo, vv);
+        hi = fmax(hi, vv);
+      }
+      const uint16_t z16 = f64_to_f16_rne_sat(lo);
+      const uint16_t s16 = f64_to_f16_rne_sat((hi - lo) / 7.0);
+      reinterpret_cast<uint16_t*>(reg + 12 * D + 32)[c] = s16;
+      reinterpret_cast<uint16_t*>(reg + 14 * D + 32)[c] = z16;
+      const double z = f16_bits_to_f64(z16), s = f16_bits_to_f64(s16);
+      for (int t = 0; t < PAGE; ++t) {
+        int code = 0;
+        if (s != 0.0) {
+          const double vv = (double)sV * (double)e4m3_to_f32(f8[fp8_off<D>(1, t, c)]);
+          double u = rint((vv - z) / s);
+          u = fmin(fmax(u, 0.0), 7.0);
+          code = (int)u;
+        }
+        vc[t * D + c] = (uint8_t)code;
+      }
+    }
+    __syncthreads();
+    // pack: threads 0..63 build K chunks (t, g), threads 64..127 V chunks (r, g)
+    if (tid < 128) {
+      uint32_t Dw[NDW];
+#pragma unroll
+      for (int w = 0; w < NDW; ++w) Dw[w] = 0;
+      uint8_t* out;
+      if (tid < 64) {
+        const int t = tid >> 2, g = tid & 3;
+        for (int q = 0; q < D / 16; ++q)
+          for (int b = 0; b < 4; ++b) quad_put<NDW>(Dw, q, b, kc[t * D + (D / 4) * g + 4 * q + b]);
+        out = reg + (t * 4 + g) * CB;
+      } else {
+        const int rr = (tid - 64) >> 2, g = (tid - 64) & 3;
+        for (int q = 0; q < CL; ++q)
+          for (int b = 0; b < 4; ++b) quad_put<NDW>(Dw, q, b, vc[(4 * g + b) * D + CL * rr + q]);
+        out = reg + 6 * D + (rr * 4 + g) * CB;
+      }
+#pragma unroll
+      for (int w = 0; w < NDW; ++w) reinterpret_cast<uint32_t*>(out)[w] = Dw[w];
+    }
+    __syncthreads();
+  }
+}
+
+__global__ __launch_bounds__(1024) void migrate_publish_kernel(int32_t* bt, uint8_t* tags,
+                                                               int max_pages, int32_t* ctrl,
+                                                               int32_t* fp8_stack,
+                                                               const int32_t* list) {
+  if (ctrl[CTRL_ABORT]) return;
+  const int n = ctrl[CTRL_NLIST];
+  const int top = ctrl[CTRL_FP8_TOP];
+  for (int k = threadIdx.x; k < n; k += blockDim.x) {
+    const int r = list[4 * k], p = list[4 * k + 1], src = list[4 * k + 2], dst = list[4 * k + 3];
+    const int64_t i = (int64_t)r * max_pages + p;
+    bt[i] = dst;
+    tags[i] = TAG_S;
+    fp8_stack[top + k] = src;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) ctrl[CTRL_FP8_TOP] = top + n;
+}
+
+// ===========================================================================
+// Compact per-format page lists
+// ===========================================================================
+__global__ __launch_bounds__(1024) void partition_kernel(const int32_t* bt, const uint8_t* tags,
+                                                         int max_pages, const int32_t* seq_lens,
+                                                         int32_t* list8, int32_t* list3,
+                                                         int32_t* counts, int32_t* err) {
+  __shared__ int scratch[32];
+  const int r = blockIdx.x, tid = threadIdx.x;
+  const int S = seq_lens[r];
+  const int np = (S + PAGE - 1) / PAGE;
+  if (S < 1 || np > max_pages) {
+    if (tid == 0) {
+      counts[2 * r] = 0;
+      counts[2 * r + 1] = 0;
+      if (err) atomicOr(err, (int)MKV_DEVERR_RANGE);
+    }
+    return;
+  }
+  int b8 = 0, b3 = 0, bad = 0;
+  for (int c0 = 0; c0 < np; c0 += blockDim.x) {
+    const int p = c0 + tid;
+    const int64_t i = (int64_t)r * max_pages + p;
+    const int tg = p < np ? tags[i] : TAG_NONE;
+    const int is8 = (p < np && (tg == TAG_R || tg == TAG_A)) ? 1 : 0;
+    const int is3 = (p < np && tg == TAG_S) ? 1 : 0;
+    if (p < np && !is8 && !is3) bad = 1;
+    int t8, t3;
+    const int r8 = block_excl_scan(is8, scratch, &t8);
+    const int r3 = block_excl_scan(is3, scratch, &t3);
+    if (is8) {
+      list8[((int64_t)r * max_pages + b8 + r8) * 2] = p;
+      list8[((int64_t)r * max_pages + b8 + r8) * 2 + 1] = bt[i];
+    }
+    if (is3) {
+      list3[((int64_t)r * max_pages + b3 + r3) * 2] = p;
+      list3[((int64_t)r * max_pages + b3 + r3) * 2 + 1] = bt[i];
+    }
+    b8 += t8;
+    b3 += t3;
+  }
+  if (bad && err) atomicOr(err, (int)MKV_DEVERR_BAD_TAG);
+  if (tid == 0) {
+    counts[2 * r] = b8;
+    counts[2 * r + 1] = b3;
+  }
+}
+
+__global__ void fill_zero_kernel(uint32_t* p, int64_t n_words) {
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n_words;
+       i += (int64_t)gridDim.x * blockDim.x)
+    p[i] = 0;
+}
+
+// ===========================================================================
+// Launchers
+// ===========================================================================
+static int grid_for(int64_t items, int cap) {
+  return (int)(items < 1 ? 1 : (items < cap ? items : cap));
+}
+
+hipError_t launch_append(const PoolView& P, int layer, int n_req, int32_t* bt, uint8_t* tags,
+                         int max_pages, const int32_t* sb, const int32_t* cu, int n_new_total,
+                         const uint16_t* k, const uint16_t* v, hipStream_t s) {
+  hipLaunchKernelGGL(append_plan_kernel, dim3(1), dim3(1024), 0, s, n_req, bt, tags, max_pages, sb,
+                     cu, P.ctrl, P.fp8_stack, P.list, P.n_fp8, n_new_total);
+  const int n_lcall = layer < 0 ? P.n_layers : 1;
+  // upper bound on listed pages: new tokens / 16 + one partial page per request
+  const int64_t pages_bound = (int64_t)n_new_total / PAGE + n_req + 1;
+  const int grid = grid_for(pages_bound * n_lcall * P.n_kv_heads, 8192);
+  if (P.d == 256)
+    hipLaunchKernelGGL(append_quant_kernel<256>, dim3(grid), dim3(256), 0, s, P, layer, n_lcall, sb,
+                       cu, n_new_total, k, v);
+  else
+    hipLaunchKernelGGL(append_quant_kernel<128>, dim3(grid), dim3(256), 0, s, P, layer, n_lcall, sb,
+                       cu, n_new_total, k, v);
+  return hipGetLastError();
+}
+
+hipError_t launch_migrate(const PoolView& P, int n_req, int32_t* bt, uint8_t* tags, int max_pages,
+                          const uint8_t* anchor, const int32_t* seq_lens, hipStream_t s) {
+  hipLaunchKernelGGL(migrate_plan_kernel, dim3(1), dim3(1024), 0, s, n_req, bt, tags, max_pages,
+                     anchor, seq_lens, P.recent, P.ctrl, P.tq3_stack, P.list, P.n_fp8);
+  int64_t bound = (int64_t)n_req * max_pages;
+  if (bound > P.n_fp8) bound = P.n_fp8;
+  const int grid = grid_for(bound * P.n_layers * P.n_kv_heads, 4096);
+  if (P.d == 256)
+    hipLaunchKernelGGL(migrate_encode_kernel<256>, dim3(grid), dim3(256), 0, s, P);
+  else
+    hipLaunchKernelGGL(migrate_encode_kernel<128>, dim3(grid), dim3(256), 0, s, P);
+  hipLaunchKernelGGL(migrate_publish_kernel, dim3(1), dim3(1024), 0, s, bt, tags, max_pages, P.ctrl,
+                     P.fp8_stack, P.list);
+  return hipGetLastError();
+}
+
+hipError_t launch_partition(int n_req, const int32_t* bt, const uint8_t* tags, int max_pages,
+                            const int32_t* seq_lens, int32_t* list8, int32_t* list3,
+                            int32_t* counts, int32_t* err, hipStream_t s) {
+  hipLaunchKernelGGL(partition_kernel, dim3(n_req), dim3(1024), 0, s, bt, tags, max_pages, seq_lens,
+                     list8, list3, counts, err);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s) {
+  const int64_t words = (int64_t)(bytes / 4);
+  if (words == 0) return hipSuccess;
+  const int grid = grid_for((words + 255) / 256, 1024);
+  hipLaunchKernelGGL(fill_zero_kernel, dim3(grid), dim3(256), 0, s, (uint32_t*)p, words);
+  return hipGetLastError();
+}
+
+}  // namespace mkv

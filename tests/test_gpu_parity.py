@@ -1,0 +1,213 @@
+"""GPU parity of the HIP path against the CPU oracle, through the C ABI.
+
+Bit-exact: block tables, tags, free lists, FP8 codes and scales, TQ3 packed
+regions (codes, gamma, V scale/zero).  Attention output: max-abs <= 1e-3
+(fp32 accumulation), the bound the decode path must meet; lse likewise.
+"""
+import numpy as np
+import pytest
+
+import mkv_workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-3
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    assert torch.cuda.is_available()
+    import paper_2608_23834_amd as mk
+    mk.lib()
+    return torch
+
+
+def _run_decode_case(w, lens, recent=None, n_layers=1, chunk=None):
+    from _harness import Twin, max_abs
+    print(f"\n[case] {w.name} lens={lens[:6]}{'...' if len(lens) > 6 else ''} W={recent}", flush=True)
+    tw = Twin(w, n_layers=n_layers, lens=lens, recent=recent)
+    tw.fill(chunk=chunk)
+    tw.check_tables()
+    tw.migrate()
+    tw.check_tables()
+    n8, n3 = tw.check_pages()
+    for layer in range(n_layers):
+        res = tw.decode(layer=layer)
+        err = max_abs(res["out"], res["ref_out"])
+        lerr = max_abs(res["lse"], res["ref_lse"])
+        print(f"  layer {layer}: live fp8 {n8} tq3 {n3}  max|dO| {err:.3e}  max|dlse| {lerr:.3e}",
+              flush=True)
+        assert np.all(np.isfinite(res["out"]))
+        assert err <= TOL, err
+        assert lerr <= TOL, lerr
+    return tw
+
+
+def test_tiny_config_full(torch_cuda):
+    """Config 1 at full size: d=128, GQA 8, 2048 tokens, anchors 0-63, W=256."""
+    w = wl.workload(1)
+    tw = _run_decode_case(w, list(w.ctx))
+    tags = tw.tags.cpu().numpy()[0]
+    assert (tags == 1).sum() == 4 and (tags == 2).sum() == 108 and (tags == 0).sum() == 16
+
+
+def test_ragged_multi_request_d256(torch_cuda):
+    """Several requests with ragged lengths (1, page-aligned, partial pages),
+    GQA 6, d=256, a short Recent window so most pages are TQ3."""
+    w = wl.workload(2)
+    lens = [1, 15, 16, 17, 333, 1024, 2049, 4000]
+    _run_decode_case(w, lens, recent=64)
+
+
+def test_two_layers_chunked_fill(torch_cuda):
+    w = wl.workload(2)
+    _run_decode_case(w, [900, 1700], recent=128, n_layers=2, chunk=250)
+
+
+def test_single_request_16k_config(torch_cuda):
+    """Config 2 shape (one 16K request, anchors 4 + 2%), one layer."""
+    w = wl.workload(2)
+    _run_decode_case(w, list(w.ctx))
+
+
+def test_long_pair_full_size(torch_cuda):
+    """Config 3 at full size (2 x 59,008 tokens) on one layer: the launch
+    configuration the benchmark times."""
+    w = wl.workload(3)
+    tw = _run_decode_case(w, list(w.ctx))
+    tags = tw.tags.cpu().numpy()
+    for r in range(2):
+        assert (tags[r] == 0).sum() == 128
+        assert (tags[r] == 1).sum() == 8 + 36
+        assert (tags[r] == 2).sum() == 3516
+
+
+def test_decode_steps_with_appends(torch_cuda):
+    """Token-by-token decode: append one token per request, migrate, decode;
+    pages are partly filled and rescaled along the way."""
+    from _harness import Twin, max_abs
+    w = wl.workload(2)
+    tw = Twin(w, n_layers=1, lens=[200, 47], recent=32, headroom=32)
+    tw.fill()
+    tw.migrate()
+    for step in range(20):
+        tw.append([1, 1])
+        tw.migrate()
+        tw.check_tables()
+        if step % 5 == 4:
+            tw.check_pages()
+            res = tw.decode()
+            assert max_abs(res["out"], res["ref_out"]) <= TOL
+
+
+def test_partition_pages_matches_oracle(torch_cuda):
+    import oracle
+    import paper_2608_23834_amd as mk
+    torch = torch_cuda
+    rng = np.random.default_rng(3)
+    n_req, mp = 7, 300
+    tags = rng.choice([0, 1, 2], size=(n_req, mp)).astype(np.uint8)
+    bt = rng.integers(0, 10 ** 6, size=(n_req, mp)).astype(np.int32)
+    lens = np.array([1, 16, 17, 4799, 4800, 2000, 333], np.int32)
+    o8, o3, cnt = oracle.partition(bt, tags, lens)
+    g8 = torch.full((n_req, mp, 2), -1, dtype=torch.int32, device="cuda")
+    g3 = torch.full((n_req, mp, 2), -1, dtype=torch.int32, device="cuda")
+    gc = torch.zeros((n_req, 2), dtype=torch.int32, device="cuda")
+    mk.kv_partition_pages(torch.from_numpy(bt).cuda(), torch.from_numpy(tags).cuda(),
+                          torch.from_numpy(lens).cuda(), g8, g3, gc)
+    assert np.array_equal(gc.cpu().numpy(), cnt)
+    assert np.array_equal(g8.cpu().numpy(), o8)
+    assert np.array_equal(g3.cpu().numpy(), o3)
+
+
+def test_e4m3_encode_all_bf16_inputs(torch_cuda):
+    """Every bf16 value in [-448, 448] through the append path with page scale
+    exactly 1 (each page-head's amax is 448): codes must equal the oracle's
+    E4M3 rounding of the same value."""
+    import oracle
+    import paper_2608_23834_amd as mk
+    torch = torch_cuda
+    d = 128
+    bits = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    vals = wl.bf16_to_f32(bits)
+    keep = np.isfinite(vals) & (np.abs(vals) <= 448.0)
+    bits = bits[keep]
+    per_tok = d - 1
+    n_tok = -(-bits.size // per_tok)
+    n_tok = -(-n_tok // 16) * 16
+    x = np.zeros((n_tok, d), np.uint16)
+    flat = np.zeros(n_tok * per_tok, np.uint16)
+    flat[: bits.size] = bits
+    x[:, 1:] = flat.reshape(n_tok, per_tok)
+    x[:, 0] = wl.bf16_round(np.float32(448.0))
+    K = x.reshape(1, n_tok, 1, d)
+    pages = n_tok // 16
+    gp = mk.Pool(1, 1, 1, d, pages, 1, 10 ** 6, np.ones(d, np.int8))
+    bt = torch.full((1, pages), -1, dtype=torch.int32, device="cuda")
+    tg = torch.full((1, pages), 0xFF, dtype=torch.uint8, device="cuda")
+    kk = torch.from_numpy(K.view(np.int16)).cuda()
+    mk.kv_append_fp8(gp, -1, bt, tg, torch.zeros(1, dtype=torch.int32, device="cuda"),
+                     torch.tensor([0, n_tok], dtype=torch.int32, device="cuda"), kk, kk)
+    torch.cuda.synchronize()
+    assert np.all(gp.fp8_scales_view().cpu().numpy() == 1.0)
+    ids = bt.cpu().numpy()[0]
+    codes = gp.fp8_view()[0, torch.from_numpy(ids).long().cuda(), 0, : 16 * d].cpu().numpy()
+    codes = codes.reshape(n_tok, d)
+    want = oracle.e4m3_from_f32(wl.bf16_to_f32(x))
+    assert np.array_equal(codes, want)
+
+
+def test_workspace_reuse_and_repeat(torch_cuda):
+    """Split counters reset themselves: repeated calls on one workspace agree."""
+    import paper_2608_23834_amd as mk
+    from _harness import Twin
+    torch = torch_cuda
+    w = wl.workload(2)
+    tw = Twin(w, lens=[3000, 100, 5000], recent=64, with_oracle=False)
+    tw.fill()
+    tw.migrate()
+    q = torch.from_numpy(wl.q_decode(w, 0)[:1].repeat(3, 0).view(np.int16)).cuda()
+    sl = torch.tensor(tw.cur, dtype=torch.int32, device="cuda")
+    ws = mk.workspace(tw.gpu, 3, tw.max_pages)
+    outs = []
+    for _ in range(4):
+        out = torch.zeros((3, w.n_q_heads, w.head_dim), device="cuda")
+        mk.paged_attn_decode(tw.gpu, 0, q, tw.bt, tw.tags, sl, out, None, ws)
+        outs.append(out.cpu().numpy())
+    for o in outs[1:]:
+        assert np.array_equal(o, outs[0])
+    c = mk.kv_pool_counters(tw.gpu)
+    assert c["decode_routes"] == 4 and c["fallbacks"] == 0 and c["dense_shadow_bytes"] == 0
+
+
+def test_device_errors_fail_closed(torch_cuda):
+    """Free lists too short: the call changes nothing and sets the error word."""
+    import paper_2608_23834_amd as mk
+    torch = torch_cuda
+    d = 128
+    gp = mk.Pool(1, 2, 1, d, 3, 1, 16, np.ones(d, np.int8))
+    bt = torch.full((1, 8), -1, dtype=torch.int32, device="cuda")
+    tg = torch.full((1, 8), 0xFF, dtype=torch.uint8, device="cuda")
+    x = torch.zeros((1, 64, 1, d), dtype=torch.int16, device="cuda")
+    mk.kv_append_fp8(gp, -1, bt, tg, torch.zeros(1, dtype=torch.int32, device="cuda"),
+                     torch.tensor([0, 64], dtype=torch.int32, device="cuda"), x, x)
+    assert mk.kv_pool_check_errors(gp, clear=True) & mk.DEVERR["FP8_EXHAUSTED"]
+    assert (bt.cpu().numpy() == -1).all() and mk.kv_pool_free_counts(gp) == (3, 1)
+    x = x[:, :48].contiguous()
+    mk.kv_append_fp8(gp, -1, bt, tg, torch.zeros(1, dtype=torch.int32, device="cuda"),
+                     torch.tensor([0, 48], dtype=torch.int32, device="cuda"), x, x)
+    assert mk.kv_pool_check_errors(gp) == 0
+    # window 16 tokens, 48 tokens live: pages 0 and 1 leave it, TQ3 pool holds 1 page
+    before = (bt.cpu().numpy().copy(), tg.cpu().numpy().copy())
+    mk.kv_migrate_to_tq3(gp, bt, tg, None, torch.tensor([48], dtype=torch.int32, device="cuda"))
+    assert mk.kv_pool_check_errors(gp, clear=True) & mk.DEVERR["TQ3_EXHAUSTED"]
+    assert np.array_equal(bt.cpu().numpy(), before[0]) and np.array_equal(tg.cpu().numpy(), before[1])
+    # an invalid sequence length gives zero output and the RANGE bit
+    ws = mk.workspace(gp, 1, 8)
+    out = torch.full((1, 2, d), 7.0, device="cuda")
+    q = torch.zeros((1, 2, d), dtype=torch.int16, device="cuda")
+    mk.paged_attn_decode(gp, 0, q, bt, tg, torch.tensor([0], dtype=torch.int32, device="cuda"),
+                         out, None, ws)
+    assert (out.cpu().numpy() == 0).all()
+    assert mk.kv_pool_check_errors(gp, clear=True) & mk.DEVERR["RANGE"]
