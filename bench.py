@@ -1,0 +1,269 @@
+#!/usr/bin/env python3
+"""Benchmark of the Minima-KV mixed FP8/TQ3 decode path on one MI355X.
+
+Workload: the long-context pair (2 requests x 59,008 tokens, 16 full-attention
+layers, 24 query / 4 KV heads, head dim 256, 16-token pages, Recent window
+2,048 tokens, anchors = first 8 pages + 1 % of the rest), synthetic seeded
+data with the distributions of mkv_workloads.
+
+One step is one decode step of the whole path: for each of the 16 layers,
+kv_append_fp8 (the new token of each request) then paged_attn_decode; after
+the last layer kv_migrate_to_tq3 (pages leaving the Recent window).  All inputs
+are resident in HBM before the timed region.  The headline value is the step
+time per layer (us/layer, lower is better); the decode kernel's own time, its
+effective KV bandwidth and its fraction of the 8 TB/s HBM peak are reported
+next to it, measured with HIP events on the stream the kernels run on.
+
+    python bench.py [--gpus 1] [--steps 20] [--warmup 3]
+"""
+from __future__ import annotations
+
+import argparse
+import concurrent.futures as cf
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import mkv_workloads as wl  # noqa: E402
+
+HBM_PEAK = 8.0e12  # MI355X HBM3E, bytes/s
+PAGE = 16
+
+
+def kv_bytes_of(tags_row: np.ndarray, seq_len: int, d: int, n_kv_heads: int) -> int:
+    """Algorithmic KV bytes one decode reads for one request: per attended
+    page-head, FP8 = 2*B*d codes + 8 B scales, TQ3 = 2*B*3d/8 codes + 2*B gamma
+    + 4*d V scale/zero (B = valid tokens of the page)."""
+    tot = 0
+    npg = (seq_len + PAGE - 1) // PAGE
+    for p in range(npg):
+        b = min(PAGE, seq_len - p * PAGE)
+        if tags_row[p] == 2:
+            tot += 2 * b * 3 * d // 8 + 2 * b + 4 * d
+        else:
+            tot += 2 * b * d + 8
+    return tot * n_kv_heads
+
+
+def build_state(w, n_layers, extra_tokens, mk, torch):
+    """Pool for `n_layers` layers filled with the workload's context, migrated."""
+    lens = list(w.ctx)
+    n_req = len(lens)
+    max_pages = (max(lens) + extra_tokens + PAGE - 1) // PAGE
+    tot_pages = sum((l + extra_tokens + PAGE - 1) // PAGE for l in lens)
+    pool = mk.Pool(n_layers, w.n_q_heads, w.n_kv_heads, w.head_dim, tot_pages + 16, tot_pages + 16,
+                   w.recent, wl.rot_signs(w), wl.free_order(w, tot_pages + 16, "fp8"),
+                   wl.free_order(w, tot_pages + 16, "tq3"))
+    bt = torch.full((n_req, max_pages), -1, dtype=torch.int32, device="cuda")
+    tags = torch.full((n_req, max_pages), 0xFF, dtype=torch.uint8, device="cuda")
+    sb = torch.zeros(n_req, dtype=torch.int32, device="cuda")
+    cu = torch.tensor(np.r_[0, np.cumsum(lens)], dtype=torch.int32, device="cuda")
+
+    def gen(layer):
+        ks, vs = [], []
+        for r, L in enumerate(lens):
+            k, v = wl.kv_layer(w, layer, L, token_offset=r * 1_000_000)
+            ks.append(k)
+            vs.append(v)
+        return np.concatenate(ks), np.concatenate(vs)
+
+    with cf.ThreadPoolExecutor(max_workers=4) as ex:
+        futs = [ex.submit(gen, l) for l in range(n_layers)]
+        for l, f in enumerate(futs):
+            k, v = f.result()
+            kt = torch.from_numpy(k.view(np.int16)).cuda()
+            vt = torch.from_numpy(v.view(np.int16)).cuda()
+            mk.kv_append_fp8(pool, l, bt, tags, sb, cu, kt, vt)
+            torch.cuda.synchronize()
+            del kt, vt
+    am = torch.from_numpy(wl.anchor_mask(w, max_pages)).cuda()
+    sl = torch.tensor(lens, dtype=torch.int32, device="cuda")
+    mk.kv_migrate_to_tq3(pool, bt, tags, am, sl)
+    torch.cuda.synchronize()
+    err = mk.kv_pool_check_errors(pool)
+    if err:
+        raise RuntimeError(f"device error word {err:#x} while building the state")
+    return pool, bt, tags, am, max_pages
+
+
+def cpu_baseline(w, budget_s=25.0):
+    """The CPU oracle, as it stands, on a bounded sample of the same workload:
+    one layer of the long pair (both requests, all heads), state built by the
+    oracle's own append + migrate (not timed); the oracle's decode is timed."""
+    import oracle
+    lens = list(w.ctx)
+    n_req = len(lens)
+    max_pages = (max(lens) + PAGE - 1) // PAGE
+    tot = sum((l + PAGE - 1) // PAGE for l in lens) + 16
+    P = oracle.Pool(1, w.n_q_heads, w.n_kv_heads, w.head_dim, tot, tot, w.recent, wl.rot_signs(w),
+                    wl.free_order(w, tot, "fp8"), wl.free_order(w, tot, "tq3"))
+    bt = np.full((n_req, max_pages), -1, np.int32)
+    tags = np.full((n_req, max_pages), 0xFF, np.uint8)
+    ks, vs = zip(*(wl.kv_layer(w, 0, L, token_offset=r * 1_000_000) for r, L in enumerate(lens)))
+    k = np.concatenate(ks)[None]
+    v = np.concatenate(vs)[None]
+    assert P.append(-1, bt, tags, np.zeros(n_req, np.int32),
+                    np.r_[0, np.cumsum(lens)].astype(np.int32), k, v) == 0
+    P.migrate(bt, tags, wl.anchor_mask(w, max_pages), np.array(lens, np.int32))
+    q = wl.q_decode(w, 0)
+    sl = np.array(lens, np.int32)
+    times = []
+    t_end = time.perf_counter() + budget_s
+    while True:
+        t0 = time.perf_counter()
+        P.decode(0, q, bt, tags, sl)
+        times.append(time.perf_counter() - t0)
+        if time.perf_counter() + times[-1] > t_end or len(times) >= 5:
+            break
+    kvb = sum(kv_bytes_of(tags[r], lens[r], w.head_dim, w.n_kv_heads) for r in range(n_req))
+    med = float(np.median(times))
+    return {"value": med * 1e6, "unit": "us/layer", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"one layer of {w.name} (2 requests x {lens[0]} tokens, all 24/4 heads), "
+                      f"fp64 decode over the reconstructed cache, median of {len(times)} runs",
+            "kv_gb_per_s": kvb / med / 1e9,
+            "cpu": _cpu_model()}
+
+
+def _cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--cfg", type=int, default=3)
+    ap.add_argument("--layers", type=int, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
+              "(the decode path shards by request or KV head without any exchange; see the "
+              "design notes)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2608_23834_amd as mk
+    mk.lib()
+    torch.cuda.init()
+    w = wl.workload(args.cfg)
+    n_layers = args.layers or w.n_layers
+    n_steps = args.steps + args.warmup
+    t_setup = time.perf_counter()
+    pool, bt, tags, am, max_pages = build_state(w, n_layers, n_steps + 16, mk, torch)
+    lens = list(w.ctx)
+    n_req = len(lens)
+    Hkv, d = w.n_kv_heads, w.head_dim
+
+    # per-step inputs, resident before timing
+    q_all = torch.from_numpy(np.stack([wl.q_decode(w, l) for l in range(n_layers)]).view(np.int16)).cuda()
+    new_k = np.zeros((n_layers, n_steps, n_req, Hkv, d), np.uint16)
+    new_v = np.zeros_like(new_k)
+    for l in range(n_layers):
+        for r in range(n_req):
+            k, v = wl.kv_layer(w, l, n_steps, token_offset=r * 1_000_000 + lens[r])
+            new_k[l, :, r] = k
+            new_v[l, :, r] = v
+    nk = torch.from_numpy(new_k.view(np.int16)).cuda()
+    nv = torch.from_numpy(new_v.view(np.int16)).cuda()
+    seq_before = torch.tensor([[L + s for L in lens] for s in range(n_steps)], dtype=torch.int32,
+                              device="cuda")
+    seq_after = seq_before + 1
+    cu1 = torch.arange(n_req + 1, dtype=torch.int32, device="cuda")
+    out = torch.zeros((n_req, w.n_q_heads, d), device="cuda")
+    ws = mk.workspace(pool, n_req, max_pages)
+    torch.cuda.synchronize()
+    setup_s = time.perf_counter() - t_setup
+
+    stream = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(args.steps * n_layers)]
+    tags_start = None
+
+    def step(s, timed):
+        for l in range(n_layers):
+            mk.kv_append_fp8(pool, l, bt, tags, seq_before[s], cu1, nk[l, s], nv[l, s])
+            if timed:
+                e0, e1 = ev[(s - args.warmup) * n_layers + l]
+                e0.record(stream)
+            mk.paged_attn_decode(pool, l, q_all[l], bt, tags, seq_after[s], out, None, ws)
+            if timed:
+                e1.record(stream)
+        mk.kv_migrate_to_tq3(pool, bt, tags, am, seq_after[s])
+
+    for s in range(args.warmup):
+        step(s, False)
+    torch.cuda.synchronize()
+    tags_start = tags.cpu().numpy()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record(stream)
+    for s in range(args.warmup, n_steps):
+        step(s, True)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    total_ms = t0.elapsed_time(t1)
+    dec_ms = np.array([a.elapsed_time(b) for a, b in ev])
+    err = mk.kv_pool_check_errors(pool)
+    if err:
+        raise RuntimeError(f"device error word {err:#x} during the benchmark")
+    tags_end = tags.cpu().numpy()
+    sl0 = [L + args.warmup + 1 for L in lens]
+    sl1 = [L + n_steps for L in lens]
+    kvb0 = sum(kv_bytes_of(tags_start[r], sl0[r], d, Hkv) for r in range(n_req))
+    kvb1 = sum(kv_bytes_of(tags_end[r], sl1[r], d, Hkv) for r in range(n_req))
+    kv_bytes = 0.5 * (kvb0 + kvb1)
+    dec_us = float(dec_ms.mean() * 1e3)
+    achieved = kv_bytes / (dec_us * 1e-6)
+    ms_per_step = total_ms / args.steps
+    counters = mk.kv_pool_counters(pool)
+
+    res = {
+        "metric": "mixed FP8/TQ3 decode attn: us/layer, effective KV GB/s, % of HBM roofline",
+        "value": round(ms_per_step * 1e3 / n_layers, 3),
+        "unit": "us/layer",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "n_req": n_req, "seq_len": lens[0], "layers": n_layers,
+                   "q_heads": w.n_q_heads, "kv_heads": Hkv, "head_dim": d, "page_tokens": PAGE,
+                   "recent_tokens": w.recent, "kv_formats": "fp8-e4m3 (R,A) + tq3 (S)",
+                   "step": "per layer: append 1 token/request + decode; then migrate"},
+        "decode_attn_us_per_layer": round(dec_us, 3),
+        "decode_attn_us_p50": round(float(np.median(dec_ms) * 1e3), 3),
+        "kv_bytes_per_layer": int(kv_bytes),
+        "effective_kv_gb_per_s": round(achieved / 1e9, 1),
+        "roofline": {"bound": "hbm", "achieved": round(achieved / 1e9, 1), "peak": HBM_PEAK / 1e9,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK, 4), "traffic": None,
+                     "kernel": "decode_kernel<256>"},
+        "counters": {k: int(v) for k, v in counters.items()},
+        "setup_s": round(setup_s, 1),
+    }
+    if not args.no_cpu_baseline and args.cfg == 3:
+        res["cpu_baseline"] = cpu_baseline(w)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

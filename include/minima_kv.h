@@ -159,9 +159,8 @@ mkv_status kv_migrate_to_tq3(mkv_pool* pool, int32_t n_req, int32_t* block_table
 mkv_status paged_attn_workspace_bytes(const mkv_pool* pool, int32_t n_req, int32_t max_pages,
                                       int32_t n_q_total, size_t* bytes);
 
-/* Zero the part of a workspace that must start at zero (the split counters).
- * A workspace from torch.zeros/hipMemset needs no call; every completed
- * attention call leaves that part zero again. */
+/* Zero a workspace (optional: the attention calls write every workspace word
+ * they read, so a workspace needs no initialisation). */
 mkv_status paged_attn_workspace_init(void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Mixed-format decode attention (Sec. 3.3; Sec. 4.1 direct fused decode).
@@ -174,10 +173,10 @@ mkv_status paged_attn_workspace_init(void* ws, size_t ws_bytes, hipStream_t stre
  * (softmax-merge).  q: device bf16 [n_req][n_q_heads][d]; out: device fp32
  * [n_req][n_q_heads][d]; lse: device fp32 [n_req][n_q_heads] (natural log of
  * the softmax denominator, scores in units of q.k/sqrt(d)) or NULL.
- * ws: device, >= paged_attn_workspace_bytes(pool, n_req, max_pages, 0), whose
- * counter part is zero (see paged_attn_workspace_init).  An invalid seq_len
- * or an unmapped page below seq_len sets the error word; such requests get
- * zero outputs. */
+ * ws: device, >= paged_attn_workspace_bytes(pool, n_req, max_pages, 0); it
+ * holds the split partials (O(splits x heads x d) floats).  max_pages is at
+ * most 262144.  An invalid seq_len or an unmapped page below seq_len sets the
+ * error word; such requests get zero outputs. */
 mkv_status paged_attn_decode(mkv_pool* pool, int32_t layer, int32_t n_req, const uint16_t* q,
                              const int32_t* block_table, const uint8_t* tags, int32_t max_pages,
                              const int32_t* seq_lens, float* out, float* lse, void* ws,

@@ -171,15 +171,26 @@ _BLOCK = 4096
 
 def _rows(seed, key, layer, start, n, width):
     """N(0,1) rows [start, start+n) of a (virtually infinite) row stream;
-    each block of 4096 rows has its own generator."""
+    each block of 4096 rows has its own generator (blocks drawn in parallel)."""
     res = np.empty((n, width), np.float32)
-    b0, b1 = start // _BLOCK, (start + n - 1) // _BLOCK if n > 0 else start // _BLOCK - 1
-    for b in range(b0, b1 + 1):
+    if n <= 0:
+        return res
+    b0, b1 = start // _BLOCK, (start + n - 1) // _BLOCK
+
+    def one(b):
         g = _rng(seed, key, layer, b)
         blk = g.standard_normal((_BLOCK, width), dtype=np.float32)
         lo = max(start, b * _BLOCK)
         hi = min(start + n, (b + 1) * _BLOCK)
         res[lo - start:hi - start] = blk[lo - b * _BLOCK:hi - b * _BLOCK]
+
+    if b1 - b0 >= 2:
+        import concurrent.futures as cf
+        with cf.ThreadPoolExecutor(max_workers=min(8, b1 - b0 + 1)) as ex:
+            list(ex.map(one, range(b0, b1 + 1)))
+    else:
+        for b in range(b0, b1 + 1):
+            one(b)
     return res
 
 

@@ -59,6 +59,11 @@ def lib():
     return _lib
 
 
+def num_threads() -> int:
+    """OpenMP threads the oracle's parallel loops use."""
+    return lib().orc_num_threads()
+
+
 def _p(a):
     return a.ctypes.data_as(ctypes.c_void_p)
 
@@ -100,6 +105,8 @@ def _declare(L):
     L.orc_decode.argtypes = [vp, i32, i32, i32, vp, vp, vp, i32, vp, vp, vp]
     L.orc_chunk.argtypes = [vp, i32, i32, i32, vp, vp, vp, vp, i32, vp, vp, i64]
     L.orc_merge.argtypes = [i32, i32, vp, vp, vp, vp, vp]
+    L.orc_num_threads.restype = i32
+    L.orc_num_threads.argtypes = []
 
 
 # --------------------------------------------------------------------------

@@ -36,6 +36,7 @@
  * closed forms, library routines or brute force (see tests/test_oracle_*.py).
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -221,6 +222,7 @@ static const int64_t TAU16[7] = {-29, -17, -8, 0, 8, 17, 29};
 static const int64_t MU2X64[8] = {324, 121, 36, 4, 4, 36, 121, 324};
 
 double orc_codebook(int k) { return MU[k]; }
+int orc_num_threads(void) { return omp_get_max_threads(); }
 
 /* c = #{k : y > T_k * sqrt(n2)}, evaluated exactly with integers; n2 > 0. */
 int orc_tq3_decide(int64_t y, int64_t n2) {
@@ -538,36 +540,55 @@ int orc_append(orc_pool* P, int layer, int n_req, int32_t* bt, uint8_t* tags, in
     }
   }
   int l0 = layer < 0 ? 0 : layer, l1 = layer < 0 ? P->n_layers : layer + 1;
-  float* buf = (float*)malloc(sizeof(float) * ORC_PAGE * d);
-  for (int l = l0; l < l1; ++l) {
-    int64_t lbase = (int64_t)(l - l0) * n_new_total * H * d;
-    for (int r = 0; r < n_req; ++r) {
-      int n = cu_new[r + 1] - cu_new[r];
-      if (n <= 0) continue;
-      int sb = seq_before[r];
-      int p0 = sb / ORC_PAGE, p1 = (sb + n - 1) / ORC_PAGE;
-      for (int p = p0; p <= p1; ++p) {
-        int id = bt[(int64_t)r * max_pages + p];
-        int t0 = sb > p * ORC_PAGE ? sb - p * ORC_PAGE : 0;
-        int end = sb + n - p * ORC_PAGE;
-        int t1 = end < ORC_PAGE ? end : ORC_PAGE;
-        for (int h = 0; h < H; ++h) {
-          uint8_t* reg = fp8_region(P, l, id, h);
-          float* sc = fp8_scales(P, l, id, h);
-          for (int kv = 0; kv < 2; ++kv) {
-            const uint16_t* src = kv ? v : k;
-            for (int t = t0; t < t1; ++t) {
-              int row = cu_new[r] + (p * ORC_PAGE + t - sb);
-              for (int c = 0; c < d; ++c)
-                buf[(t - t0) * d + c] = bf16_to_f32(src[lbase + ((int64_t)row * H + h) * d + c]);
-            }
-            fp8_append_tensor(d, reg + (kv ? (int64_t)ORC_PAGE * d : 0), kv, sc + kv, t0, t1, buf);
-          }
-        }
-      }
+  /* the page-heads are independent: list them, then quantize each one */
+  int64_t n_items = 0;
+  for (int r = 0; r < n_req; ++r) {
+    int n = cu_new[r + 1] - cu_new[r];
+    if (n > 0) n_items += (seq_before[r] + n - 1) / ORC_PAGE - seq_before[r] / ORC_PAGE + 1;
+  }
+  int32_t* items = (int32_t*)malloc(sizeof(int32_t) * 2 * (n_items + 1));
+  int64_t it = 0;
+  for (int r = 0; r < n_req; ++r) {
+    int n = cu_new[r + 1] - cu_new[r];
+    if (n <= 0) continue;
+    for (int p = seq_before[r] / ORC_PAGE; p <= (seq_before[r] + n - 1) / ORC_PAGE; ++p) {
+      items[2 * it] = r;
+      items[2 * it + 1] = p;
+      it++;
     }
   }
-  free(buf);
+  int64_t total = n_items * (int64_t)(l1 - l0) * H;
+#pragma omp parallel
+  {
+    float* buf = (float*)malloc(sizeof(float) * ORC_PAGE * d);
+#pragma omp for schedule(dynamic, 64)
+    for (int64_t w = 0; w < total; ++w) {
+      int h = (int)(w % H);
+      int64_t rest = w / H;
+      int l = l0 + (int)(rest % (l1 - l0));
+      int64_t e = rest / (l1 - l0);
+      int r = items[2 * e], p = items[2 * e + 1];
+      int64_t lbase = (int64_t)(l - l0) * n_new_total * H * d;
+      int sb = seq_before[r], n = cu_new[r + 1] - cu_new[r];
+      int id = bt[(int64_t)r * max_pages + p];
+      int t0 = sb > p * ORC_PAGE ? sb - p * ORC_PAGE : 0;
+      int end = sb + n - p * ORC_PAGE;
+      int t1 = end < ORC_PAGE ? end : ORC_PAGE;
+      uint8_t* reg = fp8_region(P, l, id, h);
+      float* sc = fp8_scales(P, l, id, h);
+      for (int kv = 0; kv < 2; ++kv) {
+        const uint16_t* src = kv ? v : k;
+        for (int t = t0; t < t1; ++t) {
+          int row = cu_new[r] + (p * ORC_PAGE + t - sb);
+          for (int c = 0; c < d; ++c)
+            buf[(t - t0) * d + c] = bf16_to_f32(src[lbase + ((int64_t)row * H + h) * d + c]);
+        }
+        fp8_append_tensor(d, reg + (kv ? (int64_t)ORC_PAGE * d : 0), kv, sc + kv, t0, t1, buf);
+      }
+    }
+    free(buf);
+  }
+  free(items);
   return 0;
 }
 
@@ -600,15 +621,9 @@ int orc_migrate(orc_pool* P, int n_req, int32_t* bt, uint8_t* tags, int max_page
     }
   }
   if (n_mig > *P->tq3_top) return -1;
-  uint8_t* kcode = (uint8_t*)malloc((size_t)ORC_PAGE * d);
-  uint8_t* vcode = (uint8_t*)malloc((size_t)ORC_PAGE * d);
-  uint8_t* k8 = (uint8_t*)malloc((size_t)ORC_PAGE * d);
-  uint8_t* v8 = (uint8_t*)malloc((size_t)ORC_PAGE * d);
-  uint16_t gamma[ORC_PAGE];
-  uint16_t* vs = (uint16_t*)malloc(2 * (size_t)d);
-  uint16_t* vz = (uint16_t*)malloc(2 * (size_t)d);
-  int32_t* released = (int32_t*)malloc(sizeof(int32_t) * (n_mig + 1));
-  int n_rel = 0;
+  /* 1. tier transitions and id assignment in ascending (request, page) */
+  int32_t* mig = (int32_t*)malloc(sizeof(int32_t) * 4 * (n_mig + 1));
+  int k_mig = 0;
   for (int r = 0; r < n_req; ++r) {
     int np = (seq_lens[r] + ORC_PAGE - 1) / ORC_PAGE;
     for (int p = 0; p < np && p < max_pages; ++p) {
@@ -618,31 +633,52 @@ int orc_migrate(orc_pool* P, int n_req, int32_t* bt, uint8_t* tags, int max_page
       int z = orc_tier(p, seq_lens[r], P->recent, is_anchor);
       if (z == TAG_A) { tags[i] = TAG_A; continue; }
       if (z != TAG_S) continue;
-      int src = bt[i];
       *P->tq3_top -= 1;
-      int dst = P->tq3_stack[*P->tq3_top];
-      for (int l = 0; l < P->n_layers; ++l)
-        for (int h = 0; h < H; ++h) {
-          const uint8_t* reg = fp8_region(P, l, src, h);
-          const float* sc = fp8_scales(P, l, src, h);
-          for (int t = 0; t < ORC_PAGE; ++t)
-            for (int c = 0; c < d; ++c) {
-              k8[t * d + c] = reg[orc_fp8_k_off(d, t, c)];
-              v8[t * d + c] = reg[orc_fp8_v_off(d, t, c)];
-            }
-          orc_tq3_encode(d, k8, sc[0], v8, sc[1], P->sigma, kcode, gamma, vcode, vs, vz);
-          orc_tq3_pack(d, kcode, gamma, vcode, vs, vz, tq3_region(P, l, dst, h));
-        }
-      bt[i] = dst;
-      tags[i] = TAG_S;
-      released[n_rel++] = src;
+      mig[4 * k_mig] = r;
+      mig[4 * k_mig + 1] = p;
+      mig[4 * k_mig + 2] = bt[i];
+      mig[4 * k_mig + 3] = P->tq3_stack[*P->tq3_top];
+      k_mig++;
     }
   }
-  for (int j = 0; j < n_rel; ++j) {
-    P->fp8_stack[*P->fp8_top] = released[j];
+  /* 2. normalize-rotate-pack every page-head (independent) */
+  int64_t total = (int64_t)n_mig * P->n_layers * H;
+#pragma omp parallel
+  {
+    uint8_t* kcode = (uint8_t*)malloc((size_t)ORC_PAGE * d);
+    uint8_t* vcode = (uint8_t*)malloc((size_t)ORC_PAGE * d);
+    uint8_t* k8 = (uint8_t*)malloc((size_t)ORC_PAGE * d);
+    uint8_t* v8 = (uint8_t*)malloc((size_t)ORC_PAGE * d);
+    uint16_t gamma[ORC_PAGE];
+    uint16_t* vs = (uint16_t*)malloc(2 * (size_t)d);
+    uint16_t* vz = (uint16_t*)malloc(2 * (size_t)d);
+#pragma omp for schedule(dynamic, 16)
+    for (int64_t w = 0; w < total; ++w) {
+      int h = (int)(w % H);
+      int l = (int)((w / H) % P->n_layers);
+      int e = (int)(w / H / P->n_layers);
+      int src = mig[4 * e + 2], dst = mig[4 * e + 3];
+      const uint8_t* reg = fp8_region(P, l, src, h);
+      const float* sc = fp8_scales(P, l, src, h);
+      for (int t = 0; t < ORC_PAGE; ++t)
+        for (int c = 0; c < d; ++c) {
+          k8[t * d + c] = reg[orc_fp8_k_off(d, t, c)];
+          v8[t * d + c] = reg[orc_fp8_v_off(d, t, c)];
+        }
+      orc_tq3_encode(d, k8, sc[0], v8, sc[1], P->sigma, kcode, gamma, vcode, vs, vz);
+      orc_tq3_pack(d, kcode, gamma, vcode, vs, vz, tq3_region(P, l, dst, h));
+    }
+    free(kcode); free(vcode); free(k8); free(v8); free(vs); free(vz);
+  }
+  /* 3. publish (tag S, new id) and release the FP8 pages in the same order */
+  for (int j = 0; j < n_mig; ++j) {
+    int64_t i = (int64_t)mig[4 * j] * max_pages + mig[4 * j + 1];
+    bt[i] = mig[4 * j + 3];
+    tags[i] = TAG_S;
+    P->fp8_stack[*P->fp8_top] = mig[4 * j + 2];
     *P->fp8_top += 1;
   }
-  free(kcode); free(vcode); free(k8); free(v8); free(vs); free(vz); free(released);
+  free(mig);
   return n_mig;
 }
 

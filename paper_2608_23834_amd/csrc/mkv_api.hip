@@ -188,7 +188,7 @@ mkv_status paged_attn_decode(mkv_pool* pool, int32_t layer, int32_t n_req, const
   if (!pool || !q || !block_table || !tags || !seq_lens || !out || !ws) return MKV_EINVAL;
   if (n_req < 1 || max_pages < 1) return MKV_EINVAL;
   if (layer < 0 || layer >= pool->n_layers) return MKV_ERANGE;
-  if (n_req > 65535) return MKV_ERANGE;
+  if (n_req > 65535 || max_pages > 1024 * 256) return MKV_ERANGE;
   if (ws_bytes < decode_ws_bytes(n_req, max_pages, pool->n_kv_heads, pool->group, pool->d))
     return MKV_ENOMEM;
   mkv_status st = hip_status(launch_decode(view_of(pool), layer, n_req, q, block_table, tags,

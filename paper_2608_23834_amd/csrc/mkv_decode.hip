@@ -16,16 +16,19 @@
 //     by the hardware converter; online softmax in base 2; PV on MFMA with
 //     M = 16 channels, N = heads, K = 32 tokens (two pages), values
 //     dequantized in registers (TQ3: zero + scale * code per channel);
-//  4. the four waves merge in LDS into one (m_j, l_j, O_j) partial per chunk;
-//     the last workgroup of a (request, KV head) merges all partials of both
-//     formats (Eq. softmax-merge) and writes the output: no second launch and
-//     no cache-sized buffer.
+//  4. the four waves merge in LDS into one (m_j, l_j, O_j) partial per chunk.
+// A second kernel merges all partials of both formats per (request, query
+// head) (Eq. softmax-merge).  The workspace holds O(chunks x heads x d)
+// partials, never anything the size of the cache.
 #include <hip/hip_runtime.h>
 
 #include "mkv_internal.h"
 #include "../../include/minima_kv.h"
 
 namespace mkv {
+
+// tag slices of 1024 pages: max_pages <= 1024 * MAX_SLICES (4M tokens)
+constexpr int MAX_SLICES = 256;
 
 struct DecodeArgs {
   PoolView P;
@@ -36,7 +39,7 @@ struct DecodeArgs {
   const int32_t* seq_lens;
   float* out;
   float* lse;
-  uint32_t* counters;
+  int32_t* totals;
   float* partials;
   int c3, c8, max_chunks;
   float sm_log2;  // log2(e) / sqrt(d)
@@ -44,22 +47,22 @@ struct DecodeArgs {
 
 DecodeShape decode_shape(int n_req, int max_pages, int n_kv_heads) {
   DecodeShape s;
-  int64_t ph = (int64_t)n_req * max_pages * n_kv_heads / 512;
+  // about 512 chunk workgroups per launch (two per CU at two waves per SIMD)
+  const int64_t ph = (int64_t)n_req * max_pages * n_kv_heads;
   int c3 = 8;
-  while (c3 < 64 && 2 * c3 <= ph) c3 *= 2;
+  while (c3 < 64 && (int64_t)c3 * 512 < ph) c3 *= 2;
   s.c3 = c3;
-  s.c8 = c3 / 2;
+  s.c8 = c3;
   s.max_chunks = (max_pages + s.c8 - 1) / s.c8 + 2;
   return s;
 }
 
-static size_t counters_bytes(int n_req, int n_kv_heads) {
-  return (((size_t)n_req * n_kv_heads * 4) + 255) / 256 * 256;
-}
+// workspace: int32 chunk count per request, then the partials
+static size_t header_bytes(int n_req) { return (((size_t)n_req * 4) + 255) / 256 * 256; }
 
 size_t decode_ws_bytes(int n_req, int max_pages, int n_kv_heads, int group, int d) {
   DecodeShape s = decode_shape(n_req, max_pages, n_kv_heads);
-  return counters_bytes(n_req, n_kv_heads) +
+  return header_bytes(n_req) +
          (size_t)n_req * n_kv_heads * s.max_chunks * group * (d + 2) * sizeof(float);
 }
 
@@ -132,12 +135,12 @@ __device__ __forceinline__ half8 p_operand(const float* p, bool row_is_b) {
 }
 
 template <int D>
-__global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(256, 2) void decode_kernel(DecodeArgs a) {
   constexpr int CL = D / 16, NDW = 3 * D / 128, CB = 3 * D / 32, NS = D / 32;
   extern __shared__ float smem[];
   __shared__ int scr[8];
   __shared__ int2 s_list[64];
-  __shared__ int s_last;
+  __shared__ int s_slice[MAX_SLICES];
   const PoolView& P = a.P;
   const int r = blockIdx.z, h = blockIdx.y, chunk = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
@@ -149,57 +152,97 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
     if (chunk == 0) {
       for (int i = tid; i < G * D; i += 256) a.out[((int64_t)r * Hq + h * G) * D + i] = 0.0f;
       if (a.lse && tid < G) a.lse[(int64_t)r * Hq + h * G + tid] = -INFINITY;
-      if (tid == 0 && h == 0) atomicOr(&P.ctrl[CTRL_ERR], (int)MKV_DEVERR_RANGE);
+      if (tid == 0 && h == 0) {
+        atomicOr(&P.ctrl[CTRL_ERR], (int)MKV_DEVERR_RANGE);
+        a.totals[r] = 0;
+      }
     }
     return;
   }
   const int np = (S + PAGE - 1) / PAGE;
 
-  // ---- 1. partition the request's pages by format; pick this chunk's pages
-  const int seg = (np + 255) / 256;
-  const int pa = tid * seg, pb = min(np, pa + seg);
+  // ---- 1. partition the request's pages by format; pick this chunk's pages.
+  // Pages are visited in slices of 1024 (4 consecutive tags per thread, so each
+  // load instruction is coalesced).  Pass 1 counts FP8 / TQ3 pages per slice;
+  // pass 2 re-reads only the slices that hold this chunk's ranks and scans them.
   const uint8_t* trow = a.tags + (int64_t)r * mp;
-  int c8 = 0, c3 = 0, bad = 0;
-  for (int p = pa; p < pb; ++p) {
-    const int tg = trow[p];
-    if (tg == TAG_S) c3++;
-    else if (tg == TAG_R || tg == TAG_A) c8++;
-    else bad = 1;
+  const int n_slices = (np + 1023) / 1024;
+  {
+    for (int i = tid; i < n_slices; i += 256) s_slice[i] = 0;
+    __syncthreads();
+    int bad = 0;
+    for (int it = 0; it < n_slices; ++it) {
+      const int p0 = it * 1024 + tid * 4;
+      int c8 = 0, c3 = 0;
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const int p = p0 + b;
+        const int tg = p < np ? trow[p] : -1;
+        c3 += tg == TAG_S;
+        c8 += (tg == TAG_R || tg == TAG_A);
+        bad |= (p < np && tg != TAG_S && tg != TAG_R && tg != TAG_A);
+      }
+      int packed = c8 | (c3 << 16);
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) packed += __shfl_xor(packed, o, 64);
+      if (lane == 0) atomicAdd(&s_slice[it], packed);
+    }
+    if (bad && chunk == 0) atomicOr(&P.ctrl[CTRL_ERR], (int)MKV_DEVERR_BAD_TAG);
+    __syncthreads();
   }
-  if (bad && chunk == 0) atomicOr(&P.ctrl[CTRL_ERR], (int)MKV_DEVERR_BAD_TAG);
-  int n8, n3;
-  const int pre8 = block_excl_scan(c8, scr, &n8);
-  const int pre3 = block_excl_scan(c3, scr, &n3);
+  int n8 = 0, n3 = 0;
+  for (int it = 0; it < n_slices; ++it) {
+    n8 += s_slice[it] & 0xFFFF;
+    n3 += s_slice[it] >> 16;
+  }
   const int nch8 = (n8 + a.c8 - 1) / a.c8, nch3 = (n3 + a.c3 - 1) / a.c3;
   const int total = nch8 + nch3;
+  if (chunk == 0 && h == 0 && tid == 0) a.totals[r] = total;
   if (chunk >= total) return;
   const bool is8 = chunk < nch8;
   const int lo = is8 ? chunk * a.c8 : (chunk - nch8) * a.c3;
   const int hi = min(lo + (is8 ? a.c8 : a.c3), is8 ? n8 : n3);
   {
-    int rank = is8 ? pre8 : pre3;
     const int32_t* brow = a.bt + (int64_t)r * mp;
     const int n_ids = is8 ? P.n_fp8 : P.n_tq3;
-    for (int p = pa; p < pb; ++p) {
-      const int tg = trow[p];
-      const bool match = is8 ? (tg == TAG_R || tg == TAG_A) : (tg == TAG_S);
-      if (match) {
-        if (rank >= lo && rank < hi) {
-          int id = brow[p], lp = p;
-          if (id < 0 || id >= n_ids) {
-            // out-of-range physical id: read page 0 instead, mask every token
-            atomicOr(&P.ctrl[CTRL_ERR], (int)MKV_DEVERR_RANGE);
-            id = 0;
-            lp = 0x3FFFFFFF / PAGE;
-          }
-          s_list[rank - lo] = make_int2(lp, id);
+    int base = 0;
+    for (int it = 0; it < n_slices; ++it) {
+      const int cnt = is8 ? (s_slice[it] & 0xFFFF) : (s_slice[it] >> 16);
+      if (base < hi && base + cnt > lo) {  // uniform across the workgroup
+        const int p0 = it * 1024 + tid * 4;
+        int tg4[4], c = 0;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          const int p = p0 + b;
+          const int tg = p < np ? trow[p] : -1;
+          tg4[b] = is8 ? (tg == TAG_R || tg == TAG_A) : (tg == TAG_S);
+          c += tg4[b];
         }
-        rank++;
+        int tot;
+        int rank = base + block_excl_scan(c, scr, &tot);
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          if (tg4[b]) {
+            if (rank >= lo && rank < hi) {
+              const int p = p0 + b;
+              int id = brow[p], lp = p;
+              if (id < 0 || id >= n_ids) {
+                // out-of-range physical id: read page 0 instead, mask every token
+                atomicOr(&P.ctrl[CTRL_ERR], (int)MKV_DEVERR_RANGE);
+                id = 0;
+                lp = 0x3FFFFFFF / PAGE;
+              }
+              s_list[rank - lo] = make_int2(lp, id);
+            }
+            rank++;
+          }
+        }
       }
+      base += cnt;
     }
   }
 
-  // ---- 2. queries of the GQA group -> fp16 MFMA B operands
+  // ---- 2. queries of the GQA group -> fp16 MFMA operands in LDS
   float* qs = smem;  // [G][D]
   for (int i = tid; i < G * D; i += 256) {
     const int n = i / D, c = i % D;
@@ -229,14 +272,17 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
   const bool col_valid = col_head < G;
   const bool col_b = pair && ln >= 8;        // this column scores page b
   const bool row_b = pair && lg >= 2;        // accumulator rows 4*lg+i hold page b
-  half8 qB[NS];
+  // fp16 query operands in MFMA lane order: qop[s][lane] (16 B each)
+  half8* qop = reinterpret_cast<half8*>(smem + G * D);
+  for (int i = tid; i < NS * 64; i += 256) {
+    const int s = i / 64, l = i % 64;
+    const int lln = l & 15, llg = l >> 4;
+    const int ch = pair ? (lln & 7) : lln;
+    half8 v;
 #pragma unroll
-  for (int s = 0; s < NS; ++s) {
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const float x = col_valid ? qs[col_head * D + (D / 4) * lg + 8 * s + j] * qscale : 0.0f;
-      qB[s][j] = (_Float16)x;
-    }
+    for (int j = 0; j < 8; ++j)
+      v[j] = (_Float16)(ch < G ? qs[ch * D + (D / 4) * llg + 8 * s + j] * qscale : 0.0f);
+    qop[i] = v;
   }
   __syncthreads();
 
@@ -295,15 +341,16 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
       float4v sa = zero4, sb = zero4;
 #pragma unroll
       for (int s = 0; s < NS; ++s) {
+        const half8 qv = qop[s * 64 + lane];
         const uint32_t a0 = __builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(kA, 2 * s));
         const uint32_t a1 = __builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(kA, 2 * s + 1));
         sa = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(cvt_lo(a0), cvt_hi(a0), cvt_lo(a1), cvt_hi(a1)),
-                                                     qB[s], sa, 0, 0, 0);
+                                                     qv, sa, 0, 0, 0);
         if (pair) {
           const uint32_t b0 = __builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(kB, 2 * s));
           const uint32_t b1 = __builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(kB, 2 * s + 1));
           sb = __builtin_amdgcn_mfma_f32_16x16x32_f16(
-              h8(cvt_lo(b0), cvt_hi(b0), cvt_lo(b1), cvt_hi(b1)), qB[s], sb, 0, 0, 0);
+              h8(cvt_lo(b0), cvt_hi(b0), cvt_lo(b1), cvt_hi(b1)), qv, sb, 0, 0, 0);
         }
       }
       float sc[4];
@@ -372,13 +419,14 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
       float4v sa = zero4, sb = zero4;
 #pragma unroll
       for (int s = 0; s < NS; ++s) {
+        const half8 qv = qop[s * 64 + lane];
         sa = __builtin_amdgcn_mfma_f32_16x16x32_f16(
             h8(cvt_lo(kA[2 * s]), cvt_hi(kA[2 * s]), cvt_lo(kA[2 * s + 1]), cvt_hi(kA[2 * s + 1])),
-            qB[s], sa, 0, 0, 0);
+            qv, sa, 0, 0, 0);
         if (pair)
           sb = __builtin_amdgcn_mfma_f32_16x16x32_f16(
               h8(cvt_lo(kB[2 * s]), cvt_hi(kB[2 * s]), cvt_lo(kB[2 * s + 1]), cvt_hi(kB[2 * s + 1])),
-              qB[s], sb, 0, 0, 0);
+              qv, sb, 0, 0, 0);
       }
       float sc[4];
       {
@@ -432,6 +480,7 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
   float* macc = smem;                 // [4][G][D]
   float* mm = smem + 4 * G * D;       // [4][G]
   float* ml = mm + 4 * G;             // [4][G]
+  __syncthreads();                    // qop region is reused below
   if (!row_b) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -470,39 +519,93 @@ __global__ __launch_bounds__(256) void decode_kernel(DecodeArgs a) {
       part[G * D + G + n] = L;
     }
   }
+}
 
-  // ---- 5. the last workgroup of (request, KV head) merges all partials
-  __threadfence();
-  __syncthreads();
-  if (tid == 0) {
-    const unsigned prev = atomicInc(&a.counters[r * H + h], (unsigned)(total - 1));
-    s_last = prev == (unsigned)(total - 1);
+// Merge stage (Eq. softmax-merge): one workgroup per (request, KV head, query
+// head of the group).  The chunk partials' (m_j, l_j) go to LDS; each of the 4
+// waves then folds a quarter of the partials' normalized outputs, four
+// channels per lane with 16-byte loads, and the waves combine in LDS.
+template <int D>
+__global__ __launch_bounds__(256) void decode_merge_kernel(int G, int H, int max_chunks,
+                                                           const int32_t* totals,
+                                                           const float* partials, float* out,
+                                                           float* lse) {
+  constexpr int C4 = D / 4;  // float4 lanes per row
+  __shared__ float s_w[1024];
+  __shared__ float4 s_acc[4][C4];
+  __shared__ float s_red[8];
+  const int n = blockIdx.x, h = blockIdx.y, r = blockIdx.z;
+  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int Hq = H * G;
+  const int total = min(totals[r], max_chunks);
+  float* o = out + ((int64_t)r * Hq + h * G + n) * D;
+  if (total <= 0) {
+    for (int c = tid; c < D; c += 256) o[c] = 0.0f;
+    if (lse && tid == 0) lse[(int64_t)r * Hq + h * G + n] = -INFINITY;
+    return;
   }
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
-  const float* base = a.partials + ((int64_t)r * H + h) * a.max_chunks * G * (D + 2);
+  const float* base = partials + ((int64_t)r * H + h) * max_chunks * G * (D + 2);
   const int stride = G * (D + 2);
-  for (int i = tid; i < G * D; i += 256) {
-    const int n = i / D;
-    float M = -INFINITY;
-    for (int k = 0; k < total; ++k) {
-      const float* pk = base + (int64_t)k * stride;
-      if (pk[G * D + G + n] > 0.0f) M = fmaxf(M, pk[G * D + n]);
-    }
-    float L = 0.0f, O = 0.0f;
-    for (int k = 0; k < total; ++k) {
+  // max over the partials' m_j (empty partials have l_j = 0)
+  float M = -INFINITY;
+  for (int k = tid; k < total; k += 256) {
+    const float* pk = base + (int64_t)k * stride;
+    const float lk = pk[G * D + G + n];
+    if (lk > 0.0f) M = fmaxf(M, pk[G * D + n]);
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) M = fmaxf(M, __shfl_xor(M, off, 64));
+  if (lane == 0) s_red[wid] = M;
+  __syncthreads();
+  M = fmaxf(fmaxf(s_red[0], s_red[1]), fmaxf(s_red[2], s_red[3]));
+  __syncthreads();
+  float L = 0.0f;
+  for (int k0 = 0; k0 < total; k0 += 1024) {
+    for (int k = k0 + tid; k < min(total, k0 + 1024); k += 256) {
       const float* pk = base + (int64_t)k * stride;
       const float lk = pk[G * D + G + n];
-      if (lk > 0.0f) {
-        const float f = exp2f(pk[G * D + n] - M) * lk;
-        L += f;
-        O += f * pk[i];
+      const float wk = lk > 0.0f ? exp2f(pk[G * D + n] - M) * lk : 0.0f;
+      s_w[k - k0] = wk;
+      L += wk;
+    }
+    __syncthreads();
+    if (lane < C4) {
+      float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+      const int kend = min(total, k0 + 1024);
+#pragma unroll 8
+      for (int k = k0 + wid; k < kend; k += 4) {
+        const float wk = s_w[k - k0];
+        const float4 v = *reinterpret_cast<const float4*>(base + (int64_t)k * stride + n * D + 4 * lane);
+        acc.x += wk * v.x;
+        acc.y += wk * v.y;
+        acc.z += wk * v.z;
+        acc.w += wk * v.w;
+      }
+      if (k0 == 0) s_acc[wid][lane] = acc;
+      else {
+        s_acc[wid][lane].x += acc.x; s_acc[wid][lane].y += acc.y;
+        s_acc[wid][lane].z += acc.z; s_acc[wid][lane].w += acc.w;
       }
     }
-    a.out[((int64_t)r * Hq + h * G) * D + i] = O / L;
-    if (a.lse && i % D == 0) a.lse[(int64_t)r * Hq + h * G + n] = (M + log2f(L)) * 0.69314718055994531f;
+    __syncthreads();
   }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) L += __shfl_xor(L, off, 64);
+  if (lane == 0) s_red[4 + wid] = L;
+  __syncthreads();
+  L = s_red[4] + s_red[5] + s_red[6] + s_red[7];
+  const float inv = 1.0f / L;
+  if (tid < C4) {
+    float4 t = s_acc[0][tid];
+#pragma unroll
+    for (int w = 1; w < 4; ++w) {
+      t.x += s_acc[w][tid].x; t.y += s_acc[w][tid].y;
+      t.z += s_acc[w][tid].z; t.w += s_acc[w][tid].w;
+    }
+    t.x *= inv; t.y *= inv; t.z *= inv; t.w *= inv;
+    *reinterpret_cast<float4*>(o + 4 * tid) = t;
+  }
+  if (lse && tid == 0) lse[(int64_t)r * Hq + h * G + n] = (M + log2f(L)) * 0.69314718055994531f;
 }
 
 hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t* q,
@@ -521,19 +624,26 @@ hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t
   a.seq_lens = seq_lens;
   a.out = out;
   a.lse = lse;
-  a.counters = reinterpret_cast<uint32_t*>(ws);
-  a.partials = reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(ws) +
-                                        counters_bytes(n_req, P.n_kv_heads));
+  a.totals = reinterpret_cast<int32_t*>(ws);
+  a.partials = reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(ws) + header_bytes(n_req));
   a.c3 = sh.c3;
   a.c8 = sh.c8;
   a.max_chunks = sh.max_chunks;
   a.sm_log2 = 1.4426950408889634f / sqrtf((float)P.d);
-  const size_t lds = (size_t)(4 * P.group * P.d + 8 * P.group) * sizeof(float);
+  const size_t merge_f = (size_t)(4 * P.group * P.d + 8 * P.group);
+  const size_t qop_f = (size_t)P.group * P.d + (size_t)(P.d / 32) * 64 * 4;
+  const size_t lds = (merge_f > qop_f ? merge_f : qop_f) * sizeof(float);
   dim3 grid(sh.max_chunks, P.n_kv_heads, n_req);
-  if (P.d == 256)
+  dim3 mgrid(P.group, P.n_kv_heads, n_req);
+  if (P.d == 256) {
     hipLaunchKernelGGL(decode_kernel<256>, grid, dim3(256), lds, s, a);
-  else
+    hipLaunchKernelGGL(decode_merge_kernel<256>, mgrid, dim3(256), 0, s, P.group, P.n_kv_heads,
+                       sh.max_chunks, a.totals, a.partials, out, lse);
+  } else {
     hipLaunchKernelGGL(decode_kernel<128>, grid, dim3(256), lds, s, a);
+    hipLaunchKernelGGL(decode_merge_kernel<128>, mgrid, dim3(256), 0, s, P.group, P.n_kv_heads,
+                       sh.max_chunks, a.totals, a.partials, out, lse);
+  }
   return hipGetLastError();
 }
 
