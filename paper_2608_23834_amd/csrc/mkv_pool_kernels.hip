@@ -13,6 +13,10 @@
 
 namespace mkv {
 
+static int grid_for(int64_t items, int cap) {
+  return (int)(items < 1 ? 1 : (items < cap ? items : cap));
+}
+
 // ===========================================================================
 // Append
 // ===========================================================================
@@ -109,18 +113,6 @@ __global__ __launch_bounds__(1024) void append_plan_kernel(int n_req, int32_t* b
   }
 }
 
-__device__ __forceinline__ float block_max_f(float v, float* red) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  const int wid = threadIdx.x >> 6;
-  if ((threadIdx.x & 63) == 0) red[wid] = v;
-  __syncthreads();
-  float m = red[0];
-  for (int w = 1; w < (int)(blockDim.x >> 6); ++w) m = fmaxf(m, red[w]);
-  __syncthreads();
-  return m;
-}
-
 template <int D>
 __device__ __forceinline__ int fp8_off(int kv, int t, int c) {
   if (!kv) return t * D + c;
@@ -129,70 +121,231 @@ __device__ __forceinline__ int fp8_off(int kv, int t, int c) {
   return PAGE * D + ((r * 4 + g) * CL + m) * 4 + u;
 }
 
-// Quantize every listed page-head of every requested layer (grid-stride).
+// Quantize one tensor (K or V) of one page-head with one wave.  Slots [0, t0)
+// already hold codes with the page's scale; the new fp32 values are rows
+// row0 + t (t in [t0, t1)) of src, [row][H][D].  The scale only grows: when the
+// new amax exceeds 448 * s_old the old codes are re-rounded to the new scale.
+// All loads are issued before any store so that one wave needs about one
+// memory round trip (plus one more when old codes are re-rounded).
+template <int D>
+__device__ void quant_task(uint8_t* reg, float* sc, int kv, const uint16_t* src, int64_t row0,
+                           int t0, int t1, int H, int h, int lane) {
+  constexpr int CL = D / 16, D4 = D / 4, NC = PAGE * D4 / 64;  // NC uint2 per lane at most
+  const uint16_t* srow = src + (row0 * H + h) * D;  // token t at srow[t * H * D + c]
+  const int64_t tstride = (int64_t)H * D;
+  const float s_old = t0 > 0 ? sc[kv] : 0.0f;
+  const int n4 = (t1 - t0) * D4;  // new inputs, 4 channels per item
+  uint2 x[NC];
+  float amax = 0.0f;
+#pragma unroll
+  for (int k = 0; k < NC; ++k) {
+    const int idx = lane + 64 * k;
+    x[k] = make_uint2(0u, 0u);
+    if (idx < n4) {
+      const int t = t0 + idx / D4, c = 4 * (idx % D4);
+      x[k] = *reinterpret_cast<const uint2*>(srow + t * tstride + c);
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < NC; ++k) {
+    amax = fmaxf(amax, fmaxf(fmaxf(fabsf(__uint_as_float(x[k].x << 16)),
+                                   fabsf(__uint_as_float(x[k].x & 0xFFFF0000u))),
+                             fmaxf(fabsf(__uint_as_float(x[k].y << 16)),
+                                   fabsf(__uint_as_float(x[k].y & 0xFFFF0000u)))));
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) amax = fmaxf(amax, __shfl_xor(amax, o, 64));
+  float s_new = s_old;
+  bool requant = false;
+  if (t0 == 0) {
+    s_new = amax / 448.0f;
+  } else if (!(amax <= 448.0f * s_old)) {
+    s_new = amax / 448.0f;
+    requant = true;
+  }
+  uint32_t* rw = reinterpret_cast<uint32_t*>(reg + (kv ? PAGE * D : 0));
+  if (requant) {
+    // dwords holding old codes: K rows t < t0; V token groups g < ceil(t0/4)
+    const int gn = (t0 + 3) / 4;  // V dwords of token groups g < gn: 16 * gn * CL = gn * D
+    const int n_old = kv ? gn * D : t0 * D4;
+    uint32_t ow[NC];
+#pragma unroll
+    for (int k = 0; k < NC; ++k) {
+      const int w = lane + 64 * k;
+      const int wi = kv ? (w / (CL * gn)) * 4 * CL + (w % (CL * gn)) : w;
+      ow[k] = w < n_old ? rw[wi] : 0u;
+    }
+#pragma unroll
+    for (int k = 0; k < NC; ++k) {
+      const int w = lane + 64 * k;
+      if (w < n_old) {
+        const int wi = kv ? (w / (CL * gn)) * 4 * CL + (w % (CL * gn)) : w;
+        const int g = (wi / CL) % 4;
+        uint32_t outw = 0;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          const int t = kv ? 4 * g + b : wi / D4;
+          uint32_t code = (ow[k] >> (8 * b)) & 0xFFu;
+          if (t < t0) code = f32_to_e4m3((e4m3_to_f32(code) * s_old) / s_new);
+          outw |= code << (8 * b);
+        }
+        rw[wi] = outw;
+      }
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // re-rounded dwords land before new-code byte stores
+  }
+  // new codes
+#pragma unroll
+  for (int k = 0; k < NC; ++k) {
+    const int idx = lane + 64 * k;
+    if (idx < n4) {
+      const int t = t0 + idx / D4, c = 4 * (idx % D4);
+      uint32_t code[4];
+      const uint32_t hv[4] = {x[k].x << 16, x[k].x & 0xFFFF0000u, x[k].y << 16, x[k].y & 0xFFFF0000u};
+#pragma unroll
+      for (int b = 0; b < 4; ++b)
+        code[b] = s_new > 0.0f ? f32_to_e4m3(__uint_as_float(hv[b]) / s_new) : 0u;
+      if (!kv) {
+        rw[(t * D + c) / 4] = code[0] | (code[1] << 8) | (code[2] << 16) | (code[3] << 24);
+      } else {
+#pragma unroll
+        for (int b = 0; b < 4; ++b) reg[fp8_off<D>(1, t, c + b)] = (uint8_t)code[b];
+      }
+    }
+  }
+  // a fresh page: zero every slot past the new tokens
+  if (t0 == 0 && t1 < PAGE) {
+    if (!kv) {
+      for (int w = t1 * D4 + lane; w < PAGE * D4; w += 64) rw[w] = 0u;
+    } else {
+      for (int w = lane; w < PAGE * D4; w += 64) {
+        const int g = (w / CL) % 4;
+        if (4 * g >= t1) {
+          rw[w] = 0u;
+        } else if (4 * g + 4 > t1) {
+#pragma unroll
+          for (int b = 0; b < 4; ++b)
+            if (4 * g + b >= t1) reg[PAGE * D + 4 * w + b] = 0;
+        }
+      }
+    }
+  }
+  if (lane == 0) sc[kv] = s_new;
+}
+
+// One quantisation task = (listed page, layer, head, K or V); one wave each.
+template <int D>
+__device__ __forceinline__ void run_quant_task(const PoolView& P, int64_t task, int layer_sel,
+                                               int n_lcall, const int32_t* sb, const int32_t* cu,
+                                               int n_new_total, const uint16_t* k,
+                                               const uint16_t* v, const int32_t* lst, int lane) {
+  const int H = P.n_kv_heads;
+  const int kv = (int)(task & 1);
+  const int64_t item = task >> 1;
+  const int e = (int)(item / (n_lcall * H));
+  const int lh = (int)(item % (n_lcall * H));
+  const int li = lh / H, h = lh % H;
+  const int r = lst[4 * e], p = lst[4 * e + 1], id = lst[4 * e + 2];
+  const int layer = layer_sel < 0 ? li : layer_sel;
+  const int s0 = sb[r], n = cu[r + 1] - cu[r];
+  const int t0 = max(0, s0 - p * PAGE), t1 = min(PAGE, s0 + n - p * PAGE);
+  const int64_t ph = ((int64_t)layer * P.n_fp8 + id) * H + h;
+  const int64_t row0 = (int64_t)cu[r] + p * PAGE - s0;  // input row of slot t is row0 + t
+  const uint16_t* src = (kv ? v : k) + (int64_t)li * n_new_total * H * D;
+  quant_task<D>(P.fp8 + ph * fp8_region_bytes(D), P.fp8_scales + ph * 2, kv, src, row0, t0, t1, H,
+                h, lane);
+}
+
+// Quantize every listed page-head of every requested layer (grid-stride over
+// tasks, one wave per task).
 template <int D>
 __global__ __launch_bounds__(256) void append_quant_kernel(PoolView P, int layer_sel, int n_lcall,
                                                            const int32_t* sb, const int32_t* cu,
                                                            int n_new_total, const uint16_t* k,
                                                            const uint16_t* v) {
   if (P.ctrl[CTRL_ABORT]) return;
-  __shared__ float red[8];
-  const int H = P.n_kv_heads;
-  const int64_t n_items = (int64_t)P.ctrl[CTRL_NLIST] * n_lcall * H;
+  const int64_t n_tasks = (int64_t)P.ctrl[CTRL_NLIST] * n_lcall * P.n_kv_heads * 2;
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  for (int64_t t = (int64_t)blockIdx.x * 4 + wid; t < n_tasks; t += (int64_t)gridDim.x * 4)
+    run_quant_task<D>(P, t, layer_sel, n_lcall, sb, cu, n_new_total, k, v, P.list, lane);
+}
+
+// Small appends (decode steps: a few tokens per request) in one workgroup:
+// the allocation plan runs with one thread per request, then 16 waves
+// quantize the touched page-heads.  Same allocation order and arithmetic as
+// the two-kernel path.
+constexpr int SMALL_APPEND_MAX_TOKENS = 256;
+constexpr int SMALL_APPEND_MAX_REQ = 1024;
+constexpr int SMALL_APPEND_MAX_LIST = SMALL_APPEND_MAX_TOKENS / PAGE + SMALL_APPEND_MAX_REQ;
+
+template <int D>
+__global__ __launch_bounds__(1024) void append_small_kernel(PoolView P, int layer_sel, int n_lcall,
+                                                            int n_req, int32_t* bt, uint8_t* tags,
+                                                            int max_pages, const int32_t* sb,
+                                                            const int32_t* cu, int n_new_total,
+                                                            const uint16_t* k, const uint16_t* v) {
+  __shared__ int scratch[32];
+  __shared__ int s_err;
+  __shared__ int s_lst[4 * SMALL_APPEND_MAX_LIST];
   const int tid = threadIdx.x;
-  for (int64_t item = blockIdx.x; item < n_items; item += gridDim.x) {
-    const int e = (int)(item / (n_lcall * H));
-    const int lh = (int)(item % (n_lcall * H));
-    const int li = lh / H, h = lh % H;
-    const int r = P.list[4 * e], p = P.list[4 * e + 1], id = P.list[4 * e + 2];
-    const int layer = layer_sel < 0 ? li : layer_sel;
-    const int s0 = sb[r], n = cu[r + 1] - cu[r];
-    const int t0 = max(0, s0 - p * PAGE), t1 = min(PAGE, s0 + n - p * PAGE);
-    const int64_t ph = ((int64_t)layer * P.n_fp8 + id) * H + h;
-    uint8_t* reg = P.fp8 + ph * fp8_region_bytes(D);
-    float* sc = P.fp8_scales + ph * 2;
-    const int64_t row0 = (int64_t)cu[r] + p * PAGE - s0;  // input row of slot t is row0 + t
-    for (int kv = 0; kv < 2; ++kv) {
-      const uint16_t* src = (kv ? v : k) + (int64_t)li * n_new_total * H * D;
-      float amax = 0.0f;
-      for (int idx = tid; idx < (t1 - t0) * D; idx += blockDim.x) {
-        const int t = t0 + idx / D, c = idx % D;
-        amax = fmaxf(amax, fabsf(bf16_to_f32(src[((row0 + t) * H + h) * D + c])));
+  if (tid == 0) s_err = (cu[0] != 0 || cu[n_req] != n_new_total) ? (int)MKV_DEVERR_RANGE : 0;
+  __syncthreads();
+  int p0 = 0, p1 = -1, need = 0, bad = 0;
+  const int r = tid;
+  if (r < n_req) {
+    const int n = cu[r + 1] - cu[r], s0 = sb[r];
+    if (n < 0 || s0 < 0) bad |= MKV_DEVERR_RANGE;
+    else if (n > 0) {
+      p0 = s0 / PAGE;
+      p1 = (s0 + n - 1) / PAGE;
+      if (p1 >= max_pages) { bad |= MKV_DEVERR_RANGE; p1 = p0 - 1; }
+      for (int p = p0; p <= p1; ++p) {
+        const int64_t i = (int64_t)r * max_pages + p;
+        if (bt[i] < 0) need++;
+        else if (tags[i] != TAG_R) bad |= MKV_DEVERR_NOT_RECENT;
+        else if (bt[i] >= P.n_fp8) bad |= MKV_DEVERR_RANGE;
       }
-      amax = block_max_f(amax, red);
-      const float s_old = t0 > 0 ? sc[kv] : 0.0f;
-      float s_new = s_old;
-      bool requant = false;
-      if (t0 == 0) {
-        s_new = amax / 448.0f;
-      } else if (!(amax <= 448.0f * s_old)) {
-        s_new = amax / 448.0f;
-        requant = true;
-      }
-      __syncthreads();
-      if (requant) {
-        for (int idx = tid; idx < t0 * D; idx += blockDim.x) {
-          const int t = idx / D, c = idx % D;
-          const int off = fp8_off<D>(kv, t, c);
-          const float deq = e4m3_to_f32(reg[off]) * s_old;
-          reg[off] = (uint8_t)f32_to_e4m3(deq / s_new);
-        }
-      }
-      for (int idx = tid; idx < (t1 - t0) * D; idx += blockDim.x) {
-        const int t = t0 + idx / D, c = idx % D;
-        const float x = bf16_to_f32(src[((row0 + t) * H + h) * D + c]);
-        reg[fp8_off<D>(kv, t, c)] = s_new > 0.0f ? (uint8_t)f32_to_e4m3(x / s_new) : (uint8_t)0;
-      }
-      if (t0 == 0) {
-        for (int idx = tid; idx < (PAGE - t1) * D; idx += blockDim.x) {
-          const int t = t1 + idx / D, c = idx % D;
-          reg[fp8_off<D>(kv, t, c)] = 0;
-        }
-      }
-      if (tid == 0) sc[kv] = s_new;
-      __syncthreads();
     }
   }
+  if (bad) atomicOr(&s_err, bad);
+  int tot_need, tot_touch;
+  const int nb = block_excl_scan(need, scratch, &tot_need);
+  const int touch = p1 - p0 + 1;
+  const int tb = block_excl_scan(touch, scratch, &tot_touch);
+  const int top = P.ctrl[CTRL_FP8_TOP];
+  if (tid == 0) {
+    if (s_err == 0 && tot_need > top) s_err |= MKV_DEVERR_FP8_EXHAUSTED;
+    if (s_err == 0 && tot_touch > SMALL_APPEND_MAX_LIST) s_err |= MKV_DEVERR_RANGE;
+  }
+  __syncthreads();
+  if (s_err) {
+    if (tid == 0) atomicOr(&P.ctrl[CTRL_ERR], s_err);
+    return;
+  }
+  if (r < n_req) {
+    int k_alloc = 0;
+    for (int p = p0; p <= p1; ++p) {
+      const int64_t i = (int64_t)r * max_pages + p;
+      int id = bt[i];
+      if (id < 0) {
+        id = P.fp8_stack[top - 1 - (nb + k_alloc)];
+        k_alloc++;
+        bt[i] = id;
+        tags[i] = TAG_R;
+      }
+      int* e = s_lst + 4 * (tb + (p - p0));
+      e[0] = r;
+      e[1] = p;
+      e[2] = id;
+      e[3] = 0;
+    }
+  }
+  __syncthreads();
+  if (tid == 0) P.ctrl[CTRL_FP8_TOP] = top - tot_need;
+  const int lane = tid & 63, wid = tid >> 6;
+  const int64_t n_tasks = (int64_t)tot_touch * n_lcall * P.n_kv_heads * 2;
+  for (int64_t t = wid; t < n_tasks; t += 16)
+    run_quant_task<D>(P, t, layer_sel, n_lcall, sb, cu, n_new_total, k, v, s_lst, lane);
 }
 
 // ===========================================================================
@@ -477,19 +630,25 @@ __global__ void fill_zero_kernel(uint32_t* p, int64_t n_words) {
 // ===========================================================================
 // Launchers
 // ===========================================================================
-static int grid_for(int64_t items, int cap) {
-  return (int)(items < 1 ? 1 : (items < cap ? items : cap));
-}
 
 hipError_t launch_append(const PoolView& P, int layer, int n_req, int32_t* bt, uint8_t* tags,
                          int max_pages, const int32_t* sb, const int32_t* cu, int n_new_total,
                          const uint16_t* k, const uint16_t* v, hipStream_t s) {
+  const int n_lcall = layer < 0 ? P.n_layers : 1;
+  if (n_new_total <= SMALL_APPEND_MAX_TOKENS && n_req <= SMALL_APPEND_MAX_REQ) {
+    if (P.d == 256)
+      hipLaunchKernelGGL(append_small_kernel<256>, dim3(1), dim3(1024), 0, s, P, layer, n_lcall,
+                         n_req, bt, tags, max_pages, sb, cu, n_new_total, k, v);
+    else
+      hipLaunchKernelGGL(append_small_kernel<128>, dim3(1), dim3(1024), 0, s, P, layer, n_lcall,
+                         n_req, bt, tags, max_pages, sb, cu, n_new_total, k, v);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL(append_plan_kernel, dim3(1), dim3(1024), 0, s, n_req, bt, tags, max_pages, sb,
                      cu, P.ctrl, P.fp8_stack, P.list, P.n_fp8, n_new_total);
-  const int n_lcall = layer < 0 ? P.n_layers : 1;
   // upper bound on listed pages: new tokens / 16 + one partial page per request
   const int64_t pages_bound = (int64_t)n_new_total / PAGE + n_req + 1;
-  const int grid = grid_for(pages_bound * n_lcall * P.n_kv_heads, 8192);
+  const int grid = grid_for((pages_bound * n_lcall * P.n_kv_heads * 2 + 3) / 4, 8192);
   if (P.d == 256)
     hipLaunchKernelGGL(append_quant_kernel<256>, dim3(grid), dim3(256), 0, s, P, layer, n_lcall, sb,
                        cu, n_new_total, k, v);
