@@ -149,11 +149,13 @@ def main():
     ap.add_argument("--cfg", type=int, default=3)
     ap.add_argument("--layers", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe", action="store_true",
+                    help="also run one 1 GiB device-to-device copy (calibrates HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py: this build runs on one GPU; --gpus {args.gpus} is not supported "
-              "(the decode path shards by request or KV head without any exchange; see the "
-              "design notes)", file=sys.stderr)
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the decode path would shard by request or KV head with no exchange between "
+              "GPUs)", file=sys.stderr)
         sys.exit(2)
 
     import torch
@@ -267,6 +269,14 @@ def main():
         "counters": {k: int(v) for k, v in counters.items()},
         "setup_s": round(setup_s, 1),
     }
+    if args.copy_probe:
+        a_ = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        b_ = torch.empty_like(a_)
+        torch.cuda.synchronize()
+        b_.copy_(a_)
+        torch.cuda.synchronize()
+        res["copy_probe_bytes"] = 1 << 30
+        del a_, b_
     if not args.no_cpu_baseline and args.cfg == 3:
         res["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(res), flush=True)
