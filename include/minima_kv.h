@@ -174,9 +174,11 @@ mkv_status paged_attn_workspace_init(void* ws, size_t ws_bytes, hipStream_t stre
  * [n_req][n_q_heads][d]; lse: device fp32 [n_req][n_q_heads] (natural log of
  * the softmax denominator, scores in units of q.k/sqrt(d)) or NULL.
  * ws: device, >= paged_attn_workspace_bytes(pool, n_req, max_pages, 0); it
- * holds the split partials (O(splits x heads x d) floats).  max_pages is at
- * most 262144.  An invalid seq_len or an unmapped page below seq_len sets the
- * error word; such requests get zero outputs. */
+ * holds the split partials (O(splits x heads x d) floats).  q and ws must be
+ * 16-byte aligned (MKV_EINVAL otherwise).  max_pages is at most 262144.  An
+ * invalid seq_len sets the error word and gives that request zero outputs; a
+ * page below seq_len with an invalid tag or an out-of-range physical id sets
+ * the error word and is left out of the softmax. */
 mkv_status paged_attn_decode(mkv_pool* pool, int32_t layer, int32_t n_req, const uint16_t* q,
                              const int32_t* block_table, const uint8_t* tags, int32_t max_pages,
                              const int32_t* seq_lens, float* out, float* lse, void* ws,

@@ -170,7 +170,7 @@ mkv_status paged_attn_workspace_bytes(const mkv_pool* pool, int32_t n_req, int32
                                       int32_t n_q_total, size_t* bytes) {
   if (!pool || !bytes || n_req < 1 || max_pages < 1 || n_q_total < 0) return MKV_EINVAL;
   if (n_q_total == 0)
-    *bytes = decode_ws_bytes(n_req, max_pages, pool->n_kv_heads, pool->group, pool->d);
+    *bytes = decode_ws_bytes(n_req, max_pages, pool->n_kv_heads, pool->group, pool->d, pool->recent);
   else
     *bytes = chunk_ws_bytes(n_req, max_pages, n_q_total, pool->n_kv_heads, pool->group, pool->d);
   return MKV_OK;
@@ -187,9 +187,10 @@ mkv_status paged_attn_decode(mkv_pool* pool, int32_t layer, int32_t n_req, const
                              size_t ws_bytes, hipStream_t stream) {
   if (!pool || !q || !block_table || !tags || !seq_lens || !out || !ws) return MKV_EINVAL;
   if (n_req < 1 || max_pages < 1) return MKV_EINVAL;
+  if (!aligned16(q) || !aligned16(ws)) return MKV_EINVAL;
   if (layer < 0 || layer >= pool->n_layers) return MKV_ERANGE;
   if (n_req > 65535 || max_pages > 1024 * 256) return MKV_ERANGE;
-  if (ws_bytes < decode_ws_bytes(n_req, max_pages, pool->n_kv_heads, pool->group, pool->d))
+  if (ws_bytes < decode_ws_bytes(n_req, max_pages, pool->n_kv_heads, pool->group, pool->d, pool->recent))
     return MKV_ENOMEM;
   mkv_status st = hip_status(launch_decode(view_of(pool), layer, n_req, q, block_table, tags,
                                            max_pages, seq_lens, out, lse, ws, stream));

@@ -1,34 +1,43 @@
 // Mixed-format paged decode attention (Sec. 3.3, Eq. softmax-merge; Sec. 4.1
 // direct fused decode) for gfx950.
 //
-// One launch per layer.  Grid (chunk, KV head, request); 256 threads = 4
-// wave64s.  Each workgroup
-//  1. partitions the request's logical pages by format (Sec. 4.1 compact
-//     per-format lists, stable, logical order kept) and takes one chunk of
-//     either the FP8 list (Recent/Anchor) or the TQ3 list (Stale): format is
-//     uniform per workgroup, so both scans are branch-free;
-//  2. loads the GQA group's queries once; for TQ3 it rotates them (q_rot =
-//     R q, exact algebra since k_hat = gamma R^T mu_c) so keys are never
-//     de-rotated;
-//  3. each wave walks page pairs: QK^T on MFMA 16x16x32 f16 (M = 16 tokens of
-//     a page, N = the group's query heads, K = 32 channels), the 3-bit codes
-//     turned into E4M3 codebook bytes by one v_perm per 4 codes and into fp16
-//     by the hardware converter; online softmax in base 2; PV on MFMA with
-//     M = 16 channels, N = heads, K = 32 tokens (two pages), values
-//     dequantized in registers (TQ3: zero + scale * code per channel);
-//  4. the four waves merge in LDS into one (m_j, l_j, O_j) partial per chunk.
-// A second kernel merges all partials of both formats per (request, query
-// head) (Eq. softmax-merge).  The workspace holds O(chunks x heads x d)
-// partials, never anything the size of the cache.
+// One launch per layer.  Grid (chunk, KV head, request); 512 threads = 8
+// wave64s, one workgroup per CU.  Chunks are ranges of logical pages: the old
+// part of a request (pages wholly outside the Recent window) in ranges of C
+// pages, the Recent part in ranges of C/2 (FP8 pages carry twice the bytes of
+// TQ3 pages, so every chunk moves about the same amount).  Each workgroup
+//  1. loads the GQA group's queries and builds two fp16 MFMA operands in LDS:
+//     the plain queries for FP8 pages and the rotated ones for TQ3 pages
+//     (q_rot = R q, exact algebra since k_hat = gamma R^T mu_c, so keys are
+//     never de-rotated), the Hadamard transform done in registers;
+//  2. splits its pages by format into compact lists in logical order (Sec.
+//     4.1 per-format lists, built per chunk with wave ballots) and turns them
+//     into stages of equal size: a pair of TQ3 pages or one FP8 page;
+//  3. each wave streams its run of stages through a two-slot LDS ring fed by
+//     direct HBM -> LDS copies, two stages in flight behind the one computed:
+//     QK^T on MFMA 16x16x32 f16 (M = 16 tokens, N = query heads, K = 32
+//     channels), 3-bit codes turned into E4M3 codebook bytes by one v_perm per
+//     4 codes and into fp16 by the hardware converter; online softmax in base
+//     2; PV on MFMA with M = 16 channels, N = heads, K = 32 tokens, the TQ3
+//     values entering as exact integer codes with the per-channel scale and
+//     zero applied in fp32;
+//  4. the eight waves merge in LDS into one (m_j, l_j, O_j) partial per chunk.
+// A second kernel merges all partials of a request and query head (Eq.
+// softmax-merge).  The workspace holds O(chunks x heads x d) partials, never
+// anything the size of the cache.
 #include <hip/hip_runtime.h>
+
+#include <type_traits>
 
 #include "mkv_internal.h"
 #include "../../include/minima_kv.h"
 
 namespace mkv {
 
-// tag slices of 1024 pages: max_pages <= 1024 * MAX_SLICES (4M tokens)
-constexpr int MAX_SLICES = 256;
+constexpr int NW = 8;                  // waves per decode workgroup
+constexpr int NT = 64 * NW;            // threads per decode workgroup
+constexpr int MAX_CHUNK_PAGES = 256;   // upper bound of C
+constexpr int MASK_LP = 0x3FFFFFFF / PAGE;  // logical page whose tokens are all masked
 
 struct DecodeArgs {
   PoolView P;
@@ -41,27 +50,32 @@ struct DecodeArgs {
   float* lse;
   int32_t* totals;
   float* partials;
-  int c3, c8, max_chunks;
+  int cpages, max_chunks;
   float sm_log2;  // log2(e) / sqrt(d)
 };
 
-DecodeShape decode_shape(int n_req, int max_pages, int n_kv_heads) {
+// Pages per chunk C: about one workgroup per CU for the whole launch when the
+// requests fill their tables, never below 16 or above MAX_CHUNK_PAGES.
+DecodeShape decode_shape(int n_req, int max_pages, int n_kv_heads, int recent) {
   DecodeShape s;
-  // about 512 chunk workgroups per launch (two per CU at two waves per SIMD)
   const int64_t ph = (int64_t)n_req * max_pages * n_kv_heads;
-  int c3 = 8;
-  while (c3 < 64 && (int64_t)c3 * 512 < ph) c3 *= 2;
-  s.c3 = c3;
-  s.c8 = c3;
-  s.max_chunks = (max_pages + s.c8 - 1) / s.c8 + 2;
+  int64_t c = (ph + 255) / 256;
+  c = (c + 15) / 16 * 16;
+  if (c < 16) c = 16;
+  if (c > MAX_CHUNK_PAGES) c = MAX_CHUNK_PAGES;
+  s.cpages = (int)c;
+  // Recent pages of a request: at most recent/16 + 3 (whole and partial pages)
+  int64_t rec = (int64_t)recent / PAGE + 3;
+  if (rec > max_pages) rec = max_pages;
+  s.max_chunks = (int)((max_pages + c - 1) / c + (rec + c / 2 - 1) / (c / 2));
   return s;
 }
 
 // workspace: int32 chunk count per request, then the partials
 static size_t header_bytes(int n_req) { return (((size_t)n_req * 4) + 255) / 256 * 256; }
 
-size_t decode_ws_bytes(int n_req, int max_pages, int n_kv_heads, int group, int d) {
-  DecodeShape s = decode_shape(n_req, max_pages, n_kv_heads);
+size_t decode_ws_bytes(int n_req, int max_pages, int n_kv_heads, int group, int d, int recent) {
+  DecodeShape s = decode_shape(n_req, max_pages, n_kv_heads, recent);
   return header_bytes(n_req) +
          (size_t)n_req * n_kv_heads * s.max_chunks * group * (d + 2) * sizeof(float);
 }
@@ -80,6 +94,55 @@ __device__ __forceinline__ half2v cvt_hi(uint32_t w) {
 }
 __device__ __forceinline__ float exp2_safe(float s, float m) {
   return s == -INFINITY ? 0.0f : exp2f(s - m);
+}
+
+// Direct HBM -> LDS copies issued by one wave.  dma16: lane l copies 16 bytes
+// from its own src to dst + 16 l; dma4: 4 bytes to dst + 4 l (dst is the
+// wave-uniform LDS byte address).  They are inline assembly on purpose: the
+// compiler then does not order later LDS reads behind them (it cannot tell
+// which ring slot a copy fills and would wait for all of them), and the caller
+// gates every stage with an explicit vmcnt wait.  The kernel has no other
+// user of m0.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"  // m0 is reserved; no compiler code here uses it
+__device__ __forceinline__ void dma16(const uint8_t* src, uint32_t dst) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(src), "s"(dst)
+               : "memory", "m0");
+}
+__device__ __forceinline__ void dma4(const uint8_t* src, uint32_t dst) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
+               :
+               : "v"(src), "s"(dst)
+               : "memory", "m0");
+}
+#pragma clang diagnostic pop
+// One region of R bytes (16-byte aligned): whole KiB blocks by 16-byte lanes,
+// the tail by 4-byte lanes.
+template <int R>
+__device__ __forceinline__ void dma_region(uint32_t dst, const uint8_t* src, int lane) {
+#pragma unroll
+  for (int i = 0; i < R / 1024; ++i) dma16(src + 1024 * i + 16 * lane, dst + 1024 * i);
+  constexpr int TAIL = R % 1024;
+  static_assert(TAIL % 4 == 0 && TAIL <= 256, "tail must fit one 4-byte copy");
+  if (TAIL > 0 && lane < TAIL / 4) dma4(src + (R - TAIL) + 4 * lane, dst + (R - TAIL));
+}
+// vector-memory instructions dma_region<R> issues per wave
+template <int R>
+constexpr int dma_ops() { return R / 1024 + (R % 1024 ? 1 : 0); }
+
+// Wait until at most N vector-memory operations of this wave are in flight
+// (gfx9 s_waitcnt: vmcnt in bits [3:0] and [15:14]; expcnt/lgkmcnt left free).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+  __asm__ __volatile__("" ::: "memory");
+}
+__device__ __forceinline__ void wait_lgkm0() {
+  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0), vmcnt/expcnt free
+  __asm__ __volatile__("" ::: "memory");
 }
 
 template <int D>
@@ -135,22 +198,51 @@ __device__ __forceinline__ half8 p_operand(const float* p, bool row_is_b) {
 }
 
 template <int D>
-__global__ __launch_bounds__(256, 2) void decode_kernel(DecodeArgs a) {
-  constexpr int CL = D / 16, NDW = 3 * D / 128, CB = 3 * D / 32, NS = D / 32;
-  extern __shared__ float smem[];
-  __shared__ int scr[8];
-  __shared__ int2 s_list[64];
-  __shared__ int s_slice[MAX_SLICES];
+__global__ __launch_bounds__(NT, 1) void decode_kernel(DecodeArgs a) {
+  constexpr int CL = D / 16, NDW = 3 * D / 128, CB = 3 * D / 32, NS = D / 32, QV = D / 64;
+  constexpr int R3 = (int)tq3_region_bytes(D);  // K codes, V codes, gamma, V scale, V zero
+  constexpr int R8 = (int)fp8_region_bytes(D);  // K codes then V codes
+  constexpr int STAGE = 2 * R3;                 // a TQ3 page pair, or one FP8 page + scales
+  constexpr int OPS3 = dma_ops<R3>(), OPS8 = dma_ops<R8>() + 1;
+  static_assert(R8 + 8 <= STAGE, "an FP8 page and its two scales fit one stage");
+  extern __shared__ __align__(16) uint8_t smem[];
+  __shared__ int4 s_stage[MAX_CHUNK_PAGES];  // {lp_a, id_a, lp_b, id_b}; id_b < 0: FP8 stage
+  __shared__ int s_cnt[2 * NW];
   const PoolView& P = a.P;
   const int r = blockIdx.z, h = blockIdx.y, chunk = blockIdx.x;
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int G = P.group, H = P.n_kv_heads, Hq = H * G;
   const int mp = a.max_pages;
-  const int S = a.seq_lens[r];
+  const bool pair = G <= 8;  // two pages share one score tile: columns [0,8) page a, [8,16) page b
+  // LDS: [rotated-query operand][plain-query operand][page ring | wave merge]
+  half8* qrot = reinterpret_cast<half8*>(smem);
+  half8* qpl = qrot + NS * 64;
+  uint8_t* ring = smem + 2 * NS * 64 * 16;
 
+  // ---- 1. queries: wave w owns query head w (and w + 8 when G > 8); lane l
+  // holds channels QV l .. QV l + QV - 1.  The loads go out before anything
+  // else so their latency hides behind the page-table loads.
+  static_assert(QV == 2 || QV == 4, "QV bf16 channels per lane form one 4- or 8-byte load");
+  using qvec = typename std::conditional<QV == 4, uint2, uint32_t>::type;
+  float qx[2][QV];
+  int sg[QV];
+#pragma unroll
+  for (int ps = 0; ps < 2; ++ps) {
+    const int n = wid + 8 * ps;
+    const int nn = n < G ? n : G - 1;  // loads stay in bounds; values of n >= G are dropped
+    const qvec raw = *reinterpret_cast<const qvec*>(a.q + ((int64_t)r * Hq + h * G + nn) * D + QV * lane);
+    const uint16_t* rh = reinterpret_cast<const uint16_t*>(&raw);
+#pragma unroll
+    for (int i = 0; i < QV; ++i) qx[ps][i] = n < G ? bf16_to_f32(rh[i]) : 0.0f;
+  }
+#pragma unroll
+  for (int i = 0; i < QV; ++i) sg[i] = P.sigma[QV * lane + i];
+
+  const int S = a.seq_lens[r];
   if (S < 1 || S > mp * PAGE) {
     if (chunk == 0) {
-      for (int i = tid; i < G * D; i += 256) a.out[((int64_t)r * Hq + h * G) * D + i] = 0.0f;
+      for (int i = tid; i < G * D; i += NT) a.out[((int64_t)r * Hq + h * G) * D + i] = 0.0f;
       if (a.lse && tid < G) a.lse[(int64_t)r * Hq + h * G + tid] = -INFINITY;
       if (tid == 0 && h == 0) {
         atomicOr(&P.ctrl[CTRL_ERR], (int)MKV_DEVERR_RANGE);
@@ -159,189 +251,205 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeArgs a) {
     }
     return;
   }
+  // ---- chunk -> logical page range
   const int np = (S + PAGE - 1) / PAGE;
-
-  // ---- 1. partition the request's pages by format; pick this chunk's pages.
-  // Pages are visited in slices of 1024 (4 consecutive tags per thread, so each
-  // load instruction is coalesced).  Pass 1 counts FP8 / TQ3 pages per slice;
-  // pass 2 re-reads only the slices that hold this chunk's ranks and scans them.
-  const uint8_t* trow = a.tags + (int64_t)r * mp;
-  const int n_slices = (np + 1023) / 1024;
-  {
-    for (int i = tid; i < n_slices; i += 256) s_slice[i] = 0;
-    __syncthreads();
-    int bad = 0;
-    for (int it = 0; it < n_slices; ++it) {
-      const int p0 = it * 1024 + tid * 4;
-      int c8 = 0, c3 = 0;
-#pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        const int p = p0 + b;
-        const int tg = p < np ? trow[p] : -1;
-        c3 += tg == TAG_S;
-        c8 += (tg == TAG_R || tg == TAG_A);
-        bad |= (p < np && tg != TAG_S && tg != TAG_R && tg != TAG_A);
-      }
-      int packed = c8 | (c3 << 16);
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) packed += __shfl_xor(packed, o, 64);
-      if (lane == 0) atomicAdd(&s_slice[it], packed);
-    }
-    if (bad && chunk == 0) atomicOr(&P.ctrl[CTRL_ERR], (int)MKV_DEVERR_BAD_TAG);
-    __syncthreads();
-  }
-  int n8 = 0, n3 = 0;
-  for (int it = 0; it < n_slices; ++it) {
-    n8 += s_slice[it] & 0xFFFF;
-    n3 += s_slice[it] >> 16;
-  }
-  const int nch8 = (n8 + a.c8 - 1) / a.c8, nch3 = (n3 + a.c3 - 1) / a.c3;
-  const int total = nch8 + nch3;
-  if (chunk == 0 && h == 0 && tid == 0) a.totals[r] = total;
-  if (chunk >= total) return;
-  const bool is8 = chunk < nch8;
-  const int lo = is8 ? chunk * a.c8 : (chunk - nch8) * a.c3;
-  const int hi = min(lo + (is8 ? a.c8 : a.c3), is8 ? n8 : n3);
-  {
-    const int32_t* brow = a.bt + (int64_t)r * mp;
-    const int n_ids = is8 ? P.n_fp8 : P.n_tq3;
-    int base = 0;
-    for (int it = 0; it < n_slices; ++it) {
-      const int cnt = is8 ? (s_slice[it] & 0xFFFF) : (s_slice[it] >> 16);
-      if (base < hi && base + cnt > lo) {  // uniform across the workgroup
-        const int p0 = it * 1024 + tid * 4;
-        int tg4[4], c = 0;
-#pragma unroll
-        for (int b = 0; b < 4; ++b) {
-          const int p = p0 + b;
-          const int tg = p < np ? trow[p] : -1;
-          tg4[b] = is8 ? (tg == TAG_R || tg == TAG_A) : (tg == TAG_S);
-          c += tg4[b];
-        }
-        int tot;
-        int rank = base + block_excl_scan(c, scr, &tot);
-#pragma unroll
-        for (int b = 0; b < 4; ++b) {
-          if (tg4[b]) {
-            if (rank >= lo && rank < hi) {
-              const int p = p0 + b;
-              int id = brow[p], lp = p;
-              if (id < 0 || id >= n_ids) {
-                // out-of-range physical id: read page 0 instead, mask every token
-                atomicOr(&P.ctrl[CTRL_ERR], (int)MKV_DEVERR_RANGE);
-                id = 0;
-                lp = 0x3FFFFFFF / PAGE;
-              }
-              s_list[rank - lo] = make_int2(lp, id);
-            }
-            rank++;
-          }
-        }
-      }
-      base += cnt;
-    }
+  const int n_old = S > P.recent ? (S - P.recent) / PAGE : 0;  // pages wholly outside the window
+  const int C = a.cpages, CR = a.cpages / 2;
+  const int nco = (n_old + C - 1) / C, ncr = (np - n_old + CR - 1) / CR;
+  if (chunk == 0 && h == 0 && tid == 0) a.totals[r] = nco + ncr;
+  if (chunk >= nco + ncr) return;
+  const int p0 = chunk < nco ? chunk * C : n_old + (chunk - nco) * CR;
+  const int p1 = chunk < nco ? min(p0 + C, n_old) : min(p0 + CR, np);
+  const int n_pg = p1 - p0;
+  int tg = -1, id = 0;
+  if (tid < n_pg) {
+    tg = a.tags[(int64_t)r * mp + p0 + tid];
+    id = a.bt[(int64_t)r * mp + p0 + tid];
   }
 
-  // ---- 2. queries of the GQA group -> fp16 MFMA operands in LDS
-  float* qs = smem;  // [G][D]
-  for (int i = tid; i < G * D; i += 256) {
-    const int n = i / D, c = i % D;
-    float x = bf16_to_f32(a.q[((int64_t)r * Hq + h * G + n) * D + c]);
-    if (!is8) x *= (float)P.sigma[c];
-    qs[i] = x;
+  // ---- 2. per-format compact lists of the chunk (logical order) -> stages
+  const bool is3 = tg == TAG_S, is8 = (tg == TAG_R || tg == TAG_A);
+  if (tid < n_pg && !is3 && !is8) atomicOr(&P.ctrl[CTRL_ERR], (int)MKV_DEVERR_BAD_TAG);
+  const uint64_t m3 = __ballot(is3), m8 = __ballot(is8);
+  if (lane == 0) {
+    s_cnt[wid] = __popcll(m3);
+    s_cnt[NW + wid] = __popcll(m8);
   }
   __syncthreads();
-  if (!is8) {
-    for (int s = 1; s < D; s <<= 1) {
-      for (int b = tid; b < G * D / 2; b += 256) {
-        const int n = b / (D / 2), bb = b % (D / 2);
-        const int i = n * D + (bb / s) * 2 * s + (bb % s);
-        const float x0 = qs[i], x1 = qs[i + s];
-        qs[i] = x0 + x1;
-        qs[i + s] = x0 - x1;
-      }
-      __syncthreads();
-    }
-  }
-  // Columns of the score tile: with G <= 8 two pages share one MFMA tile,
-  // columns [0, 8) holding the heads for page a and [8, 16) for page b.
-  const bool pair = G <= 8;
-  const float qscale = is8 ? 1.0f : rsqrtf((float)D);
-  const int ln = lane & 15, lg = lane >> 4;
-  const int col_head = pair ? (ln & 7) : ln;
-  const bool col_valid = col_head < G;
-  const bool col_b = pair && ln >= 8;        // this column scores page b
-  const bool row_b = pair && lg >= 2;        // accumulator rows 4*lg+i hold page b
-  // fp16 query operands in MFMA lane order: qop[s][lane] (16 B each)
-  half8* qop = reinterpret_cast<half8*>(smem + G * D);
-  for (int i = tid; i < NS * 64; i += 256) {
-    const int s = i / 64, l = i % 64;
-    const int lln = l & 15, llg = l >> 4;
-    const int ch = pair ? (lln & 7) : lln;
-    half8 v;
+  int b3 = 0, b8 = 0, n3 = 0, n8 = 0;
 #pragma unroll
-    for (int j = 0; j < 8; ++j)
-      v[j] = (_Float16)(ch < G ? qs[ch * D + (D / 4) * llg + 8 * s + j] * qscale : 0.0f);
-    qop[i] = v;
+  for (int w = 0; w < NW; ++w) {
+    const int c3 = s_cnt[w], c8 = s_cnt[NW + w];
+    b3 += w < wid ? c3 : 0;
+    b8 += w < wid ? c8 : 0;
+    n3 += c3;
+    n8 += c8;
+  }
+  n3 = __builtin_amdgcn_readfirstlane(n3);
+  n8 = __builtin_amdgcn_readfirstlane(n8);
+  const int st3 = pair ? (n3 + 1) / 2 : n3;
+  const int n_st = st3 + n8;
+  if (is3 || is8) {
+    const uint64_t below = (1ull << lane) - 1ull;
+    int lp = p0 + tid;
+    if (id < 0 || id >= (is3 ? P.n_tq3 : P.n_fp8)) {
+      // out-of-range physical id: read page 0 instead, mask every token
+      atomicOr(&P.ctrl[CTRL_ERR], (int)MKV_DEVERR_RANGE);
+      id = 0;
+      lp = MASK_LP;
+    }
+    int2* s2 = reinterpret_cast<int2*>(s_stage);
+    if (is3) {
+      const int rank = b3 + __popcll(m3 & below);
+      if (pair) {
+        s2[rank] = make_int2(lp, id);  // stage rank / 2, half rank % 2
+        if (rank == n3 - 1 && !(rank & 1)) s2[rank + 1] = make_int2(MASK_LP, id);
+      } else {
+        s_stage[rank] = make_int4(lp, id, MASK_LP, id);
+      }
+    } else {
+      s_stage[st3 + b8 + __popcll(m8 & below)] = make_int4(lp, id, 0, -1);
+    }
   }
   __syncthreads();
 
-  // ---- 3. per-wave scan over page pairs
+  // ---- 3. per-wave stream over stages [s0, s1)
   WaveState<D> st;
 #pragma unroll
   for (int m = 0; m < CL; ++m) st.acc[m] = float4v{0.f, 0.f, 0.f, 0.f};
   st.m_run = -INFINITY;
   st.l_run = 0.0f;
-
-  const int npg = hi - lo;
-  const int per_wave = (is8 ? a.c8 : a.c3) / 4;
-  const int w0 = wid * per_wave, w1 = min(npg, w0 + per_wave);
-  const int step = pair ? 2 : 1;
-  const int layer = a.layer;
+  const int ln = lane & 15, lg = lane >> 4;
+  const int col_head = pair ? (ln & 7) : ln;
+  const bool col_valid = col_head < G;
+  const bool col_b = pair && ln >= 8;  // this column scores page b
+  const bool row_b = pair && lg >= 2;  // accumulator rows 4*lg+i hold page b
+  const int s0 = wid * n_st / NW, s1 = (wid + 1) * n_st / NW;
   const float smk = a.sm_log2;
   const float4v zero4 = {0.f, 0.f, 0.f, 0.f};
+  const int layer = a.layer;
+  const uint8_t* tq3_l = P.tq3 + (int64_t)layer * P.n_tq3 * H * R3;
+  const uint8_t* fp8_l = P.fp8 + (int64_t)layer * P.n_fp8 * H * R8;
+  const uint8_t* scl_l = reinterpret_cast<const uint8_t*>(P.fp8_scales + (int64_t)layer * P.n_fp8 * H * 2);
+  uint8_t* wring = ring + wid * 2 * STAGE;
+  const uint32_t wring_lds = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)wring);
+  auto stage_at = [&](int j) {
+    const int4 e = s_stage[j];
+    return make_int4(__builtin_amdgcn_readfirstlane(e.x), __builtin_amdgcn_readfirstlane(e.y),
+                     __builtin_amdgcn_readfirstlane(e.z), __builtin_amdgcn_readfirstlane(e.w));
+  };
+  auto issue = [&](const int4& e, int slot) {
+    const uint32_t dst = wring_lds + slot * STAGE;
+    if (e.w >= 0) {
+      dma_region<R3>(dst, tq3_l + ((int64_t)e.y * H + h) * R3, lane);
+      if (pair) dma_region<R3>(dst + R3, tq3_l + ((int64_t)e.w * H + h) * R3, lane);
+    } else {
+      dma_region<R8>(dst, fp8_l + ((int64_t)e.y * H + h) * R8, lane);
+      if (lane < 2) dma4(scl_l + ((int64_t)e.y * H + h) * 8 + 4 * lane, dst + R8);
+    }
+  };
+  if (s0 < s1) issue(stage_at(s0), 0);
+  if (s0 + 1 < s1) issue(stage_at(s0 + 1), 1);
 
-  if (!is8) {
-    for (int ia = w0; ia < w1; ia += step) {
-      const bool hasb = pair && ia + 1 < w1;
-      const int2 ea = s_list[ia];
-      const int2 eb = hasb ? s_list[ia + 1] : ea;
-      const uint8_t* ra = P.tq3 + (((int64_t)layer * P.n_tq3 + ea.y) * H + h) * tq3_region_bytes(D);
-      const uint8_t* rb = P.tq3 + (((int64_t)layer * P.n_tq3 + eb.y) * H + h) * tq3_region_bytes(D);
+  // ---- query operands, built while the first stages are in flight, in MFMA
+  // lane order: q?[s][lane] holds channels (D/4) lg + 8 s + j, j < 8, of
+  // column ln's head (ln = lane % 16, lg = lane / 16)
+  {
+    _Float16* qr = reinterpret_cast<_Float16*>(qrot);
+    _Float16* qp = reinterpret_cast<_Float16*>(qpl);
+    const float qscale = rsqrtf((float)D);  // R = d^-1/2 H diag(sigma)
+#pragma unroll
+    for (int ps = 0; ps < 2; ++ps) {
+      const int n = wid + 8 * ps;
+      if (ps == 1 && pair) break;
+      float xr[QV];
+#pragma unroll
+      for (int i = 0; i < QV; ++i) xr[i] = qx[ps][i] * (float)sg[i];
+      // fast Walsh-Hadamard transform: strides below QV inside the lane,
+      // the rest across lanes (partner lane = lane ^ (stride / QV))
+#pragma unroll
+      for (int st = 1; st < QV; st <<= 1)
+#pragma unroll
+        for (int i = 0; i < QV; ++i)
+          if (!(i & st)) {
+            const float x0 = xr[i], x1 = xr[i + st];
+            xr[i] = x0 + x1;
+            xr[i + st] = x0 - x1;
+          }
+#pragma unroll
+      for (int m = 1; m < 64; m <<= 1) {
+        const bool hi = lane & m;
+#pragma unroll
+        for (int i = 0; i < QV; ++i) {
+          const float y = __shfl_xor(xr[i], m, 64);
+          xr[i] = hi ? y - xr[i] : xr[i] + y;
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < QV; ++i) {
+        const int c = QV * lane + i;
+        const int lgc = c / (D / 4), sc = (c % (D / 4)) / 8, j = c % 8;
+        const _Float16 vr = (_Float16)(n < G ? xr[i] * qscale : 0.0f);
+        const _Float16 vp = (_Float16)(n < G ? qx[ps][i] : 0.0f);
+        const int e0 = ((sc * 64) + lgc * 16 + n) * 8 + j;
+        qr[e0] = vr;
+        qp[e0] = vp;
+        if (pair) {
+          qr[e0 + 8 * 8] = vr;  // column n + 8 scores page b with the same head
+          qp[e0 + 8 * 8] = vp;
+        }
+      }
+    }
+  }
+
+  __syncthreads();  // query operands visible to every wave
+  for (int j = s0; j < s1; ++j) {
+    const int slot = (j - s0) & 1;
+    const int4 e = stage_at(j);
+    // wait for this stage while the next one stays in flight
+    {
+      const int nops = j + 1 < s1 ? (stage_at(j + 1).w >= 0 ? (pair ? 2 : 1) * OPS3 : OPS8) : 0;
+      if (nops == 2 * OPS3)
+        wait_vmcnt<2 * OPS3>();
+      else if (nops == OPS8)
+        wait_vmcnt<OPS8>();
+      else if (nops == OPS3)
+        wait_vmcnt<OPS3>();
+      else
+        wait_vmcnt<0>();
+    }
+    const bool refill = j + 2 < s1;
+    const int4 e2 = refill ? stage_at(j + 2) : e;
+    const uint8_t* ra = wring + slot * STAGE;
+    if (e.w >= 0) {
+      // TQ3 pair (page b absent: same page, every token masked)
+      const uint8_t* rb = pair ? ra + R3 : ra;
       const uint8_t* rown = row_b ? rb : ra;
       uint32_t kA[NDW], kB[NDW], vA[NDW], vB[NDW];
-      {
-        const uint32_t* pkA = reinterpret_cast<const uint32_t*>(ra + (ln * 4 + lg) * CB);
-        const uint32_t* pkB = reinterpret_cast<const uint32_t*>(rb + (ln * 4 + lg) * CB);
-        const uint32_t* pvA = reinterpret_cast<const uint32_t*>(ra + 6 * D + (ln * 4 + lg) * CB);
-        const uint32_t* pvB = reinterpret_cast<const uint32_t*>(rb + 6 * D + (ln * 4 + lg) * CB);
 #pragma unroll
-        for (int w = 0; w < NDW; ++w) {
-          kA[w] = pkA[w];
-          kB[w] = pkB[w];
-          vA[w] = pvA[w];
-          vB[w] = pvB[w];
-        }
+      for (int w = 0; w < NDW; ++w) {
+        kA[w] = reinterpret_cast<const uint32_t*>(ra + (ln * 4 + lg) * CB)[w];
+        kB[w] = reinterpret_cast<const uint32_t*>(rb + (ln * 4 + lg) * CB)[w];
+        vA[w] = reinterpret_cast<const uint32_t*>(ra + 6 * D + (ln * 4 + lg) * CB)[w];
+        vB[w] = reinterpret_cast<const uint32_t*>(rb + 6 * D + (ln * 4 + lg) * CB)[w];
       }
       const uint2 gw = *reinterpret_cast<const uint2*>((col_b ? rb : ra) + 12 * D + 8 * lg);
       // per-channel V scale of this lane's row page, V zero of both pages
       half2v sO[CL / 2], zA[CL / 2], zB[CL / 2];
-      {
-        const half2v* s0 = reinterpret_cast<const half2v*>(rown + 12 * D + 32 + 2 * CL * ln);
-        const half2v* z0 = reinterpret_cast<const half2v*>(ra + 14 * D + 32 + 2 * CL * ln);
-        const half2v* z1 = reinterpret_cast<const half2v*>(rb + 14 * D + 32 + 2 * CL * ln);
 #pragma unroll
-        for (int i = 0; i < CL / 2; ++i) {
-          sO[i] = s0[i];
-          zA[i] = z0[i];
-          zB[i] = z1[i];
-        }
+      for (int i = 0; i < CL / 2; ++i) {
+        sO[i] = reinterpret_cast<const half2v*>(rown + 12 * D + 32 + 2 * CL * ln)[i];
+        zA[i] = reinterpret_cast<const half2v*>(ra + 14 * D + 32 + 2 * CL * ln)[i];
+        zB[i] = reinterpret_cast<const half2v*>(rb + 14 * D + 32 + 2 * CL * ln)[i];
       }
+      wait_lgkm0();  // the stage is in registers: refill its slot
+      if (refill) issue(e2, slot);
       // QK^T: rows = tokens of the page, columns = (page, head)
       float4v sa = zero4, sb = zero4;
 #pragma unroll
       for (int s = 0; s < NS; ++s) {
-        const half8 qv = qop[s * 64 + lane];
+        const half8 qv = qrot[s * 64 + lane];
         const uint32_t a0 = __builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(kA, 2 * s));
         const uint32_t a1 = __builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(kA, 2 * s + 1));
         sa = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(cvt_lo(a0), cvt_hi(a0), cvt_lo(a1), cvt_hi(a1)),
@@ -355,7 +463,7 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeArgs a) {
       }
       float sc[4];
       {
-        const int vcnt = col_b ? (hasb ? S - eb.x * PAGE : 0) : S - ea.x * PAGE;
+        const int vcnt = S - (col_b ? e.z : e.x) * PAGE;
         const _Float16* gh = reinterpret_cast<const _Float16*>(&gw);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -378,80 +486,61 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeArgs a) {
         const _Float16 za = zA[m >> 1][m & 1], zb = zB[m >> 1][m & 1];
         half8 zz;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          zz[j] = za;
-          zz[4 + j] = zb;
+        for (int k = 0; k < 4; ++k) {
+          zz[k] = za;
+          zz[4 + k] = zb;
         }
         st.acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(pT, zz, st.acc[m], 0, 0, 0);
       }
-    }
-  } else {
-    for (int ia = w0; ia < w1; ia += step) {
-      const bool hasb = pair && ia + 1 < w1;
-      const int2 ea = s_list[ia];
-      const int2 eb = hasb ? s_list[ia + 1] : ea;
-      const int64_t pha = ((int64_t)layer * P.n_fp8 + ea.y) * H + h;
-      const int64_t phb = ((int64_t)layer * P.n_fp8 + eb.y) * H + h;
-      const uint8_t* ra = P.fp8 + pha * fp8_region_bytes(D);
-      const uint8_t* rb = P.fp8 + phb * fp8_region_bytes(D);
+    } else {
+      // one FP8 page (score columns of page b stay empty)
       constexpr int KW = D / 16;  // dwords of K per lane (D/4 bytes)
-      uint32_t kA[KW], kB[KW], vA[CL], vB[CL];
+      uint32_t kA[KW], vA[CL];
       {
-        const uint4* pkA = reinterpret_cast<const uint4*>(ra + ln * D + (D / 4) * lg);
-        const uint4* pkB = reinterpret_cast<const uint4*>(rb + ln * D + (D / 4) * lg);
-        const uint4* pvA = reinterpret_cast<const uint4*>(ra + PAGE * D + (ln * 4 + lg) * 4 * CL);
-        const uint4* pvB = reinterpret_cast<const uint4*>(rb + PAGE * D + (ln * 4 + lg) * 4 * CL);
+        const uint4* pk = reinterpret_cast<const uint4*>(ra + ln * D + (D / 4) * lg);
+        const uint4* pv = reinterpret_cast<const uint4*>(ra + PAGE * D + (ln * 4 + lg) * 4 * CL);
 #pragma unroll
         for (int w = 0; w < KW / 4; ++w) {
-          const uint4 x = pkA[w], y = pkB[w];
+          const uint4 x = pk[w];
           kA[4 * w] = x.x; kA[4 * w + 1] = x.y; kA[4 * w + 2] = x.z; kA[4 * w + 3] = x.w;
-          kB[4 * w] = y.x; kB[4 * w + 1] = y.y; kB[4 * w + 2] = y.z; kB[4 * w + 3] = y.w;
         }
 #pragma unroll
         for (int w = 0; w < CL / 4; ++w) {
-          const uint4 x = pvA[w], y = pvB[w];
+          const uint4 x = pv[w];
           vA[4 * w] = x.x; vA[4 * w + 1] = x.y; vA[4 * w + 2] = x.z; vA[4 * w + 3] = x.w;
-          vB[4 * w] = y.x; vB[4 * w + 1] = y.y; vB[4 * w + 2] = y.z; vB[4 * w + 3] = y.w;
         }
       }
-      const float sK = P.fp8_scales[(col_b ? phb : pha) * 2];
-      const float sV = P.fp8_scales[(row_b ? phb : pha) * 2 + 1];
-      float4v sa = zero4, sb = zero4;
+      const float2 ksv = *reinterpret_cast<const float2*>(ra + R8);
+      wait_lgkm0();  // the stage is in registers: refill its slot
+      if (refill) issue(e2, slot);
+      float4v sa = zero4;
 #pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        const half8 qv = qop[s * 64 + lane];
+      for (int s = 0; s < NS; ++s)
         sa = __builtin_amdgcn_mfma_f32_16x16x32_f16(
             h8(cvt_lo(kA[2 * s]), cvt_hi(kA[2 * s]), cvt_lo(kA[2 * s + 1]), cvt_hi(kA[2 * s + 1])),
-            qv, sa, 0, 0, 0);
-        if (pair)
-          sb = __builtin_amdgcn_mfma_f32_16x16x32_f16(
-              h8(cvt_lo(kB[2 * s]), cvt_hi(kB[2 * s]), cvt_lo(kB[2 * s + 1]), cvt_hi(kB[2 * s + 1])),
-              qv, sb, 0, 0, 0);
-      }
+            qpl[s * 64 + lane], sa, 0, 0, 0);
       float sc[4];
       {
-        const int vcnt = col_b ? (hasb ? S - eb.x * PAGE : 0) : S - ea.x * PAGE;
-        const float kk = sK * smk;
+        const int vcnt = col_b ? 0 : S - e.x * PAGE;
+        const float kk = ksv.x * smk;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float sv = col_b ? sb[i] : sa[i];
-          sc[i] = (col_valid && 4 * lg + i < vcnt) ? sv * kk : -INFINITY;
-        }
+        for (int i = 0; i < 4; ++i) sc[i] = (col_valid && 4 * lg + i < vcnt) ? sa[i] * kk : -INFINITY;
       }
       softmax_step<D>(st, sc, lg);
       const half8 pT = p_operand(sc, col_b);
+      const half2v z2 = {(_Float16)0.0f, (_Float16)0.0f};
 #pragma unroll
       for (int m = 0; m < CL; ++m) {
         const float4v X = __builtin_amdgcn_mfma_f32_16x16x32_f16(
-            pT, h8(cvt_lo(vA[m]), cvt_hi(vA[m]), cvt_lo(vB[m]), cvt_hi(vB[m])), zero4, 0, 0, 0);
-        st.acc[m] += sV * X;
+            pT, h8(cvt_lo(vA[m]), cvt_hi(vA[m]), z2, z2), zero4, 0, 0, 0);
+        st.acc[m] += ksv.y * X;
       }
     }
   }
 
   // ---- 4. rows -> heads: fetch each accumulator row's (m, l); merge the two
   // page parities (rows h and h + 8 sit in lanes l and l ^ 32); then merge the
-  // four waves in LDS into one (m_j, l_j, O_j) partial per chunk
+  // eight waves in LDS into one (m_j, l_j, O_j) partial per chunk
   float l_col = st.l_run;
   l_col += __shfl_xor(l_col, 16, 64);
   l_col += __shfl_xor(l_col, 32, 64);
@@ -477,10 +566,10 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeArgs a) {
       mrow[i] = M;
     }
   }
-  float* macc = smem;                 // [4][G][D]
-  float* mm = smem + 4 * G * D;       // [4][G]
-  float* ml = mm + 4 * G;             // [4][G]
-  __syncthreads();                    // qop region is reused below
+  float* macc = reinterpret_cast<float*>(ring);  // [NW][G][D]
+  float* mm = macc + NW * G * D;                 // [NW][G]
+  float* ml = mm + NW * G;                       // [NW][G]
+  __syncthreads();  // every wave is done with its ring (all copies waited for)
   if (!row_b) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
@@ -497,15 +586,15 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeArgs a) {
   }
   __syncthreads();
   float* part = a.partials + (((int64_t)r * H + h) * a.max_chunks + chunk) * G * (D + 2);
-  for (int i = tid; i < G * D; i += 256) {
+  for (int i = tid; i < G * D; i += NT) {
     const int n = i / D;
     float M = -INFINITY;
 #pragma unroll
-    for (int w = 0; w < 4; ++w)
+    for (int w = 0; w < NW; ++w)
       if (ml[w * G + n] > 0.0f) M = fmaxf(M, mm[w * G + n]);
     float L = 0.0f, O = 0.0f;
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {
+    for (int w = 0; w < NW; ++w) {
       const float lw = ml[w * G + n];
       if (lw > 0.0f) {
         const float f = exp2f(mm[w * G + n] - M);
@@ -513,7 +602,7 @@ __global__ __launch_bounds__(256, 2) void decode_kernel(DecodeArgs a) {
         O += f * macc[(w * G + n) * D + (i % D)];
       }
     }
-    part[i] = O / L;
+    part[i] = L > 0.0f ? O / L : 0.0f;
     if (i % D == 0) {
       part[G * D + n] = M;
       part[G * D + G + n] = L;
@@ -608,11 +697,16 @@ __global__ __launch_bounds__(256) void decode_merge_kernel(int G, int H, int max
   if (lse && tid == 0) lse[(int64_t)r * Hq + h * G + n] = (M + log2f(L)) * 0.69314718055994531f;
 }
 
+// dynamic LDS a decode workgroup may use: 160 KiB per CU minus the static arrays
+static constexpr size_t lds_limit() {
+  return 160 * 1024 - sizeof(int4) * MAX_CHUNK_PAGES - sizeof(int) * 2 * NW - 256;
+}
+
 hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t* q,
                          const int32_t* bt, const uint8_t* tags, int max_pages,
                          const int32_t* seq_lens, float* out, float* lse, void* ws,
                          hipStream_t s) {
-  DecodeShape sh = decode_shape(n_req, max_pages, P.n_kv_heads);
+  const DecodeShape sh = decode_shape(n_req, max_pages, P.n_kv_heads, P.recent);
   DecodeArgs a;
   a.P = P;
   a.layer = layer;
@@ -626,21 +720,31 @@ hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t
   a.lse = lse;
   a.totals = reinterpret_cast<int32_t*>(ws);
   a.partials = reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(ws) + header_bytes(n_req));
-  a.c3 = sh.c3;
-  a.c8 = sh.c8;
+  a.cpages = sh.cpages;
   a.max_chunks = sh.max_chunks;
   a.sm_log2 = 1.4426950408889634f / sqrtf((float)P.d);
-  const size_t merge_f = (size_t)(4 * P.group * P.d + 8 * P.group);
-  const size_t qop_f = (size_t)P.group * P.d + (size_t)(P.d / 32) * 64 * 4;
-  const size_t lds = (merge_f > qop_f ? merge_f : qop_f) * sizeof(float);
+  // dynamic LDS: two query operands, then the page ring (reused by the wave merge)
+  const size_t qop_b = 2 * (size_t)(P.d / 32) * 64 * 16;
+  const size_t ring_b = (size_t)NW * 2 * 2 * tq3_region_bytes(P.d);
+  const size_t merge_b = ((size_t)NW * P.group * P.d + 2 * NW * P.group) * sizeof(float);
+  const size_t lds = qop_b + (ring_b > merge_b ? ring_b : merge_b);
+  static bool attr_set[2] = {false, false};
+  const int di = P.d == 256;
+  if (!attr_set[di]) {
+    const void* k = di ? (const void*)decode_kernel<256> : (const void*)decode_kernel<128>;
+    hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_limit());
+    if (e != hipSuccess) return e;
+    attr_set[di] = true;
+  }
+  if (lds > lds_limit()) return hipErrorInvalidValue;
   dim3 grid(sh.max_chunks, P.n_kv_heads, n_req);
   dim3 mgrid(P.group, P.n_kv_heads, n_req);
-  if (P.d == 256) {
-    hipLaunchKernelGGL(decode_kernel<256>, grid, dim3(256), lds, s, a);
+  if (di) {
+    hipLaunchKernelGGL(decode_kernel<256>, grid, dim3(NT), lds, s, a);
     hipLaunchKernelGGL(decode_merge_kernel<256>, mgrid, dim3(256), 0, s, P.group, P.n_kv_heads,
                        sh.max_chunks, a.totals, a.partials, out, lse);
   } else {
-    hipLaunchKernelGGL(decode_kernel<128>, grid, dim3(256), lds, s, a);
+    hipLaunchKernelGGL(decode_kernel<128>, grid, dim3(NT), lds, s, a);
     hipLaunchKernelGGL(decode_merge_kernel<128>, mgrid, dim3(256), 0, s, P.group, P.n_kv_heads,
                        sh.max_chunks, a.totals, a.partials, out, lse);
   }

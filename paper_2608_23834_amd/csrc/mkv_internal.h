@@ -64,10 +64,10 @@ hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
 
 // mkv_decode.hip
 struct DecodeShape {
-  int c3, c8, max_chunks;
+  int cpages, max_chunks;
 };
-DecodeShape decode_shape(int n_req, int max_pages, int n_kv_heads);
-size_t decode_ws_bytes(int n_req, int max_pages, int n_kv_heads, int group, int d);
+DecodeShape decode_shape(int n_req, int max_pages, int n_kv_heads, int recent);
+size_t decode_ws_bytes(int n_req, int max_pages, int n_kv_heads, int group, int d, int recent);
 hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t* q,
                          const int32_t* bt, const uint8_t* tags, int max_pages,
                          const int32_t* seq_lens, float* out, float* lse, void* ws,
