@@ -27,6 +27,7 @@
 // anything the size of the cache.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <type_traits>
 
 #include "mkv_internal.h"
@@ -92,41 +93,71 @@ __device__ __forceinline__ half2v cvt_lo(uint32_t w) {
 __device__ __forceinline__ half2v cvt_hi(uint32_t w) {
   return __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w, 1.0f, true);
 }
+// code bytes 0..7 -> fp16 0..7: each byte read as an E4M3 subnormal (c * 2^-9)
+// and scaled by 2^9 in the converter, exactly
+template <bool HI>
+__device__ __forceinline__ half2v cvt_code(uint32_t w) {
+  return __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w, 512.0f, HI);
+}
 __device__ __forceinline__ float exp2_safe(float s, float m) {
   return s == -INFINITY ? 0.0f : exp2f(s - m);
 }
 
-// Direct HBM -> LDS copies issued by one wave.  dma16: lane l copies 16 bytes
-// from its own src to dst + 16 l; dma4: 4 bytes to dst + 4 l (dst is the
-// wave-uniform LDS byte address).  They are inline assembly on purpose: the
-// compiler then does not order later LDS reads behind them (it cannot tell
-// which ring slot a copy fills and would wait for all of them), and the caller
-// gates every stage with an explicit vmcnt wait.  The kernel has no other
-// user of m0.
+// Direct HBM -> LDS copies issued by one wave.  dma16<OFF>: lane l copies
+// 16 bytes from base + voff_l + OFF to LDS m0 + OFF + 16 l; dma4<OFF>: 4 bytes
+// to m0 + OFF + 4 l (the immediate offset applies to both addresses; base and
+// m0 are wave-uniform).  They are inline assembly on purpose: the compiler
+// then does not order later LDS reads behind them (it cannot tell which ring
+// slot a copy fills and would wait for all of them), and the caller gates
+// every stage with an explicit vmcnt wait.  The kernel has no other user of m0.
 #pragma clang diagnostic push
 #pragma clang diagnostic ignored "-Winline-asm"  // m0 is reserved; no compiler code here uses it
-__device__ __forceinline__ void dma16(const uint8_t* src, uint32_t dst) {
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+template <int OFF>
+__device__ __forceinline__ void dma16(uint32_t voff, const uint8_t* base, uint32_t m0) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1 offset:%3"
                :
-               : "v"(src), "s"(dst)
+               : "v"(voff), "s"(base), "s"(m0), "n"(OFF)
                : "memory", "m0");
 }
-__device__ __forceinline__ void dma4(const uint8_t* src, uint32_t dst) {
-  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dword %0, off"
+__device__ __forceinline__ void dma4(uint32_t voff, const uint8_t* base, uint32_t m0) {
+  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %0, %1 offset:0"
                :
-               : "v"(src), "s"(dst)
+               : "v"(voff), "s"(base), "s"(m0)
                : "memory", "m0");
 }
 #pragma clang diagnostic pop
-// One region of R bytes (16-byte aligned): whole KiB blocks by 16-byte lanes,
-// the tail by 4-byte lanes.
+
+// Per-lane byte offsets of the copies (constant for the kernel).
+struct DmaLanes {
+  uint32_t lo, hi;  // 16 l and 4096 + 16 l
+};
+// One region of R bytes (16-byte aligned, R <= 8 KiB + 256): whole KiB blocks
+// by 16-byte lanes, the tail by 4-byte lanes.
 template <int R>
-__device__ __forceinline__ void dma_region(uint32_t dst, const uint8_t* src, int lane) {
+__device__ __forceinline__ void dma_region(uint32_t dst, const uint8_t* src, const DmaLanes& dl,
+                                           int lane) {
+  static_assert(R <= 8192 + 256, "region too large for the offset scheme");
 #pragma unroll
-  for (int i = 0; i < R / 1024; ++i) dma16(src + 1024 * i + 16 * lane, dst + 1024 * i);
+  for (int i = 0; i < R / 1024 && i < 4; ++i) {
+    switch (i) {
+      case 0: dma16<0>(dl.lo, src, dst); break;
+      case 1: dma16<1024>(dl.lo, src, dst); break;
+      case 2: dma16<2048>(dl.lo, src, dst); break;
+      default: dma16<3072>(dl.lo, src, dst); break;
+    }
+  }
+#pragma unroll
+  for (int i = 4; i < R / 1024; ++i) {
+    switch (i) {
+      case 4: dma16<0>(dl.hi, src, dst + 4096); break;
+      case 5: dma16<1024>(dl.hi, src, dst + 4096); break;
+      case 6: dma16<2048>(dl.hi, src, dst + 4096); break;
+      default: dma16<3072>(dl.hi, src, dst + 4096); break;
+    }
+  }
   constexpr int TAIL = R % 1024;
   static_assert(TAIL % 4 == 0 && TAIL <= 256, "tail must fit one 4-byte copy");
-  if (TAIL > 0 && lane < TAIL / 4) dma4(src + (R - TAIL) + 4 * lane, dst + (R - TAIL));
+  if (TAIL > 0 && lane < TAIL / 4) dma4((R - TAIL) + 4 * lane, src, dst + (R - TAIL));
 }
 // vector-memory instructions dma_region<R> issues per wave
 template <int R>
@@ -197,7 +228,9 @@ __device__ __forceinline__ half8 p_operand(const float* p, bool row_is_b) {
   return r;
 }
 
-template <int D>
+// PAIR (query group of at most 8 heads): two pages share one score tile,
+// columns [0, 8) scoring page a and [8, 16) page b.
+template <int D, bool PAIR>
 __global__ __launch_bounds__(NT, 1) void decode_kernel(DecodeArgs a) {
   constexpr int CL = D / 16, NDW = 3 * D / 128, CB = 3 * D / 32, NS = D / 32, QV = D / 64;
   constexpr int R3 = (int)tq3_region_bytes(D);  // K codes, V codes, gamma, V scale, V zero
@@ -214,7 +247,7 @@ __global__ __launch_bounds__(NT, 1) void decode_kernel(DecodeArgs a) {
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int G = P.group, H = P.n_kv_heads, Hq = H * G;
   const int mp = a.max_pages;
-  const bool pair = G <= 8;  // two pages share one score tile: columns [0,8) page a, [8,16) page b
+  constexpr bool pair = PAIR;
   // LDS: [rotated-query operand][plain-query operand][page ring | wave merge]
   half8* qrot = reinterpret_cast<half8*>(smem);
   half8* qpl = qrot + NS * 64;
@@ -327,6 +360,9 @@ __global__ __launch_bounds__(NT, 1) void decode_kernel(DecodeArgs a) {
   const int s0 = wid * n_st / NW, s1 = (wid + 1) * n_st / NW;
   const float smk = a.sm_log2;
   const float4v zero4 = {0.f, 0.f, 0.f, 0.f};
+  half8 ones8;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) ones8[j] = (_Float16)1.0f;
   const int layer = a.layer;
   const uint8_t* tq3_l = P.tq3 + (int64_t)layer * P.n_tq3 * H * R3;
   const uint8_t* fp8_l = P.fp8 + (int64_t)layer * P.n_fp8 * H * R8;
@@ -339,14 +375,15 @@ __global__ __launch_bounds__(NT, 1) void decode_kernel(DecodeArgs a) {
     return make_int4(__builtin_amdgcn_readfirstlane(e.x), __builtin_amdgcn_readfirstlane(e.y),
                      __builtin_amdgcn_readfirstlane(e.z), __builtin_amdgcn_readfirstlane(e.w));
   };
+  const DmaLanes dl = {16u * lane, 4096u + 16u * lane};
   auto issue = [&](const int4& e, int slot) {
     const uint32_t dst = wring_lds + slot * STAGE;
     if (e.w >= 0) {
-      dma_region<R3>(dst, tq3_l + ((int64_t)e.y * H + h) * R3, lane);
-      if (pair) dma_region<R3>(dst + R3, tq3_l + ((int64_t)e.w * H + h) * R3, lane);
+      dma_region<R3>(dst, tq3_l + ((int64_t)e.y * H + h) * R3, dl, lane);
+      if (pair) dma_region<R3>(dst + R3, tq3_l + ((int64_t)e.w * H + h) * R3, dl, lane);
     } else {
-      dma_region<R8>(dst, fp8_l + ((int64_t)e.y * H + h) * R8, lane);
-      if (lane < 2) dma4(scl_l + ((int64_t)e.y * H + h) * 8 + 4 * lane, dst + R8);
+      dma_region<R8>(dst, fp8_l + ((int64_t)e.y * H + h) * R8, dl, lane);
+      if (lane < 2) dma4(4 * lane, scl_l + ((int64_t)e.y * H + h) * 8, dst + R8);
     }
   };
   if (s0 < s1) issue(stage_at(s0), 0);
@@ -404,137 +441,153 @@ __global__ __launch_bounds__(NT, 1) void decode_kernel(DecodeArgs a) {
   }
 
   __syncthreads();  // query operands visible to every wave
-  for (int j = s0; j < s1; ++j) {
+  half8 qreg[NS];  // rotated-query operand of this lane, kept in registers
+#pragma unroll
+  for (int s = 0; s < NS; ++s) qreg[s] = qrot[s * 64 + lane];
+  // Wait for stage j to land in its slot; stage j + 1 may stay in flight (the
+  // allowed count is the number of copies stage j + 1 was issued as).
+  auto begin_stage = [&](int j) {
+    const int nops = j + 1 < s1 ? (stage_at(j + 1).w >= 0 ? (pair ? 2 : 1) * OPS3 : OPS8) : 0;
+    if (nops == 2 * OPS3)
+      wait_vmcnt<2 * OPS3>();
+    else if (nops == OPS8)
+      wait_vmcnt<OPS8>();
+    else if (nops == OPS3)
+      wait_vmcnt<OPS3>();
+    else
+      wait_vmcnt<0>();
+  };
+  // TQ3 stages come first in the list, FP8 stages after them; the two loops
+  // share the ring (a copy in flight may belong to either format).
+  const int s_mid = max(s0, min(s1, st3));
+  for (int j = s0; j < s_mid; ++j) {
     const int slot = (j - s0) & 1;
     const int4 e = stage_at(j);
-    // wait for this stage while the next one stays in flight
-    {
-      const int nops = j + 1 < s1 ? (stage_at(j + 1).w >= 0 ? (pair ? 2 : 1) * OPS3 : OPS8) : 0;
-      if (nops == 2 * OPS3)
-        wait_vmcnt<2 * OPS3>();
-      else if (nops == OPS8)
-        wait_vmcnt<OPS8>();
-      else if (nops == OPS3)
-        wait_vmcnt<OPS3>();
-      else
-        wait_vmcnt<0>();
-    }
+    begin_stage(j);
     const bool refill = j + 2 < s1;
     const int4 e2 = refill ? stage_at(j + 2) : e;
     const uint8_t* ra = wring + slot * STAGE;
-    if (e.w >= 0) {
-      // TQ3 pair (page b absent: same page, every token masked)
-      const uint8_t* rb = pair ? ra + R3 : ra;
-      const uint8_t* rown = row_b ? rb : ra;
-      uint32_t kA[NDW], kB[NDW], vA[NDW], vB[NDW];
+    // TQ3 pair (page b absent: same page, every token masked)
+    const uint8_t* rb = pair ? ra + R3 : ra;
+    const uint8_t* rown = row_b ? rb : ra;
+    uint32_t kA[NDW], kB[NDW], vA[NDW], vB[NDW];
 #pragma unroll
-      for (int w = 0; w < NDW; ++w) {
-        kA[w] = reinterpret_cast<const uint32_t*>(ra + (ln * 4 + lg) * CB)[w];
-        kB[w] = reinterpret_cast<const uint32_t*>(rb + (ln * 4 + lg) * CB)[w];
-        vA[w] = reinterpret_cast<const uint32_t*>(ra + 6 * D + (ln * 4 + lg) * CB)[w];
-        vB[w] = reinterpret_cast<const uint32_t*>(rb + 6 * D + (ln * 4 + lg) * CB)[w];
+    for (int w = 0; w < NDW; ++w) {
+      kA[w] = reinterpret_cast<const uint32_t*>(ra + (ln * 4 + lg) * CB)[w];
+      kB[w] = reinterpret_cast<const uint32_t*>(rb + (ln * 4 + lg) * CB)[w];
+      vA[w] = reinterpret_cast<const uint32_t*>(ra + 6 * D + (ln * 4 + lg) * CB)[w];
+      vB[w] = reinterpret_cast<const uint32_t*>(rb + 6 * D + (ln * 4 + lg) * CB)[w];
+    }
+    const uint2 gw = *reinterpret_cast<const uint2*>((col_b ? rb : ra) + 12 * D + 8 * lg);
+    // per-channel V scale and zero of this lane's row page
+    half2v sO[CL / 2], zO[CL / 2];
+#pragma unroll
+    for (int i = 0; i < CL / 2; ++i) {
+      sO[i] = reinterpret_cast<const half2v*>(rown + 12 * D + 32 + 2 * CL * ln)[i];
+      zO[i] = reinterpret_cast<const half2v*>(rown + 14 * D + 32 + 2 * CL * ln)[i];
+    }
+    wait_lgkm0();  // the stage is in registers: refill its slot
+    if (refill) issue(e2, slot);
+    // QK^T: rows = tokens of the page, columns = (page, head)
+    float4v sa = zero4, sb = zero4;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      const half8 qv = qreg[s];
+      const uint32_t a0 = __builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(kA, 2 * s));
+      const uint32_t a1 = __builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(kA, 2 * s + 1));
+      sa = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(cvt_lo(a0), cvt_hi(a0), cvt_lo(a1), cvt_hi(a1)),
+                                                   qv, sa, 0, 0, 0);
+      if (pair) {
+        const uint32_t b0 = __builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(kB, 2 * s));
+        const uint32_t b1 = __builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(kB, 2 * s + 1));
+        sb = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+            h8(cvt_lo(b0), cvt_hi(b0), cvt_lo(b1), cvt_hi(b1)), qv, sb, 0, 0, 0);
       }
-      const uint2 gw = *reinterpret_cast<const uint2*>((col_b ? rb : ra) + 12 * D + 8 * lg);
-      // per-channel V scale of this lane's row page, V zero of both pages
-      half2v sO[CL / 2], zA[CL / 2], zB[CL / 2];
+    }
+    float sc[4];
+    {
+      const int vcnt = S - (col_b ? e.z : e.x) * PAGE;
+      const _Float16* gh = reinterpret_cast<const _Float16*>(&gw);
 #pragma unroll
-      for (int i = 0; i < CL / 2; ++i) {
-        sO[i] = reinterpret_cast<const half2v*>(rown + 12 * D + 32 + 2 * CL * ln)[i];
-        zA[i] = reinterpret_cast<const half2v*>(ra + 14 * D + 32 + 2 * CL * ln)[i];
-        zB[i] = reinterpret_cast<const half2v*>(rb + 14 * D + 32 + 2 * CL * ln)[i];
+      for (int i = 0; i < 4; ++i) {
+        const float sv = col_b ? sb[i] : sa[i];
+        sc[i] = (col_valid && 4 * lg + i < vcnt) ? sv * (float)gh[i] * smk : -INFINITY;
       }
-      wait_lgkm0();  // the stage is in registers: refill its slot
-      if (refill) issue(e2, slot);
-      // QK^T: rows = tokens of the page, columns = (page, head)
-      float4v sa = zero4, sb = zero4;
+    }
+    softmax_step<D>(st, sc, lg);
+    const half8 pT = p_operand(sc, col_b);
+    // PV: the codes enter the MFMA exactly (a code byte read as an E4M3
+    // subnormal is c * 2^-9; the converter's power-of-two scale 2^9 makes it
+    // c); v = zero + scale * code is applied in fp32 to the MFMA output,
+    // the zero term through the rows' weight sums PS (one MFMA against ones)
+    const float4v PS = __builtin_amdgcn_mfma_f32_16x16x32_f16(pT, ones8, zero4, 0, 0, 0);
+    auto pv = [&](int m) {
+      const uint32_t ua = quad_sel<NDW>(vA, m), ub = quad_sel<NDW>(vB, m);
+      return __builtin_amdgcn_mfma_f32_16x16x32_f16(
+          pT, h8(cvt_code<false>(ua), cvt_code<true>(ua), cvt_code<false>(ub), cvt_code<true>(ub)),
+          zero4, 0, 0, 0);
+    };
+    // one tile ahead, so the MFMA of tile m + 1 runs while tile m is scaled
+    float4v X = pv(0);
 #pragma unroll
-      for (int s = 0; s < NS; ++s) {
-        const half8 qv = qrot[s * 64 + lane];
-        const uint32_t a0 = __builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(kA, 2 * s));
-        const uint32_t a1 = __builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(kA, 2 * s + 1));
-        sa = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(cvt_lo(a0), cvt_hi(a0), cvt_lo(a1), cvt_hi(a1)),
-                                                     qv, sa, 0, 0, 0);
-        if (pair) {
-          const uint32_t b0 = __builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(kB, 2 * s));
-          const uint32_t b1 = __builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(kB, 2 * s + 1));
-          sb = __builtin_amdgcn_mfma_f32_16x16x32_f16(
-              h8(cvt_lo(b0), cvt_hi(b0), cvt_lo(b1), cvt_hi(b1)), qv, sb, 0, 0, 0);
-        }
+    for (int m = 0; m < CL; ++m) {
+      float4v Xn = X;
+      if (m + 1 < CL) Xn = pv(m + 1);
+      const _Float16 sm = sO[m >> 1][m & 1], zm = zO[m >> 1][m & 1];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        st.acc[m][i] = fmaf((float)zm, PS[i], fmaf((float)sm, X[i], st.acc[m][i]));
+      X = Xn;
+    }
+  }
+  for (int j = s_mid; j < s1; ++j) {
+    const int slot = (j - s0) & 1;
+    const int4 e = stage_at(j);
+    begin_stage(j);
+    const bool refill = j + 2 < s1;
+    const int4 e2 = refill ? stage_at(j + 2) : e;
+    const uint8_t* ra = wring + slot * STAGE;
+    // one FP8 page (score columns of page b stay empty)
+    constexpr int KW = D / 16;  // dwords of K per lane (D/4 bytes)
+    uint32_t kA[KW], vA[CL];
+    {
+      const uint4* pk = reinterpret_cast<const uint4*>(ra + ln * D + (D / 4) * lg);
+      const uint4* pv = reinterpret_cast<const uint4*>(ra + PAGE * D + (ln * 4 + lg) * 4 * CL);
+#pragma unroll
+      for (int w = 0; w < KW / 4; ++w) {
+        const uint4 x = pk[w];
+        kA[4 * w] = x.x; kA[4 * w + 1] = x.y; kA[4 * w + 2] = x.z; kA[4 * w + 3] = x.w;
       }
-      float sc[4];
-      {
-        const int vcnt = S - (col_b ? e.z : e.x) * PAGE;
-        const _Float16* gh = reinterpret_cast<const _Float16*>(&gw);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float sv = col_b ? sb[i] : sa[i];
-          sc[i] = (col_valid && 4 * lg + i < vcnt) ? sv * (float)gh[i] * smk : -INFINITY;
-        }
+      for (int w = 0; w < CL / 4; ++w) {
+        const uint4 x = pv[w];
+        vA[4 * w] = x.x; vA[4 * w + 1] = x.y; vA[4 * w + 2] = x.z; vA[4 * w + 3] = x.w;
       }
-      softmax_step<D>(st, sc, lg);
-      const half8 pT = p_operand(sc, col_b);
-      // PV: codes enter the MFMA exactly; per-channel scale folded in fp32,
-      // the zero term added by a second MFMA against the broadcast zeros
+    }
+    const float2 ksv = *reinterpret_cast<const float2*>(ra + R8);
+    wait_lgkm0();  // the stage is in registers: refill its slot
+    if (refill) issue(e2, slot);
+    float4v sa = zero4;
 #pragma unroll
-      for (int m = 0; m < CL; ++m) {
-        const uint32_t ua = __builtin_amdgcn_perm(VLUT_HI, VLUT_LO, quad_sel<NDW>(vA, m));
-        const uint32_t ub = __builtin_amdgcn_perm(VLUT_HI, VLUT_LO, quad_sel<NDW>(vB, m));
-        const float4v X = __builtin_amdgcn_mfma_f32_16x16x32_f16(
-            pT, h8(cvt_lo(ua), cvt_hi(ua), cvt_lo(ub), cvt_hi(ub)), zero4, 0, 0, 0);
-        const float sm = (float)sO[m >> 1][m & 1];
-        st.acc[m] += sm * X;
-        const _Float16 za = zA[m >> 1][m & 1], zb = zB[m >> 1][m & 1];
-        half8 zz;
+    for (int s = 0; s < NS; ++s)
+      sa = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+          h8(cvt_lo(kA[2 * s]), cvt_hi(kA[2 * s]), cvt_lo(kA[2 * s + 1]), cvt_hi(kA[2 * s + 1])),
+          qpl[s * 64 + lane], sa, 0, 0, 0);
+    float sc[4];
+    {
+      const int vcnt = col_b ? 0 : S - e.x * PAGE;
+      const float kk = ksv.x * smk;
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          zz[k] = za;
-          zz[4 + k] = zb;
-        }
-        st.acc[m] = __builtin_amdgcn_mfma_f32_16x16x32_f16(pT, zz, st.acc[m], 0, 0, 0);
-      }
-    } else {
-      // one FP8 page (score columns of page b stay empty)
-      constexpr int KW = D / 16;  // dwords of K per lane (D/4 bytes)
-      uint32_t kA[KW], vA[CL];
-      {
-        const uint4* pk = reinterpret_cast<const uint4*>(ra + ln * D + (D / 4) * lg);
-        const uint4* pv = reinterpret_cast<const uint4*>(ra + PAGE * D + (ln * 4 + lg) * 4 * CL);
+      for (int i = 0; i < 4; ++i) sc[i] = (col_valid && 4 * lg + i < vcnt) ? sa[i] * kk : -INFINITY;
+    }
+    softmax_step<D>(st, sc, lg);
+    const half8 pT = p_operand(sc, col_b);
+    const half2v z2 = {(_Float16)0.0f, (_Float16)0.0f};
 #pragma unroll
-        for (int w = 0; w < KW / 4; ++w) {
-          const uint4 x = pk[w];
-          kA[4 * w] = x.x; kA[4 * w + 1] = x.y; kA[4 * w + 2] = x.z; kA[4 * w + 3] = x.w;
-        }
-#pragma unroll
-        for (int w = 0; w < CL / 4; ++w) {
-          const uint4 x = pv[w];
-          vA[4 * w] = x.x; vA[4 * w + 1] = x.y; vA[4 * w + 2] = x.z; vA[4 * w + 3] = x.w;
-        }
-      }
-      const float2 ksv = *reinterpret_cast<const float2*>(ra + R8);
-      wait_lgkm0();  // the stage is in registers: refill its slot
-      if (refill) issue(e2, slot);
-      float4v sa = zero4;
-#pragma unroll
-      for (int s = 0; s < NS; ++s)
-        sa = __builtin_amdgcn_mfma_f32_16x16x32_f16(
-            h8(cvt_lo(kA[2 * s]), cvt_hi(kA[2 * s]), cvt_lo(kA[2 * s + 1]), cvt_hi(kA[2 * s + 1])),
-            qpl[s * 64 + lane], sa, 0, 0, 0);
-      float sc[4];
-      {
-        const int vcnt = col_b ? 0 : S - e.x * PAGE;
-        const float kk = ksv.x * smk;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) sc[i] = (col_valid && 4 * lg + i < vcnt) ? sa[i] * kk : -INFINITY;
-      }
-      softmax_step<D>(st, sc, lg);
-      const half8 pT = p_operand(sc, col_b);
-      const half2v z2 = {(_Float16)0.0f, (_Float16)0.0f};
-#pragma unroll
-      for (int m = 0; m < CL; ++m) {
-        const float4v X = __builtin_amdgcn_mfma_f32_16x16x32_f16(
-            pT, h8(cvt_lo(vA[m]), cvt_hi(vA[m]), z2, z2), zero4, 0, 0, 0);
-        st.acc[m] += ksv.y * X;
-      }
+    for (int m = 0; m < CL; ++m) {
+      const float4v X = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+          pT, h8(cvt_lo(vA[m]), cvt_hi(vA[m]), z2, z2), zero4, 0, 0, 0);
+      st.acc[m] += ksv.y * X;
     }
   }
 
@@ -728,26 +781,32 @@ hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t
   const size_t ring_b = (size_t)NW * 2 * 2 * tq3_region_bytes(P.d);
   const size_t merge_b = ((size_t)NW * P.group * P.d + 2 * NW * P.group) * sizeof(float);
   const size_t lds = qop_b + (ring_b > merge_b ? ring_b : merge_b);
-  static bool attr_set[2] = {false, false};
-  const int di = P.d == 256;
-  if (!attr_set[di]) {
-    const void* k = di ? (const void*)decode_kernel<256> : (const void*)decode_kernel<128>;
-    hipError_t e = hipFuncSetAttribute(k, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_limit());
-    if (e != hipSuccess) return e;
-    attr_set[di] = true;
-  }
   if (lds > lds_limit()) return hipErrorInvalidValue;
+  const bool pair = P.group <= 8;
+  const void* kern = P.d == 256 ? (pair ? (const void*)decode_kernel<256, true> : (const void*)decode_kernel<256, false>)
+                                : (pair ? (const void*)decode_kernel<128, true> : (const void*)decode_kernel<128, false>);
+  // the dynamic-LDS limit is raised once per kernel instance and device
+  static std::atomic<uint32_t> attr_done[64];
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  const uint32_t bit = 1u << ((P.d == 256 ? 2 : 0) + (pair ? 1 : 0));
+  if (dev < 0 || dev >= 64 || !(attr_done[dev].load() & bit)) {
+    e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_limit());
+    if (e != hipSuccess) return e;
+    if (dev >= 0 && dev < 64) attr_done[dev].fetch_or(bit);
+  }
   dim3 grid(sh.max_chunks, P.n_kv_heads, n_req);
   dim3 mgrid(P.group, P.n_kv_heads, n_req);
-  if (di) {
-    hipLaunchKernelGGL(decode_kernel<256>, grid, dim3(NT), lds, s, a);
+  void* args[] = {&a};
+  e = hipLaunchKernel(kern, grid, dim3(NT), args, lds, s);
+  if (e != hipSuccess) return e;
+  if (P.d == 256)
     hipLaunchKernelGGL(decode_merge_kernel<256>, mgrid, dim3(256), 0, s, P.group, P.n_kv_heads,
                        sh.max_chunks, a.totals, a.partials, out, lse);
-  } else {
-    hipLaunchKernelGGL(decode_kernel<128>, grid, dim3(NT), lds, s, a);
+  else
     hipLaunchKernelGGL(decode_merge_kernel<128>, mgrid, dim3(256), 0, s, P.group, P.n_kv_heads,
                        sh.max_chunks, a.totals, a.partials, out, lse);
-  }
   return hipGetLastError();
 }
 
