@@ -35,8 +35,16 @@
 
 namespace mkv {
 
-constexpr int NW = 8;                  // waves per decode workgroup
-constexpr int NT = 64 * NW;            // threads per decode workgroup
+// Workgroup shape per instance: with the paired score layout (G <= 8) 12
+// waves, each with a one-stage ring slot (a stage is moved into registers as
+// soon as it lands and the slot refilled at once); otherwise 8 waves with two
+// slots.  Either way one workgroup fills a CU's LDS.
+template <bool PAIR> struct DecodeCfg {
+  static constexpr int NW = PAIR ? 12 : 8;  // waves per workgroup
+  static constexpr int SLOTS = PAIR ? 1 : 2;  // ring slots per wave
+  static constexpr int NT = 64 * NW;
+};
+constexpr int NW_MAX = 12;
 constexpr int MAX_CHUNK_PAGES = 256;   // upper bound of C
 constexpr int MASK_LP = 0x3FFFFFFF / PAGE;  // logical page whose tokens are all masked
 
@@ -49,7 +57,6 @@ struct DecodeArgs {
   const int32_t* seq_lens;
   float* out;
   float* lse;
-  int32_t* totals;
   float* partials;
   int cpages, max_chunks;
   float sm_log2;  // log2(e) / sqrt(d)
@@ -72,13 +79,13 @@ DecodeShape decode_shape(int n_req, int max_pages, int n_kv_heads, int recent) {
   return s;
 }
 
-// workspace: int32 chunk count per request, then the partials
-static size_t header_bytes(int n_req) { return (((size_t)n_req * 4) + 255) / 256 * 256; }
+// workspace: the partials, one (O_j[G][d], m_j[G], l_j[G]) block per chunk
+// slot; every slot of the grid is written on every call (l_j = 0 when the
+// chunk is empty or past the request's end), so the merge needs no count
 
 size_t decode_ws_bytes(int n_req, int max_pages, int n_kv_heads, int group, int d, int recent) {
   DecodeShape s = decode_shape(n_req, max_pages, n_kv_heads, recent);
-  return header_bytes(n_req) +
-         (size_t)n_req * n_kv_heads * s.max_chunks * group * (d + 2) * sizeof(float);
+  return (size_t)n_req * n_kv_heads * s.max_chunks * group * (d + 2) * sizeof(float);
 }
 
 __device__ __forceinline__ half8 h8(half2v a, half2v b, half2v c, half2v d) {
@@ -176,6 +183,57 @@ __device__ __forceinline__ void wait_lgkm0() {
   __asm__ __volatile__("" ::: "memory");
 }
 
+// Cross-lane exchanges on the VALU (gfx950 permlane swaps).  With both operands
+// x, v_permlane16_swap yields (rows 0,0,2,2 ; rows 1,1,3,3) of x (a row is 16
+// lanes) and v_permlane32_swap yields (low half twice ; high half twice).
+__device__ __forceinline__ uint2 swap16(float x) {
+  const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return make_uint2(p[0], p[1]);
+}
+__device__ __forceinline__ uint2 swap32(float x) {
+  const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return make_uint2(p[0], p[1]);
+}
+// max / sum over the four lanes l, l ^ 16, l ^ 32, l ^ 48
+__device__ __forceinline__ float max4rows(float x) {
+  uint2 p = swap16(x);
+  x = fmaxf(__uint_as_float(p.x), __uint_as_float(p.y));
+  p = swap32(x);
+  return fmaxf(__uint_as_float(p.x), __uint_as_float(p.y));
+}
+__device__ __forceinline__ float sum4rows(float x) {
+  uint2 p = swap16(x);
+  x = __uint_as_float(p.x) + __uint_as_float(p.y);
+  p = swap32(x);
+  return __uint_as_float(p.x) + __uint_as_float(p.y);
+}
+// value of lane l ^ M, on the VALU: DPP within rows (quad_perm for 1 and 2,
+// half-row mirror then quad reverse for 4, row rotate by 8 for 8) and the
+// permlane swaps across rows
+template <int M>
+__device__ __forceinline__ float lane_xor(float x, int lane) {
+  const int xi = __float_as_int(x);
+  if constexpr (M == 1) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(xi, 0xB1, 0xF, 0xF, false));
+  } else if constexpr (M == 2) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(xi, 0x4E, 0xF, 0xF, false));
+  } else if constexpr (M == 4) {
+    const int t = __builtin_amdgcn_mov_dpp(xi, 0x141, 0xF, 0xF, false);
+    return __int_as_float(__builtin_amdgcn_mov_dpp(t, 0x1B, 0xF, 0xF, false));
+  } else if constexpr (M == 8) {
+    return __int_as_float(__builtin_amdgcn_mov_dpp(xi, 0x128, 0xF, 0xF, false));
+  } else if constexpr (M == 16) {
+    const uint2 p = swap16(x);
+    return __uint_as_float((lane & 16) ? p.x : p.y);
+  } else {
+    static_assert(M == 32, "lane_xor: M is a power of two below 64");
+    const uint2 p = swap32(x);
+    return __uint_as_float((lane & 32) ? p.x : p.y);
+  }
+}
+// value of lane l + 32 (valid in lanes l < 32)
+__device__ __forceinline__ float upper_half(float x) { return __uint_as_float(swap32(x).y); }
+
 template <int D>
 struct WaveState {
   float4v acc[D / 16];  // rows (page parity, head) x channels, see below
@@ -189,9 +247,7 @@ struct WaveState {
 // are fetched from those lanes when the reference max moves.
 template <int D>
 __device__ __forceinline__ void softmax_step(WaveState<D>& st, float* sc, int lg) {
-  float mx = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
-  mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-  mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+  const float mx = max4rows(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])));
   // lazy rescale: keep the reference max while new scores stay within 2^8
   const bool need = mx > st.m_run + 8.0f;
   if (__any(need)) {
@@ -231,7 +287,9 @@ __device__ __forceinline__ half8 p_operand(const float* p, bool row_is_b) {
 // PAIR (query group of at most 8 heads): two pages share one score tile,
 // columns [0, 8) scoring page a and [8, 16) page b.
 template <int D, bool PAIR>
-__global__ __launch_bounds__(NT, 1) void decode_kernel(DecodeArgs a) {
+__global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeArgs a) {
+  constexpr int NW = DecodeCfg<PAIR>::NW, NT = DecodeCfg<PAIR>::NT, SLOTS = DecodeCfg<PAIR>::SLOTS;
+  constexpr int NCH = PAIR ? 8 : 16;  // query heads a score tile holds
   constexpr int CL = D / 16, NDW = 3 * D / 128, CB = 3 * D / 32, NS = D / 32, QV = D / 64;
   constexpr int R3 = (int)tq3_region_bytes(D);  // K codes, V codes, gamma, V scale, V zero
   constexpr int R8 = (int)fp8_region_bytes(D);  // K codes then V codes
@@ -253,7 +311,7 @@ __global__ __launch_bounds__(NT, 1) void decode_kernel(DecodeArgs a) {
   half8* qpl = qrot + NS * 64;
   uint8_t* ring = smem + 2 * NS * 64 * 16;
 
-  // ---- 1. queries: wave w owns query head w (and w + 8 when G > 8); lane l
+  // ---- 1. queries: wave w owns query heads w and w + NW below NCH; lane l
   // holds channels QV l .. QV l + QV - 1.  The loads go out before anything
   // else so their latency hides behind the page-table loads.
   static_assert(QV == 2 || QV == 4, "QV bf16 channels per lane form one 4- or 8-byte load");
@@ -262,7 +320,7 @@ __global__ __launch_bounds__(NT, 1) void decode_kernel(DecodeArgs a) {
   int sg[QV];
 #pragma unroll
   for (int ps = 0; ps < 2; ++ps) {
-    const int n = wid + 8 * ps;
+    const int n = wid + NW * ps;
     const int nn = n < G ? n : G - 1;  // loads stay in bounds; values of n >= G are dropped
     const qvec raw = *reinterpret_cast<const qvec*>(a.q + ((int64_t)r * Hq + h * G + nn) * D + QV * lane);
     const uint16_t* rh = reinterpret_cast<const uint16_t*>(&raw);
@@ -272,16 +330,11 @@ __global__ __launch_bounds__(NT, 1) void decode_kernel(DecodeArgs a) {
 #pragma unroll
   for (int i = 0; i < QV; ++i) sg[i] = P.sigma[QV * lane + i];
 
+  float* part = a.partials + (((int64_t)r * H + h) * a.max_chunks + chunk) * G * (D + 2);
   const int S = a.seq_lens[r];
   if (S < 1 || S > mp * PAGE) {
-    if (chunk == 0) {
-      for (int i = tid; i < G * D; i += NT) a.out[((int64_t)r * Hq + h * G) * D + i] = 0.0f;
-      if (a.lse && tid < G) a.lse[(int64_t)r * Hq + h * G + tid] = -INFINITY;
-      if (tid == 0 && h == 0) {
-        atomicOr(&P.ctrl[CTRL_ERR], (int)MKV_DEVERR_RANGE);
-        a.totals[r] = 0;
-      }
-    }
+    if (chunk == 0 && h == 0 && tid == 0) atomicOr(&P.ctrl[CTRL_ERR], (int)MKV_DEVERR_RANGE);
+    if (tid < G) part[G * D + G + tid] = 0.0f;  // empty partial: the merge writes zeros
     return;
   }
   // ---- chunk -> logical page range
@@ -289,8 +342,10 @@ __global__ __launch_bounds__(NT, 1) void decode_kernel(DecodeArgs a) {
   const int n_old = S > P.recent ? (S - P.recent) / PAGE : 0;  // pages wholly outside the window
   const int C = a.cpages, CR = a.cpages / 2;
   const int nco = (n_old + C - 1) / C, ncr = (np - n_old + CR - 1) / CR;
-  if (chunk == 0 && h == 0 && tid == 0) a.totals[r] = nco + ncr;
-  if (chunk >= nco + ncr) return;
+  if (chunk >= nco + ncr) {
+    if (tid < G) part[G * D + G + tid] = 0.0f;  // slot past the request's end
+    return;
+  }
   const int p0 = chunk < nco ? chunk * C : n_old + (chunk - nco) * CR;
   const int p1 = chunk < nco ? min(p0 + C, n_old) : min(p0 + CR, np);
   const int n_pg = p1 - p0;
@@ -367,7 +422,7 @@ __global__ __launch_bounds__(NT, 1) void decode_kernel(DecodeArgs a) {
   const uint8_t* tq3_l = P.tq3 + (int64_t)layer * P.n_tq3 * H * R3;
   const uint8_t* fp8_l = P.fp8 + (int64_t)layer * P.n_fp8 * H * R8;
   const uint8_t* scl_l = reinterpret_cast<const uint8_t*>(P.fp8_scales + (int64_t)layer * P.n_fp8 * H * 2);
-  uint8_t* wring = ring + wid * 2 * STAGE;
+  uint8_t* wring = ring + wid * SLOTS * STAGE;
   const uint32_t wring_lds = __builtin_amdgcn_readfirstlane(
       (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)wring);
   auto stage_at = [&](int j) {
@@ -386,8 +441,9 @@ __global__ __launch_bounds__(NT, 1) void decode_kernel(DecodeArgs a) {
       if (lane < 2) dma4(4 * lane, scl_l + ((int64_t)e.y * H + h) * 8, dst + R8);
     }
   };
-  if (s0 < s1) issue(stage_at(s0), 0);
-  if (s0 + 1 < s1) issue(stage_at(s0 + 1), 1);
+#pragma unroll
+  for (int k = 0; k < SLOTS; ++k)
+    if (s0 + k < s1) issue(stage_at(s0 + k), k);
 
   // ---- query operands, built while the first stages are in flight, in MFMA
   // lane order: q?[s][lane] holds channels (D/4) lg + 8 s + j, j < 8, of
@@ -398,8 +454,8 @@ __global__ __launch_bounds__(NT, 1) void decode_kernel(DecodeArgs a) {
     const float qscale = rsqrtf((float)D);  // R = d^-1/2 H diag(sigma)
 #pragma unroll
     for (int ps = 0; ps < 2; ++ps) {
-      const int n = wid + 8 * ps;
-      if (ps == 1 && pair) break;
+      const int n = wid + NW * ps;
+      if (n >= NCH) break;  // wave-uniform
       float xr[QV];
 #pragma unroll
       for (int i = 0; i < QV; ++i) xr[i] = qx[ps][i] * (float)sg[i];
@@ -414,15 +470,18 @@ __global__ __launch_bounds__(NT, 1) void decode_kernel(DecodeArgs a) {
             xr[i] = x0 + x1;
             xr[i + st] = x0 - x1;
           }
+      auto stage = [&](auto mc) {
+        constexpr int m = decltype(mc)::value;
+        const float sg_m = (lane & m) ? -1.0f : 1.0f;  // this lane holds the upper element
 #pragma unroll
-      for (int m = 1; m < 64; m <<= 1) {
-        const bool hi = lane & m;
-#pragma unroll
-        for (int i = 0; i < QV; ++i) {
-          const float y = __shfl_xor(xr[i], m, 64);
-          xr[i] = hi ? y - xr[i] : xr[i] + y;
-        }
-      }
+        for (int i = 0; i < QV; ++i) xr[i] = fmaf(sg_m, xr[i], lane_xor<m>(xr[i], lane));
+      };
+      stage(std::integral_constant<int, 1>{});
+      stage(std::integral_constant<int, 2>{});
+      stage(std::integral_constant<int, 4>{});
+      stage(std::integral_constant<int, 8>{});
+      stage(std::integral_constant<int, 16>{});
+      stage(std::integral_constant<int, 32>{});
 #pragma unroll
       for (int i = 0; i < QV; ++i) {
         const int c = QV * lane + i;
@@ -441,13 +500,10 @@ __global__ __launch_bounds__(NT, 1) void decode_kernel(DecodeArgs a) {
   }
 
   __syncthreads();  // query operands visible to every wave
-  half8 qreg[NS];  // rotated-query operand of this lane, kept in registers
-#pragma unroll
-  for (int s = 0; s < NS; ++s) qreg[s] = qrot[s * 64 + lane];
-  // Wait for stage j to land in its slot; stage j + 1 may stay in flight (the
-  // allowed count is the number of copies stage j + 1 was issued as).
+  // Wait for stage j to land in its slot; with two slots stage j + 1 may stay
+  // in flight (the allowed count is the number of copies it was issued as).
   auto begin_stage = [&](int j) {
-    const int nops = j + 1 < s1 ? (stage_at(j + 1).w >= 0 ? (pair ? 2 : 1) * OPS3 : OPS8) : 0;
+    const int nops = (SLOTS > 1 && j + 1 < s1) ? (stage_at(j + 1).w >= 0 ? (pair ? 2 : 1) * OPS3 : OPS8) : 0;
     if (nops == 2 * OPS3)
       wait_vmcnt<2 * OPS3>();
     else if (nops == OPS8)
@@ -461,11 +517,11 @@ __global__ __launch_bounds__(NT, 1) void decode_kernel(DecodeArgs a) {
   // share the ring (a copy in flight may belong to either format).
   const int s_mid = max(s0, min(s1, st3));
   for (int j = s0; j < s_mid; ++j) {
-    const int slot = (j - s0) & 1;
+    const int slot = (j - s0) % SLOTS;
     const int4 e = stage_at(j);
     begin_stage(j);
-    const bool refill = j + 2 < s1;
-    const int4 e2 = refill ? stage_at(j + 2) : e;
+    const bool refill = j + SLOTS < s1;
+    const int4 e2 = refill ? stage_at(j + SLOTS) : e;
     const uint8_t* ra = wring + slot * STAGE;
     // TQ3 pair (page b absent: same page, every token masked)
     const uint8_t* rb = pair ? ra + R3 : ra;
@@ -492,7 +548,7 @@ __global__ __launch_bounds__(NT, 1) void decode_kernel(DecodeArgs a) {
     float4v sa = zero4, sb = zero4;
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      const half8 qv = qreg[s];
+      const half8 qv = qrot[s * 64 + lane];
       const uint32_t a0 = __builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(kA, 2 * s));
       const uint32_t a1 = __builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(kA, 2 * s + 1));
       sa = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(cvt_lo(a0), cvt_hi(a0), cvt_lo(a1), cvt_hi(a1)),
@@ -541,11 +597,11 @@ __global__ __launch_bounds__(NT, 1) void decode_kernel(DecodeArgs a) {
     }
   }
   for (int j = s_mid; j < s1; ++j) {
-    const int slot = (j - s0) & 1;
+    const int slot = (j - s0) % SLOTS;
     const int4 e = stage_at(j);
     begin_stage(j);
-    const bool refill = j + 2 < s1;
-    const int4 e2 = refill ? stage_at(j + 2) : e;
+    const bool refill = j + SLOTS < s1;
+    const int4 e2 = refill ? stage_at(j + SLOTS) : e;
     const uint8_t* ra = wring + slot * STAGE;
     // one FP8 page (score columns of page b stay empty)
     constexpr int KW = D / 16;  // dwords of K per lane (D/4 bytes)
@@ -594,9 +650,7 @@ __global__ __launch_bounds__(NT, 1) void decode_kernel(DecodeArgs a) {
   // ---- 4. rows -> heads: fetch each accumulator row's (m, l); merge the two
   // page parities (rows h and h + 8 sit in lanes l and l ^ 32); then merge the
   // eight waves in LDS into one (m_j, l_j, O_j) partial per chunk
-  float l_col = st.l_run;
-  l_col += __shfl_xor(l_col, 16, 64);
-  l_col += __shfl_xor(l_col, 32, 64);
+  const float l_col = sum4rows(st.l_run);
   float mrow[4], lrow[4];
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -606,30 +660,37 @@ __global__ __launch_bounds__(NT, 1) void decode_kernel(DecodeArgs a) {
   if (pair) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const float m2 = __shfl_xor(mrow[i], 32, 64), l2 = __shfl_xor(lrow[i], 32, 64);
+      // rows of page b sit in lanes l + 32; only lanes l < 32 keep the result
+      const float m2 = upper_half(mrow[i]), l2 = upper_half(lrow[i]);
       const float M = fmaxf(lrow[i] > 0.0f ? mrow[i] : -INFINITY, l2 > 0.0f ? m2 : -INFINITY);
       const float f1 = lrow[i] > 0.0f ? exp2f(mrow[i] - M) : 0.0f;
       const float f2 = l2 > 0.0f ? exp2f(m2 - M) : 0.0f;
 #pragma unroll
       for (int m = 0; m < CL; ++m) {
-        const float o2 = __shfl_xor(st.acc[m][i], 32, 64);
+        const float o2 = upper_half(st.acc[m][i]);
         st.acc[m][i] = f1 * st.acc[m][i] + f2 * o2;
       }
       lrow[i] = f1 * lrow[i] + f2 * l2;
       mrow[i] = M;
     }
   }
+  // macc row (wave, head) keeps channel c = CL ln + 4 k + t at position
+  // (16 k + ln) 4 + t: every lane stores float4s and the 16 lanes of a row
+  // store consecutive 16-byte words (no bank conflicts)
   float* macc = reinterpret_cast<float*>(ring);  // [NW][G][D]
   float* mm = macc + NW * G * D;                 // [NW][G]
-  float* ml = mm + NW * G;                       // [NW][G]
+  float* ml = mm + NW * G;                       // [NW][G], then fw [NW][G]
   __syncthreads();  // every wave is done with its ring (all copies waited for)
   if (!row_b) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int head = 4 * lg + i;
       if (head < G) {
+        float4* row = reinterpret_cast<float4*>(macc + (wid * G + head) * D);
 #pragma unroll
-        for (int m = 0; m < CL; ++m) macc[(wid * G + head) * D + CL * ln + m] = st.acc[m][i];
+        for (int k = 0; k < CL / 4; ++k)
+          row[16 * k + ln] = make_float4(st.acc[4 * k][i], st.acc[4 * k + 1][i], st.acc[4 * k + 2][i],
+                                         st.acc[4 * k + 3][i]);
         if (ln == 0) {
           mm[wid * G + head] = mrow[i];
           ml[wid * G + head] = lrow[i];
@@ -638,121 +699,97 @@ __global__ __launch_bounds__(NT, 1) void decode_kernel(DecodeArgs a) {
     }
   }
   __syncthreads();
-  float* part = a.partials + (((int64_t)r * H + h) * a.max_chunks + chunk) * G * (D + 2);
-  for (int i = tid; i < G * D; i += NT) {
-    const int n = i / D;
+  // per-head combine weights of the waves, then O_j = sum_w f_w O_w with
+  // f_w = 2^(m_w - M) / L (rows with l_w = 0 take no part)
+  float* fw = ml + NW * G;  // [NW][G]
+  if (tid < G) {
     float M = -INFINITY;
 #pragma unroll
     for (int w = 0; w < NW; ++w)
-      if (ml[w * G + n] > 0.0f) M = fmaxf(M, mm[w * G + n]);
-    float L = 0.0f, O = 0.0f;
+      if (ml[w * G + tid] > 0.0f) M = fmaxf(M, mm[w * G + tid]);
+    float L = 0.0f;
 #pragma unroll
     for (int w = 0; w < NW; ++w) {
-      const float lw = ml[w * G + n];
-      if (lw > 0.0f) {
-        const float f = exp2f(mm[w * G + n] - M);
-        L += f * lw;
-        O += f * macc[(w * G + n) * D + (i % D)];
-      }
+      const float lw = ml[w * G + tid];
+      const float f = lw > 0.0f ? exp2f(mm[w * G + tid] - M) : 0.0f;
+      fw[w * G + tid] = f;
+      L += f * lw;
     }
-    part[i] = L > 0.0f ? O / L : 0.0f;
-    if (i % D == 0) {
-      part[G * D + n] = M;
-      part[G * D + G + n] = L;
+    const float inv = L > 0.0f ? 1.0f / L : 0.0f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) fw[w * G + tid] *= inv;
+    part[G * D + tid] = M;
+    part[G * D + G + tid] = L;
+  }
+  __syncthreads();
+  // four consecutive positions of a macc row are four consecutive channels
+  for (int it = tid; it < G * D / 4; it += NT) {
+    const int n = it / (D / 4), pos = 4 * (it % (D / 4));
+    const int c = CL * ((pos >> 2) & 15) + 4 * (pos >> 6);
+    float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const float f = fw[w * G + n];
+      const float4 x = *reinterpret_cast<const float4*>(macc + (w * G + n) * D + pos);
+      o.x += f * x.x;
+      o.y += f * x.y;
+      o.z += f * x.z;
+      o.w += f * x.w;
     }
+    *reinterpret_cast<float4*>(part + n * D + c) = o;
   }
 }
 
-// Merge stage (Eq. softmax-merge): one workgroup per (request, KV head, query
-// head of the group).  The chunk partials' (m_j, l_j) go to LDS; each of the 4
-// waves then folds a quarter of the partials' normalized outputs, four
-// channels per lane with 16-byte loads, and the waves combine in LDS.
+// Merge stage (Eq. softmax-merge): one workgroup per (query head of the
+// group, KV head, request), one thread per channel.  Every chunk slot's
+// (m_j, l_j, O_j[c]) is loaded in batches of 16 (all loads of a batch in
+// flight together; slots with l_j = 0 contribute nothing) and folded into a
+// running (M, L, O) that is rescaled once per batch.
 template <int D>
-__global__ __launch_bounds__(256) void decode_merge_kernel(int G, int H, int max_chunks,
-                                                           const int32_t* totals,
-                                                           const float* partials, float* out,
-                                                           float* lse) {
-  constexpr int C4 = D / 4;  // float4 lanes per row
-  __shared__ float s_w[1024];
-  __shared__ float4 s_acc[4][C4];
-  __shared__ float s_red[8];
-  const int n = blockIdx.x, h = blockIdx.y, r = blockIdx.z;
-  const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+__global__ __launch_bounds__(D) void decode_merge_kernel(int G, int H, int max_chunks,
+                                                        const float* partials, float* out,
+                                                        float* lse) {
+  constexpr int B = 16;
+  const int n = blockIdx.x, h = blockIdx.y, r = blockIdx.z, c = threadIdx.x;
   const int Hq = H * G;
-  const int total = min(totals[r], max_chunks);
-  float* o = out + ((int64_t)r * Hq + h * G + n) * D;
-  if (total <= 0) {
-    for (int c = tid; c < D; c += 256) o[c] = 0.0f;
-    if (lse && tid == 0) lse[(int64_t)r * Hq + h * G + n] = -INFINITY;
-    return;
-  }
-  const float* base = partials + ((int64_t)r * H + h) * max_chunks * G * (D + 2);
   const int stride = G * (D + 2);
-  // max over the partials' m_j (empty partials have l_j = 0)
-  float M = -INFINITY;
-  for (int k = tid; k < total; k += 256) {
-    const float* pk = base + (int64_t)k * stride;
-    const float lk = pk[G * D + G + n];
-    if (lk > 0.0f) M = fmaxf(M, pk[G * D + n]);
-  }
+  const float* base = partials + ((int64_t)r * H + h) * max_chunks * stride;
+  float M = -INFINITY, L = 0.0f, O = 0.0f;
+  for (int k0 = 0; k0 < max_chunks; k0 += B) {
+    float mk[B], lk[B], ok[B];
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1) M = fmaxf(M, __shfl_xor(M, off, 64));
-  if (lane == 0) s_red[wid] = M;
-  __syncthreads();
-  M = fmaxf(fmaxf(s_red[0], s_red[1]), fmaxf(s_red[2], s_red[3]));
-  __syncthreads();
-  float L = 0.0f;
-  for (int k0 = 0; k0 < total; k0 += 1024) {
-    for (int k = k0 + tid; k < min(total, k0 + 1024); k += 256) {
+    for (int j = 0; j < B; ++j) {
+      const int k = min(k0 + j, max_chunks - 1);
       const float* pk = base + (int64_t)k * stride;
-      const float lk = pk[G * D + G + n];
-      const float wk = lk > 0.0f ? exp2f(pk[G * D + n] - M) * lk : 0.0f;
-      s_w[k - k0] = wk;
-      L += wk;
+      mk[j] = pk[G * D + n];
+      lk[j] = k0 + j < max_chunks ? pk[G * D + G + n] : 0.0f;
+      ok[j] = pk[n * D + c];
     }
-    __syncthreads();
-    if (lane < C4) {
-      float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-      const int kend = min(total, k0 + 1024);
-#pragma unroll 8
-      for (int k = k0 + wid; k < kend; k += 4) {
-        const float wk = s_w[k - k0];
-        const float4 v = *reinterpret_cast<const float4*>(base + (int64_t)k * stride + n * D + 4 * lane);
-        acc.x += wk * v.x;
-        acc.y += wk * v.y;
-        acc.z += wk * v.z;
-        acc.w += wk * v.w;
-      }
-      if (k0 == 0) s_acc[wid][lane] = acc;
-      else {
-        s_acc[wid][lane].x += acc.x; s_acc[wid][lane].y += acc.y;
-        s_acc[wid][lane].z += acc.z; s_acc[wid][lane].w += acc.w;
-      }
-    }
-    __syncthreads();
-  }
+    float Mb = M;
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1) L += __shfl_xor(L, off, 64);
-  if (lane == 0) s_red[4 + wid] = L;
-  __syncthreads();
-  L = s_red[4] + s_red[5] + s_red[6] + s_red[7];
-  const float inv = 1.0f / L;
-  if (tid < C4) {
-    float4 t = s_acc[0][tid];
+    for (int j = 0; j < B; ++j)
+      if (lk[j] > 0.0f) Mb = fmaxf(Mb, mk[j]);
+    if (Mb == -INFINITY) continue;  // nothing in this batch, nothing before it
+    const float f = M == -INFINITY ? 0.0f : exp2f(M - Mb);
+    L *= f;
+    O *= f;
 #pragma unroll
-    for (int w = 1; w < 4; ++w) {
-      t.x += s_acc[w][tid].x; t.y += s_acc[w][tid].y;
-      t.z += s_acc[w][tid].z; t.w += s_acc[w][tid].w;
-    }
-    t.x *= inv; t.y *= inv; t.z *= inv; t.w *= inv;
-    *reinterpret_cast<float4*>(o + 4 * tid) = t;
+    for (int j = 0; j < B; ++j)
+      if (lk[j] > 0.0f) {
+        const float w = exp2f(mk[j] - Mb) * lk[j];
+        L += w;
+        O += w * ok[j];
+      }
+    M = Mb;
   }
-  if (lse && tid == 0) lse[(int64_t)r * Hq + h * G + n] = (M + log2f(L)) * 0.69314718055994531f;
+  const int64_t row = (int64_t)r * Hq + h * G + n;
+  out[row * D + c] = L > 0.0f ? O / L : 0.0f;
+  if (lse && c == 0) lse[row] = L > 0.0f ? (M + log2f(L)) * 0.69314718055994531f : -INFINITY;
 }
 
 // dynamic LDS a decode workgroup may use: 160 KiB per CU minus the static arrays
 static constexpr size_t lds_limit() {
-  return 160 * 1024 - sizeof(int4) * MAX_CHUNK_PAGES - sizeof(int) * 2 * NW - 256;
+  return 160 * 1024 - sizeof(int4) * MAX_CHUNK_PAGES - sizeof(int) * 2 * NW_MAX - 256;
 }
 
 hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t* q,
@@ -771,18 +808,19 @@ hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t
   a.seq_lens = seq_lens;
   a.out = out;
   a.lse = lse;
-  a.totals = reinterpret_cast<int32_t*>(ws);
-  a.partials = reinterpret_cast<float*>(reinterpret_cast<uint8_t*>(ws) + header_bytes(n_req));
+  a.partials = reinterpret_cast<float*>(ws);
   a.cpages = sh.cpages;
   a.max_chunks = sh.max_chunks;
   a.sm_log2 = 1.4426950408889634f / sqrtf((float)P.d);
   // dynamic LDS: two query operands, then the page ring (reused by the wave merge)
+  const bool pair = P.group <= 8;
+  const int nw = pair ? DecodeCfg<true>::NW : DecodeCfg<false>::NW;
+  const int slots = pair ? DecodeCfg<true>::SLOTS : DecodeCfg<false>::SLOTS;
   const size_t qop_b = 2 * (size_t)(P.d / 32) * 64 * 16;
-  const size_t ring_b = (size_t)NW * 2 * 2 * tq3_region_bytes(P.d);
-  const size_t merge_b = ((size_t)NW * P.group * P.d + 2 * NW * P.group) * sizeof(float);
+  const size_t ring_b = (size_t)nw * slots * 2 * tq3_region_bytes(P.d);
+  const size_t merge_b = ((size_t)nw * P.group * P.d + 3 * nw * P.group) * sizeof(float);
   const size_t lds = qop_b + (ring_b > merge_b ? ring_b : merge_b);
   if (lds > lds_limit()) return hipErrorInvalidValue;
-  const bool pair = P.group <= 8;
   const void* kern = P.d == 256 ? (pair ? (const void*)decode_kernel<256, true> : (const void*)decode_kernel<256, false>)
                                 : (pair ? (const void*)decode_kernel<128, true> : (const void*)decode_kernel<128, false>);
   // the dynamic-LDS limit is raised once per kernel instance and device
@@ -799,14 +837,14 @@ hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t
   dim3 grid(sh.max_chunks, P.n_kv_heads, n_req);
   dim3 mgrid(P.group, P.n_kv_heads, n_req);
   void* args[] = {&a};
-  e = hipLaunchKernel(kern, grid, dim3(NT), args, lds, s);
+  e = hipLaunchKernel(kern, grid, dim3(64 * nw), args, lds, s);
   if (e != hipSuccess) return e;
   if (P.d == 256)
     hipLaunchKernelGGL(decode_merge_kernel<256>, mgrid, dim3(256), 0, s, P.group, P.n_kv_heads,
-                       sh.max_chunks, a.totals, a.partials, out, lse);
+                       sh.max_chunks, a.partials, out, lse);
   else
-    hipLaunchKernelGGL(decode_merge_kernel<128>, mgrid, dim3(256), 0, s, P.group, P.n_kv_heads,
-                       sh.max_chunks, a.totals, a.partials, out, lse);
+    hipLaunchKernelGGL(decode_merge_kernel<128>, mgrid, dim3(128), 0, s, P.group, P.n_kv_heads,
+                       sh.max_chunks, a.partials, out, lse);
   return hipGetLastError();
 }
 
