@@ -20,6 +20,7 @@ from __future__ import annotations
 
 import argparse
 import concurrent.futures as cf
+import hashlib
 import json
 import os
 import sys
@@ -49,6 +50,34 @@ def kv_bytes_of(tags_row: np.ndarray, seq_len: int, d: int, n_kv_heads: int) -> 
         else:
             tot += 2 * b * d + 8
     return tot * n_kv_heads
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_kernel_long_pair_2x59008_hbm_traffic.txt")
+DECODE_SOURCES = [os.path.join(ROOT, "paper_2608_23834_amd", "csrc", f)
+                  for f in ("mkv_decode.hip", "mkv_device.h")]
+
+
+def decode_source_hash() -> str:
+    h = hashlib.sha256()
+    for f in DECODE_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic(workload_name: str):
+    """HBM bytes per decode launch from the committed rocprofv3 FETCH_SIZE /
+    WRITE_SIZE summary (copy-calibrated), or None when that summary was taken
+    on other decode sources or another workload."""
+    try:
+        with open(TRAFFIC_FILE) as fh:
+            kv = dict(line.split(":", 1) for line in fh if ":" in line and not line.startswith(" "))
+    except OSError:
+        return None
+    kv = {k.strip(): v.strip() for k, v in kv.items()}
+    if kv.get("decode_sources_sha256") != decode_source_hash() or kv.get("workload") != workload_name:
+        return None
+    return int(kv["hbm_bytes_per_launch"])
 
 
 def build_state(w, n_layers, extra_tokens, mk, torch):
@@ -196,14 +225,10 @@ def main():
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(n_ev)]
 
-    def step(s, events=None):
+    def step(s):
         for l in range(n_layers):
             mk.kv_append_fp8(pool, l, bt, tags, seq_before[s], cu1, nk[l, s], nv[l, s])
-            if events is not None:
-                events[l][0].record(stream)
             mk.paged_attn_decode(pool, l, q_all[l], bt, tags, seq_after[s], out, None, ws)
-            if events is not None:
-                events[l][1].record(stream)
         mk.kv_migrate_to_tq3(pool, bt, tags, am, seq_after[s])
 
     for s in range(args.warmup):
@@ -221,11 +246,27 @@ def main():
     torch.cuda.synchronize()
     total_ms = t0.elapsed_time(t1)
     tags_mid = tags.cpu().numpy()
-    # pass B: the same steps again with events around every decode call
+    # pass B: the same steps again with HIP events around every decode call;
+    # the library's own events (same stream) time the split-scan and merge
+    # kernels of each step's last decode call, read once the step is queued
+    mk.paged_attn_set_timing(pool, True)
+    scan_us, merge_us = [], []
     for i, s in enumerate(range(args.warmup + args.steps, n_steps)):
-        step(s, ev[i * n_layers:(i + 1) * n_layers])
+        evs = ev[i * n_layers:(i + 1) * n_layers]
+        for l in range(n_layers):
+            mk.kv_append_fp8(pool, l, bt, tags, seq_before[s], cu1, nk[l, s], nv[l, s])
+            evs[l][0].record(stream)
+            mk.paged_attn_decode(pool, l, q_all[l], bt, tags, seq_after[s], out, None, ws)
+            evs[l][1].record(stream)
+        a_us, m_us = mk.paged_attn_last_times(pool)
+        scan_us.append(a_us)
+        merge_us.append(m_us)
+        mk.kv_migrate_to_tq3(pool, bt, tags, am, seq_after[s])
     torch.cuda.synchronize()
+    mk.paged_attn_set_timing(pool, False)
     dec_ms = np.array([a.elapsed_time(b) for a, b in ev])
+    scan_us = np.array(scan_us)
+    merge_us = np.array(merge_us)
     err = mk.kv_pool_check_errors(pool)
     if err:
         raise RuntimeError(f"device error word {err:#x} during the benchmark")
@@ -236,7 +277,9 @@ def main():
     kvb1 = sum(kv_bytes_of(tags_end[r], sl1[r], d, Hkv) for r in range(n_req))
     kv_bytes = 0.5 * (kvb0 + kvb1)
     dec_us = float(dec_ms.mean() * 1e3)
-    achieved = kv_bytes / (dec_us * 1e-6)
+    scan_mean = float(scan_us.mean())
+    achieved = kv_bytes / (scan_mean * 1e-6)
+    traffic = measured_traffic(w.name)
     ms_per_step = total_ms / args.steps
     counters = mk.kv_pool_counters(pool)
 
@@ -258,14 +301,16 @@ def main():
                    "recent_tokens": w.recent, "kv_formats": "fp8-e4m3 (R,A) + tq3 (S)",
                    "step": "per layer: append 1 token/request + decode; then migrate"},
         "decode_attn_us_per_layer": round(dec_us, 3),
-        "decode_timing": "HIP events around each paged_attn_decode call (scan + merge "
-                         "kernels) in a second pass of the same steps",
-        "decode_attn_us_p50": round(float(np.median(dec_ms) * 1e3), 3),
+        "decode_scan_us": round(scan_mean, 3),
+        "decode_merge_us": round(float(merge_us.mean()), 3),
+        "decode_timing": "second pass of the same steps: HIP events around each "
+                         "paged_attn_decode call; the library's events (same stream) around "
+                         "the split-scan and merge kernels of each step's last call",
         "kv_bytes_per_layer": int(kv_bytes),
-        "effective_kv_gb_per_s": round(achieved / 1e9, 1),
+        "effective_kv_gb_per_s": round(kv_bytes / (dec_us * 1e-6) / 1e9, 1),
         "roofline": {"bound": "hbm", "achieved": round(achieved / 1e9, 1), "peak": HBM_PEAK / 1e9,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK, 4), "traffic": None,
-                     "kernel": "decode_kernel<256>"},
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK, 4), "traffic": traffic,
+                     "kernel": "decode_kernel<256, true> (split scan, one launch per layer)"},
         "counters": {k: int(v) for k, v in counters.items()},
         "setup_s": round(setup_s, 1),
     }

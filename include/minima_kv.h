@@ -217,6 +217,16 @@ mkv_status kv_pool_read_free_lists(mkv_pool* pool, int32_t* fp8_ids, int32_t* n_
 /* Route / fallback / dense-shadow / physical-byte counters (synchronizes). */
 mkv_status kv_pool_counters(mkv_pool* pool, mkv_counters* out);
 
+/* Kernel timing for measurement tools; correct use never needs it.  When
+ * enabled, each paged_attn_decode call on this pool records HIP events on its
+ * stream before and after its split-scan kernel and after its merge kernel.
+ * paged_attn_last_times waits for the last call's events and returns the
+ * durations of the scan and of the merge in microseconds (MKV_ESTATE when
+ * timing is off or no call was timed).  Enabling creates the events on the
+ * current device; the pool owns them. */
+mkv_status paged_attn_set_timing(mkv_pool* pool, int32_t enable);
+mkv_status paged_attn_last_times(mkv_pool* pool, float* scan_us, float* merge_us);
+
 /* Read (and optionally clear) the device error word; synchronizes. */
 mkv_status kv_pool_check_errors(mkv_pool* pool, uint32_t* err_word, int32_t clear);
 

@@ -26,7 +26,7 @@ EXPORTS = ["kv_pool_bytes", "kv_pool_create", "kv_pool_destroy", "kv_append_fp8"
            "kv_migrate_to_tq3", "paged_attn_workspace_bytes", "paged_attn_workspace_init",
            "paged_attn_decode", "paged_attn_chunk", "kv_partition_pages", "kv_pool_free_counts",
            "kv_pool_read_free_lists", "kv_pool_counters", "kv_pool_check_errors",
-           "mkv_status_string"]
+           "paged_attn_set_timing", "paged_attn_last_times", "mkv_status_string"]
 
 _lib = None
 
@@ -82,6 +82,8 @@ def lib() -> ctypes.CDLL:
         L.kv_pool_read_free_lists.argtypes = [vp, vp, vp, vp, vp]
         L.kv_pool_counters.argtypes = [vp, vp]
         L.kv_pool_check_errors.argtypes = [vp, vp, i32]
+        L.paged_attn_set_timing.argtypes = [vp, i32]
+        L.paged_attn_last_times.argtypes = [vp, vp, vp]
         L.mkv_status_string.argtypes = [ctypes.c_int]
         _lib = L
     return _lib
@@ -244,6 +246,18 @@ def kv_pool_counters(pool: Pool) -> dict:
     c = Counters()
     _check("kv_pool_counters", lib().kv_pool_counters(pool.handle, ctypes.byref(c)))
     return {n: getattr(c, n) for n, _ in Counters._fields_}
+
+
+def paged_attn_set_timing(pool: Pool, enable: bool) -> None:
+    _check("paged_attn_set_timing", lib().paged_attn_set_timing(pool.handle, int(bool(enable))))
+
+
+def paged_attn_last_times(pool: Pool) -> tuple:
+    """(scan_us, merge_us) of the last timed paged_attn_decode call (waits for it)."""
+    a, b = ctypes.c_float(), ctypes.c_float()
+    _check("paged_attn_last_times", lib().paged_attn_last_times(pool.handle, ctypes.byref(a),
+                                                                ctypes.byref(b)))
+    return a.value, b.value
 
 
 def kv_pool_check_errors(pool: Pool, clear=False) -> int:

@@ -120,6 +120,7 @@ mkv_status kv_pool_create(const mkv_pool_desc* desc, mkv_pool** out) {
   p->ctrl = static_cast<int32_t*>(desc->ctrl);
   p->cl = ctrl_layout(p->n_fp8, p->n_tq3, p->d);
   p->decode_routes = p->chunk_routes = 0;
+  p->timing = p->timed = 0;
   // host image of ctrl: header, stacks (next id handed out = last element)
   std::vector<int32_t> img((size_t)p->cl.total_words, 0);
   img[CTRL_FP8_TOP] = p->n_fp8;
@@ -141,6 +142,7 @@ mkv_status kv_pool_create(const mkv_pool_desc* desc, mkv_pool** out) {
 
 mkv_status kv_pool_destroy(mkv_pool* pool) {
   if (!pool) return MKV_EINVAL;
+  (void)paged_attn_set_timing(pool, 0);
   delete pool;
   return MKV_OK;
 }
@@ -193,9 +195,44 @@ mkv_status paged_attn_decode(mkv_pool* pool, int32_t layer, int32_t n_req, const
   if (ws_bytes < decode_ws_bytes(n_req, max_pages, pool->n_kv_heads, pool->group, pool->d, pool->recent))
     return MKV_ENOMEM;
   mkv_status st = hip_status(launch_decode(view_of(pool), layer, n_req, q, block_table, tags,
-                                           max_pages, seq_lens, out, lse, ws, stream));
-  if (st == MKV_OK) pool->decode_routes++;
+                                           max_pages, seq_lens, out, lse, ws, stream,
+                                           pool->timing ? pool->timing_ev : nullptr));
+  if (st == MKV_OK) {
+    pool->decode_routes++;
+    if (pool->timing) pool->timed = 1;
+  }
   return st;
+}
+
+mkv_status paged_attn_set_timing(mkv_pool* pool, int32_t enable) {
+  if (!pool) return MKV_EINVAL;
+  if (enable && !pool->timing) {
+    for (int i = 0; i < 3; ++i) {
+      if (hipEventCreate(&pool->timing_ev[i]) != hipSuccess) {
+        for (int k = 0; k < i; ++k) (void)hipEventDestroy(pool->timing_ev[k]);
+        return MKV_EHIP;
+      }
+    }
+    pool->timing = 1;
+    pool->timed = 0;
+  } else if (!enable && pool->timing) {
+    for (int i = 0; i < 3; ++i) (void)hipEventDestroy(pool->timing_ev[i]);
+    pool->timing = pool->timed = 0;
+  }
+  return MKV_OK;
+}
+
+mkv_status paged_attn_last_times(mkv_pool* pool, float* scan_us, float* merge_us) {
+  if (!pool || !scan_us || !merge_us) return MKV_EINVAL;
+  if (!pool->timing || !pool->timed) return MKV_ESTATE;
+  float a = 0.0f, b = 0.0f;
+  if (hipEventSynchronize(pool->timing_ev[2]) != hipSuccess ||
+      hipEventElapsedTime(&a, pool->timing_ev[0], pool->timing_ev[1]) != hipSuccess ||
+      hipEventElapsedTime(&b, pool->timing_ev[1], pool->timing_ev[2]) != hipSuccess)
+    return MKV_EHIP;
+  *scan_us = a * 1000.0f;
+  *merge_us = b * 1000.0f;
+  return MKV_OK;
 }
 
 mkv_status paged_attn_chunk(mkv_pool* pool, int32_t layer, int32_t n_req, const uint16_t* q,

@@ -795,7 +795,7 @@ static constexpr size_t lds_limit() {
 hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t* q,
                          const int32_t* bt, const uint8_t* tags, int max_pages,
                          const int32_t* seq_lens, float* out, float* lse, void* ws,
-                         hipStream_t s) {
+                         hipStream_t s, hipEvent_t* ev) {
   const DecodeShape sh = decode_shape(n_req, max_pages, P.n_kv_heads, P.recent);
   DecodeArgs a;
   a.P = P;
@@ -837,15 +837,19 @@ hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t
   dim3 grid(sh.max_chunks, P.n_kv_heads, n_req);
   dim3 mgrid(P.group, P.n_kv_heads, n_req);
   void* args[] = {&a};
+  if (ev && (e = hipEventRecord(ev[0], s)) != hipSuccess) return e;
   e = hipLaunchKernel(kern, grid, dim3(64 * nw), args, lds, s);
   if (e != hipSuccess) return e;
+  if (ev && (e = hipEventRecord(ev[1], s)) != hipSuccess) return e;
   if (P.d == 256)
     hipLaunchKernelGGL(decode_merge_kernel<256>, mgrid, dim3(256), 0, s, P.group, P.n_kv_heads,
                        sh.max_chunks, a.partials, out, lse);
   else
     hipLaunchKernelGGL(decode_merge_kernel<128>, mgrid, dim3(128), 0, s, P.group, P.n_kv_heads,
                        sh.max_chunks, a.partials, out, lse);
-  return hipGetLastError();
+  e = hipGetLastError();
+  if (e == hipSuccess && ev) e = hipEventRecord(ev[2], s);
+  return e;
 }
 
 }  // namespace mkv

@@ -15,6 +15,8 @@ struct mkv_pool {
   int32_t* ctrl;      // device
   mkv::CtrlLayout cl;
   uint64_t decode_routes, chunk_routes;
+  hipEvent_t timing_ev[3];  // scan start, scan end, merge end (timing on)
+  int timing, timed;
 };
 
 namespace mkv {
@@ -71,7 +73,7 @@ size_t decode_ws_bytes(int n_req, int max_pages, int n_kv_heads, int group, int 
 hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t* q,
                          const int32_t* bt, const uint8_t* tags, int max_pages,
                          const int32_t* seq_lens, float* out, float* lse, void* ws,
-                         hipStream_t s);
+                         hipStream_t s, hipEvent_t* ev);
 
 // mkv_chunk.hip
 size_t chunk_ws_bytes(int n_req, int max_pages, int n_q_total, int n_kv_heads, int group, int d);

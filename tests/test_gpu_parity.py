@@ -179,6 +179,16 @@ def test_workspace_reuse_and_repeat(torch_cuda):
         assert np.array_equal(o, outs[0])
     c = mk.kv_pool_counters(tw.gpu)
     assert c["decode_routes"] == 4 and c["fallbacks"] == 0 and c["dense_shadow_bytes"] == 0
+    # the optional kernel timing leaves results unchanged
+    with pytest.raises(mk.MkvError):
+        mk.paged_attn_last_times(tw.gpu)  # timing off: no timed call
+    mk.paged_attn_set_timing(tw.gpu, True)
+    out = torch.zeros((3, w.n_q_heads, w.head_dim), device="cuda")
+    mk.paged_attn_decode(tw.gpu, 0, q, tw.bt, tw.tags, sl, out, None, ws)
+    scan_us, merge_us = mk.paged_attn_last_times(tw.gpu)
+    mk.paged_attn_set_timing(tw.gpu, False)
+    assert scan_us > 0.0 and merge_us > 0.0
+    assert np.array_equal(out.cpu().numpy(), outs[0])
 
 
 def test_device_errors_fail_closed(torch_cuda):
