@@ -54,7 +54,7 @@ def kv_bytes_of(tags_row: np.ndarray, seq_len: int, d: int, n_kv_heads: int) -> 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_kernel_long_pair_2x59008_hbm_traffic.txt")
 DECODE_SOURCES = [os.path.join(ROOT, "paper_2608_23834_amd", "csrc", f)
-                  for f in ("mkv_decode.hip", "mkv_device.h")]
+                  for f in ("mkv_decode.hip", "mkv_attn.h", "mkv_device.h")]
 
 
 def decode_source_hash() -> str:

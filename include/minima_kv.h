@@ -189,7 +189,10 @@ mkv_status paged_attn_decode(mkv_pool* pool, int32_t layer, int32_t n_req, const
  * seq_lens[r] - n_r + i and attends to keys t <= that position (the chunk's
  * own KV must already be appended as FP8).  q: device bf16
  * [n_q_total][n_q_heads][d]; cu_q: device int32 [n_req+1]; out: device fp32
- * [n_q_total][n_q_heads][d]; ws >= paged_attn_workspace_bytes(..., n_q_total).
+ * [n_q_total][n_q_heads][d]; ws >= paged_attn_workspace_bytes(..., n_q_total)
+ * (it holds the compact per-format page lists).  q, out and ws must be
+ * 16-byte aligned (MKV_EINVAL otherwise).  A request whose query range or
+ * length is invalid sets the error word and its locatable rows get zeros.
  * (The paper runs prefill on a generic dense path, Sec. 4.1; this variant
  * keeps the mixed pages and uses MFMA for the dense contraction.) */
 mkv_status paged_attn_chunk(mkv_pool* pool, int32_t layer, int32_t n_req, const uint16_t* q,

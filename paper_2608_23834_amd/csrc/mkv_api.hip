@@ -241,7 +241,10 @@ mkv_status paged_attn_chunk(mkv_pool* pool, int32_t layer, int32_t n_req, const 
                             float* out, void* ws, size_t ws_bytes, hipStream_t stream) {
   if (!pool || !q || !cu_q || !block_table || !tags || !seq_lens || !out || !ws) return MKV_EINVAL;
   if (n_req < 1 || max_pages < 1 || n_q_total < 1) return MKV_EINVAL;
+  if (!aligned16(q) || !aligned16(out) || !aligned16(ws)) return MKV_EINVAL;
   if (layer < 0 || layer >= pool->n_layers) return MKV_ERANGE;
+  if (n_req > 65535 || max_pages > 1024 * 256) return MKV_ERANGE;
+  if ((int64_t)n_q_total * pool->group > ((int64_t)1 << 31) / 2) return MKV_ERANGE;
   if (ws_bytes < chunk_ws_bytes(n_req, max_pages, n_q_total, pool->n_kv_heads, pool->group, pool->d))
     return MKV_ENOMEM;
   hipError_t e = launch_chunk(view_of(pool), layer, n_req, q, cu_q, n_q_total, block_table, tags,

@@ -30,6 +30,7 @@
 #include <atomic>
 #include <type_traits>
 
+#include "mkv_attn.h"
 #include "mkv_internal.h"
 #include "../../include/minima_kv.h"
 
@@ -88,152 +89,6 @@ size_t decode_ws_bytes(int n_req, int max_pages, int n_kv_heads, int group, int 
   return (size_t)n_req * n_kv_heads * s.max_chunks * group * (d + 2) * sizeof(float);
 }
 
-__device__ __forceinline__ half8 h8(half2v a, half2v b, half2v c, half2v d) {
-  half8 r;
-  r[0] = a[0]; r[1] = a[1]; r[2] = b[0]; r[3] = b[1];
-  r[4] = c[0]; r[5] = c[1]; r[6] = d[0]; r[7] = d[1];
-  return r;
-}
-__device__ __forceinline__ half2v cvt_lo(uint32_t w) {
-  return __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w, 1.0f, false);
-}
-__device__ __forceinline__ half2v cvt_hi(uint32_t w) {
-  return __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w, 1.0f, true);
-}
-// code bytes 0..7 -> fp16 0..7: each byte read as an E4M3 subnormal (c * 2^-9)
-// and scaled by 2^9 in the converter, exactly
-template <bool HI>
-__device__ __forceinline__ half2v cvt_code(uint32_t w) {
-  return __builtin_amdgcn_cvt_scalef32_pk_f16_fp8(w, 512.0f, HI);
-}
-__device__ __forceinline__ float exp2_safe(float s, float m) {
-  return s == -INFINITY ? 0.0f : exp2f(s - m);
-}
-
-// Direct HBM -> LDS copies issued by one wave.  dma16<OFF>: lane l copies
-// 16 bytes from base + voff_l + OFF to LDS m0 + OFF + 16 l; dma4<OFF>: 4 bytes
-// to m0 + OFF + 4 l (the immediate offset applies to both addresses; base and
-// m0 are wave-uniform).  They are inline assembly on purpose: the compiler
-// then does not order later LDS reads behind them (it cannot tell which ring
-// slot a copy fills and would wait for all of them), and the caller gates
-// every stage with an explicit vmcnt wait.  The kernel has no other user of m0.
-#pragma clang diagnostic push
-#pragma clang diagnostic ignored "-Winline-asm"  // m0 is reserved; no compiler code here uses it
-template <int OFF>
-__device__ __forceinline__ void dma16(uint32_t voff, const uint8_t* base, uint32_t m0) {
-  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1 offset:%3"
-               :
-               : "v"(voff), "s"(base), "s"(m0), "n"(OFF)
-               : "memory", "m0");
-}
-__device__ __forceinline__ void dma4(uint32_t voff, const uint8_t* base, uint32_t m0) {
-  asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dword %0, %1 offset:0"
-               :
-               : "v"(voff), "s"(base), "s"(m0)
-               : "memory", "m0");
-}
-#pragma clang diagnostic pop
-
-// Per-lane byte offsets of the copies (constant for the kernel).
-struct DmaLanes {
-  uint32_t lo, hi;  // 16 l and 4096 + 16 l
-};
-// One region of R bytes (16-byte aligned, R <= 8 KiB + 256): whole KiB blocks
-// by 16-byte lanes, the tail by 4-byte lanes.
-template <int R>
-__device__ __forceinline__ void dma_region(uint32_t dst, const uint8_t* src, const DmaLanes& dl,
-                                           int lane) {
-  static_assert(R <= 8192 + 256, "region too large for the offset scheme");
-#pragma unroll
-  for (int i = 0; i < R / 1024 && i < 4; ++i) {
-    switch (i) {
-      case 0: dma16<0>(dl.lo, src, dst); break;
-      case 1: dma16<1024>(dl.lo, src, dst); break;
-      case 2: dma16<2048>(dl.lo, src, dst); break;
-      default: dma16<3072>(dl.lo, src, dst); break;
-    }
-  }
-#pragma unroll
-  for (int i = 4; i < R / 1024; ++i) {
-    switch (i) {
-      case 4: dma16<0>(dl.hi, src, dst + 4096); break;
-      case 5: dma16<1024>(dl.hi, src, dst + 4096); break;
-      case 6: dma16<2048>(dl.hi, src, dst + 4096); break;
-      default: dma16<3072>(dl.hi, src, dst + 4096); break;
-    }
-  }
-  constexpr int TAIL = R % 1024;
-  static_assert(TAIL % 4 == 0 && TAIL <= 256, "tail must fit one 4-byte copy");
-  if (TAIL > 0 && lane < TAIL / 4) dma4((R - TAIL) + 4 * lane, src, dst + (R - TAIL));
-}
-// vector-memory instructions dma_region<R> issues per wave
-template <int R>
-constexpr int dma_ops() { return R / 1024 + (R % 1024 ? 1 : 0); }
-
-// Wait until at most N vector-memory operations of this wave are in flight
-// (gfx9 s_waitcnt: vmcnt in bits [3:0] and [15:14]; expcnt/lgkmcnt left free).
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
-  __asm__ __volatile__("" ::: "memory");
-}
-__device__ __forceinline__ void wait_lgkm0() {
-  __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0), vmcnt/expcnt free
-  __asm__ __volatile__("" ::: "memory");
-}
-
-// Cross-lane exchanges on the VALU (gfx950 permlane swaps).  With both operands
-// x, v_permlane16_swap yields (rows 0,0,2,2 ; rows 1,1,3,3) of x (a row is 16
-// lanes) and v_permlane32_swap yields (low half twice ; high half twice).
-__device__ __forceinline__ uint2 swap16(float x) {
-  const auto p = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return make_uint2(p[0], p[1]);
-}
-__device__ __forceinline__ uint2 swap32(float x) {
-  const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return make_uint2(p[0], p[1]);
-}
-// max / sum over the four lanes l, l ^ 16, l ^ 32, l ^ 48
-__device__ __forceinline__ float max4rows(float x) {
-  uint2 p = swap16(x);
-  x = fmaxf(__uint_as_float(p.x), __uint_as_float(p.y));
-  p = swap32(x);
-  return fmaxf(__uint_as_float(p.x), __uint_as_float(p.y));
-}
-__device__ __forceinline__ float sum4rows(float x) {
-  uint2 p = swap16(x);
-  x = __uint_as_float(p.x) + __uint_as_float(p.y);
-  p = swap32(x);
-  return __uint_as_float(p.x) + __uint_as_float(p.y);
-}
-// value of lane l ^ M, on the VALU: DPP within rows (quad_perm for 1 and 2,
-// half-row mirror then quad reverse for 4, row rotate by 8 for 8) and the
-// permlane swaps across rows
-template <int M>
-__device__ __forceinline__ float lane_xor(float x, int lane) {
-  const int xi = __float_as_int(x);
-  if constexpr (M == 1) {
-    return __int_as_float(__builtin_amdgcn_mov_dpp(xi, 0xB1, 0xF, 0xF, false));
-  } else if constexpr (M == 2) {
-    return __int_as_float(__builtin_amdgcn_mov_dpp(xi, 0x4E, 0xF, 0xF, false));
-  } else if constexpr (M == 4) {
-    const int t = __builtin_amdgcn_mov_dpp(xi, 0x141, 0xF, 0xF, false);
-    return __int_as_float(__builtin_amdgcn_mov_dpp(t, 0x1B, 0xF, 0xF, false));
-  } else if constexpr (M == 8) {
-    return __int_as_float(__builtin_amdgcn_mov_dpp(xi, 0x128, 0xF, 0xF, false));
-  } else if constexpr (M == 16) {
-    const uint2 p = swap16(x);
-    return __uint_as_float((lane & 16) ? p.x : p.y);
-  } else {
-    static_assert(M == 32, "lane_xor: M is a power of two below 64");
-    const uint2 p = swap32(x);
-    return __uint_as_float((lane & 32) ? p.x : p.y);
-  }
-}
-// value of lane l + 32 (valid in lanes l < 32)
-__device__ __forceinline__ float upper_half(float x) { return __uint_as_float(swap32(x).y); }
-
 template <int D>
 struct WaveState {
   float4v acc[D / 16];  // rows (page parity, head) x channels, see below
@@ -273,15 +128,20 @@ __device__ __forceinline__ void softmax_step(WaveState<D>& st, float* sc, int lg
 // P^T operand of the PV product: row ln = this lane's column; tokens
 // (4*lg + j) of page a for j < 4 and of page b for j >= 4 (block-diagonal:
 // page-a rows see only page-a tokens).
-__device__ __forceinline__ half8 p_operand(const float* p, bool row_is_b) {
-  half8 r;
+// The weights go in as an fp16 hi + lo pair (hi: rounded weight, lo: the
+// rounding remainder): a token holding most of a row's mass has, against a
+// lagging reference max, a weight that fp16 alone would round by up to 2^-12
+// of that token's value.
+__device__ __forceinline__ void p_operand(const float* p, bool row_is_b, half8& hi, half8& lo) {
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const _Float16 v = (_Float16)p[j];
-    r[j] = row_is_b ? (_Float16)0.0f : v;
-    r[4 + j] = row_is_b ? v : (_Float16)0.0f;
+    const _Float16 w = (_Float16)(p[j] - (float)v);
+    hi[j] = row_is_b ? (_Float16)0.0f : v;
+    hi[4 + j] = row_is_b ? v : (_Float16)0.0f;
+    lo[j] = row_is_b ? (_Float16)0.0f : w;
+    lo[4 + j] = row_is_b ? w : (_Float16)0.0f;
   }
-  return r;
 }
 
 // PAIR (query group of at most 8 heads): two pages share one score tile,
@@ -306,10 +166,11 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   const int G = P.group, H = P.n_kv_heads, Hq = H * G;
   const int mp = a.max_pages;
   constexpr bool pair = PAIR;
-  // LDS: [rotated-query operand][plain-query operand][page ring | wave merge]
-  half8* qrot = reinterpret_cast<half8*>(smem);
-  half8* qpl = qrot + NS * 64;
-  uint8_t* ring = smem + 2 * NS * 64 * 16;
+  // LDS: [rotated-query operand hi, lo][plain-query operand][page ring | wave merge]
+  half8* qrot = reinterpret_cast<half8*>(smem);  // rotated query, fp16 high part
+  half8* qrlo = qrot + NS * 64;                   // rotated query, fp16 low part
+  half8* qpl = qrlo + NS * 64;                    // plain query (bf16 -> fp16 is exact)
+  uint8_t* ring = smem + 3 * NS * 64 * 16;
 
   // ---- 1. queries: wave w owns query heads w and w + NW below NCH; lane l
   // holds channels QV l .. QV l + QV - 1.  The loads go out before anything
@@ -450,6 +311,7 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   // column ln's head (ln = lane % 16, lg = lane / 16)
   {
     _Float16* qr = reinterpret_cast<_Float16*>(qrot);
+    _Float16* ql = reinterpret_cast<_Float16*>(qrlo);
     _Float16* qp = reinterpret_cast<_Float16*>(qpl);
     const float qscale = rsqrtf((float)D);  // R = d^-1/2 H diag(sigma)
 #pragma unroll
@@ -486,13 +348,18 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
       for (int i = 0; i < QV; ++i) {
         const int c = QV * lane + i;
         const int lgc = c / (D / 4), sc = (c % (D / 4)) / 8, j = c % 8;
-        const _Float16 vr = (_Float16)(n < G ? xr[i] * qscale : 0.0f);
+        // q_rot as an fp16 pair hi + lo (fp32 accuracy through two MFMAs)
+        const float xq = n < G ? xr[i] * qscale : 0.0f;
+        const _Float16 vr = (_Float16)xq;
+        const _Float16 vl = (_Float16)(xq - (float)vr);
         const _Float16 vp = (_Float16)(n < G ? qx[ps][i] : 0.0f);
         const int e0 = ((sc * 64) + lgc * 16 + n) * 8 + j;
         qr[e0] = vr;
+        ql[e0] = vl;
         qp[e0] = vp;
         if (pair) {
           qr[e0 + 8 * 8] = vr;  // column n + 8 scores page b with the same head
+          ql[e0 + 8 * 8] = vl;
           qp[e0 + 8 * 8] = vp;
         }
       }
@@ -548,16 +415,18 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
     float4v sa = zero4, sb = zero4;
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      const half8 qv = qrot[s * 64 + lane];
+      const half8 qv = qrot[s * 64 + lane], ql = qrlo[s * 64 + lane];
       const uint32_t a0 = __builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(kA, 2 * s));
       const uint32_t a1 = __builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(kA, 2 * s + 1));
-      sa = __builtin_amdgcn_mfma_f32_16x16x32_f16(h8(cvt_lo(a0), cvt_hi(a0), cvt_lo(a1), cvt_hi(a1)),
-                                                   qv, sa, 0, 0, 0);
+      const half8 Ka = h8(cvt_lo(a0), cvt_hi(a0), cvt_lo(a1), cvt_hi(a1));
+      sa = __builtin_amdgcn_mfma_f32_16x16x32_f16(Ka, qv, sa, 0, 0, 0);
+      sa = __builtin_amdgcn_mfma_f32_16x16x32_f16(Ka, ql, sa, 0, 0, 0);
       if (pair) {
         const uint32_t b0 = __builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(kB, 2 * s));
         const uint32_t b1 = __builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(kB, 2 * s + 1));
-        sb = __builtin_amdgcn_mfma_f32_16x16x32_f16(
-            h8(cvt_lo(b0), cvt_hi(b0), cvt_lo(b1), cvt_hi(b1)), qv, sb, 0, 0, 0);
+        const half8 Kb = h8(cvt_lo(b0), cvt_hi(b0), cvt_lo(b1), cvt_hi(b1));
+        sb = __builtin_amdgcn_mfma_f32_16x16x32_f16(Kb, qv, sb, 0, 0, 0);
+        sb = __builtin_amdgcn_mfma_f32_16x16x32_f16(Kb, ql, sb, 0, 0, 0);
       }
     }
     float sc[4];
@@ -571,17 +440,19 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
       }
     }
     softmax_step<D>(st, sc, lg);
-    const half8 pT = p_operand(sc, col_b);
+    half8 pT, pTl;
+    p_operand(sc, col_b, pT, pTl);
     // PV: the codes enter the MFMA exactly (a code byte read as an E4M3
     // subnormal is c * 2^-9; the converter's power-of-two scale 2^9 makes it
     // c); v = zero + scale * code is applied in fp32 to the MFMA output,
-    // the zero term through the rows' weight sums PS (one MFMA against ones)
-    const float4v PS = __builtin_amdgcn_mfma_f32_16x16x32_f16(pT, ones8, zero4, 0, 0, 0);
+    // the zero term through the rows' weight sums PS (MFMAs against ones)
+    const float4v PS = __builtin_amdgcn_mfma_f32_16x16x32_f16(
+        pTl, ones8, __builtin_amdgcn_mfma_f32_16x16x32_f16(pT, ones8, zero4, 0, 0, 0), 0, 0, 0);
     auto pv = [&](int m) {
       const uint32_t ua = quad_sel<NDW>(vA, m), ub = quad_sel<NDW>(vB, m);
+      const half8 c = h8(cvt_code<false>(ua), cvt_code<true>(ua), cvt_code<false>(ub), cvt_code<true>(ub));
       return __builtin_amdgcn_mfma_f32_16x16x32_f16(
-          pT, h8(cvt_code<false>(ua), cvt_code<true>(ua), cvt_code<false>(ub), cvt_code<true>(ub)),
-          zero4, 0, 0, 0);
+          pTl, c, __builtin_amdgcn_mfma_f32_16x16x32_f16(pT, c, zero4, 0, 0, 0), 0, 0, 0);
     };
     // one tile ahead, so the MFMA of tile m + 1 runs while tile m is scaled
     float4v X = pv(0);
@@ -637,12 +508,14 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
       for (int i = 0; i < 4; ++i) sc[i] = (col_valid && 4 * lg + i < vcnt) ? sa[i] * kk : -INFINITY;
     }
     softmax_step<D>(st, sc, lg);
-    const half8 pT = p_operand(sc, col_b);
+    half8 pT, pTl;
+    p_operand(sc, col_b, pT, pTl);
     const half2v z2 = {(_Float16)0.0f, (_Float16)0.0f};
 #pragma unroll
     for (int m = 0; m < CL; ++m) {
+      const half8 v = h8(cvt_lo(vA[m]), cvt_hi(vA[m]), z2, z2);
       const float4v X = __builtin_amdgcn_mfma_f32_16x16x32_f16(
-          pT, h8(cvt_lo(vA[m]), cvt_hi(vA[m]), z2, z2), zero4, 0, 0, 0);
+          pTl, v, __builtin_amdgcn_mfma_f32_16x16x32_f16(pT, v, zero4, 0, 0, 0), 0, 0, 0);
       st.acc[m] += ksv.y * X;
     }
   }
@@ -816,7 +689,7 @@ hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t
   const bool pair = P.group <= 8;
   const int nw = pair ? DecodeCfg<true>::NW : DecodeCfg<false>::NW;
   const int slots = pair ? DecodeCfg<true>::SLOTS : DecodeCfg<false>::SLOTS;
-  const size_t qop_b = 2 * (size_t)(P.d / 32) * 64 * 16;
+  const size_t qop_b = 3 * (size_t)(P.d / 32) * 64 * 16;
   const size_t ring_b = (size_t)nw * slots * 2 * tq3_region_bytes(P.d);
   const size_t merge_b = ((size_t)nw * P.group * P.d + 3 * nw * P.group) * sizeof(float);
   const size_t lds = qop_b + (ring_b > merge_b ? ring_b : merge_b);

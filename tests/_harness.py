@@ -87,6 +87,12 @@ class Twin:
             step = [min(t - c, chunk or (t - c)) for c, t in zip(self.cur, target)]
             self.append(step)
 
+    def fill_to(self, targets, chunk=None):
+        """Append until request r holds targets[r] tokens."""
+        while any(c < t for c, t in zip(self.cur, targets)):
+            step = [max(0, min(t - c, chunk or (t - c))) for c, t in zip(self.cur, targets)]
+            self.append(step)
+
     def anchor(self):
         return wl.anchor_mask(self.w, self.max_pages, self.lens)
 
@@ -119,6 +125,30 @@ class Twin:
         if self.orc is not None:
             o, l = self.orc.decode(layer, q, self.obt, self.otags, sl)
             res["ref_out"], res["ref_lse"] = o, l
+        return res
+
+    def chunk(self, n_q, layer=0, sample_stride=1):
+        """Chunk attention for the last n_q[r] tokens of each request (already
+        appended).  The oracle computes every sample_stride-th query of each
+        request and its last one; the other rows of ref_out stay NaN."""
+        import paper_2608_23834_amd as mk
+        torch = _torch()
+        w = self.w
+        n_q = [int(x) for x in n_q]
+        mx = max(n_q)
+        qa = wl.q_chunk(w, layer, mx)
+        q = np.concatenate([qa[r * mx: r * mx + n_q[r]] for r in range(self.n_req)])
+        cu = np.r_[0, np.cumsum(n_q)].astype(np.int32)
+        sl = np.array(self.cur, np.int32)
+        out = torch.full((q.shape[0], w.n_q_heads, w.head_dim), float("nan"), device="cuda")
+        ws = mk.workspace(self.gpu, self.n_req, self.max_pages, q.shape[0])
+        mk.paged_attn_chunk(self.gpu, layer, torch.from_numpy(q.view(np.int16)).cuda(),
+                            torch.from_numpy(cu).cuda(), self.bt, self.tags,
+                            torch.from_numpy(sl).cuda(), out, ws)
+        torch.cuda.synchronize()
+        res = dict(out=out.cpu().numpy(), q=q, cu=cu, seq_lens=sl)
+        if self.orc is not None:
+            res["ref_out"] = self.orc.chunk(layer, q, cu, self.obt, self.otags, sl, sample_stride)
         return res
 
     # -- comparisons -------------------------------------------------------

@@ -221,3 +221,46 @@ def test_device_errors_fail_closed(torch_cuda):
                          out, None, ws)
     assert (out.cpu().numpy() == 0).all()
     assert mk.kv_pool_check_errors(gp, clear=True) & mk.DEVERR["RANGE"]
+
+
+def _run_chunk_case(w, lens, n_q, recent=None, sample_stride=1):
+    """Context of each request appended and migrated, then its chunk of n_q[r]
+    tokens appended as FP8; chunk attention of those queries vs the oracle."""
+    from _harness import Twin, max_abs
+    print(f"\n[chunk case] {w.name} lens={lens[:6]} n_q={n_q[:6]} W={recent}", flush=True)
+    tw = Twin(w, lens=lens, recent=recent)
+    tw.fill_to([l - n for l, n in zip(lens, n_q)])
+    tw.migrate()
+    tw.append(list(n_q))
+    tw.check_tables()
+    res = tw.chunk(n_q, sample_stride=sample_stride)
+    ref = res["ref_out"]
+    rows = ~np.isnan(ref[:, 0, 0])
+    err = max_abs(res["out"][rows], ref[rows])
+    print(f"  rows compared {int(rows.sum())} of {rows.size}  max|dO| {err:.3e}", flush=True)
+    assert np.all(np.isfinite(res["out"]))
+    assert err <= TOL, err
+    import paper_2608_23834_amd as mk
+    assert mk.kv_pool_check_errors(tw.gpu) == 0
+    return tw, res
+
+
+def test_chunk_tiny_d128(torch_cuda):
+    """d = 128, GQA 8: a 64-query chunk at the end of 2,048 tokens, every query."""
+    w = wl.workload(1)
+    _run_chunk_case(w, [2048], [64])
+
+
+def test_chunk_ragged_d256(torch_cuda):
+    """d = 256, GQA 6: ragged chunks (100, 33, 1 and a whole short request)
+    over mixed pages with a short Recent window, every query."""
+    w = wl.scaled(wl.workload(5), (3000, 1500, 700, 40), n_layers=1, name="chunk-ragged")
+    _run_chunk_case(w, list(w.ctx), [100, 33, 1, 40], recent=64)
+
+
+def test_chunk_config5_full_size(torch_cuda):
+    """Config 5 at full size: 8 requests, a 512-query chunk each against
+    65,536 tokens of mixed pages (sampled queries: every 64th and the last)."""
+    w = wl.workload(5)
+    tw, res = _run_chunk_case(w, list(w.ctx), [512] * 8, sample_stride=64)
+    assert np.all(np.isfinite(res["out"]))
