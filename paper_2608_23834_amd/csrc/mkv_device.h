@@ -25,6 +25,7 @@ enum CtrlSlot {
   CTRL_ERR = 2,
   CTRL_NLIST = 3,
   CTRL_ABORT = 4,
+  CTRL_APPEND_ARRIVE = 5,  // waves of a decode-step append that have finished (reset by the last)
   CTRL_HEADER = 64
 };
 struct CtrlLayout {

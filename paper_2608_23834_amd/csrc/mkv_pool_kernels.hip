@@ -270,82 +270,324 @@ __global__ __launch_bounds__(256) void append_quant_kernel(PoolView P, int layer
     run_quant_task<D>(P, t, layer_sel, n_lcall, sb, cu, n_new_total, k, v, P.list, lane);
 }
 
-// Small appends (decode steps: a few tokens per request) in one workgroup:
-// the allocation plan runs with one thread per request, then 16 waves
-// quantize the touched page-heads.  Same allocation order and arithmetic as
-// the two-kernel path.
-constexpr int SMALL_APPEND_MAX_TOKENS = 256;
-constexpr int SMALL_APPEND_MAX_REQ = 1024;
-constexpr int SMALL_APPEND_MAX_LIST = SMALL_APPEND_MAX_TOKENS / PAGE + SMALL_APPEND_MAX_REQ;
+// Small appends (decode steps: a few tokens per request): one wave per task
+// (touched page, layer, head, K or V) and no barrier.  Every wave reads the
+// whole call (rows and start positions, block-table entries and tags of the
+// touched pages, the head of the FP8 free list) and so reaches the same
+// validation and the same fresh-page ids; the wave that arrives last on a
+// counter in the control block (by then every other wave has finished its
+// reads) records the fresh pages in the block table, pops them off the free
+// list and resets the counter.  Three dependent memory round trips: (1) rows,
+// starts and the free-list top; (2) table entries, free-list head and the
+// task's new rows; (3) the page-head's codes and scale when it already holds
+// tokens.  A task assembles the page-head's code block in LDS (old codes,
+// re-rounded through a 256-entry table when the scale grows; new codes; zeros
+// past the new tokens of a fresh page) and stores it with whole-dword writes.
+// Same validation, allocation order and arithmetic as the two-kernel path.
+constexpr int STEP_APPEND_MAX_TOKENS = 256;  // also bounds the touched pages
+constexpr int STEP_APPEND_MAX_REQ = 256;
+constexpr int STEP_APPEND_MAX_WAVES = 4096;
 
 template <int D>
-__global__ __launch_bounds__(1024) void append_small_kernel(PoolView P, int layer_sel, int n_lcall,
-                                                            int n_req, int32_t* bt, uint8_t* tags,
-                                                            int max_pages, const int32_t* sb,
-                                                            const int32_t* cu, int n_new_total,
-                                                            const uint16_t* k, const uint16_t* v) {
-  __shared__ int scratch[32];
-  __shared__ int s_err;
-  __shared__ int s_lst[4 * SMALL_APPEND_MAX_LIST];
-  const int tid = threadIdx.x;
-  if (tid == 0) s_err = (cu[0] != 0 || cu[n_req] != n_new_total) ? (int)MKV_DEVERR_RANGE : 0;
-  __syncthreads();
-  int p0 = 0, p1 = -1, need = 0, bad = 0;
-  const int r = tid;
-  if (r < n_req) {
-    const int n = cu[r + 1] - cu[r], s0 = sb[r];
-    if (n < 0 || s0 < 0) bad |= MKV_DEVERR_RANGE;
-    else if (n > 0) {
-      p0 = s0 / PAGE;
-      p1 = (s0 + n - 1) / PAGE;
-      if (p1 >= max_pages) { bad |= MKV_DEVERR_RANGE; p1 = p0 - 1; }
-      for (int p = p0; p <= p1; ++p) {
-        const int64_t i = (int64_t)r * max_pages + p;
-        if (bt[i] < 0) need++;
-        else if (tags[i] != TAG_R) bad |= MKV_DEVERR_NOT_RECENT;
-        else if (bt[i] >= P.n_fp8) bad |= MKV_DEVERR_RANGE;
-      }
+struct SmallTask {
+  static constexpr int D4 = D / 4, NC = PAGE * D4 / 64, NV = PAGE * D / (16 * 64);
+  int r, p, row0, t0, t1, layer, li, h, kv;
+  uint2 x[NC];
+  uint4 old[NV];
+  float s_old;
+  bool have_old;
+};
+
+template <int D>
+__device__ __forceinline__ void small_task_load_x(SmallTask<D>& T, int H, int n_new_total,
+                                                  const uint16_t* k, const uint16_t* v, int lane) {
+  constexpr int D4 = SmallTask<D>::D4;
+  const uint16_t* src = (T.kv ? v : k) + (int64_t)T.li * n_new_total * H * D;
+  const uint16_t* srow = src + ((int64_t)T.row0 * H + T.h) * D;  // token t at srow[t * H * D + c]
+  const int64_t tstride = (int64_t)H * D;
+  const int n4 = (T.t1 - T.t0) * D4;
+#pragma unroll
+  for (int j = 0; j < SmallTask<D>::NC; ++j) {
+    const int idx = (threadIdx.x & 63) + 64 * j;
+    T.x[j] = make_uint2(0u, 0u);
+    if (idx < n4) {
+      const int t = T.t0 + idx / D4, c = 4 * (idx % D4);
+      T.x[j] = *reinterpret_cast<const uint2*>(srow + t * tstride + c);
     }
   }
-  if (bad) atomicOr(&s_err, bad);
-  int tot_need, tot_touch;
-  const int nb = block_excl_scan(need, scratch, &tot_need);
-  const int touch = p1 - p0 + 1;
-  const int tb = block_excl_scan(touch, scratch, &tot_touch);
+  (void)lane;
+}
+
+// codes and scale of page-head (T.layer, id, T.h), part T.kv; only a page with
+// tokens below t0 has any
+template <int D>
+__device__ __forceinline__ void small_task_load_old(SmallTask<D>& T, const PoolView& P, int id,
+                                                    int lane) {
+  T.have_old = T.t0 > 0;
+  T.s_old = 0.0f;
+  if (!T.have_old) return;
+  const int64_t ph = ((int64_t)T.layer * P.n_fp8 + id) * P.n_kv_heads + T.h;
+  const uint4* reg = reinterpret_cast<const uint4*>(P.fp8 + ph * fp8_region_bytes(D) + T.kv * PAGE * D);
+#pragma unroll
+  for (int j = 0; j < SmallTask<D>::NV; ++j) T.old[j] = reg[lane + 64 * j];
+  T.s_old = P.fp8_scales[ph * 2 + T.kv];
+}
+
+template <int D>
+__device__ void small_task_run(SmallTask<D>& T, const PoolView& P, int id, uint32_t* img,
+                               uint8_t* lut, int lane) {
+  constexpr int D4 = SmallTask<D>::D4, NC = SmallTask<D>::NC, NV = SmallTask<D>::NV;
+  const int t0 = T.t0, t1 = T.t1;
+  const int n4 = (t1 - t0) * D4;
+  float amax = 0.0f;
+#pragma unroll
+  for (int j = 0; j < NC; ++j) {
+    amax = fmaxf(amax, fmaxf(fmaxf(fabsf(__uint_as_float(T.x[j].x << 16)),
+                                   fabsf(__uint_as_float(T.x[j].x & 0xFFFF0000u))),
+                             fmaxf(fabsf(__uint_as_float(T.x[j].y << 16)),
+                                   fabsf(__uint_as_float(T.x[j].y & 0xFFFF0000u)))));
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) amax = fmaxf(amax, __shfl_xor(amax, o, 64));
+  const float s_old = T.s_old;
+  float s_new = s_old;
+  bool requant = false;
+  if (t0 == 0) {
+    s_new = amax / 448.0f;
+  } else if (!(amax <= 448.0f * s_old)) {
+    s_new = amax / 448.0f;
+    requant = true;
+  }
+  // old codes (zeros for a page without tokens below t0) into the LDS block
+  if (requant) {
+    // re-rounding table: old code byte -> code at the new scale
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const uint32_t c = (uint32_t)(lane + 64 * i);
+      lut[c] = (uint8_t)f32_to_e4m3((e4m3_to_f32(c) * s_old) / s_new);
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < NV; ++j)
+    reinterpret_cast<uint4*>(img)[lane + 64 * j] = T.have_old ? T.old[j] : make_uint4(0u, 0u, 0u, 0u);
+  __builtin_amdgcn_wave_barrier();
+  if (requant) {
+    // each lane re-rounds the bytes of tokens below t0 in its own words
+#pragma unroll 1
+    for (int i = 0; i < 4 * NV; ++i) {
+      const int w = 4 * (lane + 64 * (i >> 2)) + (i & 3);  // word of the block
+      const uint32_t ow = img[w];
+      uint32_t outw = 0;
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        // token of byte b: K rows are token-major, V words hold tokens 4g .. 4g+3
+        const int t = T.kv ? 4 * ((w / (D / 16)) % 4) + b : w / D4;
+        const uint32_t code = (ow >> (8 * b)) & 0xFFu;
+        outw |= (t < t0 ? (uint32_t)lut[code] : code) << (8 * b);
+      }
+      img[w] = outw;
+    }
+  }
+  __builtin_amdgcn_wave_barrier();
+  // new codes over the block
+#pragma unroll
+  for (int j = 0; j < NC; ++j) {
+    const int idx = lane + 64 * j;
+    if (idx < n4) {
+      const int t = t0 + idx / D4, c = 4 * (idx % D4);
+      uint32_t code[4];
+      const uint32_t hv[4] = {T.x[j].x << 16, T.x[j].x & 0xFFFF0000u, T.x[j].y << 16,
+                              T.x[j].y & 0xFFFF0000u};
+#pragma unroll
+      for (int b = 0; b < 4; ++b)
+        code[b] = s_new > 0.0f ? f32_to_e4m3(__uint_as_float(hv[b]) / s_new) : 0u;
+      if (!T.kv) {
+        img[(t * D + c) / 4] = code[0] | (code[1] << 8) | (code[2] << 16) | (code[3] << 24);
+      } else {
+        uint8_t* ib = reinterpret_cast<uint8_t*>(img);
+#pragma unroll
+        for (int b = 0; b < 4; ++b) ib[fp8_off<D>(1, t, c + b) - PAGE * D] = (uint8_t)code[b];
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);  // one item at a time: bounded register use
+  }
+  __builtin_amdgcn_wave_barrier();
+  const int64_t ph = ((int64_t)T.layer * P.n_fp8 + id) * P.n_kv_heads + T.h;
+  uint4* reg = reinterpret_cast<uint4*>(P.fp8 + ph * fp8_region_bytes(D) + T.kv * PAGE * D);
+#pragma unroll
+  for (int j = 0; j < NV; ++j) reg[lane + 64 * j] = reinterpret_cast<const uint4*>(img)[lane + 64 * j];
+  if (lane == 0) P.fp8_scales[ph * 2 + T.kv] = s_new;
+  __builtin_amdgcn_wave_barrier();  // the block and table are free for the wave's next task
+}
+
+// Inclusive prefix sum over the wave's lanes.
+__device__ __forceinline__ int wave_incl_scan(int x, int lane) {
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  return x;
+}
+__device__ __forceinline__ int wave_or(int x) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) x |= __shfl_xor(x, o, 64);
+  return x;
+}
+
+template <int D>
+__global__ __launch_bounds__(64) void append_step_kernel(PoolView P, int layer_sel, int n_lcall,
+                                                         int n_req, int32_t* bt, uint8_t* tags,
+                                                         int max_pages, const int32_t* sb,
+                                                         const int32_t* cu, int n_new_total,
+                                                         const uint16_t* k, const uint16_t* v) {
+  constexpr int RQ = STEP_APPEND_MAX_REQ / 64, EQ = STEP_APPEND_MAX_TOKENS / 64;
+  __shared__ int s_base[STEP_APPEND_MAX_REQ + 1];  // first list entry of request r
+  __shared__ int s_cu[STEP_APPEND_MAX_REQ], s_n[STEP_APPEND_MAX_REQ], s_s0[STEP_APPEND_MAX_REQ];
+  __shared__ __align__(16) uint32_t s_img[PAGE * D / 4];
+  __shared__ uint8_t s_lut[256];
+  const int lane = threadIdx.x;
+  const int H = P.n_kv_heads;
+  // ---- round trip 1: rows, starts, free-list top
   const int top = P.ctrl[CTRL_FP8_TOP];
-  if (tid == 0) {
-    if (s_err == 0 && tot_need > top) s_err |= MKV_DEVERR_FP8_EXHAUSTED;
-    if (s_err == 0 && tot_touch > SMALL_APPEND_MAX_LIST) s_err |= MKV_DEVERR_RANGE;
+  int bad = (cu[0] != 0 || cu[n_req] != n_new_total) ? (int)MKV_DEVERR_RANGE : 0;
+  int run = 0;  // list entries of the requests before this group of 64
+#pragma unroll
+  for (int i = 0; i < RQ; ++i) {
+    const int r = lane + 64 * i;
+    int touch = 0;
+    if (r < n_req) {
+      const int c_r = cu[r], n = cu[r + 1] - c_r, s0 = sb[r];
+      // rows outside the input stay unread: inputs are loaded before the call
+      // as a whole is known to be valid
+      if (n < 0 || s0 < 0 || c_r < 0 || c_r + n > n_new_total) {
+        bad |= MKV_DEVERR_RANGE;
+      } else if (n > 0) {
+        const int p0 = s0 / PAGE, p1 = (s0 + n - 1) / PAGE;
+        if (p1 >= max_pages) bad |= MKV_DEVERR_RANGE;
+        else touch = p1 - p0 + 1;
+      }
+      s_cu[r] = c_r;
+      s_n[r] = n;
+      s_s0[r] = s0;
+    }
+    const int incl = wave_incl_scan(touch, lane);
+    if (r < n_req) s_base[r] = run + incl - touch;
+    run += __shfl(incl, 63, 64);
   }
-  __syncthreads();
-  if (s_err) {
-    if (tid == 0) atomicOr(&P.ctrl[CTRL_ERR], s_err);
-    return;
-  }
-  if (r < n_req) {
-    int k_alloc = 0;
-    for (int p = p0; p <= p1; ++p) {
+  const int n_ent = run;
+  if (lane == 0) s_base[n_req] = n_ent;
+  __builtin_amdgcn_wave_barrier();
+  // list entry e -> (request, page): the last request whose first entry is <= e
+  auto locate = [&](int e, int& r, int& p) {
+    int lo = 0, hi = n_req - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (s_base[mid] <= e) lo = mid;
+      else hi = mid - 1;
+    }
+    r = lo;
+    p = s_s0[lo] / PAGE + (e - s_base[lo]);
+  };
+  // ---- round trip 2: table entries of the list, the free-list head, the
+  // task's new rows
+  int ent_bt[EQ], ent_tag[EQ];
+#pragma unroll
+  for (int j = 0; j < EQ; ++j) {
+    const int e = lane + 64 * j;
+    ent_bt[j] = 0;
+    ent_tag[j] = TAG_R;
+    if (e < n_ent) {
+      int r, p;
+      locate(e, r, p);
       const int64_t i = (int64_t)r * max_pages + p;
-      int id = bt[i];
-      if (id < 0) {
-        id = P.fp8_stack[top - 1 - (nb + k_alloc)];
-        k_alloc++;
-        bt[i] = id;
+      ent_bt[j] = bt[i];
+      ent_tag[j] = tags[i];
+    }
+  }
+  const int stk = lane < top ? P.fp8_stack[top - 1 - lane] : -1;  // ids handed out first
+  const int64_t n_tasks = (int64_t)n_ent * n_lcall * H * 2;
+  const int64_t task = blockIdx.x;
+  SmallTask<D> T;
+  int e_t = 0;
+  if (task < n_tasks) {
+    T.kv = (int)(task & 1);
+    const int64_t item = task >> 1;
+    e_t = (int)(item / (n_lcall * H));
+    const int lh = (int)(item % (n_lcall * H));
+    T.li = lh / H;
+    T.h = lh % H;
+    T.layer = layer_sel < 0 ? T.li : layer_sel;
+    int r, p;
+    locate(e_t, r, p);
+    T.r = __builtin_amdgcn_readfirstlane(r);
+    T.p = __builtin_amdgcn_readfirstlane(p);
+    const int c_r = __builtin_amdgcn_readfirstlane(s_cu[T.r]);
+    const int s0 = __builtin_amdgcn_readfirstlane(s_s0[T.r]);
+    const int n = __builtin_amdgcn_readfirstlane(s_n[T.r]);
+    T.row0 = c_r + T.p * PAGE - s0;  // input row of slot t is row0 + t
+    T.t0 = max(0, s0 - T.p * PAGE);
+    T.t1 = min(PAGE, s0 + n - T.p * PAGE);
+    // a listed page belongs to a request whose rows passed the range checks
+    small_task_load_x<D>(T, H, n_new_total, k, v, lane);
+  }
+  // ---- validation and fresh-page ranks (identical in every wave)
+  int fresh[EQ], rank[EQ], n_fresh = 0;
+#pragma unroll
+  for (int j = 0; j < EQ; ++j) {
+    const int e = lane + 64 * j;
+    fresh[j] = (e < n_ent && ent_bt[j] < 0) ? 1 : 0;
+    if (e < n_ent && !fresh[j]) {
+      if (ent_tag[j] != TAG_R) bad |= MKV_DEVERR_NOT_RECENT;
+      else if (ent_bt[j] >= P.n_fp8) bad |= MKV_DEVERR_RANGE;
+    }
+    const int incl = wave_incl_scan(fresh[j], lane);
+    rank[j] = n_fresh + incl - fresh[j];
+    n_fresh += __shfl(incl, 63, 64);
+  }
+  if (n_fresh > top) bad |= MKV_DEVERR_FP8_EXHAUSTED;
+  bad = wave_or(bad);
+  // id of each entry: its table entry, or the free-list element of its rank
+  int ent_id[EQ];
+#pragma unroll
+  for (int j = 0; j < EQ; ++j) {
+    ent_id[j] = ent_bt[j];
+    const int sl = rank[j] < 64 ? __shfl(stk, rank[j] & 63, 64) : -1;
+    if (fresh[j] && bad == 0) ent_id[j] = rank[j] < 64 ? sl : P.fp8_stack[top - 1 - rank[j]];
+  }
+  if (bad == 0 && task < n_tasks) {
+    // ---- round trip 3 and the task
+    int idv = 0;
+#pragma unroll
+    for (int j = 0; j < EQ; ++j) idv = (e_t >> 6) == j ? ent_id[j] : idv;
+    const int id = __builtin_amdgcn_readfirstlane(__shfl(idv, e_t & 63, 64));
+    small_task_load_old<D>(T, P, id, lane);
+    small_task_run<D>(T, P, id, s_img, s_lut, lane);
+  }
+  // ---- arrive; the last wave records the fresh pages
+  __threadfence();
+  int prev = 0;
+  if (lane == 0) prev = atomicAdd(&P.ctrl[CTRL_APPEND_ARRIVE], 1);
+  prev = __shfl(prev, 0, 64);
+  if (prev != (int)gridDim.x - 1) return;
+  __threadfence();
+  if (bad) {
+    if (lane == 0) atomicOr(&P.ctrl[CTRL_ERR], bad);
+  } else {
+#pragma unroll
+    for (int j = 0; j < EQ; ++j) {
+      const int e = lane + 64 * j;
+      if (e < n_ent && fresh[j]) {
+        int r, p;
+        locate(e, r, p);
+        const int64_t i = (int64_t)r * max_pages + p;
+        bt[i] = ent_id[j];
         tags[i] = TAG_R;
       }
-      int* e = s_lst + 4 * (tb + (p - p0));
-      e[0] = r;
-      e[1] = p;
-      e[2] = id;
-      e[3] = 0;
     }
+    if (lane == 0) P.ctrl[CTRL_FP8_TOP] = top - n_fresh;
   }
-  __syncthreads();
-  if (tid == 0) P.ctrl[CTRL_FP8_TOP] = top - tot_need;
-  const int lane = tid & 63, wid = tid >> 6;
-  const int64_t n_tasks = (int64_t)tot_touch * n_lcall * P.n_kv_heads * 2;
-  for (int64_t t = wid; t < n_tasks; t += 16)
-    run_quant_task<D>(P, t, layer_sel, n_lcall, sb, cu, n_new_total, k, v, s_lst, lane);
+  if (lane == 0) P.ctrl[CTRL_APPEND_ARRIVE] = 0;
 }
 
 // ===========================================================================
@@ -635,12 +877,17 @@ hipError_t launch_append(const PoolView& P, int layer, int n_req, int32_t* bt, u
                          int max_pages, const int32_t* sb, const int32_t* cu, int n_new_total,
                          const uint16_t* k, const uint16_t* v, hipStream_t s) {
   const int n_lcall = layer < 0 ? P.n_layers : 1;
-  if (n_new_total <= SMALL_APPEND_MAX_TOKENS && n_req <= SMALL_APPEND_MAX_REQ) {
+  // decode-step appends: one wave per task, as many waves as the call can have
+  // tasks (every touched page receives at least one token)
+  const int64_t step_waves = (int64_t)n_new_total * n_lcall * P.n_kv_heads * 2;
+  if (n_new_total <= STEP_APPEND_MAX_TOKENS && n_req <= STEP_APPEND_MAX_REQ &&
+      step_waves <= STEP_APPEND_MAX_WAVES) {
+    const int grid = step_waves < 1 ? 1 : (int)step_waves;
     if (P.d == 256)
-      hipLaunchKernelGGL(append_small_kernel<256>, dim3(1), dim3(1024), 0, s, P, layer, n_lcall,
+      hipLaunchKernelGGL(append_step_kernel<256>, dim3(grid), dim3(64), 0, s, P, layer, n_lcall,
                          n_req, bt, tags, max_pages, sb, cu, n_new_total, k, v);
     else
-      hipLaunchKernelGGL(append_small_kernel<128>, dim3(1), dim3(1024), 0, s, P, layer, n_lcall,
+      hipLaunchKernelGGL(append_step_kernel<128>, dim3(grid), dim3(64), 0, s, P, layer, n_lcall,
                          n_req, bt, tags, max_pages, sb, cu, n_new_total, k, v);
     return hipGetLastError();
   }

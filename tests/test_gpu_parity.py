@@ -233,6 +233,7 @@ def _run_chunk_case(w, lens, n_q, recent=None, sample_stride=1):
     tw.migrate()
     tw.append(list(n_q))
     tw.check_tables()
+    tw.check_pages()  # multi-token appends into partly filled pages, bit-exact
     res = tw.chunk(n_q, sample_stride=sample_stride)
     ref = res["ref_out"]
     rows = ~np.isnan(ref[:, 0, 0])
