@@ -178,7 +178,9 @@ mkv_status paged_attn_workspace_init(void* ws, size_t ws_bytes, hipStream_t stre
  * 16-byte aligned (MKV_EINVAL otherwise).  max_pages is at most 262144.  An
  * invalid seq_len sets the error word and gives that request zero outputs; a
  * page below seq_len with an invalid tag or an out-of-range physical id sets
- * the error word and is left out of the softmax. */
+ * the error word and is left out of the softmax.  The waves of a split claim
+ * its pages at run time, so the fp32 summation order (and the last bits of
+ * out and lse) can differ from call to call. */
 mkv_status paged_attn_decode(mkv_pool* pool, int32_t layer, int32_t n_req, const uint16_t* q,
                              const int32_t* block_table, const uint8_t* tags, int32_t max_pages,
                              const int32_t* seq_lens, float* out, float* lse, void* ws,

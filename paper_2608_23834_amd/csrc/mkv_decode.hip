@@ -159,6 +159,7 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   extern __shared__ __align__(16) uint8_t smem[];
   __shared__ int4 s_stage[MAX_CHUNK_PAGES];  // {lp_a, id_a, lp_b, id_b}; id_b < 0: FP8 stage
   __shared__ int s_cnt[2 * NW];
+  __shared__ int s_next;  // next unclaimed stage (one-slot schedule)
   const PoolView& P = a.P;
   const int r = blockIdx.z, h = blockIdx.y, chunk = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63;
@@ -260,6 +261,7 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
       s_stage[st3 + b8 + __popcll(m8 & below)] = make_int4(lp, id, 0, -1);
     }
   }
+  if (tid == 0) s_next = NW;
   __syncthreads();
 
   // ---- 3. per-wave stream over stages [s0, s1)
@@ -273,7 +275,17 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   const bool col_valid = col_head < G;
   const bool col_b = pair && ln >= 8;  // this column scores page b
   const bool row_b = pair && lg >= 2;  // accumulator rows 4*lg+i hold page b
+  // Stage schedule.  One ring slot per wave: wave w starts with stage w and
+  // claims its next stage from an LDS counter when it begins a stage, so the
+  // waves of a SIMD finish together (stages differ in cost and the waves of a
+  // SIMD do not get equal issue shares).  Two slots: contiguous ranges.
   const int s0 = wid * n_st / NW, s1 = (wid + 1) * n_st / NW;
+  const int jend = SLOTS == 1 ? n_st : s1;
+  auto claim = [&]() {
+    int v = 0;
+    if (lane == 0) v = atomicAdd(&s_next, 1);
+    return __builtin_amdgcn_readfirstlane(v);
+  };
   const float smk = a.sm_log2;
   const float4v zero4 = {0.f, 0.f, 0.f, 0.f};
   half8 ones8;
@@ -302,9 +314,14 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
       if (lane < 2) dma4(4 * lane, scl_l + ((int64_t)e.y * H + h) * 8, dst + R8);
     }
   };
+  int jc = SLOTS == 1 ? min(wid, n_st) : s0;  // stage this wave processes next
+  if (SLOTS == 1) {
+    if (jc < n_st) issue(stage_at(jc), 0);
+  } else {
 #pragma unroll
-  for (int k = 0; k < SLOTS; ++k)
-    if (s0 + k < s1) issue(stage_at(s0 + k), k);
+    for (int k = 0; k < SLOTS; ++k)
+      if (s0 + k < s1) issue(stage_at(s0 + k), k);
+  }
 
   // ---- query operands, built while the first stages are in flight, in MFMA
   // lane order: q?[s][lane] holds channels (D/4) lg + 8 s + j, j < 8, of
@@ -382,13 +399,16 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   };
   // TQ3 stages come first in the list, FP8 stages after them; the two loops
   // share the ring (a copy in flight may belong to either format).
-  const int s_mid = max(s0, min(s1, st3));
-  for (int j = s0; j < s_mid; ++j) {
-    const int slot = (j - s0) % SLOTS;
+  int k_st = 0;  // stages begun by this wave; stage k sits in slot k % SLOTS
+  while (jc < min(jend, st3)) {
+    const int j = jc;
+    const int slot = k_st % SLOTS;
+    const int jn = SLOTS == 1 ? claim() : j + 1;  // next stage of this wave
+    const int jr = SLOTS == 1 ? jn : j + SLOTS;   // stage that refills this slot
     const int4 e = stage_at(j);
     begin_stage(j);
-    const bool refill = j + SLOTS < s1;
-    const int4 e2 = refill ? stage_at(j + SLOTS) : e;
+    const bool refill = jr < jend;
+    const int4 e2 = refill ? stage_at(jr) : e;
     const uint8_t* ra = wring + slot * STAGE;
     // TQ3 pair (page b absent: same page, every token masked)
     const uint8_t* rb = pair ? ra + R3 : ra;
@@ -466,13 +486,18 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
         st.acc[m][i] = fmaf((float)zm, PS[i], fmaf((float)sm, X[i], st.acc[m][i]));
       X = Xn;
     }
+    jc = jn;
+    ++k_st;
   }
-  for (int j = s_mid; j < s1; ++j) {
-    const int slot = (j - s0) % SLOTS;
+  while (jc < jend) {
+    const int j = jc;
+    const int slot = k_st % SLOTS;
+    const int jn = SLOTS == 1 ? claim() : j + 1;
+    const int jr = SLOTS == 1 ? jn : j + SLOTS;
     const int4 e = stage_at(j);
     begin_stage(j);
-    const bool refill = j + SLOTS < s1;
-    const int4 e2 = refill ? stage_at(j + SLOTS) : e;
+    const bool refill = jr < jend;
+    const int4 e2 = refill ? stage_at(jr) : e;
     const uint8_t* ra = wring + slot * STAGE;
     // one FP8 page (score columns of page b stay empty)
     constexpr int KW = D / 16;  // dwords of K per lane (D/4 bytes)
@@ -518,6 +543,8 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
           pTl, v, __builtin_amdgcn_mfma_f32_16x16x32_f16(pT, v, zero4, 0, 0, 0), 0, 0, 0);
       st.acc[m] += ksv.y * X;
     }
+    jc = jn;
+    ++k_st;
   }
 
   // ---- 4. rows -> heads: fetch each accumulator row's (m, l); merge the two

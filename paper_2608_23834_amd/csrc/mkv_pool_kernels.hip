@@ -358,36 +358,39 @@ __device__ void small_task_run(SmallTask<D>& T, const PoolView& P, int id, uint3
     s_new = amax / 448.0f;
     requant = true;
   }
-  // old codes (zeros for a page without tokens below t0) into the LDS block
+  // old codes (zeros for a page without tokens below t0), re-rounded through
+  // a table when the scale grows, into the LDS block
+  uint4 o[NV];
+#pragma unroll
+  for (int j = 0; j < NV; ++j) o[j] = T.have_old ? T.old[j] : make_uint4(0u, 0u, 0u, 0u);
   if (requant) {
-    // re-rounding table: old code byte -> code at the new scale
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const uint32_t c = (uint32_t)(lane + 64 * i);
       lut[c] = (uint8_t)f32_to_e4m3((e4m3_to_f32(c) * s_old) / s_new);
     }
-  }
+    __builtin_amdgcn_wave_barrier();
 #pragma unroll
-  for (int j = 0; j < NV; ++j)
-    reinterpret_cast<uint4*>(img)[lane + 64 * j] = T.have_old ? T.old[j] : make_uint4(0u, 0u, 0u, 0u);
-  __builtin_amdgcn_wave_barrier();
-  if (requant) {
-    // each lane re-rounds the bytes of tokens below t0 in its own words
-#pragma unroll 1
-    for (int i = 0; i < 4 * NV; ++i) {
-      const int w = 4 * (lane + 64 * (i >> 2)) + (i & 3);  // word of the block
-      const uint32_t ow = img[w];
-      uint32_t outw = 0;
+    for (int j = 0; j < NV; ++j) {
+      uint32_t* ow = reinterpret_cast<uint32_t*>(&o[j]);
 #pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        // token of byte b: K rows are token-major, V words hold tokens 4g .. 4g+3
-        const int t = T.kv ? 4 * ((w / (D / 16)) % 4) + b : w / D4;
-        const uint32_t code = (ow >> (8 * b)) & 0xFFu;
-        outw |= (t < t0 ? (uint32_t)lut[code] : code) << (8 * b);
+      for (int q = 0; q < 4; ++q) {
+        const int w = 4 * (lane + 64 * j) + q;  // word of the block
+        uint32_t outw = 0;
+#pragma unroll
+        for (int b = 0; b < 4; ++b) {
+          // token of byte b: K rows are token-major, V words hold tokens 4g .. 4g+3
+          const int t = T.kv ? 4 * ((w / (D / 16)) % 4) + b : w / D4;
+          const uint32_t code = (ow[q] >> (8 * b)) & 0xFFu;
+          const uint32_t nc = lut[code];
+          outw |= (t < t0 ? nc : code) << (8 * b);
+        }
+        ow[q] = outw;
       }
-      img[w] = outw;
     }
   }
+#pragma unroll
+  for (int j = 0; j < NV; ++j) reinterpret_cast<uint4*>(img)[lane + 64 * j] = o[j];
   __builtin_amdgcn_wave_barrier();
   // new codes over the block
 #pragma unroll

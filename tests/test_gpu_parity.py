@@ -159,7 +159,7 @@ def test_e4m3_encode_all_bf16_inputs(torch_cuda):
 
 
 def test_workspace_reuse_and_repeat(torch_cuda):
-    """Split counters reset themselves: repeated calls on one workspace agree."""
+    """Repeated calls on one workspace agree (up to fp32 summation order)."""
     import paper_2608_23834_amd as mk
     from _harness import Twin
     torch = torch_cuda
@@ -175,8 +175,9 @@ def test_workspace_reuse_and_repeat(torch_cuda):
         out = torch.zeros((3, w.n_q_heads, w.head_dim), device="cuda")
         mk.paged_attn_decode(tw.gpu, 0, q, tw.bt, tw.tags, sl, out, None, ws)
         outs.append(out.cpu().numpy())
+    # the waves claim pages at run time: repeats agree up to fp32 summation order
     for o in outs[1:]:
-        assert np.array_equal(o, outs[0])
+        assert np.abs(o - outs[0]).max() <= 1e-6
     c = mk.kv_pool_counters(tw.gpu)
     assert c["decode_routes"] == 4 and c["fallbacks"] == 0 and c["dense_shadow_bytes"] == 0
     # the optional kernel timing leaves results unchanged
@@ -188,7 +189,7 @@ def test_workspace_reuse_and_repeat(torch_cuda):
     scan_us, merge_us = mk.paged_attn_last_times(tw.gpu)
     mk.paged_attn_set_timing(tw.gpu, False)
     assert scan_us > 0.0 and merge_us > 0.0
-    assert np.array_equal(out.cpu().numpy(), outs[0])
+    assert np.abs(out.cpu().numpy() - outs[0]).max() <= 1e-6
 
 
 def test_device_errors_fail_closed(torch_cuda):
