@@ -156,6 +156,7 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   constexpr int STAGE = 2 * R3;                 // a TQ3 page pair, or one FP8 page + scales
   constexpr int OPS3 = dma_ops<R3>(), OPS8 = dma_ops<R8>() + 1;
   static_assert(R8 + 8 <= STAGE, "an FP8 page and its two scales fit one stage");
+  static_assert(NW % 4 == 0, "per-head wave statistics are read as float4s");
   extern __shared__ __align__(16) uint8_t smem[];
   __shared__ int4 s_stage[MAX_CHUNK_PAGES];  // {lp_a, id_a, lp_b, id_b}; id_b < 0: FP8 stage
   __shared__ int s_cnt[2 * NW];
@@ -549,7 +550,7 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
 
   // ---- 4. rows -> heads: fetch each accumulator row's (m, l); merge the two
   // page parities (rows h and h + 8 sit in lanes l and l ^ 32); then merge the
-  // eight waves in LDS into one (m_j, l_j, O_j) partial per chunk
+  // waves in LDS into one (m_j, l_j, O_j) partial per chunk
   const float l_col = sum4rows(st.l_run);
   float mrow[4], lrow[4];
 #pragma unroll
@@ -569,6 +570,7 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
       for (int m = 0; m < CL; ++m) {
         const float o2 = upper_half(st.acc[m][i]);
         st.acc[m][i] = f1 * st.acc[m][i] + f2 * o2;
+        asm volatile("" : "+v"(st.acc[m][i]));  // merged here, not sunk past the barriers
       }
       lrow[i] = f1 * lrow[i] + f2 * l2;
       mrow[i] = M;
@@ -578,8 +580,8 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   // (16 k + ln) 4 + t: every lane stores float4s and the 16 lanes of a row
   // store consecutive 16-byte words (no bank conflicts)
   float* macc = reinterpret_cast<float*>(ring);  // [NW][G][D]
-  float* mm = macc + NW * G * D;                 // [NW][G]
-  float* ml = mm + NW * G;                       // [NW][G], then fw [NW][G]
+  float* mm = macc + NW * G * D;                 // [G][NW]
+  float* ml = mm + G * NW;                       // [G][NW]
   __syncthreads();  // every wave is done with its ring (all copies waited for)
   if (!row_b) {
 #pragma unroll
@@ -592,34 +594,39 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
           row[16 * k + ln] = make_float4(st.acc[4 * k][i], st.acc[4 * k + 1][i], st.acc[4 * k + 2][i],
                                          st.acc[4 * k + 3][i]);
         if (ln == 0) {
-          mm[wid * G + head] = mrow[i];
-          ml[wid * G + head] = lrow[i];
+          mm[head * NW + wid] = mrow[i];
+          ml[head * NW + wid] = lrow[i];
         }
       }
     }
   }
   __syncthreads();
-  // per-head combine weights of the waves, then O_j = sum_w f_w O_w with
-  // f_w = 2^(m_w - M) / L (rows with l_w = 0 take no part)
-  float* fw = ml + NW * G;  // [NW][G]
-  if (tid < G) {
-    float M = -INFINITY;
+  // combine weights f_w = 2^(m_w - M) / L, one thread per (head, wave); rows
+  // with l_w = 0 take no part
+  float* fw = ml + G * NW;  // [G][NW]
+  if (tid < G * NW) {
+    const int head = tid / NW;
+    const float4* m4 = reinterpret_cast<const float4*>(mm + head * NW);
+    const float4* l4 = reinterpret_cast<const float4*>(ml + head * NW);
+    float M = -INFINITY, L = 0.0f;
 #pragma unroll
-    for (int w = 0; w < NW; ++w)
-      if (ml[w * G + tid] > 0.0f) M = fmaxf(M, mm[w * G + tid]);
-    float L = 0.0f;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) {
-      const float lw = ml[w * G + tid];
-      const float f = lw > 0.0f ? exp2f(mm[w * G + tid] - M) : 0.0f;
-      fw[w * G + tid] = f;
-      L += f * lw;
+    for (int w4 = 0; w4 < NW / 4; ++w4) {
+      const float4 a4 = m4[w4], b4 = l4[w4];
+      M = fmaxf(M, fmaxf(fmaxf(b4.x > 0.0f ? a4.x : -INFINITY, b4.y > 0.0f ? a4.y : -INFINITY),
+                         fmaxf(b4.z > 0.0f ? a4.z : -INFINITY, b4.w > 0.0f ? a4.w : -INFINITY)));
     }
-    const float inv = L > 0.0f ? 1.0f / L : 0.0f;
 #pragma unroll
-    for (int w = 0; w < NW; ++w) fw[w * G + tid] *= inv;
-    part[G * D + tid] = M;
-    part[G * D + G + tid] = L;
+    for (int w4 = 0; w4 < NW / 4; ++w4) {
+      const float4 a4 = m4[w4], b4 = l4[w4];
+      L += (b4.x > 0.0f ? exp2f(a4.x - M) * b4.x : 0.0f) + (b4.y > 0.0f ? exp2f(a4.y - M) * b4.y : 0.0f) +
+           (b4.z > 0.0f ? exp2f(a4.z - M) * b4.z : 0.0f) + (b4.w > 0.0f ? exp2f(a4.w - M) * b4.w : 0.0f);
+    }
+    const float lw = ml[tid];
+    fw[tid] = lw > 0.0f ? exp2f(mm[tid] - M) / L : 0.0f;
+    if (tid % NW == 0) {
+      part[G * D + head] = M;
+      part[G * D + G + head] = L;
+    }
   }
   __syncthreads();
   // four consecutive positions of a macc row are four consecutive channels
@@ -629,7 +636,7 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
     float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
     for (int w = 0; w < NW; ++w) {
-      const float f = fw[w * G + n];
+      const float f = fw[n * NW + w];
       const float4 x = *reinterpret_cast<const float4*>(macc + (w * G + n) * D + pos);
       o.x += f * x.x;
       o.y += f * x.y;
