@@ -371,14 +371,14 @@ void orc_tq3_bit_pos(int d, int q, int b, int k, int* byte_out, int* bit_out) {
 /* K code of (token t, channel c) -> (chunk byte offset, quad, pos) */
 static void kcode_place(int d, int t, int c, int64_t* chunk_off, int* q, int* b) {
   int per = d / 4, g = c / per, cc = c % per;
-  *chunk_off = (int64_t)(t * 4 + g) * chunk_bytes(d);
+  *chunk_off = (int64_t)(g * 16 + t) * chunk_bytes(d);
   *q = cc / 4;
   *b = cc % 4;
 }
 /* V code of (token t, channel c) */
 static void vcode_place(int d, int t, int c, int64_t* chunk_off, int* q, int* b) {
   int CL = d / 16, r = c / CL, m = c % CL, g = t / 4, u = t % 4;
-  *chunk_off = (int64_t)(r * 4 + g) * chunk_bytes(d);
+  *chunk_off = (int64_t)(g * 16 + r) * chunk_bytes(d);
   *q = m;
   *b = u;
 }

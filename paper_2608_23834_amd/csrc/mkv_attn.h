@@ -88,6 +88,43 @@ __device__ __forceinline__ void dma_region(uint32_t dst, const uint8_t* src, con
   static_assert(TAIL % 4 == 0 && TAIL <= 256, "tail must fit one 4-byte copy");
   if (TAIL > 0 && lane < TAIL / 4) dma4((R - TAIL) + 4 * lane, src, dst + (R - TAIL));
 }
+// One FP8 page-head (K then V, 16 d bytes each) into LDS with its 16-byte
+// blocks permuted so that the MFMA lanes read it without bank conflicts: LDS
+// block 64 w + l of each half holds the w-th 16 bytes of what lane l = 16 lg +
+// ln consumes (K: token ln, channels (d/4) lg + 16 w ..; V: the lane-chunk
+// (ln, lg), bytes 16 w ..).  2 d / 64 copies; the caller adds the scales.
+template <int D>
+__device__ __forceinline__ void dma_fp8_page(uint32_t dst, const uint8_t* src, int lane) {
+  constexpr int NI = D / 64;  // copies per half (16 d / 1024)
+  const int ln = lane & 15, lg = lane >> 4;
+  const uint32_t vk = 16u * (uint32_t)(ln * (D / 16) + lg * NI);
+  const uint32_t vv = 16u * (uint32_t)((ln * 4 + lg) * NI);
+#pragma unroll
+  for (int i = 0; i < NI; ++i) dma16<0>(vk, src + 16 * i, dst + 1024 * i);
+#pragma unroll
+  for (int i = 0; i < NI; ++i) dma16<0>(vv, src + 16 * D + 16 * i, dst + 16 * D + 1024 * i);
+}
+
+// The code dwords of chunk idx of a TQ3 code block in LDS (8-byte reads when
+// the chunk size allows).
+template <int NDW>
+__device__ __forceinline__ void read_chunk(uint32_t* dst, const uint8_t* block, int idx) {
+  constexpr int CB = 4 * NDW;
+  if constexpr (CB % 8 == 0) {
+    const uint2* p = reinterpret_cast<const uint2*>(block + idx * CB);
+#pragma unroll
+    for (int w = 0; w < NDW / 2; ++w) {
+      const uint2 x = p[w];
+      dst[2 * w] = x.x;
+      dst[2 * w + 1] = x.y;
+    }
+  } else {
+    const uint32_t* p = reinterpret_cast<const uint32_t*>(block + idx * CB);
+#pragma unroll
+    for (int w = 0; w < NDW; ++w) dst[w] = p[w];
+  }
+}
+
 // vector-memory instructions dma_region<R> issues per wave
 template <int R>
 constexpr int dma_ops() { return R / 1024 + (R % 1024 ? 1 : 0); }

@@ -155,6 +155,7 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   constexpr int R8 = (int)fp8_region_bytes(D);  // K codes then V codes
   constexpr int STAGE = 2 * R3;                 // a TQ3 page pair, or one FP8 page + scales
   constexpr int OPS3 = dma_ops<R3>(), OPS8 = dma_ops<R8>() + 1;
+  static_assert(dma_ops<R8>() == 2 * (D / 64), "dma_fp8_page issues 2 d / 64 copies");
   static_assert(R8 + 8 <= STAGE, "an FP8 page and its two scales fit one stage");
   static_assert(NW % 4 == 0, "per-head wave statistics are read as float4s");
   extern __shared__ __align__(16) uint8_t smem[];
@@ -311,7 +312,7 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
       dma_region<R3>(dst, tq3_l + ((int64_t)e.y * H + h) * R3, dl, lane);
       if (pair) dma_region<R3>(dst + R3, tq3_l + ((int64_t)e.w * H + h) * R3, dl, lane);
     } else {
-      dma_region<R8>(dst, fp8_l + ((int64_t)e.y * H + h) * R8, dl, lane);
+      dma_fp8_page<D>(dst, fp8_l + ((int64_t)e.y * H + h) * R8, lane);
       if (lane < 2) dma4(4 * lane, scl_l + ((int64_t)e.y * H + h) * 8, dst + R8);
     }
   };
@@ -415,13 +416,10 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
     const uint8_t* rb = pair ? ra + R3 : ra;
     const uint8_t* rown = row_b ? rb : ra;
     uint32_t kA[NDW], kB[NDW], vA[NDW], vB[NDW];
-#pragma unroll
-    for (int w = 0; w < NDW; ++w) {
-      kA[w] = reinterpret_cast<const uint32_t*>(ra + (ln * 4 + lg) * CB)[w];
-      kB[w] = reinterpret_cast<const uint32_t*>(rb + (ln * 4 + lg) * CB)[w];
-      vA[w] = reinterpret_cast<const uint32_t*>(ra + 6 * D + (ln * 4 + lg) * CB)[w];
-      vB[w] = reinterpret_cast<const uint32_t*>(rb + 6 * D + (ln * 4 + lg) * CB)[w];
-    }
+    read_chunk<NDW>(kA, ra, 16 * lg + ln);
+    read_chunk<NDW>(kB, rb, 16 * lg + ln);
+    read_chunk<NDW>(vA, ra + 6 * D, 16 * lg + ln);
+    read_chunk<NDW>(vB, rb + 6 * D, 16 * lg + ln);
     const uint2 gw = *reinterpret_cast<const uint2*>((col_b ? rb : ra) + 12 * D + 8 * lg);
     // per-channel V scale and zero of this lane's row page
     half2v sO[CL / 2], zO[CL / 2];
@@ -504,16 +502,17 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
     constexpr int KW = D / 16;  // dwords of K per lane (D/4 bytes)
     uint32_t kA[KW], vA[CL];
     {
-      const uint4* pk = reinterpret_cast<const uint4*>(ra + ln * D + (D / 4) * lg);
-      const uint4* pv = reinterpret_cast<const uint4*>(ra + PAGE * D + (ln * 4 + lg) * 4 * CL);
+      // block-permuted page (see dma_fp8_page): lane l's w-th 16 bytes at 64 w + l
+      const uint4* pk = reinterpret_cast<const uint4*>(ra) + lane;
+      const uint4* pv = reinterpret_cast<const uint4*>(ra + PAGE * D) + lane;
 #pragma unroll
       for (int w = 0; w < KW / 4; ++w) {
-        const uint4 x = pk[w];
+        const uint4 x = pk[64 * w];
         kA[4 * w] = x.x; kA[4 * w + 1] = x.y; kA[4 * w + 2] = x.z; kA[4 * w + 3] = x.w;
       }
 #pragma unroll
       for (int w = 0; w < CL / 4; ++w) {
-        const uint4 x = pv[w];
+        const uint4 x = pv[64 * w];
         vA[4 * w] = x.x; vA[4 * w + 1] = x.y; vA[4 * w + 2] = x.z; vA[4 * w + 3] = x.w;
       }
     }

@@ -49,9 +49,10 @@ __host__ __device__ inline CtrlLayout ctrl_layout(int n_fp8, int n_tq3, int d) {
 //  TQ3 region: 16*d + 32 bytes: K codes [0, 6d), V codes [6d, 12d), gamma
 //  fp16[16] at 12d, V scale fp16[d] at 12d+32, V zero fp16[d] at 14d+32.
 //  Codes live in "chunks" of 3d/32 bytes holding d/16 quads of 4 codes:
-//   K chunk (t, g) at (t*4+g)*3d/32: quad q, position b = channel d/4*g+4q+b
-//   V chunk (r, g) at (r*4+g)*3d/32: quad q = channel CL*r+q, position b =
-//   token 4g+b.
+//   K chunk (t, g) at (g*16+t)*3d/32: quad q, position b = channel d/4*g+4q+b
+//   V chunk (r, g) at (g*16+r)*3d/32: quad q = channel CL*r+q, position b =
+//   token 4g+b.  Chunks are ordered g-major: the 16 lanes of an MFMA row
+//   group read chunks 16g .. 16g+15, contiguous in LDS, without bank conflicts.
 //  Within a chunk of n_dw = 3d/128 dwords, quad q < 2*n_dw occupies bits
 //  [8b + 3(q%2), +3) of dword q/2; the remaining quads use bits 6-7 of every
 //  byte (see quad_sel below).

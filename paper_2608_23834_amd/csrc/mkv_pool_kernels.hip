@@ -786,12 +786,12 @@ __global__ __launch_bounds__(256) void migrate_encode_kernel(PoolView P) {
         const int t = tid >> 2, g = tid & 3;
         for (int q = 0; q < D / 16; ++q)
           for (int b = 0; b < 4; ++b) quad_put<NDW>(Dw, q, b, kc[t * D + (D / 4) * g + 4 * q + b]);
-        out = reg + (t * 4 + g) * CB;
+        out = reg + (g * 16 + t) * CB;
       } else {
         const int rr = (tid - 64) >> 2, g = (tid - 64) & 3;
         for (int q = 0; q < CL; ++q)
           for (int b = 0; b < 4; ++b) quad_put<NDW>(Dw, q, b, vc[(4 * g + b) * D + CL * rr + q]);
-        out = reg + 6 * D + (rr * 4 + g) * CB;
+        out = reg + 6 * D + (g * 16 + rr) * CB;
       }
 #pragma unroll
       for (int w = 0; w < NDW; ++w) reinterpret_cast<uint32_t*>(out)[w] = Dw[w];
