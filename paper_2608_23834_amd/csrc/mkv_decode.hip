@@ -160,7 +160,6 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   static_assert(NW % 4 == 0, "per-head wave statistics are read as float4s");
   extern __shared__ __align__(16) uint8_t smem[];
   __shared__ int4 s_stage[MAX_CHUNK_PAGES];  // {lp_a, id_a, lp_b, id_b}; id_b < 0: FP8 stage
-  __shared__ int s_cnt[2 * NW];
   __shared__ int s_next;  // next unclaimed stage (one-slot schedule)
   const PoolView& P = a.P;
   const int r = blockIdx.z, h = blockIdx.y, chunk = blockIdx.x;
@@ -213,119 +212,24 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   const int p0 = chunk < nco ? chunk * C : n_old + (chunk - nco) * CR;
   const int p1 = chunk < nco ? min(p0 + C, n_old) : min(p0 + CR, np);
   const int n_pg = p1 - p0;
-  int tg = -1, id = 0;
-  if (tid < n_pg) {
-    tg = a.tags[(int64_t)r * mp + p0 + tid];
-    id = a.bt[(int64_t)r * mp + p0 + tid];
-  }
-
-  // ---- 2. per-format compact lists of the chunk (logical order) -> stages
-  const bool is3 = tg == TAG_S, is8 = (tg == TAG_R || tg == TAG_A);
-  if (tid < n_pg && !is3 && !is8) atomicOr(&P.ctrl[CTRL_ERR], (int)MKV_DEVERR_BAD_TAG);
-  const uint64_t m3 = __ballot(is3), m8 = __ballot(is8);
-  if (lane == 0) {
-    s_cnt[wid] = __popcll(m3);
-    s_cnt[NW + wid] = __popcll(m8);
-  }
-  __syncthreads();
-  int b3 = 0, b8 = 0, n3 = 0, n8 = 0;
+  // ---- 2. per-format compact lists of the chunk (logical order) -> stages.
+  // Every wave reads the tags and ids of the whole chunk (lane l holds pages
+  // l + 64 k), so each finds its first stages from its own ballots and starts
+  // their copies before any workgroup barrier; wave 0 writes the stage list
+  // that later claims read from LDS.
+  constexpr int PW = MAX_CHUNK_PAGES / 64;
+  const uint64_t below = (1ull << lane) - 1ull;
+  int pg_lp[PW], pg_id[PW];
+  uint64_t m3w[PW], m8w[PW];
+  int n3 = 0, n8 = 0;
+  int tg_w[PW];
 #pragma unroll
-  for (int w = 0; w < NW; ++w) {
-    const int c3 = s_cnt[w], c8 = s_cnt[NW + w];
-    b3 += w < wid ? c3 : 0;
-    b8 += w < wid ? c8 : 0;
-    n3 += c3;
-    n8 += c8;
+  for (int k = 0; k < PW; ++k) {  // all loads in flight together (clamped to the chunk)
+    const int64_t pi = (int64_t)r * mp + p0 + min(lane + 64 * k, n_pg - 1);
+    tg_w[k] = a.tags[pi];
+    pg_id[k] = a.bt[pi];
   }
-  n3 = __builtin_amdgcn_readfirstlane(n3);
-  n8 = __builtin_amdgcn_readfirstlane(n8);
-  const int st3 = pair ? (n3 + 1) / 2 : n3;
-  const int n_st = st3 + n8;
-  if (is3 || is8) {
-    const uint64_t below = (1ull << lane) - 1ull;
-    int lp = p0 + tid;
-    if (id < 0 || id >= (is3 ? P.n_tq3 : P.n_fp8)) {
-      // out-of-range physical id: read page 0 instead, mask every token
-      atomicOr(&P.ctrl[CTRL_ERR], (int)MKV_DEVERR_RANGE);
-      id = 0;
-      lp = MASK_LP;
-    }
-    int2* s2 = reinterpret_cast<int2*>(s_stage);
-    if (is3) {
-      const int rank = b3 + __popcll(m3 & below);
-      if (pair) {
-        s2[rank] = make_int2(lp, id);  // stage rank / 2, half rank % 2
-        if (rank == n3 - 1 && !(rank & 1)) s2[rank + 1] = make_int2(MASK_LP, id);
-      } else {
-        s_stage[rank] = make_int4(lp, id, MASK_LP, id);
-      }
-    } else {
-      s_stage[st3 + b8 + __popcll(m8 & below)] = make_int4(lp, id, 0, -1);
-    }
-  }
-  if (tid == 0) s_next = NW;
-  __syncthreads();
-
-  // ---- 3. per-wave stream over stages [s0, s1)
-  WaveState<D> st;
-#pragma unroll
-  for (int m = 0; m < CL; ++m) st.acc[m] = float4v{0.f, 0.f, 0.f, 0.f};
-  st.m_run = -INFINITY;
-  st.l_run = 0.0f;
-  const int ln = lane & 15, lg = lane >> 4;
-  const int col_head = pair ? (ln & 7) : ln;
-  const bool col_valid = col_head < G;
-  const bool col_b = pair && ln >= 8;  // this column scores page b
-  const bool row_b = pair && lg >= 2;  // accumulator rows 4*lg+i hold page b
-  // Stage schedule.  One ring slot per wave: wave w starts with stage w and
-  // claims its next stage from an LDS counter when it begins a stage, so the
-  // waves of a SIMD finish together (stages differ in cost and the waves of a
-  // SIMD do not get equal issue shares).  Two slots: contiguous ranges.
-  const int s0 = wid * n_st / NW, s1 = (wid + 1) * n_st / NW;
-  const int jend = SLOTS == 1 ? n_st : s1;
-  auto claim = [&]() {
-    int v = 0;
-    if (lane == 0) v = atomicAdd(&s_next, 1);
-    return __builtin_amdgcn_readfirstlane(v);
-  };
-  const float smk = a.sm_log2;
-  const float4v zero4 = {0.f, 0.f, 0.f, 0.f};
-  half8 ones8;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) ones8[j] = (_Float16)1.0f;
-  const int layer = a.layer;
-  const uint8_t* tq3_l = P.tq3 + (int64_t)layer * P.n_tq3 * H * R3;
-  const uint8_t* fp8_l = P.fp8 + (int64_t)layer * P.n_fp8 * H * R8;
-  const uint8_t* scl_l = reinterpret_cast<const uint8_t*>(P.fp8_scales + (int64_t)layer * P.n_fp8 * H * 2);
-  uint8_t* wring = ring + wid * SLOTS * STAGE;
-  const uint32_t wring_lds = __builtin_amdgcn_readfirstlane(
-      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)wring);
-  auto stage_at = [&](int j) {
-    const int4 e = s_stage[j];
-    return make_int4(__builtin_amdgcn_readfirstlane(e.x), __builtin_amdgcn_readfirstlane(e.y),
-                     __builtin_amdgcn_readfirstlane(e.z), __builtin_amdgcn_readfirstlane(e.w));
-  };
-  const DmaLanes dl = {16u * lane, 4096u + 16u * lane};
-  auto issue = [&](const int4& e, int slot) {
-    const uint32_t dst = wring_lds + slot * STAGE;
-    if (e.w >= 0) {
-      dma_region<R3>(dst, tq3_l + ((int64_t)e.y * H + h) * R3, dl, lane);
-      if (pair) dma_region<R3>(dst + R3, tq3_l + ((int64_t)e.w * H + h) * R3, dl, lane);
-    } else {
-      dma_fp8_page<D>(dst, fp8_l + ((int64_t)e.y * H + h) * R8, lane);
-      if (lane < 2) dma4(4 * lane, scl_l + ((int64_t)e.y * H + h) * 8, dst + R8);
-    }
-  };
-  int jc = SLOTS == 1 ? min(wid, n_st) : s0;  // stage this wave processes next
-  if (SLOTS == 1) {
-    if (jc < n_st) issue(stage_at(jc), 0);
-  } else {
-#pragma unroll
-    for (int k = 0; k < SLOTS; ++k)
-      if (s0 + k < s1) issue(stage_at(s0 + k), k);
-  }
-
-  // ---- query operands, built while the first stages are in flight, in MFMA
+  // ---- query operands, built while the page-table loads are in flight, in MFMA
   // lane order: q?[s][lane] holds channels (D/4) lg + 8 s + j, j < 8, of
   // column ln's head (ln = lane % 16, lg = lane / 16)
   {
@@ -383,6 +287,139 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
         }
       }
     }
+  }
+
+#pragma unroll
+  for (int k = 0; k < PW; ++k) {
+    const int pi = lane + 64 * k;
+    const int tg = pi < n_pg ? tg_w[k] : -1;
+    int id = pg_id[k];
+    const bool is3 = tg == TAG_S, is8 = (tg == TAG_R || tg == TAG_A);
+    if (wid == 0 && pi < n_pg && !is3 && !is8) atomicOr(&P.ctrl[CTRL_ERR], (int)MKV_DEVERR_BAD_TAG);
+    int lp = p0 + pi;
+    if ((is3 || is8) && (id < 0 || id >= (is3 ? P.n_tq3 : P.n_fp8))) {
+      // out-of-range physical id: read page 0 instead, mask every token
+      if (wid == 0) atomicOr(&P.ctrl[CTRL_ERR], (int)MKV_DEVERR_RANGE);
+      id = 0;
+      lp = MASK_LP;
+    }
+    pg_lp[k] = lp;
+    pg_id[k] = id;
+    m3w[k] = __ballot(is3);
+    m8w[k] = __ballot(is8);
+    n3 += __popcll(m3w[k]);
+    n8 += __popcll(m8w[k]);
+  }
+  const int st3 = pair ? (n3 + 1) / 2 : n3;
+  const int n_st = st3 + n8;
+  // (logical page, id) of the page of rank q among the chunk's TQ3 (fmt 0) or
+  // FP8 (fmt 1) pages
+  auto page_of = [&](int fmt, int q) {
+    int2 res = make_int2(MASK_LP, 0);
+    int base = 0;
+#pragma unroll
+    for (int k = 0; k < PW; ++k) {
+      const uint64_t m = fmt ? m8w[k] : m3w[k];
+      const int cnt = __popcll(m);
+      if (q >= base && q < base + cnt) {
+        const uint64_t hit = __ballot(((m >> lane) & 1ull) && base + __popcll(m & below) == q);
+        const int src = __builtin_amdgcn_readfirstlane(__ffsll((unsigned long long)hit) - 1);
+        res = make_int2(__builtin_amdgcn_readlane(pg_lp[k], src), __builtin_amdgcn_readlane(pg_id[k], src));
+      }
+      base += cnt;
+    }
+    return res;
+  };
+  // stage j -> {lp_a, id_a, lp_b, id_b}; id_b < 0 marks an FP8 stage (the
+  // same entries wave 0 writes to s_stage)
+  auto stage_of = [&](int j) {
+    if (j < st3) {
+      const int2 ea = page_of(0, pair ? 2 * j : j);
+      const int2 eb = (pair && 2 * j + 1 < n3) ? page_of(0, 2 * j + 1) : make_int2(MASK_LP, ea.y);
+      return make_int4(ea.x, ea.y, eb.x, eb.y);
+    }
+    const int2 e8 = page_of(1, j - st3);
+    return make_int4(e8.x, e8.y, 0, -1);
+  };
+  if (wid == 0) {
+    int2* s2 = reinterpret_cast<int2*>(s_stage);
+    int base3 = 0, base8 = 0;
+#pragma unroll
+    for (int k = 0; k < PW; ++k) {
+      if ((m3w[k] >> lane) & 1ull) {
+        const int rank = base3 + __popcll(m3w[k] & below);
+        if (pair) {
+          s2[rank] = make_int2(pg_lp[k], pg_id[k]);  // stage rank / 2, half rank % 2
+          if (rank == n3 - 1 && !(rank & 1)) s2[rank + 1] = make_int2(MASK_LP, pg_id[k]);
+        } else {
+          s_stage[rank] = make_int4(pg_lp[k], pg_id[k], MASK_LP, pg_id[k]);
+        }
+      }
+      if ((m8w[k] >> lane) & 1ull)
+        s_stage[st3 + base8 + __popcll(m8w[k] & below)] = make_int4(pg_lp[k], pg_id[k], 0, -1);
+      base3 += __popcll(m3w[k]);
+      base8 += __popcll(m8w[k]);
+    }
+  }
+  if (tid == 0) s_next = NW;
+
+  // ---- 3. per-wave stream over stages [s0, s1)
+  WaveState<D> st;
+#pragma unroll
+  for (int m = 0; m < CL; ++m) st.acc[m] = float4v{0.f, 0.f, 0.f, 0.f};
+  st.m_run = -INFINITY;
+  st.l_run = 0.0f;
+  const int ln = lane & 15, lg = lane >> 4;
+  const int col_head = pair ? (ln & 7) : ln;
+  const bool col_valid = col_head < G;
+  const bool col_b = pair && ln >= 8;  // this column scores page b
+  const bool row_b = pair && lg >= 2;  // accumulator rows 4*lg+i hold page b
+  // Stage schedule.  One ring slot per wave: wave w starts with stage w and
+  // claims its next stage from an LDS counter when it begins a stage, so the
+  // waves of a SIMD finish together (stages differ in cost and the waves of a
+  // SIMD do not get equal issue shares).  Two slots: contiguous ranges.
+  const int s0 = wid * n_st / NW, s1 = (wid + 1) * n_st / NW;
+  const int jend = SLOTS == 1 ? n_st : s1;
+  auto claim = [&]() {
+    int v = 0;
+    if (lane == 0) v = atomicAdd(&s_next, 1);
+    return __builtin_amdgcn_readfirstlane(v);
+  };
+  const float smk = a.sm_log2;
+  const float4v zero4 = {0.f, 0.f, 0.f, 0.f};
+  half8 ones8;
+#pragma unroll
+  for (int j = 0; j < 8; ++j) ones8[j] = (_Float16)1.0f;
+  const int layer = a.layer;
+  const uint8_t* tq3_l = P.tq3 + (int64_t)layer * P.n_tq3 * H * R3;
+  const uint8_t* fp8_l = P.fp8 + (int64_t)layer * P.n_fp8 * H * R8;
+  const uint8_t* scl_l = reinterpret_cast<const uint8_t*>(P.fp8_scales + (int64_t)layer * P.n_fp8 * H * 2);
+  uint8_t* wring = ring + wid * SLOTS * STAGE;
+  const uint32_t wring_lds = __builtin_amdgcn_readfirstlane(
+      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)wring);
+  auto stage_at = [&](int j) {
+    const int4 e = s_stage[j];
+    return make_int4(__builtin_amdgcn_readfirstlane(e.x), __builtin_amdgcn_readfirstlane(e.y),
+                     __builtin_amdgcn_readfirstlane(e.z), __builtin_amdgcn_readfirstlane(e.w));
+  };
+  const DmaLanes dl = {16u * lane, 4096u + 16u * lane};
+  auto issue = [&](const int4& e, int slot) {
+    const uint32_t dst = wring_lds + slot * STAGE;
+    if (e.w >= 0) {
+      dma_region<R3>(dst, tq3_l + ((int64_t)e.y * H + h) * R3, dl, lane);
+      if (pair) dma_region<R3>(dst + R3, tq3_l + ((int64_t)e.w * H + h) * R3, dl, lane);
+    } else {
+      dma_fp8_page<D>(dst, fp8_l + ((int64_t)e.y * H + h) * R8, lane);
+      if (lane < 2) dma4(4 * lane, scl_l + ((int64_t)e.y * H + h) * 8, dst + R8);
+    }
+  };
+  int jc = SLOTS == 1 ? min(wid, n_st) : s0;  // stage this wave processes next
+  if (SLOTS == 1) {
+    if (jc < n_st) issue(stage_of(jc), 0);
+  } else {
+#pragma unroll
+    for (int k = 0; k < SLOTS; ++k)
+      if (s0 + k < s1) issue(stage_of(s0 + k), k);
   }
 
   __syncthreads();  // query operands visible to every wave
@@ -695,7 +732,7 @@ __global__ __launch_bounds__(D) void decode_merge_kernel(int G, int H, int max_c
 
 // dynamic LDS a decode workgroup may use: 160 KiB per CU minus the static arrays
 static constexpr size_t lds_limit() {
-  return 160 * 1024 - sizeof(int4) * MAX_CHUNK_PAGES - sizeof(int) * 2 * NW_MAX - 256;
+  return 160 * 1024 - sizeof(int4) * MAX_CHUNK_PAGES - 256;  // s_stage; s_next and slack
 }
 
 hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t* q,
