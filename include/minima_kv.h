@@ -174,8 +174,8 @@ mkv_status paged_attn_workspace_init(void* ws, size_t ws_bytes, hipStream_t stre
  * [n_req][n_q_heads][d]; lse: device fp32 [n_req][n_q_heads] (natural log of
  * the softmax denominator, scores in units of q.k/sqrt(d)) or NULL.
  * ws: device, >= paged_attn_workspace_bytes(pool, n_req, max_pages, 0); it
- * holds the split partials (O(splits x heads x d) floats).  q and ws must be
- * 16-byte aligned (MKV_EINVAL otherwise).  max_pages is at most 262144.  An
+ * holds the split partials (O(splits x heads x d) floats).  q, out and ws must
+ * be 16-byte aligned (MKV_EINVAL otherwise).  max_pages is at most 262144.  An
  * invalid seq_len sets the error word and gives that request zero outputs; a
  * page below seq_len with an invalid tag or an out-of-range physical id sets
  * the error word and is left out of the softmax.  The waves of a split claim

@@ -189,7 +189,7 @@ mkv_status paged_attn_decode(mkv_pool* pool, int32_t layer, int32_t n_req, const
                              size_t ws_bytes, hipStream_t stream) {
   if (!pool || !q || !block_table || !tags || !seq_lens || !out || !ws) return MKV_EINVAL;
   if (n_req < 1 || max_pages < 1) return MKV_EINVAL;
-  if (!aligned16(q) || !aligned16(ws)) return MKV_EINVAL;
+  if (!aligned16(q) || !aligned16(out) || !aligned16(ws)) return MKV_EINVAL;
   if (layer < 0 || layer >= pool->n_layers) return MKV_ERANGE;
   if (n_req > 65535 || max_pages > 1024 * 256) return MKV_ERANGE;
   if (ws_bytes < decode_ws_bytes(n_req, max_pages, pool->n_kv_heads, pool->group, pool->d, pool->recent))

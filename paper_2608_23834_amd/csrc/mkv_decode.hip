@@ -81,12 +81,14 @@ DecodeShape decode_shape(int n_req, int max_pages, int n_kv_heads, int recent) {
 }
 
 // workspace: the partials, one (O_j[G][d], m_j[G], l_j[G]) block per chunk
-// slot; every slot of the grid is written on every call (l_j = 0 when the
-// chunk is empty or past the request's end), so the merge needs no count
+// slot, padded to a multiple of 4 floats (16-byte aligned O rows); every slot
+// of the grid is written on every call (l_j = 0 when the chunk is empty or
+// past the request's end), so the merge needs no count
+__host__ __device__ constexpr int part_stride(int G, int D) { return (G * (D + 2) + 3) / 4 * 4; }
 
 size_t decode_ws_bytes(int n_req, int max_pages, int n_kv_heads, int group, int d, int recent) {
   DecodeShape s = decode_shape(n_req, max_pages, n_kv_heads, recent);
-  return (size_t)n_req * n_kv_heads * s.max_chunks * group * (d + 2) * sizeof(float);
+  return (size_t)n_req * n_kv_heads * s.max_chunks * part_stride(group, d) * sizeof(float);
 }
 
 template <int D>
@@ -193,7 +195,7 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
 #pragma unroll
   for (int i = 0; i < QV; ++i) sg[i] = P.sigma[QV * lane + i];
 
-  float* part = a.partials + (((int64_t)r * H + h) * a.max_chunks + chunk) * G * (D + 2);
+  float* part = a.partials + (((int64_t)r * H + h) * a.max_chunks + chunk) * part_stride(G, D);
   const int S = a.seq_lens[r];
   if (S < 1 || S > mp * PAGE) {
     if (chunk == 0 && h == 0 && tid == 0) atomicOr(&P.ctrl[CTRL_ERR], (int)MKV_DEVERR_RANGE);
@@ -684,50 +686,67 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
 }
 
 // Merge stage (Eq. softmax-merge): one workgroup per (query head of the
-// group, KV head, request), one thread per channel.  Every chunk slot's
-// (m_j, l_j, O_j[c]) is loaded in batches of 16 (all loads of a batch in
-// flight together; slots with l_j = 0 contribute nothing) and folded into a
-// running (M, L, O) that is rescaled once per batch.
+// group, KV head, request), one thread per four channels.  The O_j rows of up
+// to 32 chunk slots are loaded together (one memory round trip for the usual
+// grid) while thread j stages slot j's (m_j, l_j) in LDS; slots with l_j = 0
+// contribute nothing; a running (M, L, O) is rescaled once per batch.
 template <int D>
-__global__ __launch_bounds__(D) void decode_merge_kernel(int G, int H, int max_chunks,
-                                                        const float* partials, float* out,
-                                                        float* lse) {
-  constexpr int B = 16;
-  const int n = blockIdx.x, h = blockIdx.y, r = blockIdx.z, c = threadIdx.x;
+__global__ __launch_bounds__(D / 4) void decode_merge_kernel(int G, int H, int max_chunks,
+                                                            const float* partials, float* out,
+                                                            float* lse) {
+  constexpr int B = 32;
+  static_assert(D / 4 >= B, "one thread stages each slot's (m, l)");
+  __shared__ float s_m[B], s_l[B];
+  const int n = blockIdx.x, h = blockIdx.y, r = blockIdx.z, c4 = threadIdx.x;
   const int Hq = H * G;
-  const int stride = G * (D + 2);
+  const int stride = part_stride(G, D);
   const float* base = partials + ((int64_t)r * H + h) * max_chunks * stride;
-  float M = -INFINITY, L = 0.0f, O = 0.0f;
+  float M = -INFINITY, L = 0.0f;
+  float4 O = make_float4(0.f, 0.f, 0.f, 0.f);
   for (int k0 = 0; k0 < max_chunks; k0 += B) {
-    float mk[B], lk[B], ok[B];
+    float4 ok[B];
 #pragma unroll
     for (int j = 0; j < B; ++j) {
       const int k = min(k0 + j, max_chunks - 1);
-      const float* pk = base + (int64_t)k * stride;
-      mk[j] = pk[G * D + n];
-      lk[j] = k0 + j < max_chunks ? pk[G * D + G + n] : 0.0f;
-      ok[j] = pk[n * D + c];
+      ok[j] = reinterpret_cast<const float4*>(base + (int64_t)k * stride + n * D)[c4];
     }
+    if (c4 < B) {
+      const float* pk = base + (int64_t)min(k0 + c4, max_chunks - 1) * stride;
+      s_m[c4] = pk[G * D + n];
+      s_l[c4] = k0 + c4 < max_chunks ? pk[G * D + G + n] : 0.0f;
+    }
+    __syncthreads();
     float Mb = M;
 #pragma unroll
     for (int j = 0; j < B; ++j)
-      if (lk[j] > 0.0f) Mb = fmaxf(Mb, mk[j]);
-    if (Mb == -INFINITY) continue;  // nothing in this batch, nothing before it
-    const float f = M == -INFINITY ? 0.0f : exp2f(M - Mb);
-    L *= f;
-    O *= f;
+      if (s_l[j] > 0.0f) Mb = fmaxf(Mb, s_m[j]);
+    if (Mb != -INFINITY) {  // else nothing in this batch, nothing before it
+      const float f = M == -INFINITY ? 0.0f : exp2f(M - Mb);
+      L *= f;
+      O.x *= f;
+      O.y *= f;
+      O.z *= f;
+      O.w *= f;
 #pragma unroll
-    for (int j = 0; j < B; ++j)
-      if (lk[j] > 0.0f) {
-        const float w = exp2f(mk[j] - Mb) * lk[j];
-        L += w;
-        O += w * ok[j];
+      for (int j = 0; j < B; ++j) {
+        const float lj = s_l[j];
+        if (lj > 0.0f) {
+          const float w = exp2f(s_m[j] - Mb) * lj;
+          L += w;
+          O.x += w * ok[j].x;
+          O.y += w * ok[j].y;
+          O.z += w * ok[j].z;
+          O.w += w * ok[j].w;
+        }
       }
-    M = Mb;
+      M = Mb;
+    }
+    __syncthreads();  // s_m, s_l are rewritten by the next batch
   }
   const int64_t row = (int64_t)r * Hq + h * G + n;
-  out[row * D + c] = L > 0.0f ? O / L : 0.0f;
-  if (lse && c == 0) lse[row] = L > 0.0f ? (M + log2f(L)) * 0.69314718055994531f : -INFINITY;
+  const float inv = L > 0.0f ? 1.0f / L : 0.0f;
+  reinterpret_cast<float4*>(out + row * D)[c4] = make_float4(O.x * inv, O.y * inv, O.z * inv, O.w * inv);
+  if (lse && c4 == 0) lse[row] = L > 0.0f ? (M + log2f(L)) * 0.69314718055994531f : -INFINITY;
 }
 
 // dynamic LDS a decode workgroup may use: 160 KiB per CU minus the static arrays
@@ -785,10 +804,10 @@ hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t
   if (e != hipSuccess) return e;
   if (ev && (e = hipEventRecord(ev[1], s)) != hipSuccess) return e;
   if (P.d == 256)
-    hipLaunchKernelGGL(decode_merge_kernel<256>, mgrid, dim3(256), 0, s, P.group, P.n_kv_heads,
+    hipLaunchKernelGGL(decode_merge_kernel<256>, mgrid, dim3(64), 0, s, P.group, P.n_kv_heads,
                        sh.max_chunks, a.partials, out, lse);
   else
-    hipLaunchKernelGGL(decode_merge_kernel<128>, mgrid, dim3(128), 0, s, P.group, P.n_kv_heads,
+    hipLaunchKernelGGL(decode_merge_kernel<128>, mgrid, dim3(32), 0, s, P.group, P.n_kv_heads,
                        sh.max_chunks, a.partials, out, lse);
   e = hipGetLastError();
   if (e == hipSuccess && ev) e = hipEventRecord(ev[2], s);
