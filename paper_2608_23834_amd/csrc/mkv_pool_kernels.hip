@@ -567,13 +567,16 @@ __global__ __launch_bounds__(64) void append_step_kernel(PoolView P, int layer_s
     small_task_load_old<D>(T, P, id, lane);
     small_task_run<D>(T, P, id, s_img, s_lut, lane);
   }
-  // ---- arrive; the last wave records the fresh pages
-  __threadfence();
+  // ---- arrive; the last wave records the fresh pages.  Only the order of
+  // every wave's table reads before the last wave's table writes matters:
+  // a wave counts itself once all its loads have returned (no device-scope
+  // fence, which would write back this die's L2).  The page codes and the
+  // table are published to later kernels by the end of this kernel.
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   int prev = 0;
   if (lane == 0) prev = atomicAdd(&P.ctrl[CTRL_APPEND_ARRIVE], 1);
   prev = __shfl(prev, 0, 64);
   if (prev != (int)gridDim.x - 1) return;
-  __threadfence();
   if (bad) {
     if (lane == 0) atomicOr(&P.ctrl[CTRL_ERR], bad);
   } else {
