@@ -34,6 +34,7 @@ sys.path.insert(0, ROOT)
 import mkv_workloads as wl  # noqa: E402
 
 HBM_PEAK = 8.0e12  # MI355X HBM3E, bytes/s
+MFMA_F16_PEAK = 2.5e15  # MI355X dense f16 MFMA, flop/s
 PAGE = 16
 
 
@@ -160,6 +161,54 @@ def cpu_baseline(w, budget_s=25.0):
             "cpu": _cpu_model()}
 
 
+def chunk_bench(mk, torch, reps=5):
+    """Chunked prefill (paged_attn_chunk) on the chunk workload at full size:
+    8 requests, each with a 512-query chunk appended after 65,024 context
+    tokens (mixed FP8/TQ3 pages), one layer.  HIP events on the current
+    stream around `reps` calls; MFMA share = algorithmic causal-attention
+    flops (4 d flops per query-key pair and head) / time / dense f16 peak."""
+    w = wl.workload(5)
+    lens = list(w.ctx)
+    n_req, nq = len(lens), 512
+    w0 = wl.scaled(w, tuple(L - nq for L in lens), n_layers=1, name=w.name + "-context")
+    pool, bt, tags, am, mp = build_state(w0, 1, nq + 16, mk, torch)
+    ks, vs = zip(*(wl.kv_layer(w, 0, nq, token_offset=r * 1_000_000 + L - nq)
+                   for r, L in enumerate(lens)))
+    sb = torch.tensor([L - nq for L in lens], dtype=torch.int32, device="cuda")
+    cu = torch.tensor(np.r_[0, np.cumsum([nq] * n_req)], dtype=torch.int32, device="cuda")
+    mk.kv_append_fp8(pool, 0, bt, tags, sb, cu,
+                     torch.from_numpy(np.concatenate(ks).view(np.int16)).cuda(),
+                     torch.from_numpy(np.concatenate(vs).view(np.int16)).cuda())
+    q = torch.from_numpy(wl.q_chunk(w, 0, nq).view(np.int16)).cuda()
+    sl = torch.tensor(lens, dtype=torch.int32, device="cuda")
+    out = torch.empty((n_req * nq, w.n_q_heads, w.head_dim), device="cuda")
+    ws = mk.workspace(pool, n_req, mp, n_req * nq)
+    mk.paged_attn_chunk(pool, 0, q, cu, bt, tags, sl, out, ws)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(reps):
+        mk.paged_attn_chunk(pool, 0, q, cu, bt, tags, sl, out, ws)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    err = mk.kv_pool_check_errors(pool)
+    if err:
+        raise RuntimeError(f"device error word {err:#x} in the chunk benchmark")
+    us = e0.elapsed_time(e1) / reps * 1e3
+    pairs = sum(nq * (L - nq) + nq * (nq + 1) // 2 for L in lens)  # causal (query, key) pairs
+    flops = 4.0 * pairs * w.n_q_heads * w.head_dim
+    tf = flops / (us * 1e-6) / 1e12
+    del pool
+    return {"workload": f"{w.name}: {n_req} requests x {nq}-query chunk after "
+                        f"{lens[0] - nq} context tokens, 1 layer, {w.n_q_heads}/{w.n_kv_heads} "
+                        f"heads, d {w.head_dim}",
+            "us_per_call": round(us, 1), "algorithmic_tflop": round(flops / 1e12, 3),
+            "tflop_per_s": round(tf, 1), "mfma_peak_tflop_per_s": MFMA_F16_PEAK / 1e12,
+            "mfma_frac": round(tf * 1e12 / MFMA_F16_PEAK, 4),
+            "kernel": "chunk_kernel<256> (+ partition_kernel)"}
+
+
 def _cpu_model():
     try:
         for line in open("/proc/cpuinfo"):
@@ -178,6 +227,8 @@ def main():
     ap.add_argument("--cfg", type=int, default=3)
     ap.add_argument("--layers", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-chunk", action="store_true",
+                    help="skip the chunked-prefill measurement")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run one 1 GiB device-to-device copy (calibrates HBM byte counters)")
     args = ap.parse_args()
@@ -322,6 +373,10 @@ def main():
         torch.cuda.synchronize()
         res["copy_probe_bytes"] = 1 << 30
         del a_, b_
+    if not args.no_chunk:
+        del pool
+        torch.cuda.empty_cache()
+        res["chunk"] = chunk_bench(mk, torch)
     if not args.no_cpu_baseline and args.cfg == 3:
         res["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(res), flush=True)
