@@ -1,11 +1,13 @@
 // Mixed-format paged decode attention (Sec. 3.3, Eq. softmax-merge; Sec. 4.1
 // direct fused decode) for gfx950.
 //
-// One launch per layer.  Grid (chunk, KV head, request); 512 threads = 8
-// wave64s, one workgroup per CU.  Chunks are ranges of logical pages: the old
-// part of a request (pages wholly outside the Recent window) in ranges of C
-// pages, the Recent part in ranges of C/2 (FP8 pages carry twice the bytes of
-// TQ3 pages, so every chunk moves about the same amount).  Each workgroup
+// One launch per layer.  Grid (chunk, KV head, request); one workgroup of
+// 12 (or 8) wave64s per CU.  Chunks are ranges of logical pages of equal
+// cost: a page wholly outside the Recent window (a TQ3 page unless it is an
+// anchor) costs 1 unit, a Recent (FP8) page 2 units -- one FP8 page, twice
+// the bytes, takes the scan about as long as a pair of TQ3 pages; the unit
+// count per chunk is chosen so that the launch is about one workgroup per
+// CU.  Each workgroup
 //  1. loads the GQA group's queries and builds two fp16 MFMA operands in LDS:
 //     the plain queries for FP8 pages and the rotated ones for TQ3 pages
 //     (q_rot = R q, exact algebra since k_hat = gamma R^T mu_c, so keys are
@@ -46,7 +48,15 @@ template <bool PAIR> struct DecodeCfg {
   static constexpr int NT = 64 * NW;
 };
 constexpr int NW_MAX = 12;
-constexpr int MAX_CHUNK_PAGES = 256;   // upper bound of C
+// Wave priority by progress through a stage (claimed -> 1, scores done -> 2,
+// weights done -> 3): among the waves of a SIMD the one furthest into its
+// stage issues first, so stages finish roughly in the order they were claimed.
+#define STAGE_PRIO(p) __builtin_amdgcn_s_setprio(p)
+#define NCH_OF(pair) ((pair) ? 8 : 16)
+constexpr int MAX_CHUNK_PAGES = 256;   // pages a chunk may span
+// cost of a page in chunk units: wholly outside the Recent window / Recent
+constexpr int COST_OLD = 1, COST_REC = 2;
+constexpr int COST_MIN = COST_OLD < COST_REC ? COST_OLD : COST_REC;
 constexpr int MASK_LP = 0x3FFFFFFF / PAGE;  // logical page whose tokens are all masked
 
 struct DecodeArgs {
@@ -59,24 +69,38 @@ struct DecodeArgs {
   float* out;
   float* lse;
   float* partials;
-  int cpages, max_chunks;
+  int cunits, max_chunks;  // cost units per chunk, chunk slots per (request, KV head)
   float sm_log2;  // log2(e) / sqrt(d)
 };
 
-// Pages per chunk C: about one workgroup per CU for the whole launch when the
-// requests fill their tables, never below 16 or above MAX_CHUNK_PAGES.
+// Cost of a request's pages: n_old pages wholly outside the Recent window and
+// n_pages - n_old inside it.  Non-decreasing in the sequence length, so the
+// table width bounds every request's cost.
+__host__ __device__ inline int64_t request_cost(int64_t n_pages, int64_t n_old) {
+  return COST_OLD * n_old + COST_REC * (n_pages - n_old);
+}
+__host__ __device__ inline int64_t old_pages(int64_t seq_len, int recent) {
+  return seq_len > recent ? (seq_len - recent) / PAGE : 0;
+}
+// first page whose cost prefix is at least c
+__device__ inline int page_at_cost(int64_t c, int n_old) {
+  const int64_t co = (int64_t)COST_OLD * n_old;
+  if (c <= co) return (int)((c + COST_OLD - 1) / COST_OLD);
+  return n_old + (int)((c - co + COST_REC - 1) / COST_REC);
+}
+
+// Units per chunk: about one workgroup per CU for the whole launch when the
+// requests fill their tables (256 CUs), never below 16 old pages' worth and
+// never spanning more than MAX_CHUNK_PAGES pages.
 DecodeShape decode_shape(int n_req, int max_pages, int n_kv_heads, int recent) {
   DecodeShape s;
-  const int64_t ph = (int64_t)n_req * max_pages * n_kv_heads;
-  int64_t c = (ph + 255) / 256;
-  c = (c + 15) / 16 * 16;
-  if (c < 16) c = 16;
-  if (c > MAX_CHUNK_PAGES) c = MAX_CHUNK_PAGES;
-  s.cpages = (int)c;
-  // Recent pages of a request: at most recent/16 + 3 (whole and partial pages)
-  int64_t rec = (int64_t)recent / PAGE + 3;
-  if (rec > max_pages) rec = max_pages;
-  s.max_chunks = (int)((max_pages + c - 1) / c + (rec + c / 2 - 1) / (c / 2));
+  const int64_t tmax = request_cost(max_pages, old_pages((int64_t)max_pages * PAGE, recent));
+  const int64_t pairs = (int64_t)n_req * n_kv_heads;
+  int64_t u = (tmax * pairs + 255) / 256;
+  if (u < 16 * COST_OLD) u = 16 * COST_OLD;
+  if (u > (int64_t)(MAX_CHUNK_PAGES - 1) * COST_MIN) u = (int64_t)(MAX_CHUNK_PAGES - 1) * COST_MIN;
+  s.cunits = (int)u;
+  s.max_chunks = (int)((tmax + u - 1) / u);
   return s;
 }
 
@@ -151,7 +175,7 @@ __device__ __forceinline__ void p_operand(const float* p, bool row_is_b, half8& 
 template <int D, bool PAIR>
 __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeArgs a) {
   constexpr int NW = DecodeCfg<PAIR>::NW, NT = DecodeCfg<PAIR>::NT, SLOTS = DecodeCfg<PAIR>::SLOTS;
-  constexpr int NCH = PAIR ? 8 : 16;  // query heads a score tile holds
+  constexpr int NCH = NCH_OF(PAIR);  // query heads a score tile holds
   constexpr int CL = D / 16, NDW = 3 * D / 128, CB = 3 * D / 32, NS = D / 32, QV = D / 64;
   constexpr int R3 = (int)tq3_region_bytes(D);  // K codes, V codes, gamma, V scale, V zero
   constexpr int R8 = (int)fp8_region_bytes(D);  // K codes then V codes
@@ -163,6 +187,10 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   extern __shared__ __align__(16) uint8_t smem[];
   __shared__ int4 s_stage[MAX_CHUNK_PAGES];  // {lp_a, id_a, lp_b, id_b}; id_b < 0: FP8 stage
   __shared__ int s_next;  // next unclaimed stage (one-slot schedule)
+  // per (head, wave): running max, denominator, combine weight (epilogue)
+  __shared__ __align__(16) float s_mlf[3][16 * NW_MAX];
+  static_assert(NCH_OF(PAIR) * D * 4 <= SLOTS * 2 * (int)tq3_region_bytes(D),
+                "a wave's merged rows fit its own ring slot");
   const PoolView& P = a.P;
   const int r = blockIdx.z, h = blockIdx.y, chunk = blockIdx.x;
   const int tid = threadIdx.x, lane = tid & 63;
@@ -196,24 +224,15 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   for (int i = 0; i < QV; ++i) sg[i] = P.sigma[QV * lane + i];
 
   float* part = a.partials + (((int64_t)r * H + h) * a.max_chunks + chunk) * part_stride(G, D);
-  const int S = a.seq_lens[r];
-  if (S < 1 || S > mp * PAGE) {
-    if (chunk == 0 && h == 0 && tid == 0) atomicOr(&P.ctrl[CTRL_ERR], (int)MKV_DEVERR_RANGE);
-    if (tid < G) part[G * D + G + tid] = 0.0f;  // empty partial: the merge writes zeros
-    return;
-  }
-  // ---- chunk -> logical page range
-  const int np = (S + PAGE - 1) / PAGE;
-  const int n_old = S > P.recent ? (S - P.recent) / PAGE : 0;  // pages wholly outside the window
-  const int C = a.cpages, CR = a.cpages / 2;
-  const int nco = (n_old + C - 1) / C, ncr = (np - n_old + CR - 1) / CR;
-  if (chunk >= nco + ncr) {
-    if (tid < G) part[G * D + G + tid] = 0.0f;  // slot past the request's end
-    return;
-  }
-  const int p0 = chunk < nco ? chunk * C : n_old + (chunk - nco) * CR;
-  const int p1 = chunk < nco ? min(p0 + C, n_old) : min(p0 + CR, np);
-  const int n_pg = p1 - p0;
+  // ---- chunk -> logical page range: equal-cost ranges over the table width,
+  // known before any load, so the sequence length and the chunk's tags and
+  // ids are loaded together; pages at or past the request's end are dropped
+  // once the length is in (chunk < max_chunks, so the range is not empty)
+  const int n_old_t = (int)old_pages((int64_t)mp * PAGE, P.recent);
+  const int64_t c0 = (int64_t)chunk * a.cunits;
+  const int p0 = page_at_cost(c0, n_old_t);
+  const int p1 = page_at_cost(min(request_cost(mp, n_old_t), c0 + a.cunits), n_old_t);
+  const int n_pr = p1 - p0;
   // ---- 2. per-format compact lists of the chunk (logical order) -> stages.
   // Every wave reads the tags and ids of the whole chunk (lane l holds pages
   // l + 64 k), so each finds its first stages from its own ballots and starts
@@ -227,9 +246,20 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   int tg_w[PW];
 #pragma unroll
   for (int k = 0; k < PW; ++k) {  // all loads in flight together (clamped to the chunk)
-    const int64_t pi = (int64_t)r * mp + p0 + min(lane + 64 * k, n_pg - 1);
+    const int64_t pi = (int64_t)r * mp + p0 + min(lane + 64 * k, n_pr - 1);
     tg_w[k] = a.tags[pi];
     pg_id[k] = a.bt[pi];
+  }
+  const int S = a.seq_lens[r];
+  if (S < 1 || S > mp * PAGE) {
+    if (chunk == 0 && h == 0 && tid == 0) atomicOr(&P.ctrl[CTRL_ERR], (int)MKV_DEVERR_RANGE);
+    if (tid < G) part[G * D + G + tid] = 0.0f;  // empty partial: the merge writes zeros
+    return;
+  }
+  const int n_pg = min(p1, (S + PAGE - 1) / PAGE) - p0;  // pages of the chunk before the end
+  if (n_pg <= 0) {
+    if (tid < G) part[G * D + G + tid] = 0.0f;  // slot past the request's end
+    return;
   }
   // ---- query operands, built while the page-table loads are in flight, in MFMA
   // lane order: q?[s][lane] holds channels (D/4) lg + 8 s + j, j < 8, of
@@ -382,9 +412,18 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   // SIMD do not get equal issue shares).  Two slots: contiguous ranges.
   const int s0 = wid * n_st / NW, s1 = (wid + 1) * n_st / NW;
   const int jend = SLOTS == 1 ? n_st : s1;
+  // A SIMD issues the instructions of its oldest wave first: waves 0-3 of a
+  // 12-wave workgroup get most of their SIMD, waves 8-11 what is left.  Near
+  // the end of the stage list the younger waves stop claiming (a stage they
+  // take would finish last), so the last stages run on the faster waves.
   auto claim = [&]() {
     int v = 0;
-    if (lane == 0) v = atomicAdd(&s_next, 1);
+    if (lane == 0) {
+      const int rank = wid / 4;
+      const int keep = rank == 0 ? 0 : rank == 1 ? 4 : 12;  // stages left for older waves
+      const int seen = __atomic_load_n(&s_next, __ATOMIC_RELAXED);
+      v = (n_st - seen <= keep) ? n_st : atomicAdd(&s_next, 1);
+    }
     return __builtin_amdgcn_readfirstlane(v);
   };
   const float smk = a.sm_log2;
@@ -417,7 +456,10 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   };
   int jc = SLOTS == 1 ? min(wid, n_st) : s0;  // stage this wave processes next
   if (SLOTS == 1) {
-    if (jc < n_st) issue(stage_of(jc), 0);
+    // the oldest wave of each SIMD copies its first stage now, the others
+    // after the barrier: the first copies of a launch queue behind every
+    // workgroup's, and each SIMD should get its first stage early
+    if (wid < 4 && jc < n_st) issue(stage_of(jc), 0);
   } else {
 #pragma unroll
     for (int k = 0; k < SLOTS; ++k)
@@ -425,6 +467,7 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   }
 
   __syncthreads();  // query operands visible to every wave
+  if (SLOTS == 1 && wid >= 4 && jc < n_st) issue(stage_of(jc), 0);
   // Wait for stage j to land in its slot; with two slots stage j + 1 may stay
   // in flight (the allowed count is the number of copies it was issued as).
   auto begin_stage = [&](int j) {
@@ -447,6 +490,7 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
     const int jn = SLOTS == 1 ? claim() : j + 1;  // next stage of this wave
     const int jr = SLOTS == 1 ? jn : j + SLOTS;   // stage that refills this slot
     const int4 e = stage_at(j);
+    STAGE_PRIO(1);
     begin_stage(j);
     const bool refill = jr < jend;
     const int4 e2 = refill ? stage_at(jr) : e;
@@ -497,7 +541,9 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
         sc[i] = (col_valid && 4 * lg + i < vcnt) ? sv * (float)gh[i] * smk : -INFINITY;
       }
     }
+    STAGE_PRIO(2);
     softmax_step<D>(st, sc, lg);
+    STAGE_PRIO(3);
     half8 pT, pTl;
     p_operand(sc, col_b, pT, pTl);
     // PV: the codes enter the MFMA exactly (a code byte read as an E4M3
@@ -533,6 +579,7 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
     const int jn = SLOTS == 1 ? claim() : j + 1;
     const int jr = SLOTS == 1 ? jn : j + SLOTS;
     const int4 e = stage_at(j);
+    STAGE_PRIO(1);
     begin_stage(j);
     const bool refill = jr < jend;
     const int4 e2 = refill ? stage_at(jr) : e;
@@ -571,7 +618,9 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
 #pragma unroll
       for (int i = 0; i < 4; ++i) sc[i] = (col_valid && 4 * lg + i < vcnt) ? sa[i] * kk : -INFINITY;
     }
+    STAGE_PRIO(2);
     softmax_step<D>(st, sc, lg);
+    STAGE_PRIO(3);
     half8 pT, pTl;
     p_operand(sc, col_b, pT, pTl);
     const half2v z2 = {(_Float16)0.0f, (_Float16)0.0f};
@@ -614,19 +663,22 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
       mrow[i] = M;
     }
   }
-  // macc row (wave, head) keeps channel c = CL ln + 4 k + t at position
+  // Each wave writes its merged rows into its own ring slot as soon as its
+  // scan is done (its copies have all been waited for), so no barrier is
+  // needed before the store and the merge work overlaps the other waves'
+  // scans.  Row (wave, head) keeps channel c = CL ln + 4 k + t at position
   // (16 k + ln) 4 + t: every lane stores float4s and the 16 lanes of a row
-  // store consecutive 16-byte words (no bank conflicts)
-  float* macc = reinterpret_cast<float*>(ring);  // [NW][G][D]
-  float* mm = macc + NW * G * D;                 // [G][NW]
-  float* ml = mm + G * NW;                       // [G][NW]
-  __syncthreads();  // every wave is done with its ring (all copies waited for)
+  // store consecutive 16-byte words (no bank conflicts).
+  float* mm = s_mlf[0];  // [G][NW]
+  float* ml = s_mlf[1];  // [G][NW]
+  float* fw = s_mlf[2];  // [G][NW]
   if (!row_b) {
+    float* macc = reinterpret_cast<float*>(wring);  // [G][D]
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int head = 4 * lg + i;
       if (head < G) {
-        float4* row = reinterpret_cast<float4*>(macc + (wid * G + head) * D);
+        float4* row = reinterpret_cast<float4*>(macc + head * D);
 #pragma unroll
         for (int k = 0; k < CL / 4; ++k)
           row[16 * k + ln] = make_float4(st.acc[4 * k][i], st.acc[4 * k + 1][i], st.acc[4 * k + 2][i],
@@ -641,7 +693,6 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   __syncthreads();
   // combine weights f_w = 2^(m_w - M) / L, one thread per (head, wave); rows
   // with l_w = 0 take no part
-  float* fw = ml + G * NW;  // [G][NW]
   if (tid < G * NW) {
     const int head = tid / NW;
     const float4* m4 = reinterpret_cast<const float4*>(mm + head * NW);
@@ -675,7 +726,7 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
 #pragma unroll
     for (int w = 0; w < NW; ++w) {
       const float f = fw[n * NW + w];
-      const float4 x = *reinterpret_cast<const float4*>(macc + (w * G + n) * D + pos);
+      const float4 x = *reinterpret_cast<const float4*>(ring + w * SLOTS * STAGE + (n * D + pos) * 4);
       o.x += f * x.x;
       o.y += f * x.y;
       o.z += f * x.z;
@@ -751,7 +802,8 @@ __global__ __launch_bounds__(D / 4) void decode_merge_kernel(int G, int H, int m
 
 // dynamic LDS a decode workgroup may use: 160 KiB per CU minus the static arrays
 static constexpr size_t lds_limit() {
-  return 160 * 1024 - sizeof(int4) * MAX_CHUNK_PAGES - 256;  // s_stage; s_next and slack
+  // s_stage, s_mlf; s_next and slack
+  return 160 * 1024 - sizeof(int4) * MAX_CHUNK_PAGES - 3 * 16 * NW_MAX * sizeof(float) - 256;
 }
 
 hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t* q,
@@ -771,17 +823,16 @@ hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t
   a.out = out;
   a.lse = lse;
   a.partials = reinterpret_cast<float*>(ws);
-  a.cpages = sh.cpages;
+  a.cunits = sh.cunits;
   a.max_chunks = sh.max_chunks;
   a.sm_log2 = 1.4426950408889634f / sqrtf((float)P.d);
-  // dynamic LDS: two query operands, then the page ring (reused by the wave merge)
+  // dynamic LDS: three query operands, then the page ring (reused by the wave merge)
   const bool pair = P.group <= 8;
   const int nw = pair ? DecodeCfg<true>::NW : DecodeCfg<false>::NW;
   const int slots = pair ? DecodeCfg<true>::SLOTS : DecodeCfg<false>::SLOTS;
   const size_t qop_b = 3 * (size_t)(P.d / 32) * 64 * 16;
   const size_t ring_b = (size_t)nw * slots * 2 * tq3_region_bytes(P.d);
-  const size_t merge_b = ((size_t)nw * P.group * P.d + 3 * nw * P.group) * sizeof(float);
-  const size_t lds = qop_b + (ring_b > merge_b ? ring_b : merge_b);
+  const size_t lds = qop_b + ring_b;  // the epilogue reuses each wave's ring slot
   if (lds > lds_limit()) return hipErrorInvalidValue;
   const void* kern = P.d == 256 ? (pair ? (const void*)decode_kernel<256, true> : (const void*)decode_kernel<256, false>)
                                 : (pair ? (const void*)decode_kernel<128, true> : (const void*)decode_kernel<128, false>);

@@ -66,7 +66,7 @@ hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
 
 // mkv_decode.hip
 struct DecodeShape {
-  int cpages, max_chunks;
+  int cunits, max_chunks;
 };
 DecodeShape decode_shape(int n_req, int max_pages, int n_kv_heads, int recent);
 size_t decode_ws_bytes(int n_req, int max_pages, int n_kv_heads, int group, int d, int recent);
