@@ -213,3 +213,25 @@ def q_chunk(w: Workload, layer: int, n_per_req: int, step: int = 0) -> np.ndarra
 
 def max_pages_for(w: Workload, extra_tokens: int = 0) -> int:
     return n_pages_of(max(w.ctx) + extra_tokens)
+
+
+def kv_layer_device(w: Workload, layer: int, n_tok: int, device="cuda"):
+    """bf16 K and V for ``n_tok`` tokens of one layer drawn on the device
+    (torch's counter-based generator, seeded from the workload), shape
+    [n_tok][Hkv][d] int16 bits.  Same distribution as ``kv_layer`` (N(0,1)
+    times the per-(layer, head, channel) log-normal scales); used where the
+    host generator would be too slow (the 64-request batch holds 2.2 M
+    tokens).  Callers that check against the oracle copy rows back to the
+    host, so both sides read identical bytes."""
+    import torch
+    H, d = w.n_kv_heads, w.head_dim
+    out = []
+    for key, skey in ((_K_K, _K_SK), (_K_V, _K_SV)):
+        g = torch.Generator(device=device)
+        g.manual_seed(int(np.random.SeedSequence(w.seed, spawn_key=(key, layer)).generate_state(1)[0]))
+        x = torch.randn((n_tok, H, d), generator=g, device=device, dtype=torch.float32)
+        if not w.outlier_k_channels:
+            x *= torch.from_numpy(_channel_scales(w, skey, layer, H)).to(device)[None]
+        out.append(x.to(torch.bfloat16).view(torch.int16))
+        del x
+    return out[0], out[1]

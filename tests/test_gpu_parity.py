@@ -8,6 +8,7 @@ import numpy as np
 import pytest
 
 import mkv_workloads as wl
+from _harness import max_abs
 
 pytestmark = pytest.mark.gpu
 
@@ -81,6 +82,80 @@ def test_long_pair_full_size(torch_cuda):
         assert (tags[r] == 0).sum() == 128
         assert (tags[r] == 1).sum() == 8 + 36
         assert (tags[r] == 2).sum() == 3516
+
+
+def test_batch64_config_full_size(torch_cuda):
+    """Config 4 at full size: 64 requests with lengths drawn from U[4096,
+    65536], pages of every request interleaved in one pool through shuffled
+    free stacks, one layer, in the launch configuration of the benchmark's
+    decode call.  The GPU holds all 64 requests; the oracle models a sample
+    of them (the shortest, the longest and two others) from the same K/V
+    bytes, copied back from the device.  Physical ids differ between the two
+    pools (the oracle does not see the other requests), so pages are
+    compared bit for bit through each side's block table."""
+    import oracle
+    import paper_2608_23834_amd as mk
+    torch = torch_cuda
+    w = wl.workload(4)
+    lens = list(w.ctx)
+    n_req, H, d = len(lens), w.n_kv_heads, w.head_dim
+    mp = max((L + 15) // 16 for L in lens)
+    tot = sum((L + 15) // 16 for L in lens) + 8
+    print(f"\n[case] {w.name}: {n_req} requests, {sum(lens)} tokens, {tot} pages", flush=True)
+    gp = mk.Pool(1, w.n_q_heads, H, d, tot, tot, w.recent, wl.rot_signs(w),
+                 wl.free_order(w, tot, "fp8"), wl.free_order(w, tot, "tq3"))
+    bt = torch.full((n_req, mp), -1, dtype=torch.int32, device="cuda")
+    tags = torch.full((n_req, mp), 0xFF, dtype=torch.uint8, device="cuda")
+    K, V = wl.kv_layer_device(w, 0, sum(lens))
+    cu = np.r_[0, np.cumsum(lens)].astype(np.int32)
+    sl = np.array(lens, np.int32)
+    mk.kv_append_fp8(gp, 0, bt, tags, torch.zeros(n_req, dtype=torch.int32, device="cuda"),
+                     torch.from_numpy(cu).cuda(), K, V)
+    am = wl.anchor_mask(w, mp)
+    mk.kv_migrate_to_tq3(gp, bt, tags, torch.from_numpy(am).cuda(), torch.from_numpy(sl).cuda())
+    q = wl.q_decode(w, 0)
+    out = torch.full((n_req, w.n_q_heads, d), float("nan"), device="cuda")
+    ws = mk.workspace(gp, n_req, mp)
+    mk.paged_attn_decode(gp, 0, torch.from_numpy(q.view(np.int16)).cuda(), bt, tags,
+                         torch.from_numpy(sl).cuda(), out, None, ws)
+    torch.cuda.synchronize()
+    assert mk.kv_pool_check_errors(gp) == 0
+    out = out.cpu().numpy()
+    assert np.all(np.isfinite(out))
+    g_bt, g_tags = bt.cpu().numpy(), tags.cpu().numpy()
+    rng = np.random.default_rng(4)
+    rest = [r for r in range(n_req) if r not in (int(np.argmin(lens)), int(np.argmax(lens)))]
+    sample = sorted({int(np.argmin(lens)), int(np.argmax(lens)), *rng.choice(rest, 2, replace=False).tolist()})
+    s_lens = [lens[r] for r in sample]
+    s_mp = max((L + 15) // 16 for L in s_lens)
+    s_tot = sum((L + 15) // 16 for L in s_lens) + 8
+    print(f"  oracle sample {sample} lens {s_lens}", flush=True)
+    orc = oracle.Pool(1, w.n_q_heads, H, d, s_tot, s_tot, w.recent, wl.rot_signs(w),
+                      wl.free_order(w, s_tot, "fp8"), wl.free_order(w, s_tot, "tq3"))
+    o_bt = np.full((len(sample), s_mp), -1, np.int32)
+    o_tags = np.full((len(sample), s_mp), 0xFF, np.uint8)
+    ks = np.concatenate([K[cu[r]:cu[r + 1]].cpu().numpy() for r in sample]).view(np.uint16)
+    vs = np.concatenate([V[cu[r]:cu[r + 1]].cpu().numpy() for r in sample]).view(np.uint16)
+    s_cu = np.r_[0, np.cumsum(s_lens)].astype(np.int32)
+    assert orc.append(0, o_bt, o_tags, np.zeros(len(sample), np.int32), s_cu, ks[None], vs[None]) == 0
+    assert orc.migrate(o_bt, o_tags, am[sample][:, :s_mp], np.array(s_lens, np.int32)) >= 0
+    g8, gs, g3 = gp.fp8_view(), gp.fp8_scales_view(), gp.tq3_view()
+    for i, r in enumerate(sample):
+        npg = (lens[r] + 15) // 16
+        assert np.array_equal(g_tags[r, :npg], o_tags[i, :npg]), f"tags of request {r}"
+        for fmt, pick in (("fp8", g_tags[r, :npg] < 2), ("tq3", g_tags[r, :npg] == 2)):
+            gid = torch.from_numpy(g_bt[r, :npg][pick].astype(np.int64)).cuda()
+            oid = o_bt[i, :npg][pick]
+            if fmt == "fp8":
+                assert np.array_equal(g8[0, gid].cpu().numpy(), orc.fp8[0, oid]), f"fp8 pages of {r}"
+                assert np.array_equal(gs[0, gid].cpu().numpy().view(np.uint32),
+                                      orc.fp8_scale[0, oid].view(np.uint32)), f"fp8 scales of {r}"
+            else:
+                assert np.array_equal(g3[0, gid].cpu().numpy(), orc.tq3[0, oid]), f"tq3 pages of {r}"
+    ref, _ = orc.decode(0, q[sample], o_bt, o_tags, np.array(s_lens, np.int32))
+    err = max_abs(out[sample], ref)
+    print(f"  sampled requests: max|dO| {err:.3e}", flush=True)
+    assert err <= TOL, err
 
 
 def test_decode_steps_with_appends(torch_cuda):
@@ -224,9 +299,11 @@ def test_device_errors_fail_closed(torch_cuda):
     assert mk.kv_pool_check_errors(gp, clear=True) & mk.DEVERR["RANGE"]
 
 
-def _run_chunk_case(w, lens, n_q, recent=None, sample_stride=1):
+def _run_chunk_case(w, lens, n_q, recent=None, sample_stride=1, migrate_after=False):
     """Context of each request appended and migrated, then its chunk of n_q[r]
-    tokens appended as FP8; chunk attention of those queries vs the oracle."""
+    tokens appended as FP8; chunk attention of those queries vs the oracle;
+    optionally the pages that left the Recent window with the chunk are then
+    re-encoded FP8 -> TQ3 and compared bit for bit."""
     from _harness import Twin, max_abs
     print(f"\n[chunk case] {w.name} lens={lens[:6]} n_q={n_q[:6]} W={recent}", flush=True)
     tw = Twin(w, lens=lens, recent=recent)
@@ -244,6 +321,13 @@ def _run_chunk_case(w, lens, n_q, recent=None, sample_stride=1):
     assert err <= TOL, err
     import paper_2608_23834_amd as mk
     assert mk.kv_pool_check_errors(tw.gpu) == 0
+    if migrate_after:
+        before = (tw.otags == 2).sum()
+        tw.migrate()
+        tw.check_tables()
+        n8, n3 = tw.check_pages()
+        print(f"  after the chunk: {int((tw.otags == 2).sum() - before)} pages re-encoded to TQ3, "
+              f"live fp8 {n8} tq3 {n3}", flush=True)
     return tw, res
 
 
@@ -262,7 +346,14 @@ def test_chunk_ragged_d256(torch_cuda):
 
 def test_chunk_config5_full_size(torch_cuda):
     """Config 5 at full size: 8 requests, a 512-query chunk each against
-    65,536 tokens of mixed pages (sampled queries: every 64th and the last)."""
+    65,536 tokens of mixed pages (sampled queries: every 64th and the last),
+    then the migration of the pages the chunk pushed out of the Recent
+    window, bit-exact."""
     w = wl.workload(5)
-    tw, res = _run_chunk_case(w, list(w.ctx), [512] * 8, sample_stride=64)
+    tw, res = _run_chunk_case(w, list(w.ctx), [512] * 8, sample_stride=64, migrate_after=True)
     assert np.all(np.isfinite(res["out"]))
+    # 512 new tokens push 32 pages per request out of the 1,024-token window;
+    # anchors among them stay FP8
+    tags = tw.otags
+    for r in range(8):
+        assert (tags[r] == 0).sum() == 1024 // 16
