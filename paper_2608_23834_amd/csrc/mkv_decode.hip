@@ -42,9 +42,13 @@ namespace mkv {
 // waves, each with a one-stage ring slot (a stage is moved into registers as
 // soon as it lands and the slot refilled at once); otherwise 8 waves with two
 // slots.  Either way one workgroup fills a CU's LDS.
+#ifndef MKV_PAIR_NW
+#define MKV_PAIR_NW 12
+#define MKV_PAIR_SLOTS 1
+#endif
 template <bool PAIR> struct DecodeCfg {
-  static constexpr int NW = PAIR ? 12 : 8;  // waves per workgroup
-  static constexpr int SLOTS = PAIR ? 1 : 2;  // ring slots per wave
+  static constexpr int NW = PAIR ? MKV_PAIR_NW : 8;  // waves per workgroup
+  static constexpr int SLOTS = PAIR ? MKV_PAIR_SLOTS : 2;  // ring slots per wave
   static constexpr int NT = 64 * NW;
 };
 constexpr int NW_MAX = 12;
@@ -121,32 +125,44 @@ struct WaveState {
   float m_run;          // running max of this lane's column (base-2 units)
   float l_run;          // partial denominator over this lane's tokens
 };
+// Initial reference max: finite, so 2^(s - m) is 0 for masked scores (s = -inf)
+// and never NaN; a column with l = 0 takes no part in any merge.
+constexpr float M_INIT = -1.0e30f;
+
+// Column layout of a score tile (and row layout of the PV accumulator).  With
+// at most six heads per KV head, heads sit in columns 4 k + i, i < 3, so that
+// accumulator element 3 of every lane is padding and its updates are skipped.
+template <bool G6>
+__device__ __forceinline__ int head_of_col(int c) {
+  if constexpr (G6) return (c & 3) == 3 ? -1 : 3 * (c >> 2) + (c & 3);
+  else return c;
+}
 
 // Online-softmax step: sc[4] are this lane's base-2 scores (tokens 4*lg + i of
 // the page that owns column ln).  Weights are returned in place.  The
 // accumulator rows 4*lg + i belong to columns 4*lg + i, whose rescale factors
 // are fetched from those lanes when the reference max moves.
-template <int D>
+template <int D, int NI>
 __device__ __forceinline__ void softmax_step(WaveState<D>& st, float* sc, int lg) {
   const float mx = max4rows(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])));
   // lazy rescale: keep the reference max while new scores stay within 2^8
   const bool need = mx > st.m_run + 8.0f;
   if (__any(need)) {
     const float m_new = need ? mx : st.m_run;
-    const float alpha = st.m_run == -INFINITY ? 0.0f : exp2f(st.m_run - m_new);
+    const float alpha = __builtin_amdgcn_exp2f(st.m_run - m_new);
     st.l_run *= alpha;
     st.m_run = m_new;
     float ar[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) ar[i] = __shfl(alpha, 4 * lg + i, 64);
+    for (int i = 0; i < NI; ++i) ar[i] = __shfl(alpha, 4 * lg + i, 64);
 #pragma unroll
     for (int m = 0; m < D / 16; ++m)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) st.acc[m][i] *= ar[i];
+      for (int i = 0; i < NI; ++i) st.acc[m][i] *= ar[i];
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    sc[i] = exp2_safe(sc[i], st.m_run);
+    sc[i] = __builtin_amdgcn_exp2f(sc[i] - st.m_run);  // -inf -> 0
     st.l_run += sc[i];
   }
 }
@@ -158,21 +174,27 @@ __device__ __forceinline__ void softmax_step(WaveState<D>& st, float* sc, int lg
 // rounding remainder): a token holding most of a row's mass has, against a
 // lagging reference max, a weight that fp16 alone would round by up to 2^-12
 // of that token's value.
+// hi is the weight truncated to fp16, lo the truncated remainder (together 22
+// significant bits).
 __device__ __forceinline__ void p_operand(const float* p, bool row_is_b, half8& hi, half8& lo) {
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const _Float16 v = (_Float16)p[j];
-    const _Float16 w = (_Float16)(p[j] - (float)v);
-    hi[j] = row_is_b ? (_Float16)0.0f : v;
-    hi[4 + j] = row_is_b ? v : (_Float16)0.0f;
-    lo[j] = row_is_b ? (_Float16)0.0f : w;
-    lo[4 + j] = row_is_b ? w : (_Float16)0.0f;
-  }
+  typedef __fp16 h2t __attribute__((ext_vector_type(2)));
+  const h2t h01 = __builtin_amdgcn_cvt_pkrtz(p[0], p[1]);
+  const h2t h23 = __builtin_amdgcn_cvt_pkrtz(p[2], p[3]);
+  const h2t l01 = __builtin_amdgcn_cvt_pkrtz(p[0] - (float)h01[0], p[1] - (float)h01[1]);
+  const h2t l23 = __builtin_amdgcn_cvt_pkrtz(p[2] - (float)h23[0], p[3] - (float)h23[1]);
+  typedef uint32_t u4v __attribute__((ext_vector_type(4)));
+  const uint32_t a0 = __builtin_bit_cast(uint32_t, h01), a1 = __builtin_bit_cast(uint32_t, h23);
+  const uint32_t b0 = __builtin_bit_cast(uint32_t, l01), b1 = __builtin_bit_cast(uint32_t, l23);
+  const u4v H = row_is_b ? u4v{0u, 0u, a0, a1} : u4v{a0, a1, 0u, 0u};
+  const u4v L = row_is_b ? u4v{0u, 0u, b0, b1} : u4v{b0, b1, 0u, 0u};
+  hi = __builtin_bit_cast(half8, H);
+  lo = __builtin_bit_cast(half8, L);
 }
 
 // PAIR (query group of at most 8 heads): two pages share one score tile,
-// columns [0, 8) scoring page a and [8, 16) page b.
-template <int D, bool PAIR>
+// columns [0, 8) scoring page a and [8, 16) page b.  G6: at most six heads
+// (see head_of_col).
+template <int D, bool PAIR, bool G6>
 __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeArgs a) {
   constexpr int NW = DecodeCfg<PAIR>::NW, NT = DecodeCfg<PAIR>::NT, SLOTS = DecodeCfg<PAIR>::SLOTS;
   constexpr int NCH = NCH_OF(PAIR);  // query heads a score tile holds
@@ -204,21 +226,23 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   half8* qpl = qrlo + NS * 64;                    // plain query (bf16 -> fp16 is exact)
   uint8_t* ring = smem + 3 * NS * 64 * 16;
 
-  // ---- 1. queries: wave w owns query heads w and w + NW below NCH; lane l
-  // holds channels QV l .. QV l + QV - 1.  The loads go out before anything
-  // else so their latency hides behind the page-table loads.
+  // ---- 1. queries: wave w owns score columns w and w + NW below NCH (the
+  // head of a column: head_of_col); lane l holds channels QV l .. QV l + QV -
+  // 1.  The loads go out before anything else so their latency hides behind
+  // the page-table loads.
   static_assert(QV == 2 || QV == 4, "QV bf16 channels per lane form one 4- or 8-byte load");
   using qvec = typename std::conditional<QV == 4, uint2, uint32_t>::type;
   float qx[2][QV];
   int sg[QV];
 #pragma unroll
   for (int ps = 0; ps < 2; ++ps) {
-    const int n = wid + NW * ps;
-    const int nn = n < G ? n : G - 1;  // loads stay in bounds; values of n >= G are dropped
+    const int hd = head_of_col<G6>(wid + NW * ps);
+    const bool ok = hd >= 0 && hd < G;
+    const int nn = ok ? hd : 0;  // loads stay in bounds; padding columns get zeros
     const qvec raw = *reinterpret_cast<const qvec*>(a.q + ((int64_t)r * Hq + h * G + nn) * D + QV * lane);
     const uint16_t* rh = reinterpret_cast<const uint16_t*>(&raw);
 #pragma unroll
-    for (int i = 0; i < QV; ++i) qx[ps][i] = n < G ? bf16_to_f32(rh[i]) : 0.0f;
+    for (int i = 0; i < QV; ++i) qx[ps][i] = ok ? bf16_to_f32(rh[i]) : 0.0f;
   }
 #pragma unroll
   for (int i = 0; i < QV; ++i) sg[i] = P.sigma[QV * lane + i];
@@ -268,11 +292,15 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
     _Float16* qr = reinterpret_cast<_Float16*>(qrot);
     _Float16* ql = reinterpret_cast<_Float16*>(qrlo);
     _Float16* qp = reinterpret_cast<_Float16*>(qpl);
-    const float qscale = rsqrtf((float)D);  // R = d^-1/2 H diag(sigma)
+    // R = d^-1/2 H diag(sigma); the rotated query also carries the softmax
+    // scale log2(e)/sqrt(d), so TQ3 scores come out in base-2 units
+    const float qscale = rsqrtf((float)D) * a.sm_log2;
 #pragma unroll
     for (int ps = 0; ps < 2; ++ps) {
       const int n = wid + NW * ps;
       if (n >= NCH) break;  // wave-uniform
+      const int hd = head_of_col<G6>(n);
+      const bool ok = hd >= 0 && hd < G;
       float xr[QV];
 #pragma unroll
       for (int i = 0; i < QV; ++i) xr[i] = qx[ps][i] * (float)sg[i];
@@ -304,10 +332,10 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
         const int c = QV * lane + i;
         const int lgc = c / (D / 4), sc = (c % (D / 4)) / 8, j = c % 8;
         // q_rot as an fp16 pair hi + lo (fp32 accuracy through two MFMAs)
-        const float xq = n < G ? xr[i] * qscale : 0.0f;
+        const float xq = ok ? xr[i] * qscale : 0.0f;
         const _Float16 vr = (_Float16)xq;
         const _Float16 vl = (_Float16)(xq - (float)vr);
-        const _Float16 vp = (_Float16)(n < G ? qx[ps][i] : 0.0f);
+        const _Float16 vp = (_Float16)(ok ? qx[ps][i] : 0.0f);
         const int e0 = ((sc * 64) + lgc * 16 + n) * 8 + j;
         qr[e0] = vr;
         ql[e0] = vl;
@@ -395,23 +423,25 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   }
   if (tid == 0) s_next = NW;
 
-  // ---- 3. per-wave stream over stages [s0, s1)
+  // ---- 3. per-wave stream over the claimed stages
   WaveState<D> st;
 #pragma unroll
   for (int m = 0; m < CL; ++m) st.acc[m] = float4v{0.f, 0.f, 0.f, 0.f};
-  st.m_run = -INFINITY;
+  st.m_run = M_INIT;
   st.l_run = 0.0f;
   const int ln = lane & 15, lg = lane >> 4;
-  const int col_head = pair ? (ln & 7) : ln;
-  const bool col_valid = col_head < G;
+  const int col_head = head_of_col<G6>(pair ? (ln & 7) : ln);
+  const bool col_valid = col_head >= 0 && col_head < G;
   const bool col_b = pair && ln >= 8;  // this column scores page b
   const bool row_b = pair && lg >= 2;  // accumulator rows 4*lg+i hold page b
-  // Stage schedule.  One ring slot per wave: wave w starts with stage w and
-  // claims its next stage from an LDS counter when it begins a stage, so the
-  // waves of a SIMD finish together (stages differ in cost and the waves of a
-  // SIMD do not get equal issue shares).  Two slots: contiguous ranges.
-  const int s0 = wid * n_st / NW, s1 = (wid + 1) * n_st / NW;
-  const int jend = SLOTS == 1 ? n_st : s1;
+  const float col_bias = col_valid ? 0.0f : -INFINITY;  // masks padding columns
+  const float fp8_bias = (col_valid && !col_b) ? 0.0f : -INFINITY;  // FP8 stages: page a only
+  constexpr int NI = G6 ? 3 : 4;  // accumulator elements that hold a head
+  // Stage schedule: wave w starts with stage w and claims each later stage
+  // from an LDS counter when it begins a stage, so the waves of a SIMD finish
+  // together (stages differ in cost and the waves of a SIMD do not get equal
+  // issue shares).  With two slots per wave the claimed stage after the
+  // current one is already in flight.
   // A SIMD issues the instructions of its oldest wave first: waves 0-3 of a
   // 12-wave workgroup get most of their SIMD, waves 8-11 what is left.  Near
   // the end of the stage list the younger waves stop claiming (a stage they
@@ -454,24 +484,24 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
       if (lane < 2) dma4(4 * lane, scl_l + ((int64_t)e.y * H + h) * 8, dst + R8);
     }
   };
-  int jc = SLOTS == 1 ? min(wid, n_st) : s0;  // stage this wave processes next
-  if (SLOTS == 1) {
-    // the oldest wave of each SIMD copies its first stage now, the others
-    // after the barrier: the first copies of a launch queue behind every
-    // workgroup's, and each SIMD should get its first stage early
-    if (wid < 4 && jc < n_st) issue(stage_of(jc), 0);
-  } else {
-#pragma unroll
-    for (int k = 0; k < SLOTS; ++k)
-      if (s0 + k < s1) issue(stage_of(s0 + k), k);
-  }
+  int jc = min(wid, n_st);  // stage this wave processes next
+  int jq = n_st;            // two slots: the claimed stage after jc (in flight)
+  // the oldest wave of each SIMD copies its first stage now, the others after
+  // the barrier: the first copies of a launch queue behind every workgroup's,
+  // and each SIMD should get its first stage early
+  if (wid < 4 && jc < n_st) issue(stage_of(jc), 0);
 
-  __syncthreads();  // query operands visible to every wave
-  if (SLOTS == 1 && wid >= 4 && jc < n_st) issue(stage_of(jc), 0);
-  // Wait for stage j to land in its slot; with two slots stage j + 1 may stay
-  // in flight (the allowed count is the number of copies it was issued as).
+  __syncthreads();  // query operands and the stage list visible to every wave
+  if (wid >= 4 && jc < n_st) issue(stage_at(jc), 0);
+  if (SLOTS == 2 && jc < n_st) {
+    jq = claim();
+    if (jq < n_st) issue(stage_at(jq), 1);
+  }
+  // Wait for stage j to land in its slot; with two slots the stage after it
+  // may stay in flight (the allowed count is the number of copies it was
+  // issued as).
   auto begin_stage = [&](int j) {
-    const int nops = (SLOTS > 1 && j + 1 < s1) ? (stage_at(j + 1).w >= 0 ? (pair ? 2 : 1) * OPS3 : OPS8) : 0;
+    const int nops = (SLOTS > 1 && jq < n_st) ? (stage_at(jq).w >= 0 ? (pair ? 2 : 1) * OPS3 : OPS8) : 0;
     if (nops == 2 * OPS3)
       wait_vmcnt<2 * OPS3>();
     else if (nops == OPS8)
@@ -484,15 +514,14 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   // TQ3 stages come first in the list, FP8 stages after them; the two loops
   // share the ring (a copy in flight may belong to either format).
   int k_st = 0;  // stages begun by this wave; stage k sits in slot k % SLOTS
-  while (jc < min(jend, st3)) {
+  while (jc < st3) {
     const int j = jc;
     const int slot = k_st % SLOTS;
-    const int jn = SLOTS == 1 ? claim() : j + 1;  // next stage of this wave
-    const int jr = SLOTS == 1 ? jn : j + SLOTS;   // stage that refills this slot
+    const int jr = claim();  // stage that refills this slot
     const int4 e = stage_at(j);
     STAGE_PRIO(1);
     begin_stage(j);
-    const bool refill = jr < jend;
+    const bool refill = jr < n_st;
     const int4 e2 = refill ? stage_at(jr) : e;
     const uint8_t* ra = wring + slot * STAGE;
     // TQ3 pair (page b absent: same page, every token masked)
@@ -533,16 +562,20 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
     }
     float sc[4];
     {
-      const int vcnt = S - (col_b ? e.z : e.x) * PAGE;
       const _Float16* gh = reinterpret_cast<const _Float16*>(&gw);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float sv = col_b ? sb[i] : sa[i];
-        sc[i] = (col_valid && 4 * lg + i < vcnt) ? sv * (float)gh[i] * smk : -INFINITY;
+      for (int i = 0; i < 4; ++i) sc[i] = fmaf(col_b ? sb[i] : sa[i], (float)gh[i], col_bias);
+      // tokens at or past the end: only in a stage that holds the request's
+      // last page or a masked page b
+      if ((e.x + 1) * PAGE > S || (pair && (e.z + 1) * PAGE > S)) {
+        const int vcnt = S - (col_b ? e.z : e.x) * PAGE;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (4 * lg + i >= vcnt) sc[i] = -INFINITY;
       }
     }
     STAGE_PRIO(2);
-    softmax_step<D>(st, sc, lg);
+    softmax_step<D, NI>(st, sc, lg);
     STAGE_PRIO(3);
     half8 pT, pTl;
     p_operand(sc, col_b, pT, pTl);
@@ -566,22 +599,26 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
       if (m + 1 < CL) Xn = pv(m + 1);
       const _Float16 sm = sO[m >> 1][m & 1], zm = zO[m >> 1][m & 1];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < NI; ++i)
         st.acc[m][i] = fmaf((float)zm, PS[i], fmaf((float)sm, X[i], st.acc[m][i]));
       X = Xn;
     }
-    jc = jn;
+    if (SLOTS == 1) {
+      jc = jr;
+    } else {
+      jc = jq;
+      jq = jr;
+    }
     ++k_st;
   }
-  while (jc < jend) {
+  while (jc < n_st) {
     const int j = jc;
     const int slot = k_st % SLOTS;
-    const int jn = SLOTS == 1 ? claim() : j + 1;
-    const int jr = SLOTS == 1 ? jn : j + SLOTS;
+    const int jr = claim();  // stage that refills this slot
     const int4 e = stage_at(j);
     STAGE_PRIO(1);
     begin_stage(j);
-    const bool refill = jr < jend;
+    const bool refill = jr < n_st;
     const int4 e2 = refill ? stage_at(jr) : e;
     const uint8_t* ra = wring + slot * STAGE;
     // one FP8 page (score columns of page b stay empty)
@@ -613,13 +650,18 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
           qpl[s * 64 + lane], sa, 0, 0, 0);
     float sc[4];
     {
-      const int vcnt = col_b ? 0 : S - e.x * PAGE;
       const float kk = ksv.x * smk;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) sc[i] = (col_valid && 4 * lg + i < vcnt) ? sa[i] * kk : -INFINITY;
+      for (int i = 0; i < 4; ++i) sc[i] = fmaf(sa[i], kk, fp8_bias);
+      if ((e.x + 1) * PAGE > S) {
+        const int vcnt = S - e.x * PAGE;
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (4 * lg + i >= vcnt) sc[i] = -INFINITY;
+      }
     }
     STAGE_PRIO(2);
-    softmax_step<D>(st, sc, lg);
+    softmax_step<D, NI>(st, sc, lg);
     STAGE_PRIO(3);
     half8 pT, pTl;
     p_operand(sc, col_b, pT, pTl);
@@ -629,9 +671,15 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
       const half8 v = h8(cvt_lo(vA[m]), cvt_hi(vA[m]), z2, z2);
       const float4v X = __builtin_amdgcn_mfma_f32_16x16x32_f16(
           pTl, v, __builtin_amdgcn_mfma_f32_16x16x32_f16(pT, v, zero4, 0, 0, 0), 0, 0, 0);
-      st.acc[m] += ksv.y * X;
+#pragma unroll
+      for (int i = 0; i < NI; ++i) st.acc[m][i] = fmaf(ksv.y, X[i], st.acc[m][i]);
     }
-    jc = jn;
+    if (SLOTS == 1) {
+      jc = jr;
+    } else {
+      jc = jq;
+      jq = jr;
+    }
     ++k_st;
   }
 
@@ -647,7 +695,7 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   }
   if (pair) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < NI; ++i) {
       // rows of page b sit in lanes l + 32; only lanes l < 32 keep the result
       const float m2 = upper_half(mrow[i]), l2 = upper_half(lrow[i]);
       const float M = fmaxf(lrow[i] > 0.0f ? mrow[i] : -INFINITY, l2 > 0.0f ? m2 : -INFINITY);
@@ -675,9 +723,9 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   if (!row_b) {
     float* macc = reinterpret_cast<float*>(wring);  // [G][D]
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int head = 4 * lg + i;
-      if (head < G) {
+    for (int i = 0; i < NI; ++i) {
+      const int head = head_of_col<G6>(4 * lg + i);
+      if (head >= 0 && head < G) {
         float4* row = reinterpret_cast<float4*>(macc + head * D);
 #pragma unroll
         for (int k = 0; k < CL / 4; ++k)
@@ -834,14 +882,18 @@ hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t
   const size_t ring_b = (size_t)nw * slots * 2 * tq3_region_bytes(P.d);
   const size_t lds = qop_b + ring_b;  // the epilogue reuses each wave's ring slot
   if (lds > lds_limit()) return hipErrorInvalidValue;
-  const void* kern = P.d == 256 ? (pair ? (const void*)decode_kernel<256, true> : (const void*)decode_kernel<256, false>)
-                                : (pair ? (const void*)decode_kernel<128, true> : (const void*)decode_kernel<128, false>);
+  const bool g6 = pair && P.group <= 6;
+  const void* kern =
+      P.d == 256 ? (g6 ? (const void*)decode_kernel<256, true, true>
+                       : pair ? (const void*)decode_kernel<256, true, false> : (const void*)decode_kernel<256, false, false>)
+                 : (g6 ? (const void*)decode_kernel<128, true, true>
+                       : pair ? (const void*)decode_kernel<128, true, false> : (const void*)decode_kernel<128, false, false>);
   // the dynamic-LDS limit is raised once per kernel instance and device
   static std::atomic<uint32_t> attr_done[64];
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
-  const uint32_t bit = 1u << ((P.d == 256 ? 2 : 0) + (pair ? 1 : 0));
+  const uint32_t bit = 1u << ((P.d == 256 ? 3 : 0) + (g6 ? 2 : pair ? 1 : 0));
   if (dev < 0 || dev >= 64 || !(attr_done[dev].load() & bit)) {
     e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_limit());
     if (e != hipSuccess) return e;
