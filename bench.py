@@ -209,6 +209,35 @@ def chunk_bench(mk, torch, reps=5):
             "kernel": "chunk_kernel<256> (+ partition_kernel)"}
 
 
+def stream_probe(mk, torch, nbytes, achieved, reps=20):
+    """A plain streaming read of `nbytes` (the library's probe kernel, 16-byte
+    loads, each byte once), cycling through 16 buffers so no read is served
+    from the 256 MB last-level cache, timed with HIP events around each call:
+    a measured bandwidth ceiling for a kernel that reads that many bytes."""
+    n = nbytes // 16 * 16
+    bufs = [torch.ones(n // 4, dtype=torch.float32, device="cuda") for _ in range(16)]
+    sink = torch.zeros(mk.STREAM_PROBE_WORKGROUPS, dtype=torch.int32, device="cuda")
+    for b in bufs:
+        mk.mkv_stream_read(b, sink)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    ts = []
+    for i in range(reps):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        mk.mkv_stream_read(bufs[i % 16], sink)
+        e1.record(stream)
+        ts.append((e0, e1))
+    torch.cuda.synchronize()
+    us = float(np.mean([a.elapsed_time(b) for a, b in ts[2:]]) * 1e3)
+    bw = n / (us * 1e-6)
+    del bufs
+    return {"bytes": n, "us": round(us, 2), "gb_per_s": round(bw / 1e9, 1),
+            "frac_of_peak": round(bw / HBM_PEAK, 4),
+            "decode_frac_of_stream": round(achieved / bw, 4),
+            "kernel": "stream_read_kernel (mkv_stream_read), HIP events around each call"}
+
+
 def _cpu_model():
     try:
         for line in open("/proc/cpuinfo"):
@@ -231,6 +260,9 @@ def main():
                     help="skip the chunked-prefill measurement")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run one 1 GiB device-to-device copy (calibrates HBM byte counters)")
+    ap.add_argument("--stream-probe", action="store_true",
+                    help="also time a plain streaming read of the decode's byte count (torch sum "
+                         "over cycled buffers) as a measured bandwidth ceiling")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
@@ -361,10 +393,12 @@ def main():
         "effective_kv_gb_per_s": round(kv_bytes / (dec_us * 1e-6) / 1e9, 1),
         "roofline": {"bound": "hbm", "achieved": round(achieved / 1e9, 1), "peak": HBM_PEAK / 1e9,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK, 4), "traffic": traffic,
-                     "kernel": "decode_kernel<256, true> (split scan, one launch per layer)"},
+                     "kernel": "decode_kernel<256, true, true> (split scan, one launch per layer)"},
         "counters": {k: int(v) for k, v in counters.items()},
         "setup_s": round(setup_s, 1),
     }
+    if args.stream_probe:
+        res["stream_probe"] = stream_probe(mk, torch, int(kv_bytes), achieved)
     if args.copy_probe:
         a_ = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
         b_ = torch.empty_like(a_)

@@ -232,6 +232,17 @@ mkv_status kv_pool_counters(mkv_pool* pool, mkv_counters* out);
 mkv_status paged_attn_set_timing(mkv_pool* pool, int32_t enable);
 mkv_status paged_attn_last_times(mkv_pool* pool, float* scan_us, float* merge_us);
 
+/* Streaming-read probe for measurement tools; correct use never needs it.
+ * Reads bytes (a multiple of 16; buf 16-byte aligned, device memory) once with
+ * 16-byte loads and writes one word per workgroup to sink, which must hold
+ * MKV_STREAM_PROBE_WORKGROUPS uint32 values (device memory).  The words fold
+ * the data together and have no other meaning: the call exists to time a
+ * kernel that reads a buffer once, the bandwidth ceiling of the decode scan.
+ * Enqueued on stream; MKV_EINVAL on a null pointer, misalignment or a size
+ * that is not a multiple of 16. */
+#define MKV_STREAM_PROBE_WORKGROUPS 2048
+mkv_status mkv_stream_read(const void* buf, size_t bytes, uint32_t* sink, hipStream_t stream);
+
 /* Read (and optionally clear) the device error word; synchronizes. */
 mkv_status kv_pool_check_errors(mkv_pool* pool, uint32_t* err_word, int32_t clear);
 

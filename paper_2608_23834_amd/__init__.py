@@ -26,7 +26,8 @@ EXPORTS = ["kv_pool_bytes", "kv_pool_create", "kv_pool_destroy", "kv_append_fp8"
            "kv_migrate_to_tq3", "paged_attn_workspace_bytes", "paged_attn_workspace_init",
            "paged_attn_decode", "paged_attn_chunk", "kv_partition_pages", "kv_pool_free_counts",
            "kv_pool_read_free_lists", "kv_pool_counters", "kv_pool_check_errors",
-           "paged_attn_set_timing", "paged_attn_last_times", "mkv_status_string"]
+           "paged_attn_set_timing", "paged_attn_last_times", "mkv_stream_read",
+           "mkv_status_string"]
 
 _lib = None
 
@@ -84,6 +85,7 @@ def lib() -> ctypes.CDLL:
         L.kv_pool_check_errors.argtypes = [vp, vp, i32]
         L.paged_attn_set_timing.argtypes = [vp, i32]
         L.paged_attn_last_times.argtypes = [vp, vp, vp]
+        L.mkv_stream_read.argtypes = [vp, sz, vp, vp]
         L.mkv_status_string.argtypes = [ctypes.c_int]
         _lib = L
     return _lib
@@ -258,6 +260,17 @@ def paged_attn_last_times(pool: Pool) -> tuple:
     _check("paged_attn_last_times", lib().paged_attn_last_times(pool.handle, ctypes.byref(a),
                                                                 ctypes.byref(b)))
     return a.value, b.value
+
+
+STREAM_PROBE_WORKGROUPS = 2048
+
+
+def mkv_stream_read(buf, sink, stream=None):
+    """Streaming-read probe (measurement only): reads the device tensor `buf`
+    once; `sink` is a device int32 tensor of STREAM_PROBE_WORKGROUPS words."""
+    assert sink.numel() >= STREAM_PROBE_WORKGROUPS
+    _check("mkv_stream_read", lib().mkv_stream_read(
+        _ptr(buf), buf.numel() * buf.element_size(), _ptr(sink), _stream(stream)))
 
 
 def kv_pool_check_errors(pool: Pool, clear=False) -> int:

@@ -24,7 +24,7 @@ COMMON = [
 ]
 # TUs whose bit-exact outputs must follow single IEEE operations in order
 EXACT = {"mkv_pool_kernels.hip"}
-SOURCES = ["mkv_api.hip", "mkv_pool_kernels.hip", "mkv_decode.hip", "mkv_chunk.hip"]
+SOURCES = ["mkv_api.hip", "mkv_pool_kernels.hip", "mkv_decode.hip", "mkv_chunk.hip", "mkv_probe.hip"]
 
 
 def _compile(src: str) -> str:

@@ -311,6 +311,12 @@ mkv_status kv_pool_counters(mkv_pool* pool, mkv_counters* out) {
   return MKV_OK;
 }
 
+mkv_status mkv_stream_read(const void* buf, size_t bytes, uint32_t* sink, hipStream_t stream) {
+  if (!buf || !sink || !aligned16(buf) || bytes % 16 != 0) return MKV_EINVAL;
+  if (bytes == 0) return MKV_OK;
+  return hip_status(launch_stream_read(buf, bytes, sink, MKV_STREAM_PROBE_WORKGROUPS, stream));
+}
+
 mkv_status kv_pool_check_errors(mkv_pool* pool, uint32_t* err_word, int32_t clear) {
   if (!pool) return MKV_EINVAL;
   if (hipDeviceSynchronize() != hipSuccess) return MKV_EHIP;

@@ -75,6 +75,9 @@ hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t
                          const int32_t* seq_lens, float* out, float* lse, void* ws,
                          hipStream_t s, hipEvent_t* ev);
 
+// mkv_probe.hip
+hipError_t launch_stream_read(const void* buf, size_t bytes, uint32_t* sink, int n_wg, hipStream_t s);
+
 // mkv_chunk.hip
 size_t chunk_ws_bytes(int n_req, int max_pages, int n_q_total, int n_kv_heads, int group, int d);
 hipError_t launch_chunk(const PoolView& P, int layer, int n_req, const uint16_t* q,

@@ -94,3 +94,12 @@ def test_calls_reject_null_handles(mk):
     assert L.paged_attn_chunk(None, 0, 1, None, None, 1, None, None, 1, None, None, None, 0, None) == 1
     assert L.kv_partition_pages(0, None, None, 1, None, None, None, None, None) == 1
     assert L.mkv_status_string(3) == b"buffer too small"
+
+
+def test_stream_probe_rejects_bad_arguments(mk):
+    L = mk.lib()
+    sink = ctypes.c_void_p(64)  # never dereferenced: validation fails first
+    assert L.mkv_stream_read(None, 16, sink, None) == 1
+    assert L.mkv_stream_read(ctypes.c_void_p(16), 16, None, None) == 1
+    assert L.mkv_stream_read(ctypes.c_void_p(8), 16, sink, None) == 1      # misaligned
+    assert L.mkv_stream_read(ctypes.c_void_p(16), 24, sink, None) == 1     # not whole 16-byte words

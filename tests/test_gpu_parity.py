@@ -158,6 +158,31 @@ def test_batch64_config_full_size(torch_cuda):
     assert err <= TOL, err
 
 
+def test_group12_decode(torch_cuda):
+    """Twelve query heads per KV head (the kernel instance without the page
+    pair layout): ragged lengths, short Recent window."""
+    import dataclasses
+    w = dataclasses.replace(wl.workload(2), n_kv_heads=2, name="group12")
+    _run_decode_case(w, [3000, 777, 1], recent=64)
+
+
+def test_stream_probe_reads_every_word(torch_cuda):
+    """The streaming-read probe folds every 32-bit word of the buffer once:
+    the XOR of its per-workgroup words equals the XOR of the buffer."""
+    import paper_2608_23834_amd as mk
+    torch = torch_cuda
+    rng = np.random.default_rng(7)
+    for n_words in (4, 4 * 1000 + 4, 1 << 22):
+        x = rng.integers(0, 2 ** 31, size=n_words, dtype=np.int64).astype(np.int32)
+        buf = torch.from_numpy(x).cuda()
+        sink = torch.zeros(mk.STREAM_PROBE_WORKGROUPS, dtype=torch.int32, device="cuda")
+        mk.mkv_stream_read(buf, sink)
+        torch.cuda.synchronize()
+        want = np.bitwise_xor.reduce(x.view(np.uint32))
+        got = np.bitwise_xor.reduce(sink.cpu().numpy().view(np.uint32))
+        assert got == want, (n_words, got, want)
+
+
 def test_decode_steps_with_appends(torch_cuda):
     """Token-by-token decode: append one token per request, migrate, decode;
     pages are partly filled and rescaled along the way."""
