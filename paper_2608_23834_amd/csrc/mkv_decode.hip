@@ -4,10 +4,10 @@
 // One launch per layer.  Grid (chunk, KV head, request); one workgroup of
 // 12 (or 8) wave64s per CU.  Chunks are ranges of logical pages of equal
 // cost: a page wholly outside the Recent window (a TQ3 page unless it is an
-// anchor) costs 1 unit, a Recent (FP8) page 2 units -- one FP8 page, twice
-// the bytes, takes the scan about as long as a pair of TQ3 pages; the unit
-// count per chunk is chosen so that the launch is about one workgroup per
-// CU.  Each workgroup
+// anchor) costs 2 units, a Recent (FP8) page 5 units -- an FP8 page carries
+// twice the bytes of a TQ3 page, and its scattered 16-byte copies make it
+// cost the scan about 2.5 times as much (measured); the unit count per chunk
+// is chosen so that the launch is about one workgroup per CU.  Each workgroup
 //  1. loads the GQA group's queries and builds two fp16 MFMA operands in LDS:
 //     the plain queries for FP8 pages and the rotated ones for TQ3 pages
 //     (q_rot = R q, exact algebra since k_hat = gamma R^T mu_c, so keys are
@@ -59,7 +59,7 @@ constexpr int NW_MAX = 12;
 #define NCH_OF(pair) ((pair) ? 8 : 16)
 constexpr int MAX_CHUNK_PAGES = 256;   // pages a chunk may span
 // cost of a page in chunk units: wholly outside the Recent window / Recent
-constexpr int COST_OLD = 1, COST_REC = 2;
+constexpr int COST_OLD = 2, COST_REC = 5;
 constexpr int COST_MIN = COST_OLD < COST_REC ? COST_OLD : COST_REC;
 constexpr int MASK_LP = 0x3FFFFFFF / PAGE;  // logical page whose tokens are all masked
 
