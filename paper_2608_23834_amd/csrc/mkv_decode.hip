@@ -128,6 +128,12 @@ struct WaveState {
 // Initial reference max: finite, so 2^(s - m) is 0 for masked scores (s = -inf)
 // and never NaN; a column with l = 0 takes no part in any merge.
 constexpr float M_INIT = -1.0e30f;
+// The rotated query enters the TQ3 score product as a sum of E4M3 terms,
+// q sc = t0 + t1 + t2 (each term the E4M3 rounding of what the previous ones
+// left; sc a power of two that puts the head's largest |q sc| in [128, 256)).
+// The residual is below E4M3's subnormal step 2^-9, i.e. about 2^-17 of the
+// head's largest entry.
+constexpr int QF8_TERMS = 3;
 
 // Column layout of a score tile (and row layout of the PV accumulator).  With
 // at most six heads per KV head, heads sit in columns 4 k + i, i < 3, so that
@@ -199,6 +205,7 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   constexpr int NW = DecodeCfg<PAIR>::NW, NT = DecodeCfg<PAIR>::NT, SLOTS = DecodeCfg<PAIR>::SLOTS;
   constexpr int NCH = NCH_OF(PAIR);  // query heads a score tile holds
   constexpr int CL = D / 16, NDW = 3 * D / 128, CB = 3 * D / 32, NS = D / 32, QV = D / 64;
+  constexpr int NK8 = D / 128;  // 128-channel steps of the TQ3 score product (32 channels per lane group)
   constexpr int R3 = (int)tq3_region_bytes(D);  // K codes, V codes, gamma, V scale, V zero
   constexpr int R8 = (int)fp8_region_bytes(D);  // K codes then V codes
   constexpr int STAGE = 2 * R3;                 // a TQ3 page pair, or one FP8 page + scales
@@ -220,11 +227,11 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   const int G = P.group, H = P.n_kv_heads, Hq = H * G;
   const int mp = a.max_pages;
   constexpr bool pair = PAIR;
-  // LDS: [rotated-query operand hi, lo][plain-query operand][page ring | wave merge]
-  half8* qrot = reinterpret_cast<half8*>(smem);  // rotated query, fp16 high part
-  half8* qrlo = qrot + NS * 64;                   // rotated query, fp16 low part
-  half8* qpl = qrlo + NS * 64;                    // plain query (bf16 -> fp16 is exact)
-  uint8_t* ring = smem + 3 * NS * 64 * 16;
+  // LDS: [rotated query as E4M3 terms][plain-query operand][page ring | wave merge]
+  uint8_t* qf8 = smem;  // [term][step][lane][32 bytes], see the query build below
+  half8* qpl = reinterpret_cast<half8*>(smem + QF8_TERMS * NK8 * 64 * 32);  // plain query (bf16 -> fp16 is exact)
+  uint8_t* ring = smem + QF8_TERMS * NK8 * 64 * 32 + NS * 64 * 16;
+  __shared__ float s_qinv[16];  // per score column: 1 / the power-of-two scale of its terms
 
   // ---- 1. queries: wave w owns score columns w and w + NW below NCH (the
   // head of a column: head_of_col); lane l holds channels QV l .. QV l + QV -
@@ -286,11 +293,13 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
     return;
   }
   // ---- query operands, built while the page-table loads are in flight, in MFMA
-  // lane order: q?[s][lane] holds channels (D/4) lg + 8 s + j, j < 8, of
-  // column ln's head (ln = lane % 16, lg = lane / 16)
+  // lane order (ln = lane % 16 the score column, lg = lane / 16):
+  //  qpl[s][lane] holds channels (D/4) lg + 8 s + j, j < 8 (fp16, FP8 pages);
+  //  qf8[t][S][lane] holds term t of channels (D/4) lg + 32 S + j, j < 32 (the
+  //  f8f6f4 MFMA pairs byte j of lane l in A with byte j of lane l' in B
+  //  whenever l / 16 = l' / 16, so any channel order common to both operands
+  //  works; this one matches the key quads)
   {
-    _Float16* qr = reinterpret_cast<_Float16*>(qrot);
-    _Float16* ql = reinterpret_cast<_Float16*>(qrlo);
     _Float16* qp = reinterpret_cast<_Float16*>(qpl);
     // R = d^-1/2 H diag(sigma); the rotated query also carries the softmax
     // scale log2(e)/sqrt(d), so TQ3 scores come out in base-2 units
@@ -327,23 +336,37 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
       stage(std::integral_constant<int, 8>{});
       stage(std::integral_constant<int, 16>{});
       stage(std::integral_constant<int, 32>{});
+      // the head's power-of-two scale: largest |q sc| in [128, 256)
+      float amax = 0.0f;
+#pragma unroll
+      for (int i = 0; i < QV; ++i) amax = fmaxf(amax, fabsf(xr[i] * qscale));
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) amax = fmaxf(amax, __shfl_xor(amax, o, 64));
+      int ex = 0;
+      (void)frexpf(amax, &ex);  // amax in [2^(ex-1), 2^ex)
+      const float qsc = (ok && amax > 0.0f) ? ldexpf(1.0f, 7 - ex + 1) : 1.0f;
+      if (lane == 0) {
+        s_qinv[n] = 1.0f / qsc;
+        if (pair) s_qinv[n + 8] = 1.0f / qsc;
+      }
 #pragma unroll
       for (int i = 0; i < QV; ++i) {
         const int c = QV * lane + i;
         const int lgc = c / (D / 4), sc = (c % (D / 4)) / 8, j = c % 8;
-        // q_rot as an fp16 pair hi + lo (fp32 accuracy through two MFMAs)
-        const float xq = ok ? xr[i] * qscale : 0.0f;
-        const _Float16 vr = (_Float16)xq;
-        const _Float16 vl = (_Float16)(xq - (float)vr);
         const _Float16 vp = (_Float16)(ok ? qx[ps][i] : 0.0f);
         const int e0 = ((sc * 64) + lgc * 16 + n) * 8 + j;
-        qr[e0] = vr;
-        ql[e0] = vl;
         qp[e0] = vp;
-        if (pair) {
-          qr[e0 + 8 * 8] = vr;  // column n + 8 scores page b with the same head
-          ql[e0 + 8 * 8] = vl;
-          qp[e0 + 8 * 8] = vp;
+        if (pair) qp[e0 + 8 * 8] = vp;  // column n + 8 scores page b with the same head
+        // rotated query times its scale as three E4M3 terms (exact residuals)
+        float x = ok ? xr[i] * qscale * qsc : 0.0f;
+        const int S = (c % (D / 4)) / 32, slot = c % 32;
+#pragma unroll
+        for (int t = 0; t < QF8_TERMS; ++t) {
+          const uint32_t b = f32_to_e4m3(x);
+          x -= e4m3_to_f32(b);
+          const int e8 = ((t * NK8 + S) * 64 + lgc * 16 + n) * 32 + slot;
+          qf8[e8] = (uint8_t)b;
+          if (pair) qf8[e8 + 8 * 32] = (uint8_t)b;
         }
       }
     }
@@ -492,6 +515,7 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   if (wid < 4 && jc < n_st) issue(stage_of(jc), 0);
 
   __syncthreads();  // query operands and the stage list visible to every wave
+  const float qinv = s_qinv[ln];  // undoes the query-term scale of this lane's column
   if (wid >= 4 && jc < n_st) issue(stage_at(jc), 0);
   if (SLOTS == 2 && jc < n_st) {
     jq = claim();
@@ -542,29 +566,30 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
     }
     wait_lgkm0();  // the stage is in registers: refill its slot
     if (refill) issue(e2, slot);
-    // QK^T: rows = tokens of the page, columns = (page, head)
+    // QK^T: rows = tokens of the page, columns = (page, head), on the
+    // 16x16x128 fp8 MFMA: the 3-bit codes become E4M3 codebook bytes (one
+    // v_perm per 4 codes) and meet the query's E4M3 terms directly
     float4v sa = zero4, sb = zero4;
 #pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      const half8 qv = qrot[s * 64 + lane], ql = qrlo[s * 64 + lane];
-      const uint32_t a0 = __builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(kA, 2 * s));
-      const uint32_t a1 = __builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(kA, 2 * s + 1));
-      const half8 Ka = h8(cvt_lo(a0), cvt_hi(a0), cvt_lo(a1), cvt_hi(a1));
-      sa = __builtin_amdgcn_mfma_f32_16x16x32_f16(Ka, qv, sa, 0, 0, 0);
-      sa = __builtin_amdgcn_mfma_f32_16x16x32_f16(Ka, ql, sa, 0, 0, 0);
-      if (pair) {
-        const uint32_t b0 = __builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(kB, 2 * s));
-        const uint32_t b1 = __builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(kB, 2 * s + 1));
-        const half8 Kb = h8(cvt_lo(b0), cvt_hi(b0), cvt_lo(b1), cvt_hi(b1));
-        sb = __builtin_amdgcn_mfma_f32_16x16x32_f16(Kb, qv, sb, 0, 0, 0);
-        sb = __builtin_amdgcn_mfma_f32_16x16x32_f16(Kb, ql, sb, 0, 0, 0);
+    for (int S = 0; S < NK8; ++S) {
+      v8i Ka, Kb;
+#pragma unroll
+      for (int w = 0; w < 8; ++w) {
+        Ka[w] = (int)__builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(kA, 8 * S + w));
+        if (pair) Kb[w] = (int)__builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(kB, 8 * S + w));
+      }
+#pragma unroll
+      for (int t = 0; t < QF8_TERMS; ++t) {
+        const v8i qv = *reinterpret_cast<const v8i*>(qf8 + ((t * NK8 + S) * 64 + lane) * 32);
+        sa = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(Ka, qv, sa, 0, 0, 0, 0, 0, 0);
+        if (pair) sb = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(Kb, qv, sb, 0, 0, 0, 0, 0, 0);
       }
     }
     float sc[4];
     {
       const _Float16* gh = reinterpret_cast<const _Float16*>(&gw);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) sc[i] = fmaf(col_b ? sb[i] : sa[i], (float)gh[i], col_bias);
+      for (int i = 0; i < 4; ++i) sc[i] = fmaf((col_b ? sb[i] : sa[i]) * qinv, (float)gh[i], col_bias);
       // tokens at or past the end: only in a stage that holds the request's
       // last page or a masked page b
       if ((e.x + 1) * PAGE > S || (pair && (e.z + 1) * PAGE > S)) {
@@ -878,7 +903,7 @@ hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t
   const bool pair = P.group <= 8;
   const int nw = pair ? DecodeCfg<true>::NW : DecodeCfg<false>::NW;
   const int slots = pair ? DecodeCfg<true>::SLOTS : DecodeCfg<false>::SLOTS;
-  const size_t qop_b = 3 * (size_t)(P.d / 32) * 64 * 16;
+  const size_t qop_b = (size_t)QF8_TERMS * (P.d / 128) * 64 * 32 + (size_t)(P.d / 32) * 64 * 16;
   const size_t ring_b = (size_t)nw * slots * 2 * tq3_region_bytes(P.d);
   const size_t lds = qop_b + ring_b;  // the epilogue reuses each wave's ring slot
   if (lds > lds_limit()) return hipErrorInvalidValue;

@@ -15,6 +15,7 @@ constexpr int TAG_R = 0, TAG_A = 1, TAG_S = 2, TAG_NONE = 0xFF;
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 typedef float float4v __attribute__((ext_vector_type(4)));
+typedef int v8i __attribute__((ext_vector_type(8)));
 
 // ---------------------------------------------------------------------------
 // ctrl buffer (int32 words): counters, free stacks, work list, rotation signs.
