@@ -809,18 +809,20 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   }
 }
 
-// Merge stage (Eq. softmax-merge): one workgroup per (query head of the
-// group, KV head, request), one thread per four channels.  The O_j rows of up
-// to 32 chunk slots are loaded together (one memory round trip for the usual
-// grid) while thread j stages slot j's (m_j, l_j) in LDS; slots with l_j = 0
-// contribute nothing; a running (M, L, O) is rescaled once per batch.
+// Merge stage (Eq. softmax-merge): one single-wave workgroup per (query head
+// of the group, KV head, request), one thread per four channels.  The O_j
+// rows of up to 32 chunk slots and, in lane j, slot j's (m_j, l_j) are loaded
+// together (one memory round trip for the usual grid); the batch maximum and
+// the weights 2^(m_j - M) l_j come from wave reductions, and every weight is
+// read into a scalar register, so each thread's fold is 32 FMAs per channel.
+// Slots with l_j = 0 contribute nothing; a running (M, L, O) is rescaled once
+// per batch.
 template <int D>
 __global__ __launch_bounds__(D / 4) void decode_merge_kernel(int G, int H, int max_chunks,
                                                             const float* partials, float* out,
                                                             float* lse) {
   constexpr int B = 32;
-  static_assert(D / 4 >= B, "one thread stages each slot's (m, l)");
-  __shared__ float s_m[B], s_l[B];
+  static_assert(D / 4 >= B && D / 4 <= 64, "one wave; lane j holds slot j's (m, l)");
   const int n = blockIdx.x, h = blockIdx.y, r = blockIdx.z, c4 = threadIdx.x;
   const int Hq = H * G;
   const int stride = part_stride(G, D);
@@ -834,38 +836,35 @@ __global__ __launch_bounds__(D / 4) void decode_merge_kernel(int G, int H, int m
       const int k = min(k0 + j, max_chunks - 1);
       ok[j] = reinterpret_cast<const float4*>(base + (int64_t)k * stride + n * D)[c4];
     }
-    if (c4 < B) {
-      const float* pk = base + (int64_t)min(k0 + c4, max_chunks - 1) * stride;
-      s_m[c4] = pk[G * D + n];
-      s_l[c4] = k0 + c4 < max_chunks ? pk[G * D + G + n] : 0.0f;
-    }
-    __syncthreads();
-    float Mb = M;
+    const bool mine = c4 < B && k0 + c4 < max_chunks;
+    const float* pk = base + (int64_t)min(k0 + c4, max_chunks - 1) * stride;
+    const float mj = pk[G * D + n];
+    const float lj = mine ? pk[G * D + G + n] : 0.0f;
+    float mb = lj > 0.0f ? mj : -INFINITY;
 #pragma unroll
-    for (int j = 0; j < B; ++j)
-      if (s_l[j] > 0.0f) Mb = fmaxf(Mb, s_m[j]);
-    if (Mb != -INFINITY) {  // else nothing in this batch, nothing before it
+    for (int o = 1; o < D / 4; o <<= 1) mb = fmaxf(mb, __shfl_xor(mb, o, D / 4));
+    const float Mb = fmaxf(M, mb);
+    if (Mb != -INFINITY) {  // else nothing in this batch, nothing before it (wave-uniform)
       const float f = M == -INFINITY ? 0.0f : exp2f(M - Mb);
-      L *= f;
+      const float wj = lj > 0.0f ? exp2f(mj - Mb) * lj : 0.0f;
+      float ws = wj;
+#pragma unroll
+      for (int o = 1; o < D / 4; o <<= 1) ws += __shfl_xor(ws, o, D / 4);
+      L = L * f + ws;
       O.x *= f;
       O.y *= f;
       O.z *= f;
       O.w *= f;
 #pragma unroll
       for (int j = 0; j < B; ++j) {
-        const float lj = s_l[j];
-        if (lj > 0.0f) {
-          const float w = exp2f(s_m[j] - Mb) * lj;
-          L += w;
-          O.x += w * ok[j].x;
-          O.y += w * ok[j].y;
-          O.z += w * ok[j].z;
-          O.w += w * ok[j].w;
-        }
+        const float w = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, wj), j));
+        O.x = fmaf(w, ok[j].x, O.x);
+        O.y = fmaf(w, ok[j].y, O.y);
+        O.z = fmaf(w, ok[j].z, O.z);
+        O.w = fmaf(w, ok[j].w, O.w);
       }
       M = Mb;
     }
-    __syncthreads();  // s_m, s_l are rewritten by the next batch
   }
   const int64_t row = (int64_t)r * Hq + h * G + n;
   const float inv = L > 0.0f ? 1.0f / L : 0.0f;
