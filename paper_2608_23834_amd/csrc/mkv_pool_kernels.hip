@@ -567,6 +567,12 @@ __global__ __launch_bounds__(64) void append_step_kernel(PoolView P, int layer_s
     small_task_load_old<D>(T, P, id, lane);
     small_task_run<D>(T, P, id, s_img, s_lut, lane);
   }
+  // ---- nothing to publish (no fresh page; every wave reached the same
+  // verdict): the first wave reports an error, no wave waits for the others
+  if (n_fresh == 0 || bad) {
+    if (bad && blockIdx.x == 0 && lane == 0) atomicOr(&P.ctrl[CTRL_ERR], bad);
+    return;
+  }
   // ---- arrive; the last wave records the fresh pages.  Only the order of
   // every wave's table reads before the last wave's table writes matters:
   // a wave counts itself once all its loads have returned (no device-scope
@@ -577,22 +583,18 @@ __global__ __launch_bounds__(64) void append_step_kernel(PoolView P, int layer_s
   if (lane == 0) prev = atomicAdd(&P.ctrl[CTRL_APPEND_ARRIVE], 1);
   prev = __shfl(prev, 0, 64);
   if (prev != (int)gridDim.x - 1) return;
-  if (bad) {
-    if (lane == 0) atomicOr(&P.ctrl[CTRL_ERR], bad);
-  } else {
 #pragma unroll
-    for (int j = 0; j < EQ; ++j) {
-      const int e = lane + 64 * j;
-      if (e < n_ent && fresh[j]) {
-        int r, p;
-        locate(e, r, p);
-        const int64_t i = (int64_t)r * max_pages + p;
-        bt[i] = ent_id[j];
-        tags[i] = TAG_R;
-      }
+  for (int j = 0; j < EQ; ++j) {
+    const int e = lane + 64 * j;
+    if (e < n_ent && fresh[j]) {
+      int r, p;
+      locate(e, r, p);
+      const int64_t i = (int64_t)r * max_pages + p;
+      bt[i] = ent_id[j];
+      tags[i] = TAG_R;
     }
-    if (lane == 0) P.ctrl[CTRL_FP8_TOP] = top - n_fresh;
   }
+  if (lane == 0) P.ctrl[CTRL_FP8_TOP] = top - n_fresh;
   if (lane == 0) P.ctrl[CTRL_APPEND_ARRIVE] = 0;
 }
 
