@@ -24,6 +24,11 @@ COMMON = [
 ]
 # TUs whose bit-exact outputs must follow single IEEE operations in order
 EXACT = {"mkv_pool_kernels.hip"}
+# Per-TU extra flags.  The chunk kernel keeps its MFMA accumulators in
+# ordinary VGPRs: with the accumulator-register form the compiler copied all
+# 128 output accumulators into VGPRs on every pass of the stage loop (for the
+# rarely taken rescale branch).
+EXTRA = {"mkv_chunk.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 SOURCES = ["mkv_api.hip", "mkv_pool_kernels.hip", "mkv_decode.hip", "mkv_chunk.hip", "mkv_probe.hip"]
 
 
@@ -32,6 +37,7 @@ def _compile(src: str) -> str:
     flags = list(COMMON)
     if src in EXACT:
         flags.append("-ffp-contract=off")
+    flags += EXTRA.get(src, [])
     cmd = [HIPCC, *flags, "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
