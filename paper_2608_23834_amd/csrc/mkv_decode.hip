@@ -180,14 +180,16 @@ __device__ __forceinline__ void softmax_step(WaveState<D>& st, float* sc, int lg
 // rounding remainder): a token holding most of a row's mass has, against a
 // lagging reference max, a weight that fp16 alone would round by up to 2^-12
 // of that token's value.
-// hi is the weight truncated to fp16, lo the truncated remainder (together 22
-// significant bits).
+// hi is the weight rounded to fp16, lo the rounded remainder (together 22
+// significant bits; round-to-nearest: the packed round-toward-zero conversion
+// flushes fp16 subnormals, which drops the low part of every weight below
+// 2^-4).
 __device__ __forceinline__ void p_operand(const float* p, bool row_is_b, half8& hi, half8& lo) {
-  typedef __fp16 h2t __attribute__((ext_vector_type(2)));
-  const h2t h01 = __builtin_amdgcn_cvt_pkrtz(p[0], p[1]);
-  const h2t h23 = __builtin_amdgcn_cvt_pkrtz(p[2], p[3]);
-  const h2t l01 = __builtin_amdgcn_cvt_pkrtz(p[0] - (float)h01[0], p[1] - (float)h01[1]);
-  const h2t l23 = __builtin_amdgcn_cvt_pkrtz(p[2] - (float)h23[0], p[3] - (float)h23[1]);
+  typedef _Float16 h2t __attribute__((ext_vector_type(2)));
+  const h2t h01 = {(_Float16)p[0], (_Float16)p[1]};
+  const h2t h23 = {(_Float16)p[2], (_Float16)p[3]};
+  const h2t l01 = {(_Float16)(p[0] - (float)h01[0]), (_Float16)(p[1] - (float)h01[1])};
+  const h2t l23 = {(_Float16)(p[2] - (float)h23[0]), (_Float16)(p[3] - (float)h23[1])};
   typedef uint32_t u4v __attribute__((ext_vector_type(4)));
   const uint32_t a0 = __builtin_bit_cast(uint32_t, h01), a1 = __builtin_bit_cast(uint32_t, h23);
   const uint32_t b0 = __builtin_bit_cast(uint32_t, l01), b1 = __builtin_bit_cast(uint32_t, l23);
