@@ -16,6 +16,7 @@ typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef _Float16 half2v __attribute__((ext_vector_type(2)));
 typedef float float4v __attribute__((ext_vector_type(4)));
 typedef int v8i __attribute__((ext_vector_type(8)));
+typedef float float16v __attribute__((ext_vector_type(16)));
 
 // ---------------------------------------------------------------------------
 // ctrl buffer (int32 words): counters, free stacks, work list, rotation signs.
