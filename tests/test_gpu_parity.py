@@ -369,6 +369,36 @@ def test_chunk_ragged_d256(torch_cuda):
     _run_chunk_case(w, list(w.ctx), [100, 33, 1, 40], recent=64)
 
 
+def test_chunk_group12_d256(torch_cuda):
+    """Twelve query heads per KV head: chunk rows (query, head) cross the
+    32-row tiles at other boundaries; a chunk of 70 queries after 1,930
+    tokens and one of 21 after 600, short Recent window, every query."""
+    import dataclasses
+    w = dataclasses.replace(wl.scaled(wl.workload(5), (2000, 621), n_layers=1, name="chunk-g12"),
+                            n_kv_heads=2)
+    _run_chunk_case(w, list(w.ctx), [70, 21], recent=48)
+
+
+def test_chunk_last_query_matches_decode(torch_cuda):
+    """Property that holds at any size, checked without the oracle: the last
+    query of each request's chunk sees the whole context, so the chunk kernel's
+    output for it equals the decode kernel's for the same query (two kernels,
+    two tilings, one definition)."""
+    from _harness import Twin, max_abs
+    w = wl.scaled(wl.workload(5), (9000, 4100, 1500), n_layers=1, name="chunk-vs-decode")
+    n_q = [128, 40, 7]
+    tw = Twin(w, lens=list(w.ctx), with_oracle=False, recent=256)
+    tw.fill_to([l - n for l, n in zip(w.ctx, n_q)])
+    tw.migrate()
+    tw.append(n_q)
+    res = tw.chunk(n_q)
+    last = res["cu"][1:] - 1
+    dec = tw.decode(q=res["q"][last])
+    err = max_abs(res["out"][last], dec["out"])
+    print(f"\n  chunk vs decode, last query of each request: max|dO| {err:.3e}", flush=True)
+    assert err <= TOL, err
+
+
 def test_chunk_config5_full_size(torch_cuda):
     """Config 5 at full size: 8 requests, a 512-query chunk each against
     65,536 tokens of mixed pages (sampled queries: every 64th and the last),
