@@ -186,6 +186,28 @@ mkv_status paged_attn_decode(mkv_pool* pool, int32_t layer, int32_t n_req, const
                              const int32_t* seq_lens, float* out, float* lse, void* ws,
                              size_t ws_bytes, hipStream_t stream);
 
+/* Decode step with its append fused in (Alg. 1 Append, then the decode above):
+ * appends one new token per request to `layer` -- K and V rows k_new, v_new:
+ * device bf16 [n_req][n_kv_heads][d], 8-byte aligned -- at position
+ * seq_lens_before[r] (opening a fresh FP8 page, popped from the FP8 free list
+ * in request order, where the block-table entry of the position's page is
+ * negative, as kv_append_fp8 does), then runs the decode
+ * attention of paged_attn_decode over seq_lens_before[r] + 1 tokens.  The
+ * pool state, block table and tags afterwards, and the outputs, equal those
+ * of kv_append_fp8 (one token per request) followed by paged_attn_decode,
+ * up to the fp32 summation order of the outputs.  block_table and tags are
+ * written (fresh pages).  Same buffer rules as paged_attn_decode.  An append
+ * that cannot be done as a whole (a length outside [0, 16*max_pages), a
+ * page being appended to that is not Recent or has an out-of-range id, an
+ * exhausted FP8 free list) sets the error word, changes no state and gives
+ * every request of the call zero outputs. */
+mkv_status paged_attn_decode_append(mkv_pool* pool, int32_t layer, int32_t n_req,
+                                    const uint16_t* q, const uint16_t* k_new,
+                                    const uint16_t* v_new, int32_t* block_table, uint8_t* tags,
+                                    int32_t max_pages, const int32_t* seq_lens_before,
+                                    float* out, float* lse, void* ws, size_t ws_bytes,
+                                    hipStream_t stream);
+
 /* Causal chunked-prefill attention over the same mixed pages.  Request r has
  * n_r = cu_q[r+1]-cu_q[r] queries; query i sits at position
  * seq_lens[r] - n_r + i and attends to keys t <= that position (the chunk's

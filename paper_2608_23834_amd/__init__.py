@@ -24,7 +24,8 @@ DEVERR = {"FP8_EXHAUSTED": 0x1, "TQ3_EXHAUSTED": 0x2, "NOT_RECENT": 0x4, "RANGE"
           "BAD_TAG": 0x10}
 EXPORTS = ["kv_pool_bytes", "kv_pool_create", "kv_pool_destroy", "kv_append_fp8",
            "kv_migrate_to_tq3", "paged_attn_workspace_bytes", "paged_attn_workspace_init",
-           "paged_attn_decode", "paged_attn_chunk", "kv_partition_pages", "kv_pool_free_counts",
+           "paged_attn_decode", "paged_attn_decode_append", "paged_attn_chunk",
+           "kv_partition_pages", "kv_pool_free_counts",
            "kv_pool_read_free_lists", "kv_pool_counters", "kv_pool_check_errors",
            "paged_attn_set_timing", "paged_attn_last_times", "mkv_stream_read",
            "mkv_status_string"]
@@ -77,6 +78,8 @@ def lib() -> ctypes.CDLL:
         L.paged_attn_workspace_bytes.argtypes = [vp, i32, i32, i32, vp]
         L.paged_attn_workspace_init.argtypes = [vp, sz, vp]
         L.paged_attn_decode.argtypes = [vp, i32, i32, vp, vp, vp, i32, vp, vp, vp, vp, sz, vp]
+        L.paged_attn_decode_append.argtypes = [vp, i32, i32, vp, vp, vp, vp, vp, i32, vp, vp, vp,
+                                               vp, sz, vp]
         L.paged_attn_chunk.argtypes = [vp, i32, i32, vp, vp, i32, vp, vp, i32, vp, vp, vp, sz, vp]
         L.kv_partition_pages.argtypes = [i32, vp, vp, i32, vp, vp, vp, vp, vp]
         L.kv_pool_free_counts.argtypes = [vp, vp, vp]
@@ -210,6 +213,15 @@ def paged_attn_decode(pool: Pool, layer, q, block_table, tags, seq_lens, out, ls
         pool.handle, layer, n_req, _ptr(q), _ptr(block_table), _ptr(tags), max_pages,
         _ptr(seq_lens), _ptr(out), _ptr(lse), _ptr(ws), ws.numel() * ws.element_size(),
         _stream(stream)))
+
+
+def paged_attn_decode_append(pool: Pool, layer, q, k_new, v_new, block_table, tags,
+                             seq_lens_before, out, lse, ws, stream=None):
+    n_req, max_pages = block_table.shape
+    _check("paged_attn_decode_append", lib().paged_attn_decode_append(
+        pool.handle, layer, n_req, _ptr(q), _ptr(k_new), _ptr(v_new), _ptr(block_table),
+        _ptr(tags), max_pages, _ptr(seq_lens_before), _ptr(out), _ptr(lse), _ptr(ws),
+        ws.numel() * ws.element_size(), _stream(stream)))
 
 
 def paged_attn_chunk(pool: Pool, layer, q, cu_q, block_table, tags, seq_lens, out, ws,

@@ -204,6 +204,32 @@ mkv_status paged_attn_decode(mkv_pool* pool, int32_t layer, int32_t n_req, const
   return st;
 }
 
+mkv_status paged_attn_decode_append(mkv_pool* pool, int32_t layer, int32_t n_req,
+                                    const uint16_t* q, const uint16_t* k_new,
+                                    const uint16_t* v_new, int32_t* block_table, uint8_t* tags,
+                                    int32_t max_pages, const int32_t* seq_lens_before,
+                                    float* out, float* lse, void* ws, size_t ws_bytes,
+                                    hipStream_t stream) {
+  if (!pool || !q || !k_new || !v_new || !block_table || !tags || !seq_lens_before || !out || !ws)
+    return MKV_EINVAL;
+  if (n_req < 1 || max_pages < 1) return MKV_EINVAL;
+  if (!aligned16(q) || !aligned16(out) || !aligned16(ws)) return MKV_EINVAL;
+  if ((reinterpret_cast<uintptr_t>(k_new) | reinterpret_cast<uintptr_t>(v_new)) & 7) return MKV_EINVAL;
+  if (layer < 0 || layer >= pool->n_layers) return MKV_ERANGE;
+  if (n_req > 65535 || max_pages > 1024 * 256) return MKV_ERANGE;
+  if (ws_bytes < decode_ws_bytes(n_req, max_pages, pool->n_kv_heads, pool->group, pool->d, pool->recent))
+    return MKV_ENOMEM;
+  mkv_status st = hip_status(launch_decode(view_of(pool), layer, n_req, q, block_table, tags,
+                                           max_pages, seq_lens_before, out, lse, ws, stream,
+                                           pool->timing ? pool->timing_ev : nullptr, k_new, v_new,
+                                           block_table, tags));
+  if (st == MKV_OK) {
+    pool->decode_routes++;
+    if (pool->timing) pool->timed = 1;
+  }
+  return st;
+}
+
 mkv_status paged_attn_set_timing(mkv_pool* pool, int32_t enable) {
   if (!pool) return MKV_EINVAL;
   if (enable && !pool->timing) {

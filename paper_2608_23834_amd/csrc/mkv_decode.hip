@@ -32,6 +32,7 @@
 #include <atomic>
 #include <type_traits>
 
+#include "mkv_append.h"
 #include "mkv_attn.h"
 #include "mkv_internal.h"
 #include "../../include/minima_kv.h"
@@ -75,6 +76,13 @@ struct DecodeArgs {
   float* partials;
   int cunits, max_chunks;  // cost units per chunk, chunk slots per (request, KV head)
   float sm_log2;  // log2(e) / sqrt(d)
+  // decode-step append fused into the call (APP instance): one new token per
+  // request, K and V rows [n_req][n_kv_heads][d] (bf16); seq_lens then holds
+  // the lengths before the append
+  const uint16_t* k_new;
+  const uint16_t* v_new;
+  int32_t* bt_w;    // the same block table and tags, written by the append
+  uint8_t* tags_w;
 };
 
 // Cost of a request's pages: n_old pages wholly outside the Recent window and
@@ -202,7 +210,7 @@ __device__ __forceinline__ void p_operand(const float* p, bool row_is_b, half8& 
 // PAIR (query group of at most 8 heads): two pages share one score tile,
 // columns [0, 8) scoring page a and [8, 16) page b.  G6: at most six heads
 // (see head_of_col).
-template <int D, bool PAIR, bool G6>
+template <int D, bool PAIR, bool G6, bool APP>
 __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeArgs a) {
   constexpr int NW = DecodeCfg<PAIR>::NW, NT = DecodeCfg<PAIR>::NT, SLOTS = DecodeCfg<PAIR>::SLOTS;
   constexpr int NCH = NCH_OF(PAIR);  // query heads a score tile holds
@@ -218,6 +226,7 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   extern __shared__ __align__(16) uint8_t smem[];
   __shared__ int4 s_stage[MAX_CHUNK_PAGES];  // {lp_a, id_a, lp_b, id_b}; id_b < 0: FP8 stage
   __shared__ int s_next;  // next unclaimed stage (one-slot schedule)
+  __shared__ int s_app, s_app_bad;  // fused append: done flag, error bits
   // per (head, wave): running max, denominator, combine weight (epilogue)
   __shared__ __align__(16) float s_mlf[3][16 * NW_MAX];
   static_assert(NCH_OF(PAIR) * D * 4 <= SLOTS * 2 * (int)tq3_region_bytes(D),
@@ -283,7 +292,9 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
     tg_w[k] = a.tags[pi];
     pg_id[k] = a.bt[pi];
   }
-  const int S = a.seq_lens[r];
+  const int s_in = a.seq_lens[r];
+  // with the fused append the request's new token sits at position s_in
+  const int S = !APP ? s_in : (s_in >= 0 && s_in < mp * PAGE ? s_in + 1 : -1);
   if (S < 1 || S > mp * PAGE) {
     if (chunk == 0 && h == 0 && tid == 0) atomicOr(&P.ctrl[CTRL_ERR], (int)MKV_DEVERR_RANGE);
     if (tid < G) part[G * D + G + tid] = 0.0f;  // empty partial: the merge writes zeros
@@ -374,11 +385,21 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
     }
   }
 
+  // fused append: the request's new token lands in logical page p_new (a
+  // fresh page when its table entry is negative, whose physical id the
+  // workgroup learns later); the chunk that holds p_new counts it as a Recent
+  // FP8 page, the last of its FP8 stages
+  const int p_new = APP ? s_in / PAGE : -1;
+  const bool holds = APP && p_new >= p0 && p_new < p1;
 #pragma unroll
   for (int k = 0; k < PW; ++k) {
     const int pi = lane + 64 * k;
-    const int tg = pi < n_pg ? tg_w[k] : -1;
+    int tg = pi < n_pg ? tg_w[k] : -1;
     int id = pg_id[k];
+    if (APP && holds && p0 + pi == p_new) {
+      tg = TAG_R;
+      if (id < 0) id = 0;  // fresh: placeholder until the append wave has popped the id
+    }
     const bool is3 = tg == TAG_S, is8 = (tg == TAG_R || tg == TAG_A);
     if (wid == 0 && pi < n_pg && !is3 && !is8) atomicOr(&P.ctrl[CTRL_ERR], (int)MKV_DEVERR_BAD_TAG);
     int lp = p0 + pi;
@@ -446,7 +467,11 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
       base8 += __popcll(m8w[k]);
     }
   }
-  if (tid == 0) s_next = NW;
+  if (tid == 0) {
+    s_next = NW;
+    s_app = 0;
+    s_app_bad = 0;
+  }
 
   // ---- 3. per-wave stream over the claimed stages
   WaveState<D> st;
@@ -499,7 +524,16 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
                      __builtin_amdgcn_readfirstlane(e.z), __builtin_amdgcn_readfirstlane(e.w));
   };
   const DmaLanes dl = {16u * lane, 4096u + 16u * lane};
-  auto issue = [&](const int4& e, int slot) {
+  auto issue = [&](int4 e, int slot) {
+    if constexpr (APP) {
+      // the page of the appended token: its copy waits until the append wave
+      // has stored the token (and, for a fresh page, popped its id)
+      if (holds && e.w < 0 && e.x == p_new) {
+        while (__hip_atomic_load(&s_app, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) == 0)
+          __builtin_amdgcn_s_sleep(1);
+        e = stage_at(n_st - 1);
+      }
+    }
     const uint32_t dst = wring_lds + slot * STAGE;
     if (e.w >= 0) {
       dma_region<R3>(dst, tq3_l + ((int64_t)e.y * H + h) * R3, dl, lane);
@@ -509,16 +543,123 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
       if (lane < 2) dma4(4 * lane, scl_l + ((int64_t)e.y * H + h) * 8, dst + R8);
     }
   };
+  // Fused decode-step append (APP), run by the youngest wave of the workgroup
+  // that holds the request's new token, after the workgroup barrier, while the
+  // other waves start streaming: every such wave reads the whole call (each
+  // request's length, the free-list top, the table entries and tags of the
+  // pages being appended to) and so reaches the same verdict and the same
+  // fresh-page ids as the decode-step append kernel (same validation, ids
+  // popped in request order, same arithmetic); it stores K and V of head h
+  // for the new token (Alg. 1, Append), then releases the appended page's
+  // stage.  The last of these waves to arrive on the control-block counter
+  // (each arrives after its reads and stores have returned) records the
+  // fresh pages in the block table, pops them off the free list and resets
+  // the counter.  On any error nothing is written, the error word gets its
+  // bits, and the workgroup's partial is marked so that the merge writes
+  // zeros for the call.
+  auto append_token = [&]() {
+    int bad = 0, n_fresh = 0, rank = 0;
+    bool fresh = false;  // this request's page is fresh
+    const int top = P.ctrl[CTRL_FP8_TOP];
+    for (int b0 = 0; b0 < a.n_req; b0 += 64) {
+      const int rr = b0 + lane;
+      const bool in = rr < a.n_req;
+      const int sr = in ? a.seq_lens[rr] : 0;
+      const bool ok = !in || (sr >= 0 && sr < mp * PAGE);
+      bool fr = false;
+      if (!ok) {
+        bad |= MKV_DEVERR_RANGE;
+      } else if (in) {
+        // a negative table entry opens a fresh page, any other must be a
+        // Recent page in range
+        const int64_t ix = (int64_t)rr * mp + sr / PAGE;
+        const int idr = a.bt[ix];
+        fr = idr < 0;
+        if (!fr) {
+          if (a.tags[ix] != TAG_R) bad |= MKV_DEVERR_NOT_RECENT;
+          else if (idr >= P.n_fp8) bad |= MKV_DEVERR_RANGE;
+        }
+      }
+      const uint64_t fm = __ballot(fr);
+      if (r >= b0 + 64) rank += __popcll(fm);
+      else if (r >= b0) {
+        rank += __popcll(fm & ((1ull << (r - b0)) - 1ull));
+        fresh = (fm >> (r - b0)) & 1ull;
+      }
+      n_fresh += __popcll(fm);
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) bad |= __shfl_xor(bad, o, 64);
+    if (n_fresh > top) bad |= MKV_DEVERR_FP8_EXHAUSTED;
+    bad = __builtin_amdgcn_readfirstlane(bad);
+    if (!bad) {
+      const int id = __builtin_amdgcn_readfirstlane(
+          fresh ? P.fp8_stack[top - 1 - rank] : a.bt[(int64_t)r * mp + p_new]);
+      // this wave's own ring slot holds the task's code block and table
+      // (its first copy comes after)
+      uint8_t* own = ring + (NW - 1) * SLOTS * STAGE;
+#pragma unroll 1
+      for (int kv = 0; kv < 2; ++kv) {
+        SmallTask<D> T;
+        T.kv = kv;
+        T.r = r;
+        T.p = p_new;
+        T.t0 = s_in % PAGE;
+        T.t1 = T.t0 + 1;
+        T.row0 = r - T.t0;  // the token's input row is r
+        T.layer = a.layer;
+        T.li = 0;
+        T.h = h;
+        small_task_load_x<D>(T, H, a.n_req, a.k_new, a.v_new, lane);
+        small_task_load_old<D>(T, P, id, lane);
+        small_task_run<D>(T, P, id, reinterpret_cast<uint32_t*>(own), own + PAGE * D, lane);
+      }
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the token's codes and scales are stored
+      if (lane == 0) s_stage[n_st - 1].y = id;
+    } else if (lane == 0) {
+      atomicOr(&P.ctrl[CTRL_ERR], bad);
+      s_app_bad = 1;
+    }
+    if (lane == 0) __hip_atomic_store(&s_app, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+    if (bad) return;
+    int prev = 0;
+    if (lane == 0) prev = atomicAdd(&P.ctrl[CTRL_APPEND_ARRIVE], 1);
+    prev = __shfl(prev, 0, 64);
+    if (prev != a.n_req * H - 1) return;
+    // the last arrival: record the fresh pages (ids in request order)
+    int base = 0;
+    for (int b0 = 0; b0 < a.n_req; b0 += 64) {
+      const int rr = b0 + lane;
+      const int64_t ix = rr < a.n_req ? (int64_t)rr * mp + a.seq_lens[rr] / PAGE : 0;
+      const bool fr = rr < a.n_req && a.bt[ix] < 0;
+      const uint64_t fm = __ballot(fr);
+      if (fr) {
+        const int k = base + __popcll(fm & ((1ull << lane) - 1ull));
+        a.bt_w[ix] = P.fp8_stack[top - 1 - k];
+        a.tags_w[ix] = TAG_R;
+      }
+      base += __popcll(fm);
+    }
+    if (lane == 0) {
+      P.ctrl[CTRL_FP8_TOP] = top - n_fresh;
+      P.ctrl[CTRL_APPEND_ARRIVE] = 0;
+    }
+  };
   int jc = min(wid, n_st);  // stage this wave processes next
   int jq = n_st;            // two slots: the claimed stage after jc (in flight)
   // the oldest wave of each SIMD copies its first stage now, the others after
   // the barrier: the first copies of a launch queue behind every workgroup's,
   // and each SIMD should get its first stage early
-  if (wid < 4 && jc < n_st) issue(stage_of(jc), 0);
+  // (with the fused append, the appended page's stage waits for the append)
+  const bool defer0 = APP && holds && jc == n_st - 1;
+  if (wid < 4 && jc < n_st && !defer0) issue(stage_of(jc), 0);
 
   __syncthreads();  // query operands and the stage list visible to every wave
   const float qinv = s_qinv[ln];  // undoes the query-term scale of this lane's column
-  if (wid >= 4 && jc < n_st) issue(stage_at(jc), 0);
+  if constexpr (APP) {
+    if (holds && wid == NW - 1) append_token();
+  }
+  if ((wid >= 4 || defer0) && jc < n_st) issue(stage_at(jc), 0);
   if (SLOTS == 2 && jc < n_st) {
     jq = claim();
     if (jq < n_st) issue(stage_at(jq), 1);
@@ -789,7 +930,7 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
     fw[tid] = lw > 0.0f ? exp2f(mm[tid] - M) / L : 0.0f;
     if (tid % NW == 0) {
       part[G * D + head] = M;
-      part[G * D + G + head] = L;
+      part[G * D + G + head] = (APP && s_app_bad) ? -1.0f : L;  // -1: the merge writes zeros
     }
   }
   __syncthreads();
@@ -831,6 +972,7 @@ __global__ __launch_bounds__(D / 4) void decode_merge_kernel(int G, int H, int m
   const float* base = partials + ((int64_t)r * H + h) * max_chunks * stride;
   float M = -INFINITY, L = 0.0f;
   float4 O = make_float4(0.f, 0.f, 0.f, 0.f);
+  bool poisoned = false;  // a slot with l < 0: a failed fused append, write zeros
   for (int k0 = 0; k0 < max_chunks; k0 += B) {
     float4 ok[B];
 #pragma unroll
@@ -842,6 +984,7 @@ __global__ __launch_bounds__(D / 4) void decode_merge_kernel(int G, int H, int m
     const float* pk = base + (int64_t)min(k0 + c4, max_chunks - 1) * stride;
     const float mj = pk[G * D + n];
     const float lj = mine ? pk[G * D + G + n] : 0.0f;
+    poisoned |= __any(lj < 0.0f);
     float mb = lj > 0.0f ? mj : -INFINITY;
 #pragma unroll
     for (int o = 1; o < D / 4; o <<= 1) mb = fmaxf(mb, __shfl_xor(mb, o, D / 4));
@@ -869,6 +1012,7 @@ __global__ __launch_bounds__(D / 4) void decode_merge_kernel(int G, int H, int m
     }
   }
   const int64_t row = (int64_t)r * Hq + h * G + n;
+  if (poisoned) L = 0.0f;
   const float inv = L > 0.0f ? 1.0f / L : 0.0f;
   reinterpret_cast<float4*>(out + row * D)[c4] = make_float4(O.x * inv, O.y * inv, O.z * inv, O.w * inv);
   if (lse && c4 == 0) lse[row] = L > 0.0f ? (M + log2f(L)) * 0.69314718055994531f : -INFINITY;
@@ -880,10 +1024,23 @@ static constexpr size_t lds_limit() {
   return 160 * 1024 - sizeof(int4) * MAX_CHUNK_PAGES - 3 * 16 * NW_MAX * sizeof(float) - 256;
 }
 
+template <bool APP>
+static const void* decode_instance(int d, bool pair, bool g6) {
+  if (d == 256)
+    return g6 ? (const void*)decode_kernel<256, true, true, APP>
+                : pair ? (const void*)decode_kernel<256, true, false, APP>
+                       : (const void*)decode_kernel<256, false, false, APP>;
+  return g6 ? (const void*)decode_kernel<128, true, true, APP>
+              : pair ? (const void*)decode_kernel<128, true, false, APP>
+                     : (const void*)decode_kernel<128, false, false, APP>;
+}
+
 hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t* q,
                          const int32_t* bt, const uint8_t* tags, int max_pages,
                          const int32_t* seq_lens, float* out, float* lse, void* ws,
-                         hipStream_t s, hipEvent_t* ev) {
+                         hipStream_t s, hipEvent_t* ev, const uint16_t* k_new,
+                         const uint16_t* v_new, int32_t* bt_w, uint8_t* tags_w) {
+  const bool app = k_new != nullptr;
   const DecodeShape sh = decode_shape(n_req, max_pages, P.n_kv_heads, P.recent);
   DecodeArgs a;
   a.P = P;
@@ -900,6 +1057,10 @@ hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t
   a.cunits = sh.cunits;
   a.max_chunks = sh.max_chunks;
   a.sm_log2 = 1.4426950408889634f / sqrtf((float)P.d);
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.bt_w = bt_w;
+  a.tags_w = tags_w;
   // dynamic LDS: three query operands, then the page ring (reused by the wave merge)
   const bool pair = P.group <= 8;
   const int nw = pair ? DecodeCfg<true>::NW : DecodeCfg<false>::NW;
@@ -909,17 +1070,13 @@ hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t
   const size_t lds = qop_b + ring_b;  // the epilogue reuses each wave's ring slot
   if (lds > lds_limit()) return hipErrorInvalidValue;
   const bool g6 = pair && P.group <= 6;
-  const void* kern =
-      P.d == 256 ? (g6 ? (const void*)decode_kernel<256, true, true>
-                       : pair ? (const void*)decode_kernel<256, true, false> : (const void*)decode_kernel<256, false, false>)
-                 : (g6 ? (const void*)decode_kernel<128, true, true>
-                       : pair ? (const void*)decode_kernel<128, true, false> : (const void*)decode_kernel<128, false, false>);
+  const void* kern = app ? decode_instance<true>(P.d, pair, g6) : decode_instance<false>(P.d, pair, g6);
   // the dynamic-LDS limit is raised once per kernel instance and device
   static std::atomic<uint32_t> attr_done[64];
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
-  const uint32_t bit = 1u << ((P.d == 256 ? 3 : 0) + (g6 ? 2 : pair ? 1 : 0));
+  const uint32_t bit = 1u << ((app ? 6 : 0) + (P.d == 256 ? 3 : 0) + (g6 ? 2 : pair ? 1 : 0));
   if (dev < 0 || dev >= 64 || !(attr_done[dev].load() & bit)) {
     e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_limit());
     if (e != hipSuccess) return e;

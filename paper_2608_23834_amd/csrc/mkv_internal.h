@@ -73,7 +73,9 @@ size_t decode_ws_bytes(int n_req, int max_pages, int n_kv_heads, int group, int 
 hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t* q,
                          const int32_t* bt, const uint8_t* tags, int max_pages,
                          const int32_t* seq_lens, float* out, float* lse, void* ws,
-                         hipStream_t s, hipEvent_t* ev);
+                         hipStream_t s, hipEvent_t* ev, const uint16_t* k_new = nullptr,
+                         const uint16_t* v_new = nullptr, int32_t* bt_w = nullptr,
+                         uint8_t* tags_w = nullptr);
 
 // mkv_probe.hip
 hipError_t launch_stream_read(const void* buf, size_t bytes, uint32_t* sink, int n_wg, hipStream_t s);

@@ -127,6 +127,43 @@ class Twin:
             res["ref_out"], res["ref_lse"] = o, l
         return res
 
+    def decode_append(self, layer=0, q=None):
+        """One fused decode step on `layer`: append one token per request at
+        its current length, then decode over length + 1.  The oracle runs the
+        append and the decode as two calls.  Lengths advance with advance()."""
+        import paper_2608_23834_amd as mk
+        torch = _torch()
+        w = self.w
+        kk, vv = [], []
+        for r in range(self.n_req):
+            k, v = wl.kv_layer(w, layer, 1, token_offset=r * 1_000_000 + self.cur[r])
+            kk.append(k)
+            vv.append(v)
+        K, V = np.concatenate(kk), np.concatenate(vv)  # [n_req][H][d]
+        q = wl.q_decode(w, layer) if q is None else q
+        if q.shape[0] != self.n_req:
+            q = np.resize(q, (self.n_req,) + q.shape[1:])
+        sb = np.array(self.cur, np.int32)
+        out = torch.full((self.n_req, w.n_q_heads, w.head_dim), float("nan"), device="cuda")
+        lse = torch.full((self.n_req, w.n_q_heads), float("nan"), device="cuda")
+        ws = mk.workspace(self.gpu, self.n_req, self.max_pages)
+        mk.paged_attn_decode_append(
+            self.gpu, layer, torch.from_numpy(q.view(np.int16)).cuda(),
+            torch.from_numpy(K.view(np.int16)).cuda(), torch.from_numpy(V.view(np.int16)).cuda(),
+            self.bt, self.tags, torch.from_numpy(sb).cuda(), out, lse, ws)
+        torch.cuda.synchronize()
+        res = dict(out=out.cpu().numpy(), lse=lse.cpu().numpy(), q=q, seq_lens=sb + 1)
+        if self.orc is not None:
+            cu = np.arange(self.n_req + 1, dtype=np.int32)
+            rc = self.orc.append(layer, self.obt, self.otags, sb, cu, K[None], V[None])
+            assert rc == 0, rc
+            o, l = self.orc.decode(layer, q, self.obt, self.otags, sb + 1)
+            res["ref_out"], res["ref_lse"] = o, l
+        return res
+
+    def advance(self, n=1):
+        self.cur = [c + n for c in self.cur]
+
     def chunk(self, n_q, layer=0, sample_stride=1):
         """Chunk attention for the last n_q[r] tokens of each request (already
         appended).  The oracle computes every sample_stride-th query of each

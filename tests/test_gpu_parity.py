@@ -201,6 +201,117 @@ def test_decode_steps_with_appends(torch_cuda):
             assert max_abs(res["out"], res["ref_out"]) <= TOL
 
 
+def _fused_steps(w, lens, n_layers, n_steps, recent, check_every=4, headroom=None):
+    """Decode steps through the fused call (append one token per request and
+    decode, per layer), then migration; the oracle runs append, decode and
+    migrate as separate calls.  Tables, tags and free lists bit-exact after
+    every step, page bytes every few steps, outputs within TOL."""
+    from _harness import Twin, max_abs
+    print(f"\n[fused steps] {w.name} lens={lens} layers={n_layers} W={recent}", flush=True)
+    tw = Twin(w, n_layers=n_layers, lens=lens, recent=recent,
+              headroom=n_steps + 16 if headroom is None else headroom)
+    tw.fill()
+    tw.migrate()
+    worst = 0.0
+    for step in range(n_steps):
+        for layer in range(n_layers):
+            res = tw.decode_append(layer)
+            err = max(max_abs(res["out"], res["ref_out"]), max_abs(res["lse"], res["ref_lse"]))
+            worst = max(worst, err)
+            assert np.all(np.isfinite(res["out"]))
+            assert err <= TOL, (step, layer, err)
+        tw.advance()
+        tw.migrate()
+        tw.check_tables()
+        if step % check_every == check_every - 1 or step == n_steps - 1:
+            tw.check_pages()
+    print(f"  {n_steps} steps, max|dO|, max|dlse| {worst:.3e}", flush=True)
+    return tw
+
+
+def test_decode_append_fused_steps_d256(torch_cuda):
+    """Fused decode steps, d = 256, six query heads per KV head, two layers:
+    lengths 0, 1, 47, 64 and 200 cross page boundaries, so layer 0's call
+    opens fresh pages that layer 1's call then writes; partly filled pages
+    grow their FP8 scales; pages leave the short Recent window as TQ3."""
+    w = wl.workload(2)
+    _fused_steps(w, [200, 47, 64, 1, 0], n_layers=2, n_steps=36, recent=32)
+
+
+def test_decode_append_fused_steps_d128_group12(torch_cuda):
+    """Fused decode steps for the other kernel instances: d = 128 with eight
+    query heads per KV head (page pairs), and twelve query heads per KV
+    head (no pairs)."""
+    import dataclasses
+    _fused_steps(wl.workload(1), [1000, 15, 33], n_layers=1, n_steps=20, recent=48)
+    w = dataclasses.replace(wl.workload(2), n_kv_heads=2, name="group12")
+    _fused_steps(w, [700, 16, 5], n_layers=1, n_steps=20, recent=64)
+
+
+def test_decode_append_fused_full_size(torch_cuda):
+    """The long pair at full size (2 x 59,008 tokens, one layer) with the
+    table width of the benchmark's default run (3,692 pages): three fused
+    steps (the first opens a fresh page in each request), bit-exact state and
+    outputs against the oracle's append + decode."""
+    w = wl.workload(3)
+    tw = _fused_steps(w, list(w.ctx), n_layers=1, n_steps=3, recent=None, check_every=3,
+                      headroom=3 + 2 * 20 + 16)
+    assert tw.max_pages == 3692
+    assert (tw.otags == 0).sum() == 2 * 129
+
+
+def test_decode_append_fails_closed(torch_cuda):
+    """A fused step that cannot append as a whole (free list exhausted, a
+    length out of range, a page that is not Recent) changes no state, sets
+    the error word and writes zero outputs (lse -inf) for every request."""
+    import paper_2608_23834_amd as mk
+    torch = torch_cuda
+    d, Hq = 128, 2
+    gp = mk.Pool(1, Hq, 1, d, 1, 2, 16, np.ones(d, np.int8))
+    bt = torch.full((2, 4), -1, dtype=torch.int32, device="cuda")
+    tg = torch.full((2, 4), 0xFF, dtype=torch.uint8, device="cuda")
+    ws = mk.workspace(gp, 2, 4)
+    rng = np.random.default_rng(7)
+    q = torch.from_numpy(rng.integers(0x3c00, 0x3f00, (2, Hq, d)).astype(np.int16)).cuda()
+    kv = torch.from_numpy(rng.integers(0x3c00, 0x3f00, (2, 1, d)).astype(np.int16)).cuda()
+
+    def call(sl, n=2):
+        out = torch.full((n, Hq, d), 7.0, device="cuda")
+        lse = torch.full((n, Hq), 7.0, device="cuda")
+        mk.paged_attn_decode_append(gp, 0, q[:n], kv[:n], kv[:n], bt[:n], tg[:n],
+                                    torch.tensor(sl, dtype=torch.int32, device="cuda"), out, lse, ws)
+        torch.cuda.synchronize()
+        return out.cpu().numpy(), lse.cpu().numpy()
+
+    def unchanged():
+        assert (bt.cpu().numpy() == -1).all() and (tg.cpu().numpy() == 0xFF).all()
+        assert mk.kv_pool_free_counts(gp) == (1, 2)
+
+    # two fresh pages wanted, one free
+    out, lse = call([0, 0])
+    assert mk.kv_pool_check_errors(gp, clear=True) & mk.DEVERR["FP8_EXHAUSTED"]
+    assert (out == 0).all() and np.isneginf(lse).all()
+    unchanged()
+    # a length past the table
+    out, lse = call([0, 64])
+    assert mk.kv_pool_check_errors(gp, clear=True) & mk.DEVERR["RANGE"]
+    assert (out == 0).all() and np.isneginf(lse).all()
+    unchanged()
+    # one request: the page is opened, the output is the token's V (one key)
+    out, lse = call([0], n=1)
+    assert mk.kv_pool_check_errors(gp, clear=True) == 0
+    assert bt.cpu().numpy()[0, 0] >= 0 and tg.cpu().numpy()[0, 0] == mk.TAG_R
+    assert mk.kv_pool_free_counts(gp) == (0, 2)
+    v = (kv[0, 0].cpu().numpy().astype(np.uint32) << 16).view(np.float32)
+    assert np.abs(out[0] - v[None]).max() <= 0.07 * np.abs(v).max()  # one E4M3 rounding
+    # the opened page tagged Stale: appending to it is refused
+    tg[0, 0] = mk.TAG_S
+    bt_before = bt.cpu().numpy().copy()
+    out, lse = call([1], n=1)
+    assert mk.kv_pool_check_errors(gp, clear=True) & mk.DEVERR["NOT_RECENT"]
+    assert (out == 0).all() and np.array_equal(bt.cpu().numpy(), bt_before)
+
+
 def test_partition_pages_matches_oracle(torch_cuda):
     import oracle
     import paper_2608_23834_amd as mk
