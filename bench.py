@@ -7,8 +7,11 @@ layers, 24 query / 4 KV heads, head dim 256, 16-token pages, Recent window
 data with the distributions of mkv_workloads.
 
 One step is one decode step of the whole path: for each of the 16 layers,
-kv_append_fp8 (the new token of each request) then paged_attn_decode; after
-the last layer kv_migrate_to_tq3 (pages leaving the Recent window).  All inputs
+paged_attn_decode_append (the new token of each request appended inside the
+decode launch, then attention over the grown context); after the last layer
+kv_migrate_to_tq3 (pages leaving the Recent window).  The same steps with the
+append as its own call (kv_append_fp8, then paged_attn_decode) are timed too,
+for comparison.  All inputs
 are resident in HBM before the timed region.  The headline value is the step
 time per layer (us/layer, lower is better); the decode kernel's own time, its
 effective KV bandwidth and its fraction of the 8 TB/s HBM peak are reported
@@ -55,7 +58,7 @@ def kv_bytes_of(tags_row: np.ndarray, seq_len: int, d: int, n_kv_heads: int) -> 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_kernel_long_pair_2x59008_hbm_traffic.txt")
 DECODE_SOURCES = [os.path.join(ROOT, "paper_2608_23834_amd", "csrc", f)
-                  for f in ("mkv_decode.hip", "mkv_attn.h", "mkv_device.h")]
+                  for f in ("mkv_decode.hip", "mkv_append.h", "mkv_attn.h", "mkv_device.h")]
 
 
 def decode_source_hash() -> str:
@@ -235,7 +238,9 @@ def stream_probe(mk, torch, nbytes, achieved, reps=20):
     return {"bytes": n, "us": round(us, 2), "gb_per_s": round(bw / 1e9, 1),
             "frac_of_peak": round(bw / HBM_PEAK, 4),
             "decode_frac_of_stream": round(achieved / bw, 4),
-            "kernel": "stream_read_kernel (mkv_stream_read), HIP events around each call"}
+            "kernel": "stream_read_kernel (mkv_stream_read), HIP events around each call "
+                      "(these also span the launch; the decode scan is timed by its dispatch, "
+                      "so decode_frac_of_stream reads a few % high)"}
 
 
 def _cpu_model():
@@ -256,6 +261,8 @@ def main():
     ap.add_argument("--cfg", type=int, default=3)
     ap.add_argument("--layers", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-unfused", action="store_true",
+                    help="skip the comparison pass with the append as its own call")
     ap.add_argument("--no-chunk", action="store_true",
                     help="skip the chunked-prefill measurement")
     ap.add_argument("--copy-probe", action="store_true",
@@ -276,7 +283,8 @@ def main():
     torch.cuda.init()
     w = wl.workload(args.cfg)
     n_layers = args.layers or w.n_layers
-    n_steps = args.warmup + 2 * args.steps  # warmup, pass A, pass B
+    n_pass = 2 if args.no_unfused else 3
+    n_steps = args.warmup + n_pass * args.steps  # warmup, pass A, pass B (, pass C)
     t_setup = time.perf_counter()
     pool, bt, tags, am, max_pages = build_state(w, n_layers, n_steps + 16, mk, torch)
     lens = list(w.ctx)
@@ -310,6 +318,12 @@ def main():
 
     def step(s):
         for l in range(n_layers):
+            mk.paged_attn_decode_append(pool, l, q_all[l], nk[l, s], nv[l, s], bt, tags,
+                                        seq_before[s], out, None, ws)
+        mk.kv_migrate_to_tq3(pool, bt, tags, am, seq_after[s])
+
+    def step_unfused(s):
+        for l in range(n_layers):
             mk.kv_append_fp8(pool, l, bt, tags, seq_before[s], cu1, nk[l, s], nv[l, s])
             mk.paged_attn_decode(pool, l, q_all[l], bt, tags, seq_after[s], out, None, ws)
         mk.kv_migrate_to_tq3(pool, bt, tags, am, seq_after[s])
@@ -334,12 +348,12 @@ def main():
     # kernels of each step's last decode call, read once the step is queued
     mk.paged_attn_set_timing(pool, True)
     scan_us, merge_us = [], []
-    for i, s in enumerate(range(args.warmup + args.steps, n_steps)):
+    for i, s in enumerate(range(args.warmup + args.steps, args.warmup + 2 * args.steps)):
         evs = ev[i * n_layers:(i + 1) * n_layers]
         for l in range(n_layers):
-            mk.kv_append_fp8(pool, l, bt, tags, seq_before[s], cu1, nk[l, s], nv[l, s])
             evs[l][0].record(stream)
-            mk.paged_attn_decode(pool, l, q_all[l], bt, tags, seq_after[s], out, None, ws)
+            mk.paged_attn_decode_append(pool, l, q_all[l], nk[l, s], nv[l, s], bt, tags,
+                                        seq_before[s], out, None, ws)
             evs[l][1].record(stream)
         a_us, m_us = mk.paged_attn_last_times(pool)
         scan_us.append(a_us)
@@ -354,8 +368,23 @@ def main():
     if err:
         raise RuntimeError(f"device error word {err:#x} during the benchmark")
     tags_end = tags.cpu().numpy()
+    # pass C: the append as its own call (two launches per layer), whole steps
+    unfused_ms = None
+    if not args.no_unfused:
+        c0 = torch.cuda.Event(enable_timing=True)
+        c1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        c0.record(stream)
+        for s in range(args.warmup + 2 * args.steps, n_steps):
+            step_unfused(s)
+        c1.record(stream)
+        torch.cuda.synchronize()
+        unfused_ms = c0.elapsed_time(c1) / args.steps
+        err = mk.kv_pool_check_errors(pool)
+        if err:
+            raise RuntimeError(f"device error word {err:#x} during the benchmark")
     sl0 = [L + args.warmup + args.steps + 1 for L in lens]
-    sl1 = [L + n_steps for L in lens]
+    sl1 = [L + args.warmup + 2 * args.steps for L in lens]
     kvb0 = sum(kv_bytes_of(tags_mid[r], sl0[r], d, Hkv) for r in range(n_req))
     kvb1 = sum(kv_bytes_of(tags_end[r], sl1[r], d, Hkv) for r in range(n_req))
     kv_bytes = 0.5 * (kvb0 + kvb1)
@@ -382,18 +411,24 @@ def main():
         "config": {"workload": w.name, "n_req": n_req, "seq_len": lens[0], "layers": n_layers,
                    "q_heads": w.n_q_heads, "kv_heads": Hkv, "head_dim": d, "page_tokens": PAGE,
                    "recent_tokens": w.recent, "kv_formats": "fp8-e4m3 (R,A) + tq3 (S)",
-                   "step": "per layer: append 1 token/request + decode; then migrate"},
+                   "step": "per layer: decode with the append of 1 token/request fused "
+                           "(paged_attn_decode_append); then migrate"},
         "decode_attn_us_per_layer": round(dec_us, 3),
         "decode_scan_us": round(scan_mean, 3),
         "decode_merge_us": round(float(merge_us.mean()), 3),
         "decode_timing": "second pass of the same steps: HIP events around each "
-                         "paged_attn_decode call; the library's events (same stream) around "
-                         "the split-scan and merge kernels of each step's last call",
+                         "paged_attn_decode_append call; the library's events (same stream) "
+                         "around the split-scan (with the fused append) and merge kernels of "
+                         "each step's last call",
+        "unfused_us_per_layer": None if unfused_ms is None else round(unfused_ms * 1e3 / n_layers, 3),
+        "unfused_step": "third pass: the same steps with kv_append_fp8 and paged_attn_decode "
+                        "as separate calls",
         "kv_bytes_per_layer": int(kv_bytes),
         "effective_kv_gb_per_s": round(kv_bytes / (dec_us * 1e-6) / 1e9, 1),
         "roofline": {"bound": "hbm", "achieved": round(achieved / 1e9, 1), "peak": HBM_PEAK / 1e9,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK, 4), "traffic": traffic,
-                     "kernel": "decode_kernel<256, true, true> (split scan, one launch per layer)"},
+                     "kernel": "decode_kernel<256, true, true, true> (split scan with the "
+                               "fused append, one launch per layer)"},
         "counters": {k: int(v) for k, v in counters.items()},
         "setup_s": round(setup_s, 1),
     }

@@ -245,8 +245,9 @@ mkv_status kv_pool_read_free_lists(mkv_pool* pool, int32_t* fp8_ids, int32_t* n_
 mkv_status kv_pool_counters(mkv_pool* pool, mkv_counters* out);
 
 /* Kernel timing for measurement tools; correct use never needs it.  When
- * enabled, each paged_attn_decode call on this pool records HIP events on its
- * stream before and after its split-scan kernel and after its merge kernel.
+ * enabled, each paged_attn_decode or paged_attn_decode_append call on this
+ * pool launches its split-scan and merge kernels with HIP events that track
+ * each kernel's own start and end on its stream (hipExtLaunchKernel).
  * paged_attn_last_times waits for the last call's events and returns the
  * durations of the scan and of the merge in microseconds (MKV_ESTATE when
  * timing is off or no call was timed).  Enabling creates the events on the

@@ -233,7 +233,7 @@ mkv_status paged_attn_decode_append(mkv_pool* pool, int32_t layer, int32_t n_req
 mkv_status paged_attn_set_timing(mkv_pool* pool, int32_t enable) {
   if (!pool) return MKV_EINVAL;
   if (enable && !pool->timing) {
-    for (int i = 0; i < 3; ++i) {
+    for (int i = 0; i < 4; ++i) {
       if (hipEventCreate(&pool->timing_ev[i]) != hipSuccess) {
         for (int k = 0; k < i; ++k) (void)hipEventDestroy(pool->timing_ev[k]);
         return MKV_EHIP;
@@ -242,7 +242,7 @@ mkv_status paged_attn_set_timing(mkv_pool* pool, int32_t enable) {
     pool->timing = 1;
     pool->timed = 0;
   } else if (!enable && pool->timing) {
-    for (int i = 0; i < 3; ++i) (void)hipEventDestroy(pool->timing_ev[i]);
+    for (int i = 0; i < 4; ++i) (void)hipEventDestroy(pool->timing_ev[i]);
     pool->timing = pool->timed = 0;
   }
   return MKV_OK;
@@ -252,9 +252,9 @@ mkv_status paged_attn_last_times(mkv_pool* pool, float* scan_us, float* merge_us
   if (!pool || !scan_us || !merge_us) return MKV_EINVAL;
   if (!pool->timing || !pool->timed) return MKV_ESTATE;
   float a = 0.0f, b = 0.0f;
-  if (hipEventSynchronize(pool->timing_ev[2]) != hipSuccess ||
+  if (hipEventSynchronize(pool->timing_ev[3]) != hipSuccess ||
       hipEventElapsedTime(&a, pool->timing_ev[0], pool->timing_ev[1]) != hipSuccess ||
-      hipEventElapsedTime(&b, pool->timing_ev[1], pool->timing_ev[2]) != hipSuccess)
+      hipEventElapsedTime(&b, pool->timing_ev[2], pool->timing_ev[3]) != hipSuccess)
     return MKV_EHIP;
   *scan_us = a * 1000.0f;
   *merge_us = b * 1000.0f;

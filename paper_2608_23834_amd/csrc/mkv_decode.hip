@@ -27,6 +27,7 @@
 // A second kernel merges all partials of a request and query head (Eq.
 // softmax-merge).  The workspace holds O(chunks x heads x d) partials, never
 // anything the size of the cache.
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <atomic>
@@ -1084,20 +1085,19 @@ hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t
   }
   dim3 grid(sh.max_chunks, P.n_kv_heads, n_req);
   dim3 mgrid(P.group, P.n_kv_heads, n_req);
+  // with timing on, the events track each kernel's own start and end (the
+  // dispatch's timestamps, not markers around the launch)
   void* args[] = {&a};
-  if (ev && (e = hipEventRecord(ev[0], s)) != hipSuccess) return e;
-  e = hipLaunchKernel(kern, grid, dim3(64 * nw), args, lds, s);
+  e = ev ? hipExtLaunchKernel(kern, grid, dim3(64 * nw), args, lds, s, ev[0], ev[1], 0)
+         : hipLaunchKernel(kern, grid, dim3(64 * nw), args, lds, s);
   if (e != hipSuccess) return e;
-  if (ev && (e = hipEventRecord(ev[1], s)) != hipSuccess) return e;
-  if (P.d == 256)
-    hipLaunchKernelGGL(decode_merge_kernel<256>, mgrid, dim3(64), 0, s, P.group, P.n_kv_heads,
-                       sh.max_chunks, a.partials, out, lse);
-  else
-    hipLaunchKernelGGL(decode_merge_kernel<128>, mgrid, dim3(32), 0, s, P.group, P.n_kv_heads,
-                       sh.max_chunks, a.partials, out, lse);
-  e = hipGetLastError();
-  if (e == hipSuccess && ev) e = hipEventRecord(ev[2], s);
-  return e;
+  int G = P.group, H = P.n_kv_heads, mc = sh.max_chunks;
+  const float* pa = a.partials;
+  void* margs[] = {&G, &H, &mc, &pa, &out, &lse};
+  const void* mk = P.d == 256 ? (const void*)decode_merge_kernel<256> : (const void*)decode_merge_kernel<128>;
+  const dim3 mblock(P.d / 4);
+  return ev ? hipExtLaunchKernel(mk, mgrid, mblock, margs, 0, s, ev[2], ev[3], 0)
+            : hipLaunchKernel(mk, mgrid, mblock, margs, 0, s);
 }
 
 }  // namespace mkv

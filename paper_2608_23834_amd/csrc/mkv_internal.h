@@ -15,7 +15,7 @@ struct mkv_pool {
   int32_t* ctrl;      // device
   mkv::CtrlLayout cl;
   uint64_t decode_routes, chunk_routes;
-  hipEvent_t timing_ev[3];  // scan start, scan end, merge end (timing on)
+  hipEvent_t timing_ev[4];  // scan start and end, merge start and end (timing on)
   int timing, timed;
 };
 

@@ -250,13 +250,13 @@ def test_decode_append_fused_steps_d128_group12(torch_cuda):
 
 def test_decode_append_fused_full_size(torch_cuda):
     """The long pair at full size (2 x 59,008 tokens, one layer) with the
-    table width of the benchmark's default run (3,692 pages): three fused
+    table width of the benchmark's default run (3,693 pages): three fused
     steps (the first opens a fresh page in each request), bit-exact state and
     outputs against the oracle's append + decode."""
     w = wl.workload(3)
     tw = _fused_steps(w, list(w.ctx), n_layers=1, n_steps=3, recent=None, check_every=3,
-                      headroom=3 + 2 * 20 + 16)
-    assert tw.max_pages == 3692
+                      headroom=3 + 3 * 20 + 16)
+    assert tw.max_pages == 3693
     assert (tw.otags == 0).sum() == 2 * 129
 
 
