@@ -447,39 +447,75 @@ __global__ __launch_bounds__(64) void append_step_kernel(PoolView P, int layer_s
 // Migrate (Retier to TQ3)
 // ===========================================================================
 
-__global__ __launch_bounds__(1024) void migrate_plan_kernel(int n_req, const int32_t* bt,
-                                                            uint8_t* tags, int max_pages,
-                                                            const uint8_t* anchor,
+// Plan of a migration, one workgroup.  The table is walked as one run of
+// (request, page) entries, MIG_KB consecutive entries per thread with every
+// load of a batch in flight together.  Pass 1 validates the whole call
+// (lengths, candidate ids, free-list room) so that a failing call changes
+// nothing; pass 2 ranks the migrating pages in (request, page) order with one
+// block scan per batch, retags Anchors and writes the work list with the TQ3
+// ids popped in that order.  The table entries, Stale tags and FP8 releases
+// are published by the publish kernel after the encode kernel has built the
+// TQ3 pages (Alg. 1, copy before publish).
+constexpr int MIG_KB = 8;
+__global__ __launch_bounds__(1024) void migrate_plan_kernel(int n_req, const int32_t* bt, uint8_t* tags,
+                                                            int max_pages, const uint8_t* anchor,
                                                             const int32_t* seq_lens, int W,
                                                             int32_t* ctrl, const int32_t* tq3_stack,
                                                             int32_t* list, int n_fp8) {
   __shared__ int scratch[32];
   __shared__ int s_err, s_cnt;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, nt = blockDim.x;
   if (tid == 0) { s_err = 0; s_cnt = 0; }
-  __syncthreads();
-  for (int r = 0; r < n_req; ++r) {
+  const int top3 = ctrl[CTRL_TQ3_TOP];
+  int err = 0, cnt = 0;
+  for (int r = tid; r < n_req; r += nt) {
     const int S = seq_lens[r];
-    const int np = (S + PAGE - 1) / PAGE;
-    if (S < 0 || np > max_pages) {
-      if (tid == 0) atomicOr(&s_err, (int)MKV_DEVERR_RANGE);
-      continue;
+    if (S < 0 || (S + PAGE - 1) / PAGE > max_pages) err |= MKV_DEVERR_RANGE;
+  }
+  const int64_t N = (int64_t)n_req * max_pages;
+  const int64_t per_batch = (int64_t)nt * MIG_KB;
+  uint8_t tg[MIG_KB], an[MIG_KB];
+  int32_t id[MIG_KB], sl[MIG_KB], rq[MIG_KB], pg[MIG_KB];
+  // entries f0 .. f0 + MIG_KB - 1: (request, page) stepped from one division
+  auto load = [&](int64_t f0) {
+    int r = (int)(f0 / max_pages), p = (int)(f0 - (int64_t)r * max_pages);
+#pragma unroll
+    for (int j = 0; j < MIG_KB; ++j) {
+      const bool in = f0 + j < N;
+      const int64_t f = in ? f0 + j : 0;
+      rq[j] = in ? r : -1;
+      pg[j] = p;
+      tg[j] = tags[f];
+      an[j] = anchor ? anchor[f] : 0;
+      id[j] = bt[f];
+      sl[j] = seq_lens[in ? r : 0];
+      if (++p == max_pages) { p = 0; ++r; }
     }
-    int cnt = 0, bad = 0;
-    for (int p = tid; p < np; p += blockDim.x) {
-      const int64_t i = (int64_t)r * max_pages + p;
-      if (tags[i] == TAG_R && (p + 1) * PAGE <= S - W && !(anchor && anchor[i])) {
+  };
+  // 1: migrating page, 2: Anchor to retag, 0: neither
+  auto kind = [&](int j) {
+    if (rq[j] < 0) return 0;
+    const int p = pg[j], S = sl[j];
+    if (tg[j] != TAG_R || p >= (S + PAGE - 1) / PAGE || (p + 1) * PAGE > S - W) return 0;
+    return an[j] ? 2 : 1;
+  };
+  __syncthreads();
+  for (int64_t b0 = 0; b0 < N; b0 += per_batch) {
+    const int64_t f0 = b0 + (int64_t)tid * MIG_KB;
+    load(f0);
+#pragma unroll
+    for (int j = 0; j < MIG_KB; ++j) {
+      if (kind(j) == 1) {
         cnt++;
-        if (bt[i] < 0 || bt[i] >= n_fp8) bad = 1;
+        if (id[j] < 0 || id[j] >= n_fp8) err |= MKV_DEVERR_RANGE;
       }
     }
-    if (cnt) atomicAdd(&s_cnt, cnt);
-    if (bad) atomicOr(&s_err, (int)MKV_DEVERR_RANGE);
   }
+  if (cnt) atomicAdd(&s_cnt, cnt);
+  if (err) atomicOr(&s_err, err);
   __syncthreads();
-  const int top = ctrl[CTRL_TQ3_TOP];
   if (tid == 0) {
-    if (s_err == 0 && s_cnt > top) s_err |= MKV_DEVERR_TQ3_EXHAUSTED;
+    if (s_err == 0 && s_cnt > top3) s_err |= MKV_DEVERR_TQ3_EXHAUSTED;
     if (s_err == 0 && s_cnt > n_fp8) s_err |= MKV_DEVERR_RANGE;
   }
   __syncthreads();
@@ -492,31 +528,35 @@ __global__ __launch_bounds__(1024) void migrate_plan_kernel(int n_req, const int
     return;
   }
   int base = 0;
-  for (int r = 0; r < n_req; ++r) {
-    const int S = seq_lens[r];
-    const int np = (S + PAGE - 1) / PAGE;
-    for (int c0 = 0; c0 < np; c0 += blockDim.x) {
-      const int p = c0 + tid;
-      const int64_t i = (int64_t)r * max_pages + p;
-      int mig = 0;
-      if (p < np && tags[i] == TAG_R && (p + 1) * PAGE <= S - W) {
-        if (anchor && anchor[i]) tags[i] = TAG_A;  // Anchor: tag only, stays FP8
-        else mig = 1;
-      }
-      int tot;
-      const int rank = block_excl_scan(mig, scratch, &tot);
-      if (mig) {
-        int32_t* e = list + 4LL * (base + rank);
-        e[0] = r;
-        e[1] = p;
-        e[2] = bt[i];
-        e[3] = tq3_stack[top - 1 - (base + rank)];
-      }
-      base += tot;
+  for (int64_t b0 = 0; b0 < N; b0 += per_batch) {
+    const int64_t f0 = b0 + (int64_t)tid * MIG_KB;
+    load(f0);
+    int k[MIG_KB], c = 0;
+#pragma unroll
+    for (int j = 0; j < MIG_KB; ++j) {
+      k[j] = kind(j);
+      c += k[j] == 1;
     }
+    int tot;
+    int e = base + block_excl_scan(c, scratch, &tot);
+#pragma unroll
+    for (int j = 0; j < MIG_KB; ++j) {
+      const int64_t f = f0 + j;
+      if (k[j] == 2) tags[f] = TAG_A;  // Anchor: tag only, stays FP8
+      if (k[j] == 1) {
+        const int dst = tq3_stack[top3 - 1 - e];
+        int32_t* le = list + 4LL * e;
+        le[0] = rq[j];
+        le[1] = pg[j];
+        le[2] = id[j];
+        le[3] = dst;
+        e++;
+      }
+    }
+    base += tot;
   }
   if (tid == 0) {
-    ctrl[CTRL_TQ3_TOP] = top - base;
+    ctrl[CTRL_TQ3_TOP] = top3 - base;
     ctrl[CTRL_NLIST] = base;
     ctrl[CTRL_ABORT] = 0;
   }
