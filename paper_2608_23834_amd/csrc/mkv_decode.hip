@@ -227,7 +227,7 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   extern __shared__ __align__(16) uint8_t smem[];
   __shared__ int4 s_stage[MAX_CHUNK_PAGES];  // {lp_a, id_a, lp_b, id_b}; id_b < 0: FP8 stage
   __shared__ int s_next;  // next unclaimed stage (one-slot schedule)
-  __shared__ int s_app, s_app_bad;  // fused append: done flag, error bits
+  __shared__ int s_app, s_app_bad;  // fused append: append waves done, error flag
   // per (head, wave): running max, denominator, combine weight (epilogue)
   __shared__ __align__(16) float s_mlf[3][16 * NW_MAX];
   static_assert(NCH_OF(PAIR) * D * 4 <= SLOTS * 2 * (int)tq3_region_bytes(D),
@@ -530,7 +530,7 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
       // the page of the appended token: its copy waits until the append wave
       // has stored the token (and, for a fresh page, popped its id)
       if (holds && e.w < 0 && e.x == p_new) {
-        while (__hip_atomic_load(&s_app, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) == 0)
+        while (__hip_atomic_load(&s_app, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < 2)
           __builtin_amdgcn_s_sleep(1);
         e = stage_at(n_st - 1);
       }
@@ -544,15 +544,17 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
       if (lane < 2) dma4(4 * lane, scl_l + ((int64_t)e.y * H + h) * 8, dst + R8);
     }
   };
-  // Fused decode-step append (APP), run by the youngest wave of the workgroup
-  // that holds the request's new token, after the workgroup barrier, while the
-  // other waves start streaming: every such wave reads the whole call (each
+  // Fused decode-step append (APP), run by the two youngest waves of the
+  // workgroup that holds the request's new token (K by the older, V by the
+  // younger), after the workgroup barrier and each wave's first copy, while
+  // the other waves stream: every such wave reads the whole call (each
   // request's length, the free-list top, the table entries and tags of the
   // pages being appended to) and so reaches the same verdict and the same
   // fresh-page ids as the decode-step append kernel (same validation, ids
   // popped in request order, same arithmetic); it stores K and V of head h
-  // for the new token (Alg. 1, Append), then releases the appended page's
-  // stage.  The last of these waves to arrive on the control-block counter
+  // for the new token (Alg. 1, Append), then counts itself on an LDS flag; the
+  // appended page's stage is released when both have.  The last of these
+  // waves to arrive on the control-block counter
   // (each arrives after its reads and stores have returned) records the
   // fresh pages in the block table, pops them off the free list and resets
   // the counter.  On any error nothing is written, the error word gets its
@@ -596,37 +598,35 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
     if (!bad) {
       const int id = __builtin_amdgcn_readfirstlane(
           fresh ? P.fp8_stack[top - 1 - rank] : a.bt[(int64_t)r * mp + p_new]);
-      // this wave's own ring slot holds the task's code block and table
-      // (its first copy comes after)
-      uint8_t* own = ring + (NW - 1) * SLOTS * STAGE;
-#pragma unroll 1
-      for (int kv = 0; kv < 2; ++kv) {
-        SmallTask<D> T;
-        T.kv = kv;
-        T.r = r;
-        T.p = p_new;
-        T.t0 = s_in % PAGE;
-        T.t1 = T.t0 + 1;
-        T.row0 = r - T.t0;  // the token's input row is r
-        T.layer = a.layer;
-        T.li = 0;
-        T.h = h;
-        small_task_load_x<D>(T, H, a.n_req, a.k_new, a.v_new, lane);
-        small_task_load_old<D>(T, P, id, lane);
-        small_task_run<D>(T, P, id, reinterpret_cast<uint32_t*>(own), own + PAGE * D, lane);
-      }
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the token's codes and scales are stored
-      if (lane == 0) s_stage[n_st - 1].y = id;
+      // the task's code block and table: the wave's second ring slot, or
+      // (one slot per wave) a block of its own past the ring
+      const int kv = wid - (NW - 2);
+      uint8_t* own = SLOTS == 2 ? wring + STAGE : ring + NW * SLOTS * STAGE + kv * (PAGE * D + 256);
+      SmallTask<D> T;
+      T.kv = kv;
+      T.r = r;
+      T.p = p_new;
+      T.t0 = s_in % PAGE;
+      T.t1 = T.t0 + 1;
+      T.row0 = r - T.t0;  // the token's input row is r
+      T.layer = a.layer;
+      T.li = 0;
+      T.h = h;
+      small_task_load_x<D>(T, H, a.n_req, a.k_new, a.v_new, lane);
+      small_task_load_old<D>(T, P, id, lane);
+      small_task_run<D>(T, P, id, reinterpret_cast<uint32_t*>(own), own + PAGE * D, lane);
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");  // the token's codes and scale are stored
+      if (lane == 0 && kv == 0) s_stage[n_st - 1].y = id;
     } else if (lane == 0) {
       atomicOr(&P.ctrl[CTRL_ERR], bad);
       s_app_bad = 1;
     }
-    if (lane == 0) __hip_atomic_store(&s_app, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+    if (lane == 0) __hip_atomic_fetch_add(&s_app, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
     if (bad) return;
     int prev = 0;
     if (lane == 0) prev = atomicAdd(&P.ctrl[CTRL_APPEND_ARRIVE], 1);
     prev = __shfl(prev, 0, 64);
-    if (prev != a.n_req * H - 1) return;
+    if (prev != 2 * a.n_req * H - 1) return;
     // the last arrival: record the fresh pages (ids in request order)
     int base = 0;
     for (int b0 = 0; b0 < a.n_req; b0 += 64) {
@@ -657,10 +657,15 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
 
   __syncthreads();  // query operands and the stage list visible to every wave
   const float qinv = s_qinv[ln];  // undoes the query-term scale of this lane's column
-  if constexpr (APP) {
-    if (holds && wid == NW - 1) append_token();
+  if (APP && holds && wid >= NW - 2) {
+    // an append wave copies its first stage before the append (unless that
+    // stage is the appended page's), so the copy's latency overlaps the task
+    if (jc < n_st - 1) issue(stage_at(jc), 0);
+    append_token();
+    if (jc == n_st - 1) issue(stage_at(jc), 0);
+  } else if ((wid >= 4 || defer0) && jc < n_st) {
+    issue(stage_at(jc), 0);
   }
-  if ((wid >= 4 || defer0) && jc < n_st) issue(stage_at(jc), 0);
   if (SLOTS == 2 && jc < n_st) {
     jq = claim();
     if (jq < n_st) issue(stage_at(jq), 1);
@@ -1068,7 +1073,10 @@ hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t
   const int slots = pair ? DecodeCfg<true>::SLOTS : DecodeCfg<false>::SLOTS;
   const size_t qop_b = (size_t)QF8_TERMS * (P.d / 128) * 64 * 32 + (size_t)(P.d / 32) * 64 * 16;
   const size_t ring_b = (size_t)nw * slots * 2 * tq3_region_bytes(P.d);
-  const size_t lds = qop_b + ring_b;  // the epilogue reuses each wave's ring slot
+  // the epilogue reuses each wave's ring slot; with one slot per wave the two
+  // append waves of the fused call get a code block and table each past it
+  const size_t app_b = (app && slots == 1) ? 2 * ((size_t)PAGE * P.d + 256) : 0;
+  const size_t lds = qop_b + ring_b + app_b;
   if (lds > lds_limit()) return hipErrorInvalidValue;
   const bool g6 = pair && P.group <= 6;
   const void* kern = app ? decode_instance<true>(P.d, pair, g6) : decode_instance<false>(P.d, pair, g6);
