@@ -84,6 +84,10 @@ struct DecodeArgs {
   const uint16_t* v_new;
   int32_t* bt_w;    // the same block table and tags, written by the append
   uint8_t* tags_w;
+  // per request: the fresh page's id, or -1 (no fresh page, or the call
+  // failed); then the FP8 free-list top after the call, or -1.  Written by
+  // the scan, published by the merge kernel.
+  int32_t* app_rec;
 };
 
 // Cost of a request's pages: n_old pages wholly outside the Recent window and
@@ -123,9 +127,13 @@ DecodeShape decode_shape(int n_req, int max_pages, int n_kv_heads, int recent) {
 // past the request's end), so the merge needs no count
 __host__ __device__ constexpr int part_stride(int G, int D) { return (G * (D + 2) + 3) / 4 * 4; }
 
+// bytes of the split partials; the fused append's per-request records follow
+static size_t decode_part_bytes(const DecodeShape& s, int n_req, int n_kv_heads, int group, int d) {
+  return (size_t)n_req * n_kv_heads * s.max_chunks * part_stride(group, d) * sizeof(float);
+}
 size_t decode_ws_bytes(int n_req, int max_pages, int n_kv_heads, int group, int d, int recent) {
   DecodeShape s = decode_shape(n_req, max_pages, n_kv_heads, recent);
-  return (size_t)n_req * n_kv_heads * s.max_chunks * part_stride(group, d) * sizeof(float);
+  return decode_part_bytes(s, n_req, n_kv_heads, group, d) + ((size_t)(n_req + 1) * 4 + 15) / 16 * 16;
 }
 
 template <int D>
@@ -298,6 +306,10 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   const int S = !APP ? s_in : (s_in >= 0 && s_in < mp * PAGE ? s_in + 1 : -1);
   if (S < 1 || S > mp * PAGE) {
     if (chunk == 0 && h == 0 && tid == 0) atomicOr(&P.ctrl[CTRL_ERR], (int)MKV_DEVERR_RANGE);
+    if (APP && chunk == 0 && h == 0 && tid == 0) {  // no workgroup holds this request's token
+      a.app_rec[r] = -1;
+      if (r == 0) a.app_rec[a.n_req] = -1;
+    }
     if (tid < G) part[G * D + G + tid] = 0.0f;  // empty partial: the merge writes zeros
     return;
   }
@@ -553,11 +565,11 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   // fresh-page ids as the decode-step append kernel (same validation, ids
   // popped in request order, same arithmetic); it stores K and V of head h
   // for the new token (Alg. 1, Append), then counts itself on an LDS flag; the
-  // appended page's stage is released when both have.  The last of these
-  // waves to arrive on the control-block counter
-  // (each arrives after its reads and stores have returned) records the
-  // fresh pages in the block table, pops them off the free list and resets
-  // the counter.  On any error nothing is written, the error word gets its
+  // appended page's stage is released when both have.  Head 0's K wave
+  // records the request's fresh id (and request 0's the new free-list top)
+  // in the workspace; the merge kernel, which runs after every workgroup of
+  // the scan has read the table, writes them into the block table, tags and
+  // free-list top.  On any error nothing is written, the error word gets its
   // bits, and the workgroup's partial is marked so that the merge writes
   // zeros for the call.
   auto append_token = [&]() {
@@ -595,9 +607,9 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
     for (int o = 32; o > 0; o >>= 1) bad |= __shfl_xor(bad, o, 64);
     if (n_fresh > top) bad |= MKV_DEVERR_FP8_EXHAUSTED;
     bad = __builtin_amdgcn_readfirstlane(bad);
+    const int id = bad ? -1 : __builtin_amdgcn_readfirstlane(
+        fresh ? P.fp8_stack[top - 1 - rank] : a.bt[(int64_t)r * mp + p_new]);
     if (!bad) {
-      const int id = __builtin_amdgcn_readfirstlane(
-          fresh ? P.fp8_stack[top - 1 - rank] : a.bt[(int64_t)r * mp + p_new]);
       // the task's code block and table: the wave's second ring slot, or
       // (one slot per wave) a block of its own past the ring
       const int kv = wid - (NW - 2);
@@ -622,28 +634,11 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
       s_app_bad = 1;
     }
     if (lane == 0) __hip_atomic_fetch_add(&s_app, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
-    if (bad) return;
-    int prev = 0;
-    if (lane == 0) prev = atomicAdd(&P.ctrl[CTRL_APPEND_ARRIVE], 1);
-    prev = __shfl(prev, 0, 64);
-    if (prev != 2 * a.n_req * H - 1) return;
-    // the last arrival: record the fresh pages (ids in request order)
-    int base = 0;
-    for (int b0 = 0; b0 < a.n_req; b0 += 64) {
-      const int rr = b0 + lane;
-      const int64_t ix = rr < a.n_req ? (int64_t)rr * mp + a.seq_lens[rr] / PAGE : 0;
-      const bool fr = rr < a.n_req && a.bt[ix] < 0;
-      const uint64_t fm = __ballot(fr);
-      if (fr) {
-        const int k = base + __popcll(fm & ((1ull << lane) - 1ull));
-        a.bt_w[ix] = P.fp8_stack[top - 1 - k];
-        a.tags_w[ix] = TAG_R;
-      }
-      base += __popcll(fm);
-    }
-    if (lane == 0) {
-      P.ctrl[CTRL_FP8_TOP] = top - n_fresh;
-      P.ctrl[CTRL_APPEND_ARRIVE] = 0;
+    // the record the merge kernel publishes (one writer per request: head 0's
+    // K wave)
+    if (h == 0 && wid == NW - 2 && lane == 0) {
+      a.app_rec[r] = fresh ? id : -1;
+      if (r == 0) a.app_rec[a.n_req] = bad ? -1 : top - n_fresh;
     }
   };
   int jc = min(wid, n_st);  // stage this wave processes next
@@ -966,14 +961,29 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
 // read into a scalar register, so each thread's fold is 32 FMAs per channel.
 // Slots with l_j = 0 contribute nothing; a running (M, L, O) is rescaled once
 // per batch.
+// With the fused append (app_rec non-null) the workgroups of query head 0 and
+// KV head 0 also publish their request's fresh page and, for request 0, the
+// FP8 free-list top, from the records the scan left.
 template <int D>
 __global__ __launch_bounds__(D / 4) void decode_merge_kernel(int G, int H, int max_chunks,
                                                             const float* partials, float* out,
-                                                            float* lse) {
+                                                            float* lse, const int32_t* app_rec,
+                                                            int32_t* bt_w, uint8_t* tags_w,
+                                                            int max_pages, const int32_t* seq_lens,
+                                                            int32_t* ctrl) {
   constexpr int B = 32;
   static_assert(D / 4 >= B && D / 4 <= 64, "one wave; lane j holds slot j's (m, l)");
   const int n = blockIdx.x, h = blockIdx.y, r = blockIdx.z, c4 = threadIdx.x;
   const int Hq = H * G;
+  if (app_rec && n == 0 && h == 0 && c4 == 0) {
+    const int id = app_rec[r];
+    if (id >= 0) {
+      const int64_t ix = (int64_t)r * max_pages + seq_lens[r] / PAGE;
+      bt_w[ix] = id;
+      tags_w[ix] = TAG_R;
+    }
+    if (r == 0 && app_rec[gridDim.z] >= 0) ctrl[CTRL_FP8_TOP] = app_rec[gridDim.z];
+  }
   const int stride = part_stride(G, D);
   const float* base = partials + ((int64_t)r * H + h) * max_chunks * stride;
   float M = -INFINITY, L = 0.0f;
@@ -1067,6 +1077,9 @@ hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t
   a.v_new = v_new;
   a.bt_w = bt_w;
   a.tags_w = tags_w;
+  a.app_rec = app ? reinterpret_cast<int32_t*>(reinterpret_cast<uint8_t*>(ws) +
+                                              decode_part_bytes(sh, n_req, P.n_kv_heads, P.group, P.d))
+                  : nullptr;
   // dynamic LDS: three query operands, then the page ring (reused by the wave merge)
   const bool pair = P.group <= 8;
   const int nw = pair ? DecodeCfg<true>::NW : DecodeCfg<false>::NW;
@@ -1099,9 +1112,11 @@ hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t
   e = ev ? hipExtLaunchKernel(kern, grid, dim3(64 * nw), args, lds, s, ev[0], ev[1], 0)
          : hipLaunchKernel(kern, grid, dim3(64 * nw), args, lds, s);
   if (e != hipSuccess) return e;
-  int G = P.group, H = P.n_kv_heads, mc = sh.max_chunks;
+  int G = P.group, H = P.n_kv_heads, mc = sh.max_chunks, mpg = max_pages;
   const float* pa = a.partials;
-  void* margs[] = {&G, &H, &mc, &pa, &out, &lse};
+  const int32_t* rec = a.app_rec;
+  int32_t* ctrl = P.ctrl;
+  void* margs[] = {&G, &H, &mc, &pa, &out, &lse, &rec, &bt_w, &tags_w, &mpg, &seq_lens, &ctrl};
   const void* mk = P.d == 256 ? (const void*)decode_merge_kernel<256> : (const void*)decode_merge_kernel<128>;
   const dim3 mblock(P.d / 4);
   return ev ? hipExtLaunchKernel(mk, mgrid, mblock, margs, 0, s, ev[2], ev[3], 0)
