@@ -125,26 +125,37 @@ def build_state(w, n_layers, extra_tokens, mk, torch):
     return pool, bt, tags, am, max_pages
 
 
-def cpu_baseline(w, budget_s=25.0):
+def cpu_baseline(w, budget_s=25.0, max_req=4):
     """The CPU oracle, as it stands, on a bounded sample of the same workload:
-    one layer of the long pair (both requests, all heads), state built by the
-    oracle's own append + migrate (not timed); the oracle's decode is timed."""
+    one layer (all heads) of every request, or of max_req of them (the
+    shortest, the longest and two between) when there are more, with the same
+    K/V bytes as the GPU state; the state is built by the oracle's own append
+    + migrate (not timed), the oracle's decode is timed and, for a sample of
+    requests, scaled by total tokens / sampled tokens."""
     import oracle
-    lens = list(w.ctx)
+    lens_all = list(w.ctx)
+    pick = list(range(len(lens_all)))
+    if len(pick) > max_req:
+        order = np.argsort(lens_all, kind="stable")
+        n = len(order)
+        pick = sorted({int(order[0]), int(order[n // 3]), int(order[2 * n // 3]), int(order[-1])})
+    lens = [lens_all[i] for i in pick]
     n_req = len(lens)
-    max_pages = (max(lens) + PAGE - 1) // PAGE
+    max_pages = (max(lens_all) + PAGE - 1) // PAGE
     tot = sum((l + PAGE - 1) // PAGE for l in lens) + 16
     P = oracle.Pool(1, w.n_q_heads, w.n_kv_heads, w.head_dim, tot, tot, w.recent, wl.rot_signs(w),
                     wl.free_order(w, tot, "fp8"), wl.free_order(w, tot, "tq3"))
     bt = np.full((n_req, max_pages), -1, np.int32)
     tags = np.full((n_req, max_pages), 0xFF, np.uint8)
-    ks, vs = zip(*(wl.kv_layer(w, 0, L, token_offset=r * 1_000_000) for r, L in enumerate(lens)))
+    ks, vs = zip(*(wl.kv_layer(w, 0, L, token_offset=i * 1_000_000) for i, L in zip(pick, lens)))
     k = np.concatenate(ks)[None]
     v = np.concatenate(vs)[None]
     assert P.append(-1, bt, tags, np.zeros(n_req, np.int32),
                     np.r_[0, np.cumsum(lens)].astype(np.int32), k, v) == 0
-    P.migrate(bt, tags, wl.anchor_mask(w, max_pages), np.array(lens, np.int32))
-    q = wl.q_decode(w, 0)
+    del ks, vs, k, v
+    P.migrate(bt, tags, np.ascontiguousarray(wl.anchor_mask(w, max_pages)[pick]),
+              np.array(lens, np.int32))
+    q = np.ascontiguousarray(wl.q_decode(w, 0)[pick])
     sl = np.array(lens, np.int32)
     times = []
     t_end = time.perf_counter() + budget_s
@@ -156,9 +167,13 @@ def cpu_baseline(w, budget_s=25.0):
             break
     kvb = sum(kv_bytes_of(tags[r], lens[r], w.head_dim, w.n_kv_heads) for r in range(n_req))
     med = float(np.median(times))
-    return {"value": med * 1e6, "unit": "us/layer", "cores": oracle.num_threads(),
+    scale = sum(lens_all) / sum(lens)
+    what = (f"all {n_req} requests" if n_req == len(lens_all) else
+            f"{n_req} of {len(lens_all)} requests (lengths {lens}), time x {scale:.2f} = total / "
+            f"sampled tokens")
+    return {"value": med * scale * 1e6, "unit": "us/layer", "cores": oracle.num_threads(),
             "kind": "oracle",
-            "sample": f"one layer of {w.name} (2 requests x {lens[0]} tokens, all 24/4 heads), "
+            "sample": f"one layer of {w.name}, {what}, all {w.n_q_heads}/{w.n_kv_heads} heads, "
                       f"fp64 decode over the reconstructed cache, median of {len(times)} runs",
             "kv_gb_per_s": kvb / med / 1e9,
             "cpu": _cpu_model()}
@@ -310,6 +325,7 @@ def main():
     ws = mk.workspace(pool, n_req, max_pages)
     torch.cuda.synchronize()
     setup_s = time.perf_counter() - t_setup
+    print(f"[bench] {w.name}: state built in {setup_s:.1f} s", file=sys.stderr, flush=True)
 
     stream = torch.cuda.current_stream()
     n_ev = args.steps * n_layers
@@ -442,11 +458,14 @@ def main():
         torch.cuda.synchronize()
         res["copy_probe_bytes"] = 1 << 30
         del a_, b_
+    print(f"[bench] decode passes done ({ms_per_step * 1e3 / n_layers:.2f} us/layer)",
+          file=sys.stderr, flush=True)
     if not args.no_chunk:
         del pool
         torch.cuda.empty_cache()
         res["chunk"] = chunk_bench(mk, torch)
-    if not args.no_cpu_baseline and args.cfg == 3:
+    if not args.no_cpu_baseline and args.cfg != 5:
+        print("[bench] timing the CPU oracle", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(w)
     print(json.dumps(res), flush=True)
 
