@@ -30,16 +30,20 @@ enum CtrlSlot {
   CTRL_APPEND_ARRIVE = 5,  // waves of a decode-step append that have finished (reset by the last)
   CTRL_HEADER = 64
 };
+constexpr int MIG_BLOCKS = 256;  // most workgroups of a migration plan
 struct CtrlLayout {
-  int64_t fp8_stack, tq3_stack, list, sigma_bytes, total_words;
+  int64_t fp8_stack, tq3_stack, list, sigma_bytes, mig, total_words;
 };
+// mig: migration-plan scratch, per-workgroup counts [MIG_BLOCKS], per-workgroup
+// error bits [MIG_BLOCKS], the TQ3 free-list top the plan started from
 __host__ __device__ inline CtrlLayout ctrl_layout(int n_fp8, int n_tq3, int d) {
   CtrlLayout c;
   c.fp8_stack = CTRL_HEADER;
   c.tq3_stack = c.fp8_stack + n_fp8;
   c.list = c.tq3_stack + n_tq3;
   c.sigma_bytes = (c.list + 4LL * n_fp8) * 4;  // byte offset of int8 sigma[d]
-  c.total_words = c.list + 4LL * n_fp8 + (d + 3) / 4;
+  c.mig = c.list + 4LL * n_fp8 + (d + 3) / 4;
+  c.total_words = c.mig + 2LL * MIG_BLOCKS + 1;
   return c;
 }
 

@@ -447,117 +447,166 @@ __global__ __launch_bounds__(64) void append_step_kernel(PoolView P, int layer_s
 // Migrate (Retier to TQ3)
 // ===========================================================================
 
-// Plan of a migration, one workgroup.  The table is walked as one run of
+// Plan of a migration, in two launches over nb <= MIG_BLOCKS workgroups; each
+// workgroup owns a range of whole batches of the table taken as one run of
 // (request, page) entries, MIG_KB consecutive entries per thread with every
-// load of a batch in flight together.  Pass 1 validates the whole call
-// (lengths, candidate ids, free-list room) so that a failing call changes
-// nothing; pass 2 ranks the migrating pages in (request, page) order with one
-// block scan per batch, retags Anchors and writes the work list with the TQ3
-// ids popped in that order.  The table entries, Stale tags and FP8 releases
-// are published by the publish kernel after the encode kernel has built the
-// TQ3 pages (Alg. 1, copy before publish).
+// load of a batch in flight together.  The count launch validates its range
+// (lengths, candidate ids) and counts the migrating pages; the list launch
+// sums the counts of the ranges before its own, checks the whole call
+// (errors, free-list room) so that a failing call changes nothing, ranks its
+// migrating pages in (request, page) order with one block scan per batch,
+// retags Anchors and writes the work list with the TQ3 ids popped in that
+// order.  The table entries, Stale tags and FP8 releases are published by the
+// publish kernel after the encode kernel has built the TQ3 pages (Alg. 1,
+// copy before publish).
 constexpr int MIG_KB = 8;
-__global__ __launch_bounds__(1024) void migrate_plan_kernel(int n_req, const int32_t* bt, uint8_t* tags,
-                                                            int max_pages, const uint8_t* anchor,
-                                                            const int32_t* seq_lens, int W,
-                                                            int32_t* ctrl, const int32_t* tq3_stack,
-                                                            int32_t* list, int n_fp8) {
-  __shared__ int scratch[32];
-  __shared__ int s_err, s_cnt;
-  const int tid = threadIdx.x, nt = blockDim.x;
-  if (tid == 0) { s_err = 0; s_cnt = 0; }
-  const int top3 = ctrl[CTRL_TQ3_TOP];
-  int err = 0, cnt = 0;
-  for (int r = tid; r < n_req; r += nt) {
-    const int S = seq_lens[r];
-    if (S < 0 || (S + PAGE - 1) / PAGE > max_pages) err |= MKV_DEVERR_RANGE;
-  }
-  const int64_t N = (int64_t)n_req * max_pages;
-  const int64_t per_batch = (int64_t)nt * MIG_KB;
+constexpr int MIG_NT = 1024;
+constexpr int64_t MIG_BATCH = (int64_t)MIG_NT * MIG_KB;
+struct MigBatch {
   uint8_t tg[MIG_KB], an[MIG_KB];
   int32_t id[MIG_KB], sl[MIG_KB], rq[MIG_KB], pg[MIG_KB];
-  // entries f0 .. f0 + MIG_KB - 1: (request, page) stepped from one division
-  auto load = [&](int64_t f0) {
-    int r = (int)(f0 / max_pages), p = (int)(f0 - (int64_t)r * max_pages);
+};
+// entries f0 .. f0 + MIG_KB - 1: (request, page) stepped from one division
+__device__ __forceinline__ void mig_load(MigBatch& m, int64_t f0, int64_t N, int max_pages,
+                                         const int32_t* bt, const uint8_t* tags,
+                                         const uint8_t* anchor, const int32_t* seq_lens) {
+  int r = (int)(f0 / max_pages), p = (int)(f0 - (int64_t)r * max_pages);
 #pragma unroll
-    for (int j = 0; j < MIG_KB; ++j) {
-      const bool in = f0 + j < N;
-      const int64_t f = in ? f0 + j : 0;
-      rq[j] = in ? r : -1;
-      pg[j] = p;
-      tg[j] = tags[f];
-      an[j] = anchor ? anchor[f] : 0;
-      id[j] = bt[f];
-      sl[j] = seq_lens[in ? r : 0];
-      if (++p == max_pages) { p = 0; ++r; }
+  for (int j = 0; j < MIG_KB; ++j) {
+    const bool in = f0 + j < N;
+    const int64_t f = in ? f0 + j : 0;
+    m.rq[j] = in ? r : -1;
+    m.pg[j] = p;
+    m.tg[j] = tags[f];
+    m.an[j] = anchor ? anchor[f] : 0;
+    m.id[j] = bt[f];
+    m.sl[j] = seq_lens[in ? r : 0];
+    if (++p == max_pages) { p = 0; ++r; }
+  }
+}
+// 1: migrating page, 2: Anchor to retag, 0: neither
+__device__ __forceinline__ int mig_kind(const MigBatch& m, int j, int W) {
+  if (m.rq[j] < 0) return 0;
+  const int p = m.pg[j], S = m.sl[j];
+  if (m.tg[j] != TAG_R || p >= (S + PAGE - 1) / PAGE || (p + 1) * PAGE > S - W) return 0;
+  return m.an[j] ? 2 : 1;
+}
+
+// Count and validate the entries [e0, e1) (the whole workgroup); workgroup 0
+// also checks every request's length.  Returns through s_cnt / s_err.
+__device__ __forceinline__ void mig_count_range(int b, int n_req, const int32_t* bt,
+                                                const uint8_t* tags, int max_pages,
+                                                const uint8_t* anchor, const int32_t* seq_lens,
+                                                int W, int64_t e0, int64_t e1, int n_fp8,
+                                                int* s_cnt, int* s_err) {
+  const int tid = threadIdx.x;
+  int err = 0, cnt = 0;
+  if (b == 0) {
+    for (int r = tid; r < n_req; r += MIG_NT) {
+      const int S = seq_lens[r];
+      if (S < 0 || (S + PAGE - 1) / PAGE > max_pages) err |= MKV_DEVERR_RANGE;
     }
-  };
-  // 1: migrating page, 2: Anchor to retag, 0: neither
-  auto kind = [&](int j) {
-    if (rq[j] < 0) return 0;
-    const int p = pg[j], S = sl[j];
-    if (tg[j] != TAG_R || p >= (S + PAGE - 1) / PAGE || (p + 1) * PAGE > S - W) return 0;
-    return an[j] ? 2 : 1;
-  };
-  __syncthreads();
-  for (int64_t b0 = 0; b0 < N; b0 += per_batch) {
-    const int64_t f0 = b0 + (int64_t)tid * MIG_KB;
-    load(f0);
+  }
+  for (int64_t b0 = e0; b0 < e1; b0 += MIG_BATCH) {
+    MigBatch m;
+    mig_load(m, b0 + (int64_t)tid * MIG_KB, e1, max_pages, bt, tags, anchor, seq_lens);
 #pragma unroll
     for (int j = 0; j < MIG_KB; ++j) {
-      if (kind(j) == 1) {
+      if (mig_kind(m, j, W) == 1) {
         cnt++;
-        if (id[j] < 0 || id[j] >= n_fp8) err |= MKV_DEVERR_RANGE;
+        if (m.id[j] < 0 || m.id[j] >= n_fp8) err |= MKV_DEVERR_RANGE;
       }
     }
   }
-  if (cnt) atomicAdd(&s_cnt, cnt);
-  if (err) atomicOr(&s_err, err);
+  if (cnt) atomicAdd(s_cnt, cnt);
+  if (err) atomicOr(s_err, err);
+}
+
+__global__ __launch_bounds__(MIG_NT) void migrate_count_kernel(
+    int n_req, const int32_t* bt, const uint8_t* tags, int max_pages, const uint8_t* anchor,
+    const int32_t* seq_lens, int W, int32_t* ctrl, int32_t* mig, int64_t per_blk, int n_fp8) {
+  __shared__ int s_err, s_cnt;
+  const int tid = threadIdx.x, b = blockIdx.x;
+  if (tid == 0) { s_err = 0; s_cnt = 0; }
+  if (b == 0 && tid == 0) mig[2 * MIG_BLOCKS] = ctrl[CTRL_TQ3_TOP];  // read before the list launch moves it
+  const int64_t N = (int64_t)n_req * max_pages;
+  const int64_t e0 = (int64_t)b * per_blk, e1 = min(N, e0 + per_blk);
+  __syncthreads();
+  mig_count_range(b, n_req, bt, tags, max_pages, anchor, seq_lens, W, e0, e1, n_fp8, &s_cnt, &s_err);
   __syncthreads();
   if (tid == 0) {
-    if (s_err == 0 && s_cnt > top3) s_err |= MKV_DEVERR_TQ3_EXHAUSTED;
-    if (s_err == 0 && s_cnt > n_fp8) s_err |= MKV_DEVERR_RANGE;
+    mig[b] = s_cnt;
+    mig[MIG_BLOCKS + b] = s_err;
+  }
+}
+
+// ONE: a single workgroup that owns the whole table counts it itself first
+// (one launch instead of two).
+template <bool ONE>
+__global__ __launch_bounds__(MIG_NT) void migrate_list_kernel(
+    int n_req, const int32_t* bt, uint8_t* tags, int max_pages, const uint8_t* anchor,
+    const int32_t* seq_lens, int W, int32_t* ctrl, const int32_t* tq3_stack, int32_t* list,
+    const int32_t* mig, int64_t per_blk, int nb, int n_fp8) {
+  __shared__ int scratch[32];
+  __shared__ int s_err, s_tot, s_pre;
+  const int tid = threadIdx.x, b = blockIdx.x;
+  if (tid == 0) { s_err = 0; s_tot = 0; s_pre = 0; }
+  __syncthreads();
+  const int top3 = ONE ? ctrl[CTRL_TQ3_TOP] : mig[2 * MIG_BLOCKS];
+  if constexpr (ONE) {
+    mig_count_range(0, n_req, bt, tags, max_pages, anchor, seq_lens, W, 0,
+                    (int64_t)n_req * max_pages, n_fp8, &s_tot, &s_err);
+  } else if (tid < nb) {
+    const int c = mig[tid], e = mig[MIG_BLOCKS + tid];
+    if (c) atomicAdd(&s_tot, c);
+    if (c && tid < b) atomicAdd(&s_pre, c);
+    if (e) atomicOr(&s_err, e);
   }
   __syncthreads();
-  if (s_err) {
-    if (tid == 0) {
-      atomicOr(&ctrl[CTRL_ERR], s_err);
+  int err = s_err;
+  const int total = s_tot;
+  if (err == 0 && total > top3) err |= MKV_DEVERR_TQ3_EXHAUSTED;
+  if (err == 0 && total > n_fp8) err |= MKV_DEVERR_RANGE;
+  if (err) {
+    if (b == 0 && tid == 0) {
+      atomicOr(&ctrl[CTRL_ERR], err);
       ctrl[CTRL_ABORT] = 1;
       ctrl[CTRL_NLIST] = 0;
     }
     return;
   }
-  int base = 0;
-  for (int64_t b0 = 0; b0 < N; b0 += per_batch) {
-    const int64_t f0 = b0 + (int64_t)tid * MIG_KB;
-    load(f0);
+  const int64_t N = (int64_t)n_req * max_pages;
+  const int64_t e0 = (int64_t)b * per_blk, e1 = min(N, e0 + per_blk);
+  int base = s_pre;
+  for (int64_t b0 = e0; b0 < e1; b0 += MIG_BATCH) {
+    MigBatch m;
+    mig_load(m, b0 + (int64_t)tid * MIG_KB, e1, max_pages, bt, tags, anchor, seq_lens);
     int k[MIG_KB], c = 0;
 #pragma unroll
     for (int j = 0; j < MIG_KB; ++j) {
-      k[j] = kind(j);
+      k[j] = mig_kind(m, j, W);
       c += k[j] == 1;
     }
     int tot;
     int e = base + block_excl_scan(c, scratch, &tot);
+    const int64_t f0 = b0 + (int64_t)tid * MIG_KB;
 #pragma unroll
     for (int j = 0; j < MIG_KB; ++j) {
-      const int64_t f = f0 + j;
-      if (k[j] == 2) tags[f] = TAG_A;  // Anchor: tag only, stays FP8
+      if (k[j] == 2) tags[f0 + j] = TAG_A;  // Anchor: tag only, stays FP8
       if (k[j] == 1) {
-        const int dst = tq3_stack[top3 - 1 - e];
         int32_t* le = list + 4LL * e;
-        le[0] = rq[j];
-        le[1] = pg[j];
-        le[2] = id[j];
-        le[3] = dst;
+        le[0] = m.rq[j];
+        le[1] = m.pg[j];
+        le[2] = m.id[j];
+        le[3] = tq3_stack[top3 - 1 - e];
         e++;
       }
     }
     base += tot;
   }
-  if (tid == 0) {
-    ctrl[CTRL_TQ3_TOP] = top3 - base;
-    ctrl[CTRL_NLIST] = base;
+  if (b == 0 && tid == 0) {
+    ctrl[CTRL_TQ3_TOP] = top3 - total;
+    ctrl[CTRL_NLIST] = total;
     ctrl[CTRL_ABORT] = 0;
   }
 }
@@ -800,8 +849,24 @@ hipError_t launch_append(const PoolView& P, int layer, int n_req, int32_t* bt, u
 
 hipError_t launch_migrate(const PoolView& P, int n_req, int32_t* bt, uint8_t* tags, int max_pages,
                           const uint8_t* anchor, const int32_t* seq_lens, hipStream_t s) {
-  hipLaunchKernelGGL(migrate_plan_kernel, dim3(1), dim3(1024), 0, s, n_req, bt, tags, max_pages,
-                     anchor, seq_lens, P.recent, P.ctrl, P.tq3_stack, P.list, P.n_fp8);
+  // whole batches per workgroup, at most MIG_BLOCKS workgroups
+  const int64_t n_ent = (int64_t)n_req * max_pages;
+  const int64_t n_bat = (n_ent + MIG_BATCH - 1) / MIG_BATCH;
+  const int64_t bat_per = (n_bat + MIG_BLOCKS - 1) / MIG_BLOCKS;
+  const int nb = (int)((n_bat + bat_per - 1) / bat_per);
+  const int64_t per_blk = bat_per * MIG_BATCH;
+  int32_t* mig = P.ctrl + ctrl_layout(P.n_fp8, P.n_tq3, P.d).mig;
+  if (nb == 1) {
+    hipLaunchKernelGGL(migrate_list_kernel<true>, dim3(1), dim3(MIG_NT), 0, s, n_req, bt, tags,
+                       max_pages, anchor, seq_lens, P.recent, P.ctrl, P.tq3_stack, P.list, mig,
+                       per_blk, nb, P.n_fp8);
+  } else {
+    hipLaunchKernelGGL(migrate_count_kernel, dim3(nb), dim3(MIG_NT), 0, s, n_req, bt, tags,
+                       max_pages, anchor, seq_lens, P.recent, P.ctrl, mig, per_blk, P.n_fp8);
+    hipLaunchKernelGGL(migrate_list_kernel<false>, dim3(nb), dim3(MIG_NT), 0, s, n_req, bt, tags,
+                       max_pages, anchor, seq_lens, P.recent, P.ctrl, P.tq3_stack, P.list, mig,
+                       per_blk, nb, P.n_fp8);
+  }
   int64_t bound = (int64_t)n_req * max_pages;
   if (bound > P.n_fp8) bound = P.n_fp8;
   const int grid = grid_for(bound * P.n_layers * P.n_kv_heads, 4096);
