@@ -558,9 +558,9 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   };
   // Fused decode-step append (APP), run by the two youngest waves of the
   // workgroup that holds the request's new token (K by the older, V by the
-  // younger), after the workgroup barrier and each wave's first copy, while
-  // the other waves stream: every such wave reads the whole call (each
-  // request's length, the free-list top, the table entries and tags of the
+  // younger), after the workgroup barrier, while the other waves stream:
+  // every such wave reads the whole call (each request's length, the
+  // free-list top, the table entries and tags of the
   // pages being appended to) and so reaches the same verdict and the same
   // fresh-page ids as the decode-step append kernel (same validation, ids
   // popped in request order, same arithmetic); it stores K and V of head h
@@ -610,10 +610,10 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
     const int id = bad ? -1 : __builtin_amdgcn_readfirstlane(
         fresh ? P.fp8_stack[top - 1 - rank] : a.bt[(int64_t)r * mp + p_new]);
     if (!bad) {
-      // the task's code block and table: the wave's second ring slot, or
-      // (one slot per wave) a block of its own past the ring
+      // the task's code block and table: the wave's second ring slot (its
+      // first copy is in flight in the first), or its only slot
       const int kv = wid - (NW - 2);
-      uint8_t* own = SLOTS == 2 ? wring + STAGE : ring + NW * SLOTS * STAGE + kv * (PAGE * D + 256);
+      uint8_t* own = SLOTS == 2 ? wring + STAGE : wring;
       SmallTask<D> T;
       T.kv = kv;
       T.r = r;
@@ -653,10 +653,12 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   __syncthreads();  // query operands and the stage list visible to every wave
   const float qinv = s_qinv[ln];  // undoes the query-term scale of this lane's column
   if (APP && holds && wid >= NW - 2) {
-    // an append wave copies its first stage before the append (unless that
-    // stage is the appended page's), so the copy's latency overlaps the task
-    if (jc < n_st - 1) issue(stage_at(jc), 0);
+    // an append wave with two slots copies its first stage before the task
+    // (unless that stage is the appended page's), so the copy's latency
+    // overlaps it; with one slot the task uses the slot first
+    if (SLOTS == 2 && jc < n_st - 1) issue(stage_at(jc), 0);
     append_token();
+    if (SLOTS == 1 && jc < n_st - 1) issue(stage_at(jc), 0);
     if (jc == n_st - 1) issue(stage_at(jc), 0);
   } else if ((wid >= 4 || defer0) && jc < n_st) {
     issue(stage_at(jc), 0);
@@ -1086,10 +1088,7 @@ hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t
   const int slots = pair ? DecodeCfg<true>::SLOTS : DecodeCfg<false>::SLOTS;
   const size_t qop_b = (size_t)QF8_TERMS * (P.d / 128) * 64 * 32 + (size_t)(P.d / 32) * 64 * 16;
   const size_t ring_b = (size_t)nw * slots * 2 * tq3_region_bytes(P.d);
-  // the epilogue reuses each wave's ring slot; with one slot per wave the two
-  // append waves of the fused call get a code block and table each past it
-  const size_t app_b = (app && slots == 1) ? 2 * ((size_t)PAGE * P.d + 256) : 0;
-  const size_t lds = qop_b + ring_b + app_b;
+  const size_t lds = qop_b + ring_b;  // the epilogue reuses each wave's ring slot
   if (lds > lds_limit()) return hipErrorInvalidValue;
   const bool g6 = pair && P.group <= 6;
   const void* kern = app ? decode_instance<true>(P.d, pair, g6) : decode_instance<false>(P.d, pair, g6);
