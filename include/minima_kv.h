@@ -154,8 +154,10 @@ mkv_status kv_migrate_to_tq3(mkv_pool* pool, int32_t n_req, int32_t* block_table
                              int32_t max_pages, const uint8_t* anchor_mask,
                              const int32_t* seq_lens, hipStream_t stream);
 
-/* Workspace bytes for paged_attn_decode (n_q_total = 0) or paged_attn_chunk
- * (n_q_total = total chunk queries) at this batch shape. */
+/* Workspace bytes for paged_attn_decode and paged_attn_decode_append
+ * (n_q_total = 0; the split partials, then n_req + 1 words the fused append
+ * leaves for its merge kernel to publish) or paged_attn_chunk (n_q_total =
+ * total chunk queries) at this batch shape. */
 mkv_status paged_attn_workspace_bytes(const mkv_pool* pool, int32_t n_req, int32_t max_pages,
                                       int32_t n_q_total, size_t* bytes);
 
