@@ -1021,10 +1021,14 @@ __global__ __launch_bounds__(D / 4) void decode_merge_kernel(int G, int H, int m
 #pragma unroll
       for (int j = 0; j < B; ++j) {
         const float w = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, wj), j));
-        O.x = fmaf(w, ok[j].x, O.x);
-        O.y = fmaf(w, ok[j].y, O.y);
-        O.z = fmaf(w, ok[j].z, O.z);
-        O.w = fmaf(w, ok[j].w, O.w);
+        // an empty slot's O rows were never written (they may hold any bits,
+        // NaN included): skip the slot rather than multiply them by 0
+        if (w != 0.0f) {
+          O.x = fmaf(w, ok[j].x, O.x);
+          O.y = fmaf(w, ok[j].y, O.y);
+          O.z = fmaf(w, ok[j].z, O.z);
+          O.w = fmaf(w, ok[j].w, O.w);
+        }
       }
       M = Mb;
     }
@@ -1032,7 +1036,9 @@ __global__ __launch_bounds__(D / 4) void decode_merge_kernel(int G, int H, int m
   const int64_t row = (int64_t)r * Hq + h * G + n;
   if (poisoned) L = 0.0f;
   const float inv = L > 0.0f ? 1.0f / L : 0.0f;
-  reinterpret_cast<float4*>(out + row * D)[c4] = make_float4(O.x * inv, O.y * inv, O.z * inv, O.w * inv);
+  const float4 res = L > 0.0f ? make_float4(O.x * inv, O.y * inv, O.z * inv, O.w * inv)
+                              : make_float4(0.f, 0.f, 0.f, 0.f);
+  reinterpret_cast<float4*>(out + row * D)[c4] = res;
   if (lse && c4 == 0) lse[row] = L > 0.0f ? (M + log2f(L)) * 0.69314718055994531f : -INFINITY;
 }
 

@@ -131,42 +131,32 @@ __device__ __forceinline__ int32_t e4m3_times_512(uint32_t b) {
   return (b & 0x80u) ? -v : v;
 }
 
-// One round-to-nearest-even fp64 -> binary16, saturating at +-65504, done on
-// the integer significand (no intermediate rounding).
+// fp64 -> binary16, round to nearest even, saturating at +-65504 (stored
+// metadata stays finite).  Method: pick the binary16 quantum 2^e of |x| (the
+// spacing of binary16 numbers in |x|'s binade, never below the subnormal
+// quantum 2^-24), scale |x| by 2^-e -- exact, a power of two -- and round that
+// once to an integer m with rint (the default mode is ties-to-even).  m is the
+// binary16 significand; m = 2048 means the rounding carried into the next
+// binade.  One rounding, no intermediate format.
 __device__ inline uint16_t f64_to_f16_rne_sat(double x) {
-  uint64_t bits = (uint64_t)__double_as_longlong(x);
-  uint32_t sign = (uint32_t)((bits >> 48) & 0x8000u);
-  int e = (int)((bits >> 52) & 0x7FF);
-  uint64_t frac = bits & ((1ULL << 52) - 1);
-  if (e == 0x7FF) return (uint16_t)(frac ? (sign | 0x7E00u) : (sign | 0x7BFFu));
-  if (e == 0 && frac == 0) return (uint16_t)sign;
-  uint64_t sig;
-  int E;
-  if (e == 0) { sig = frac; E = -1074; }
-  else { sig = frac | (1ULL << 52); E = e - 1075; }
-  int msb = 63 - __clzll((long long)sig);
-  int q = E + msb - 10;
-  if (q < -24) q = -24;
-  int sh = q - E;
-  uint64_t h;
-  if (sh <= 0) {
-    h = sig << (-sh);
-  } else if (sh >= 64) {
-    h = 0;
-  } else {
-    uint64_t keep = sig >> sh;
-    uint64_t rem = sig & ((1ULL << sh) - 1);
-    uint64_t half = 1ULL << (sh - 1);
-    if (rem > half || (rem == half && (keep & 1))) keep += 1;
-    h = keep;
+  const uint32_t sign = signbit(x) ? 0x8000u : 0u;
+  const double ax = fabs(x);
+  if (isnan(x)) return (uint16_t)(sign | 0x7E00u);
+  if (ax >= 65504.0) return (uint16_t)(sign | 0x7BFFu);  // largest finite binary16
+  if (ax == 0.0) return (uint16_t)sign;
+  int bexp;
+  (void)frexp(ax, &bexp);            // ax in [2^(bexp-1), 2^bexp)
+  const int e = max(bexp - 11, -24);  // quantum: 11 significant bits, subnormals below 2^-14
+  double m = rint(ldexp(ax, -e));     // 0 <= m <= 2048
+  int ee = e;
+  if (m == 2048.0) {  // carried into the next binade
+    m = 1024.0;
+    ee += 1;
   }
-  if (h == 0) return (uint16_t)sign;
-  int hq = q;
-  if (h >= 2048) { h >>= 1; hq += 1; }
-  if (h < 1024) return (uint16_t)(sign | (uint32_t)h);
-  int he = hq + 25;
-  if (he >= 31) return (uint16_t)(sign | 0x7BFFu);
-  return (uint16_t)(sign | ((uint32_t)he << 10) | (uint32_t)(h - 1024));
+  const uint32_t mi = (uint32_t)m;
+  if (mi < 1024u) return (uint16_t)(sign | mi);  // subnormal (ee = -24) or zero
+  const uint32_t biased = (uint32_t)(ee + 25);   // value = mi * 2^ee, mi in [1024, 2048)
+  return (uint16_t)(sign | (biased << 10) | (mi - 1024u));
 }
 __device__ __forceinline__ double f16_bits_to_f64(uint16_t h) {
   _Float16 v = __builtin_bit_cast(_Float16, h);

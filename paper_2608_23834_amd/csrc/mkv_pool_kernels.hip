@@ -611,21 +611,20 @@ __global__ __launch_bounds__(MIG_NT) void migrate_list_kernel(
   }
 }
 
+// TQ3 key code of one rotated coordinate: the codebook level nearest to
+// z = y / sqrt(n2) * (normalised coordinate; levels +-{0.25, 0.75, 1.375,
+// 2.25}), ties to the lower level.  The decision boundaries are 0 and
+// +-{8, 17, 29} / 16, so with u = (16 y)^2 the magnitude class of z is the
+// number of boundaries b with u beyond b^2 n2 -- three exact 64-bit integer
+// comparisons (u < 2^60 and b^2 n2 < 2^54 for |X_j| <= 448 * 2^9, d <= 256).
+// A positive z takes codes 4 + class (strictly beyond a boundary to move up);
+// z <= 0 takes 3 - class (at or beyond a boundary to move down, so a tie and
+// z = 0 stay on the side of the lower code).
 __device__ __forceinline__ int tq3_decide(int32_t y, int64_t n2) {
-  const int64_t a = 16LL * y;
-  const int64_t a2 = a * a;
-  const int tau[7] = {-29, -17, -8, 0, 8, 17, 29};
-  int c = 0;
-#pragma unroll
-  for (int k = 0; k < 7; ++k) {
-    const int64_t t = tau[k];
-    bool above;
-    if (t == 0) above = a > 0;
-    else if (t > 0) above = (a > 0) && (a2 > t * t * n2);
-    else above = (a >= 0) || (a2 < t * t * n2);
-    c += above ? 1 : 0;
-  }
-  return c;
+  const int64_t u = (16LL * y) * (16LL * y);
+  const int64_t b1 = 64LL * n2, b2 = 289LL * n2, b3 = 841LL * n2;
+  if (y > 0) return 4 + (int)(u > b1) + (int)(u > b2) + (int)(u > b3);
+  return 3 - (int)(u >= b1) - (int)(u >= b2) - (int)(u >= b3);
 }
 
 // Encode one FP8 page-head into a TQ3 region per work item (grid-stride over

@@ -107,7 +107,14 @@ class Twin:
             n = self.orc.migrate(self.obt, self.otags, am, sl)
             assert n >= 0
 
-    def decode(self, layer=0, q=None, seq_lens=None):
+    def _ws(self, ws_fill):
+        import paper_2608_23834_amd as mk
+        ws = mk.workspace(self.gpu, self.n_req, self.max_pages)
+        if ws_fill is not None:  # e.g. NaN bits: the calls must not depend on the contents
+            ws.view(_torch().float32)[: ws.numel() // 4].fill_(ws_fill)
+        return ws
+
+    def decode(self, layer=0, q=None, seq_lens=None, ws_fill=None):
         import paper_2608_23834_amd as mk
         torch = _torch()
         w = self.w
@@ -117,7 +124,7 @@ class Twin:
         sl = np.array(self.cur if seq_lens is None else seq_lens, np.int32)
         out = torch.full((self.n_req, w.n_q_heads, w.head_dim), float("nan"), device="cuda")
         lse = torch.full((self.n_req, w.n_q_heads), float("nan"), device="cuda")
-        ws = mk.workspace(self.gpu, self.n_req, self.max_pages)
+        ws = self._ws(ws_fill)
         mk.paged_attn_decode(self.gpu, layer, torch.from_numpy(q.view(np.int16)).cuda(), self.bt,
                              self.tags, torch.from_numpy(sl).cuda(), out, lse, ws)
         torch.cuda.synchronize()
@@ -127,7 +134,7 @@ class Twin:
             res["ref_out"], res["ref_lse"] = o, l
         return res
 
-    def decode_append(self, layer=0, q=None):
+    def decode_append(self, layer=0, q=None, ws_fill=None):
         """One fused decode step on `layer`: append one token per request at
         its current length, then decode over length + 1.  The oracle runs the
         append and the decode as two calls.  Lengths advance with advance()."""
@@ -146,7 +153,7 @@ class Twin:
         sb = np.array(self.cur, np.int32)
         out = torch.full((self.n_req, w.n_q_heads, w.head_dim), float("nan"), device="cuda")
         lse = torch.full((self.n_req, w.n_q_heads), float("nan"), device="cuda")
-        ws = mk.workspace(self.gpu, self.n_req, self.max_pages)
+        ws = self._ws(ws_fill)
         mk.paged_attn_decode_append(
             self.gpu, layer, torch.from_numpy(q.view(np.int16)).cuda(),
             torch.from_numpy(K.view(np.int16)).cuda(), torch.from_numpy(V.view(np.int16)).cuda(),
