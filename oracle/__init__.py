@@ -9,7 +9,8 @@ and shares no code with it.
 Paper passages followed (by section / equation / algorithm):
   * Sec. 2.1, Eq. (kv-per-token): bytes per live token (``kv_bytes_per_token``)
   * Sec. 3.1: tiers R/A/S, FP8 Recent/Anchor, 3-bit rotated Stale codec
-  * Alg. 1: Append and Retier transitions (``Pool.append``, ``Pool.migrate``)
+  * Alg. 1: Append, Retier and Promote transitions (``Pool.append``,
+    ``Pool.migrate``, ``Pool.promote``)
   * Sec. 3.2, Eq. (effective-bits): effective rate (``effective_bits``)
   * Sec. 3.3, Eq. (softmax-merge): partials and merge (``merge``)
   * Sec. 4.1: compact per-format lists, TQ3 page contents, the canary's
@@ -100,6 +101,9 @@ def _declare(L):
     L.orc_append.argtypes = [vp, i32, i32, vp, vp, i32, vp, vp, vp, vp]
     L.orc_migrate.restype = i32
     L.orc_migrate.argtypes = [vp, i32, vp, vp, i32, vp, vp]
+    L.orc_promote.restype = i32
+    L.orc_promote.argtypes = [vp, i32, vp, vp, i32, vp, vp]
+    L.orc_tq3_reconstruct_f32.argtypes = [i32, vp, vp, vp, vp, vp, vp, vp, vp]
     L.orc_partition.argtypes = [i32, vp, vp, i32, vp, vp, vp, vp]
     L.orc_reconstruct.argtypes = [vp, i32, i32, i32, vp, vp, i32, i32, vp, vp]
     L.orc_decode.argtypes = [vp, i32, i32, i32, vp, vp, vp, i32, vp, vp, vp]
@@ -184,6 +188,16 @@ def tq3_dequant(d, enc, sigma):
     lib().orc_tq3_dequant(d, _p(enc["kcode"]), _p(enc["gamma"]), _p(enc["vcode"]),
                           _p(enc["vscale"]), _p(enc["vzero"]), _p(sigma), _p(kh), _p(vh))
     return kh, vh
+
+
+def tq3_reconstruct_f32(d, enc, sigma):
+    """Promote's fp32 reconstruction of one TQ3 page-head: (k32, v32) [16][d]."""
+    sigma = np.ascontiguousarray(sigma, dtype=np.int8)
+    k32 = np.empty((PAGE, d), np.float32)
+    v32 = np.empty((PAGE, d), np.float32)
+    lib().orc_tq3_reconstruct_f32(d, _p(enc["kcode"]), _p(enc["gamma"]), _p(enc["vcode"]),
+                                  _p(enc["vscale"]), _p(enc["vzero"]), _p(sigma), _p(k32), _p(v32))
+    return k32, v32
 
 
 def tq3_pack(d, enc) -> np.ndarray:
@@ -287,6 +301,14 @@ class Pool:
         an = None if anchor is None else np.ascontiguousarray(anchor, dtype=np.uint8)
         return lib().orc_migrate(self._c(), n_req, _p(block_table), _p(tags), max_pages,
                                  None if an is None else _p(an), _p(sl))
+
+    def promote(self, block_table, tags, promote_mask, seq_lens) -> int:
+        """Alg. 1 Promote of every Stale page whose mask entry is set."""
+        n_req, max_pages = block_table.shape
+        sl = np.ascontiguousarray(seq_lens, dtype=np.int32)
+        pm = np.ascontiguousarray(promote_mask, dtype=np.uint8)
+        return lib().orc_promote(self._c(), n_req, _p(block_table), _p(tags), max_pages, _p(pm),
+                                 _p(sl))
 
     def reconstruct(self, layer, r, h, block_table, tags, n_tok):
         n_req, max_pages = block_table.shape

@@ -15,7 +15,7 @@
  *   Sec. 2.1, Eq. (kv-per-token)    bytes per live token
  *   Sec. 3.1                        tiers z in {R, A, S}; Recent/Anchor FP8,
  *                                   Stale 3-bit rotated scalar quantizer
- *   Alg. 1                          Append / Retier / (Promote) transitions
+ *   Alg. 1                          Append / Retier / Promote transitions
  *   Sec. 3.3, Eq. (softmax-merge)   mixed-format partials and their merge
  *   Sec. 4.1                        compact per-format page lists, TQ3 page
  *                                   contents (rotated K codes, FP16 key-norm
@@ -680,6 +680,109 @@ int orc_migrate(orc_pool* P, int n_req, int32_t* bt, uint8_t* tags, int max_page
   }
   free(mig);
   return n_mig;
+}
+
+/* Reconstruction used by Promote, in fp32 with every step fixed:
+ *   k_hat_i = gamma * sigma_i * h_i / sqrt(d),  h = H_d mu_c   (Alg. 1 Promote
+ *   "reconstruct"; the same k_hat = gamma R^T mu_c as orc_tq3_dequant),
+ *   v_hat_c = zero_c + scale_c * code.
+ * h_i is a multiple of 1/8 with |h_i| <= 2.25 d, so gamma * sigma_i * h_i is
+ * exact in fp64; the division by the correctly rounded sqrt(d) is one fp64
+ * rounding (none at d = 256) and the result is rounded once to fp32.  The
+ * value is exact in fp64 (two binary16 numbers and a 3-bit integer) and
+ * rounded once to fp32.  Out: k32, v32 [16][d] logical order. */
+void orc_tq3_reconstruct_f32(int d, const uint8_t* kcode, const uint16_t* gamma,
+                             const uint8_t* vcode, const uint16_t* vscale, const uint16_t* vzero,
+                             const int8_t* sigma, float* k32, float* v32) {
+  double* h = (double*)malloc(sizeof(double) * d);
+  double rd = sqrt((double)d);
+  for (int t = 0; t < ORC_PAGE; ++t) {
+    double g = orc_f16_to_f64(gamma[t]);
+    for (int j = 0; j < d; ++j) h[j] = MU[kcode[t * d + j]];
+    hadamard_f64(h, d);
+    for (int i = 0; i < d; ++i) {
+      double a = g * (double)sigma[i] * h[i];
+      k32[t * d + i] = (float)(a / rd);
+    }
+    for (int c = 0; c < d; ++c) {
+      double v = orc_f16_to_f64(vzero[c]) + orc_f16_to_f64(vscale[c]) * (double)vcode[t * d + c];
+      v32[t * d + c] = (float)v;
+    }
+  }
+  free(h);
+}
+
+/* Promote(p), Alg. 1: a Stale page that re-enters the protected budget
+ * (Sec. 3.1 Anchor paragraph) is reconstructed (orc_tq3_reconstruct_f32) and
+ * quantized into a newly allocated FP8 page with the FP8 rule of a fresh
+ * page (per page-head and K/V: s = amax / 448, code = E4M3(x / s)), for every
+ * layer and KV head; then (tag Anchor, new FP8 id) is published and the TQ3
+ * page is released to its free list.  Pages promoted: tag Stale, promote
+ * mask set, logical page below ceil(seq_len / 16); other pages are left
+ * alone.  FP8 ids are taken and TQ3 ids released in ascending (request,
+ * logical page) order.  Returns the number of promoted pages, or -1 when the
+ * FP8 free list is too short (nothing changed). */
+int orc_promote(orc_pool* P, int n_req, int32_t* bt, uint8_t* tags, int max_pages,
+                const uint8_t* promote, const int32_t* seq_lens) {
+  int d = P->d, H = P->n_kv_heads;
+  int n_pro = 0;
+  for (int r = 0; r < n_req; ++r) {
+    int np = (seq_lens[r] + ORC_PAGE - 1) / ORC_PAGE;
+    for (int p = 0; p < np && p < max_pages; ++p) {
+      int64_t i = (int64_t)r * max_pages + p;
+      if (tags[i] == TAG_S && promote[i]) n_pro++;
+    }
+  }
+  if (n_pro > *P->fp8_top) return -1;
+  int32_t* pro = (int32_t*)malloc(sizeof(int32_t) * 4 * (n_pro + 1));
+  int k = 0;
+  for (int r = 0; r < n_req; ++r) {
+    int np = (seq_lens[r] + ORC_PAGE - 1) / ORC_PAGE;
+    for (int p = 0; p < np && p < max_pages; ++p) {
+      int64_t i = (int64_t)r * max_pages + p;
+      if (!(tags[i] == TAG_S && promote[i])) continue;
+      *P->fp8_top -= 1;
+      pro[4 * k] = r;
+      pro[4 * k + 1] = p;
+      pro[4 * k + 2] = bt[i];
+      pro[4 * k + 3] = P->fp8_stack[*P->fp8_top];
+      k++;
+    }
+  }
+  int64_t total = (int64_t)n_pro * P->n_layers * H;
+#pragma omp parallel
+  {
+    uint8_t* kc = (uint8_t*)malloc((size_t)ORC_PAGE * d);
+    uint8_t* vc = (uint8_t*)malloc((size_t)ORC_PAGE * d);
+    uint16_t g[ORC_PAGE];
+    uint16_t* vs = (uint16_t*)malloc(2 * (size_t)d);
+    uint16_t* vz = (uint16_t*)malloc(2 * (size_t)d);
+    float* k32 = (float*)malloc(sizeof(float) * ORC_PAGE * d);
+    float* v32 = (float*)malloc(sizeof(float) * ORC_PAGE * d);
+#pragma omp for schedule(dynamic, 16)
+    for (int64_t w = 0; w < total; ++w) {
+      int h = (int)(w % H);
+      int l = (int)((w / H) % P->n_layers);
+      int e = (int)(w / H / P->n_layers);
+      int src = pro[4 * e + 2], dst = pro[4 * e + 3];
+      orc_tq3_unpack(d, tq3_region(P, l, src, h), kc, g, vc, vs, vz);
+      orc_tq3_reconstruct_f32(d, kc, g, vc, vs, vz, P->sigma, k32, v32);
+      uint8_t* reg = fp8_region(P, l, dst, h);
+      float* sc = fp8_scales(P, l, dst, h);
+      fp8_append_tensor(d, reg, 0, sc, 0, ORC_PAGE, k32);
+      fp8_append_tensor(d, reg + (int64_t)ORC_PAGE * d, 1, sc + 1, 0, ORC_PAGE, v32);
+    }
+    free(kc); free(vc); free(vs); free(vz); free(k32); free(v32);
+  }
+  for (int j = 0; j < n_pro; ++j) {
+    int64_t i = (int64_t)pro[4 * j] * max_pages + pro[4 * j + 1];
+    bt[i] = pro[4 * j + 3];
+    tags[i] = TAG_A;
+    P->tq3_stack[*P->tq3_top] = pro[4 * j + 2];
+    *P->tq3_top += 1;
+  }
+  free(pro);
+  return n_pro;
 }
 
 /* Compact per-format page lists (Sec. 4.1): stable partition of the logical
