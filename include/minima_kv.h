@@ -210,6 +210,24 @@ mkv_status paged_attn_decode_append(mkv_pool* pool, int32_t layer, int32_t n_req
                                     float* out, float* lse, void* ws, size_t ws_bytes,
                                     hipStream_t stream);
 
+/* paged_attn_decode for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same attention, with the split partials held in a fixed
+ * device array of the library (MKV_DECODE_SCRATCH_BYTES per device, resolved
+ * when a pool is created on that device or at the first call there) instead
+ * of a caller workspace.  The call allocates nothing.  Returns MKV_ENOMEM
+ * when the partials of this shape, paged_attn_workspace_bytes(pool, n_req,
+ * max_pages, 0), exceed MKV_DECODE_SCRATCH_BYTES; other arguments and errors
+ * as paged_attn_decode.  Every call on a device shares that device's array:
+ * calls that overlap in time on one device (different streams, or processes
+ * sharing nothing else) race on it and must be serialized by the caller. */
+#define MKV_DECODE_SCRATCH_BYTES (32u * 1024u * 1024u)
+mkv_status paged_attn_decode_noalloc(mkv_pool* pool, int32_t layer, int32_t n_req,
+                                     const uint16_t* q, const int32_t* block_table,
+                                     const uint8_t* tags, int32_t max_pages,
+                                     const int32_t* seq_lens, float* out, float* lse,
+                                     hipStream_t stream);
+
 /* Causal chunked-prefill attention over the same mixed pages.  Request r has
  * n_r = cu_q[r+1]-cu_q[r] queries; query i sits at position
  * seq_lens[r] - n_r + i and attends to keys t <= that position (the chunk's

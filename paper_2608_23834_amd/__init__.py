@@ -28,7 +28,7 @@ EXPORTS = ["kv_pool_bytes", "kv_pool_create", "kv_pool_destroy", "kv_append_fp8"
            "kv_partition_pages", "kv_pool_free_counts",
            "kv_pool_read_free_lists", "kv_pool_counters", "kv_pool_check_errors",
            "paged_attn_set_timing", "paged_attn_last_times", "mkv_stream_read",
-           "mkv_status_string"]
+           "paged_attn_decode_noalloc", "mkv_status_string"]
 
 _lib = None
 
@@ -78,6 +78,7 @@ def lib() -> ctypes.CDLL:
         L.paged_attn_workspace_bytes.argtypes = [vp, i32, i32, i32, vp]
         L.paged_attn_workspace_init.argtypes = [vp, sz, vp]
         L.paged_attn_decode.argtypes = [vp, i32, i32, vp, vp, vp, i32, vp, vp, vp, vp, sz, vp]
+        L.paged_attn_decode_noalloc.argtypes = [vp, i32, i32, vp, vp, vp, i32, vp, vp, vp, vp]
         L.paged_attn_decode_append.argtypes = [vp, i32, i32, vp, vp, vp, vp, vp, i32, vp, vp, vp,
                                                vp, sz, vp]
         L.paged_attn_chunk.argtypes = [vp, i32, i32, vp, vp, i32, vp, vp, i32, vp, vp, vp, sz, vp]
@@ -213,6 +214,19 @@ def paged_attn_decode(pool: Pool, layer, q, block_table, tags, seq_lens, out, ls
         pool.handle, layer, n_req, _ptr(q), _ptr(block_table), _ptr(tags), max_pages,
         _ptr(seq_lens), _ptr(out), _ptr(lse), _ptr(ws), ws.numel() * ws.element_size(),
         _stream(stream)))
+
+
+DECODE_SCRATCH_BYTES = 32 * 1024 * 1024
+
+
+def paged_attn_decode_noalloc(pool: Pool, layer, q, block_table, tags, seq_lens, out, lse,
+                              stream=None):
+    """paged_attn_decode with the split partials in the library's fixed device
+    scratch (no workspace argument; the call allocates nothing)."""
+    n_req, max_pages = block_table.shape
+    _check("paged_attn_decode_noalloc", lib().paged_attn_decode_noalloc(
+        pool.handle, layer, n_req, _ptr(q), _ptr(block_table), _ptr(tags), max_pages,
+        _ptr(seq_lens), _ptr(out), _ptr(lse), _stream(stream)))
 
 
 def paged_attn_decode_append(pool: Pool, layer, q, k_new, v_new, block_table, tags,

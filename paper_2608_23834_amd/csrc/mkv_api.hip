@@ -132,6 +132,10 @@ mkv_status kv_pool_create(const mkv_pool_desc* desc, mkv_pool** out) {
   std::memcpy(reinterpret_cast<uint8_t*>(img.data()) + p->cl.sigma_bytes, desc->rot_signs,
               (size_t)p->d);
   hipError_t e = hipMemcpy(p->ctrl, img.data(), img.size() * 4, hipMemcpyHostToDevice);
+  int dev = -1;
+  if (e == hipSuccess) e = hipGetDevice(&dev);
+  // set-up of the allocation-free decode: the device address of its scratch
+  if (e == hipSuccess) e = decode_scratch_init(dev);
   if (e != hipSuccess) {
     delete p;
     return MKV_EHIP;
@@ -194,6 +198,32 @@ mkv_status paged_attn_decode(mkv_pool* pool, int32_t layer, int32_t n_req, const
   if (n_req > 65535 || max_pages > 1024 * 256) return MKV_ERANGE;
   if (ws_bytes < decode_ws_bytes(n_req, max_pages, pool->n_kv_heads, pool->group, pool->d, pool->recent))
     return MKV_ENOMEM;
+  mkv_status st = hip_status(launch_decode(view_of(pool), layer, n_req, q, block_table, tags,
+                                           max_pages, seq_lens, out, lse, ws, stream,
+                                           pool->timing ? pool->timing_ev : nullptr));
+  if (st == MKV_OK) {
+    pool->decode_routes++;
+    if (pool->timing) pool->timed = 1;
+  }
+  return st;
+}
+
+mkv_status paged_attn_decode_noalloc(mkv_pool* pool, int32_t layer, int32_t n_req,
+                                     const uint16_t* q, const int32_t* block_table,
+                                     const uint8_t* tags, int32_t max_pages,
+                                     const int32_t* seq_lens, float* out, float* lse,
+                                     hipStream_t stream) {
+  if (!pool || !q || !block_table || !tags || !seq_lens || !out) return MKV_EINVAL;
+  if (n_req < 1 || max_pages < 1) return MKV_EINVAL;
+  if (!aligned16(q) || !aligned16(out)) return MKV_EINVAL;
+  if (layer < 0 || layer >= pool->n_layers) return MKV_ERANGE;
+  if (n_req > 65535 || max_pages > 1024 * 256) return MKV_ERANGE;
+  if (decode_ws_bytes(n_req, max_pages, pool->n_kv_heads, pool->group, pool->d, pool->recent) >
+      (size_t)MKV_DECODE_SCRATCH_BYTES)
+    return MKV_ENOMEM;
+  int dev = -1;
+  void* ws = nullptr;
+  if (hipGetDevice(&dev) != hipSuccess || decode_scratch(dev, &ws) != hipSuccess) return MKV_EHIP;
   mkv_status st = hip_status(launch_decode(view_of(pool), layer, n_req, q, block_table, tags,
                                            max_pages, seq_lens, out, lse, ws, stream,
                                            pool->timing ? pool->timing_ev : nullptr));

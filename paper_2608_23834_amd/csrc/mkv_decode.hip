@@ -31,6 +31,7 @@
 #include <hip/hip_runtime.h>
 
 #include <atomic>
+#include <mutex>
 #include <type_traits>
 
 #include "mkv_append.h"
@@ -1040,6 +1041,50 @@ __global__ __launch_bounds__(D / 4) void decode_merge_kernel(int G, int H, int m
                               : make_float4(0.f, 0.f, 0.f, 0.f);
   reinterpret_cast<float4*>(out + row * D)[c4] = res;
   if (lse && c4 == 0) lse[row] = L > 0.0f ? (M + log2f(L)) * 0.69314718055994531f : -INFINITY;
+}
+
+// Device scratch for callers that cannot allocate (paged_attn_decode_noalloc):
+// the split partials live in this fixed array instead of a caller workspace.
+// Each device holds its own copy for the life of the process; host code
+// never passes the array's name to a kernel (on the host it only names the
+// symbol), it uses the device address resolved per device below.
+static __device__ __align__(256) uint8_t scratch[MKV_DECODE_SCRATCH_BYTES];
+
+namespace {
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[64];  // per device: the address of `scratch` on it
+}  // namespace
+
+hipError_t decode_scratch_init(int dev) {
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (g_scratch_ptr[dev]) return hipSuccess;
+  int cur = -1;
+  hipError_t e = hipGetDevice(&cur);
+  if (e != hipSuccess) return e;
+  if (cur != dev) return hipErrorInvalidDevice;  // resolved only with the device current
+  void* ptr = nullptr;
+  e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+  if (e != hipSuccess) return e;
+  if (!ptr) return hipErrorInvalidSymbol;
+  g_scratch_ptr[dev] = ptr;
+  return hipSuccess;
+}
+
+hipError_t decode_scratch(int dev, void** ptr) {
+  if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+  {
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (g_scratch_ptr[dev]) {
+      *ptr = g_scratch_ptr[dev];
+      return hipSuccess;
+    }
+  }
+  hipError_t e = decode_scratch_init(dev);  // first call on a device the pool was not created on
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
 }
 
 // dynamic LDS a decode workgroup may use: 160 KiB per CU minus the static arrays

@@ -70,6 +70,10 @@ struct DecodeShape {
 };
 DecodeShape decode_shape(int n_req, int max_pages, int n_kv_heads, int recent);
 size_t decode_ws_bytes(int n_req, int max_pages, int n_kv_heads, int group, int d, int recent);
+// the fixed device scratch of paged_attn_decode_noalloc: resolve its address on
+// device dev (dev must be current; once per device), and look it up
+hipError_t decode_scratch_init(int dev);
+hipError_t decode_scratch(int dev, void** ptr);
 hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t* q,
                          const int32_t* bt, const uint8_t* tags, int max_pages,
                          const int32_t* seq_lens, float* out, float* lse, void* ws,
