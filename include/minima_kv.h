@@ -154,6 +154,24 @@ mkv_status kv_migrate_to_tq3(mkv_pool* pool, int32_t n_req, int32_t* block_table
                              int32_t max_pages, const uint8_t* anchor_mask,
                              const int32_t* seq_lens, hipStream_t stream);
 
+/* Promote(p) of Alg. 1: a Stale page that re-enters the protected budget is
+ * materialized back into FP8 (Sec. 3.1 Anchor paragraph).  Every page of
+ * request r with tag Stale, promote_mask[r][p] != 0 and p < ceil(seq_lens[r]
+ * / 16) is reconstructed for all layers and KV heads -- keys k_c =
+ * fp32(gamma * sigma_c * (H mu_code)_c / sqrt(d)), values v_c = fp32(zero_c +
+ * scale_c * code), the reconstruction the decode attends to -- and quantized
+ * into a newly allocated FP8 page with the rule of a fresh page (s = amax /
+ * 448 per page-head and K/V, code = E4M3(x / s)); only then is (tag Anchor,
+ * new id) published and the TQ3 page released to its free list (Alg. 1
+ * copy-before-publish).  FP8 ids are taken and TQ3 ids released in ascending
+ * (request, page) order.  Other pages are left alone.  promote_mask: device
+ * uint8 [n_req][max_pages]; seq_lens: device int32 [n_req].  If the FP8 free
+ * list is too short, a length is out of range or a Stale page's id is out of
+ * range, nothing changes and the error word is set. */
+mkv_status kv_promote_to_fp8(mkv_pool* pool, int32_t n_req, int32_t* block_table, uint8_t* tags,
+                             int32_t max_pages, const uint8_t* promote_mask,
+                             const int32_t* seq_lens, hipStream_t stream);
+
 /* Workspace bytes for paged_attn_decode and paged_attn_decode_append
  * (n_q_total = 0; the split partials, then n_req + 1 words the fused append
  * leaves for its merge kernel to publish) or paged_attn_chunk (n_q_total =

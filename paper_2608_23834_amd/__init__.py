@@ -23,7 +23,7 @@ STATUS = {0: "MKV_OK", 1: "MKV_EINVAL", 2: "MKV_EUNSUP", 3: "MKV_ENOMEM", 4: "MK
 DEVERR = {"FP8_EXHAUSTED": 0x1, "TQ3_EXHAUSTED": 0x2, "NOT_RECENT": 0x4, "RANGE": 0x8,
           "BAD_TAG": 0x10}
 EXPORTS = ["kv_pool_bytes", "kv_pool_create", "kv_pool_destroy", "kv_append_fp8",
-           "kv_migrate_to_tq3", "paged_attn_workspace_bytes", "paged_attn_workspace_init",
+           "kv_migrate_to_tq3", "kv_promote_to_fp8", "paged_attn_workspace_bytes", "paged_attn_workspace_init",
            "paged_attn_decode", "paged_attn_decode_append", "paged_attn_chunk",
            "kv_partition_pages", "kv_pool_free_counts",
            "kv_pool_read_free_lists", "kv_pool_counters", "kv_pool_check_errors",
@@ -75,6 +75,7 @@ def lib() -> ctypes.CDLL:
         L.kv_pool_destroy.argtypes = [vp]
         L.kv_append_fp8.argtypes = [vp, i32, i32, vp, vp, i32, vp, vp, i32, vp, vp, vp]
         L.kv_migrate_to_tq3.argtypes = [vp, i32, vp, vp, i32, vp, vp, vp]
+        L.kv_promote_to_fp8.argtypes = [vp, i32, vp, vp, i32, vp, vp, vp]
         L.paged_attn_workspace_bytes.argtypes = [vp, i32, i32, i32, vp]
         L.paged_attn_workspace_init.argtypes = [vp, sz, vp]
         L.paged_attn_decode.argtypes = [vp, i32, i32, vp, vp, vp, i32, vp, vp, vp, vp, sz, vp]
@@ -186,6 +187,13 @@ def kv_migrate_to_tq3(pool: Pool, block_table, tags, anchor_mask, seq_lens, stre
     n_req, max_pages = block_table.shape
     _check("kv_migrate_to_tq3", lib().kv_migrate_to_tq3(
         pool.handle, n_req, _ptr(block_table), _ptr(tags), max_pages, _ptr(anchor_mask),
+        _ptr(seq_lens), _stream(stream)))
+
+
+def kv_promote_to_fp8(pool: Pool, block_table, tags, promote_mask, seq_lens, stream=None):
+    n_req, max_pages = block_table.shape
+    _check("kv_promote_to_fp8", lib().kv_promote_to_fp8(
+        pool.handle, n_req, _ptr(block_table), _ptr(tags), max_pages, _ptr(promote_mask),
         _ptr(seq_lens), _stream(stream)))
 
 

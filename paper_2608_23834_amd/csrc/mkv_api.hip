@@ -172,6 +172,15 @@ mkv_status kv_migrate_to_tq3(mkv_pool* pool, int32_t n_req, int32_t* block_table
                                    seq_lens, stream));
 }
 
+mkv_status kv_promote_to_fp8(mkv_pool* pool, int32_t n_req, int32_t* block_table, uint8_t* tags,
+                             int32_t max_pages, const uint8_t* promote_mask,
+                             const int32_t* seq_lens, hipStream_t stream) {
+  if (!pool || !block_table || !tags || !promote_mask || !seq_lens) return MKV_EINVAL;
+  if (n_req < 1 || max_pages < 1) return MKV_EINVAL;
+  return hip_status(launch_promote(view_of(pool), n_req, block_table, tags, max_pages, promote_mask,
+                                   seq_lens, stream));
+}
+
 mkv_status paged_attn_workspace_bytes(const mkv_pool* pool, int32_t n_req, int32_t max_pages,
                                       int32_t n_q_total, size_t* bytes) {
   if (!pool || !bytes || n_req < 1 || max_pages < 1 || n_q_total < 0) return MKV_EINVAL;

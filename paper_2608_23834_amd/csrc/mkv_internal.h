@@ -59,6 +59,8 @@ hipError_t launch_append(const PoolView& P, int layer, int n_req, int32_t* bt, u
                          int n_new_total, const uint16_t* k, const uint16_t* v, hipStream_t s);
 hipError_t launch_migrate(const PoolView& P, int n_req, int32_t* bt, uint8_t* tags, int max_pages,
                           const uint8_t* anchor, const int32_t* seq_lens, hipStream_t s);
+hipError_t launch_promote(const PoolView& P, int n_req, int32_t* bt, uint8_t* tags, int max_pages,
+                          const uint8_t* mask, const int32_t* seq_lens, hipStream_t s);
 hipError_t launch_partition(int n_req, const int32_t* bt, const uint8_t* tags, int max_pages,
                             const int32_t* seq_lens, int32_t* list8, int32_t* list3,
                             int32_t* counts, int32_t* err, hipStream_t s);

@@ -1,6 +1,7 @@
 // Pool-state kernels: FP8 append (Alg. 1 Append; Sec. 3.1 Recent tier), FP8 ->
-// TQ3 migration (Alg. 1 Retier; Sec. 4.3 normalize-rotate-pack), the compact
-// per-format page lists (Sec. 4.1) and a zero-fill helper.
+// TQ3 migration (Alg. 1 Retier; Sec. 4.3 normalize-rotate-pack), TQ3 -> FP8
+// promotion (Alg. 1 Promote), the compact per-format page lists (Sec. 4.1)
+// and a zero-fill helper.
 //
 // Every result that the CPU oracle fixes bit for bit (page ids, tags, free
 // lists, FP8 codes and scales, TQ3 codes, gamma, V scale/zero) is produced by
@@ -757,6 +758,227 @@ __global__ __launch_bounds__(1024) void migrate_publish_kernel(int32_t* bt, uint
 }
 
 // ===========================================================================
+// Promote (a Stale page back to FP8)
+// ===========================================================================
+
+// Plan of a promotion: one workgroup walks the table twice (count and
+// validate, then list in (request, page) order with one block scan per batch).
+// A page is promoted when it is Stale, its mask entry is set and it lies below
+// the request's length.  A failing call (bad length, out-of-range TQ3 id, FP8
+// free list too short) sets the error word and the abort flag and lists
+// nothing.  The FP8 ids are popped here; the pages are built by the build
+// kernel and published after it (copy before publish).
+__device__ __forceinline__ bool pro_hit(const MigBatch& m, int j) {
+  if (m.rq[j] < 0 || m.tg[j] != TAG_S || !m.an[j]) return false;
+  return m.pg[j] < (m.sl[j] + PAGE - 1) / PAGE;
+}
+
+__global__ __launch_bounds__(MIG_NT) void promote_plan_kernel(
+    int n_req, const int32_t* bt, const uint8_t* tags, int max_pages, const uint8_t* mask,
+    const int32_t* seq_lens, int32_t* ctrl, const int32_t* fp8_stack, int32_t* list, int n_tq3) {
+  __shared__ int scratch[32];
+  __shared__ int s_err, s_tot;
+  const int tid = threadIdx.x;
+  if (tid == 0) { s_err = 0; s_tot = 0; }
+  __syncthreads();
+  const int64_t N = (int64_t)n_req * max_pages;
+  int err = 0, cnt = 0;
+  for (int r = tid; r < n_req; r += MIG_NT) {
+    const int S = seq_lens[r];
+    if (S < 0 || (S + PAGE - 1) / PAGE > max_pages) err |= MKV_DEVERR_RANGE;
+  }
+  for (int64_t b0 = 0; b0 < N; b0 += MIG_BATCH) {
+    MigBatch m;
+    mig_load(m, b0 + (int64_t)tid * MIG_KB, N, max_pages, bt, tags, mask, seq_lens);
+#pragma unroll
+    for (int j = 0; j < MIG_KB; ++j) {
+      if (pro_hit(m, j)) {
+        cnt++;
+        if (m.id[j] < 0 || m.id[j] >= n_tq3) err |= MKV_DEVERR_RANGE;
+      }
+    }
+  }
+  if (cnt) atomicAdd(&s_tot, cnt);
+  if (err) atomicOr(&s_err, err);
+  __syncthreads();
+  const int total = s_tot;
+  const int top8 = ctrl[CTRL_FP8_TOP];
+  err = s_err;
+  if (err == 0 && total > top8) err |= MKV_DEVERR_FP8_EXHAUSTED;
+  if (err) {
+    if (tid == 0) {
+      atomicOr(&ctrl[CTRL_ERR], err);
+      ctrl[CTRL_ABORT] = 1;
+      ctrl[CTRL_NLIST] = 0;
+    }
+    return;
+  }
+  int base = 0;
+  for (int64_t b0 = 0; b0 < N; b0 += MIG_BATCH) {
+    MigBatch m;
+    const int64_t f0 = b0 + (int64_t)tid * MIG_KB;
+    mig_load(m, f0, N, max_pages, bt, tags, mask, seq_lens);
+    bool hit[MIG_KB];
+    int c = 0;
+#pragma unroll
+    for (int j = 0; j < MIG_KB; ++j) {
+      hit[j] = pro_hit(m, j);
+      c += hit[j];
+    }
+    int tot;
+    int e = base + block_excl_scan(c, scratch, &tot);
+#pragma unroll
+    for (int j = 0; j < MIG_KB; ++j) {
+      if (hit[j]) {
+        int32_t* le = list + 4LL * e;
+        le[0] = m.rq[j];
+        le[1] = m.pg[j];
+        le[2] = m.id[j];                   // TQ3 source
+        le[3] = fp8_stack[top8 - 1 - e];   // FP8 destination
+        e++;
+      }
+    }
+    base += tot;
+  }
+  if (tid == 0) {
+    ctrl[CTRL_FP8_TOP] = top8 - total;
+    ctrl[CTRL_NLIST] = total;
+    ctrl[CTRL_ABORT] = 0;
+  }
+}
+
+// Rebuild one listed page-head (layer, KV head) from its TQ3 region into its
+// new FP8 region; 256 threads, thread (t, l) = (tid / 16, tid % 16) owns token
+// t and channels l + 16 j.
+//  keys: codes -> 8 * codebook level (integers), the Walsh-Hadamard transform
+//        of each token row in int32 (exact), then
+//        k = fp32((gamma * sigma_c * (y_c / 8)) / sqrt(D)) -- the products are
+//        exact in fp64, the division the only fp64 rounding;
+//  values: v = fp32(zero_c + scale_c * code), exact in fp64 before the
+//        conversion;
+//  FP8: per K and per V, s = amax / 448 over the 16 x D values, code =
+//        E4M3(x / s) (0 when s = 0), the page written in the FP8 layout.
+template <int D>
+__global__ __launch_bounds__(256) void promote_build_kernel(PoolView P) {
+  if (P.ctrl[CTRL_ABORT]) return;
+  constexpr int NDW = 3 * D / 128, CB = 3 * D / 32, CL = D / 16, NJ = D / 16;
+  constexpr int R3W = (int)tq3_region_bytes(D) / 4;
+  constexpr int R8W = (int)fp8_region_bytes(D) / 4;
+  __shared__ uint32_t src[R3W];
+  __shared__ int32_t y[PAGE * D];
+  __shared__ uint32_t dst[R8W];
+  __shared__ float s_red[2][4];
+  const int H = P.n_kv_heads, L = P.n_layers;
+  const int64_t n_items = (int64_t)P.ctrl[CTRL_NLIST] * L * H;
+  const int tid = threadIdx.x, t = tid >> 4, l16 = tid & 15, lane = tid & 63, wv = tid >> 6;
+  // 8 * codebook level of each 3-bit code (levels +-0.25, 0.75, 1.375, 2.25)
+  const int lvl8[8] = {-18, -11, -6, -2, 2, 6, 11, 18};
+  for (int64_t item = blockIdx.x; item < n_items; item += gridDim.x) {
+    const int e = (int)(item / (L * H));
+    const int lh = (int)(item % (L * H));
+    const int layer = lh / H, h = lh % H;
+    const int sid = P.list[4 * e + 2], did = P.list[4 * e + 3];
+    const uint32_t* reg3 = reinterpret_cast<const uint32_t*>(
+        P.tq3 + (((int64_t)layer * P.n_tq3 + sid) * H + h) * tq3_region_bytes(D));
+    for (int w = tid; w < R3W; w += 256) src[w] = reg3[w];
+    __syncthreads();
+    const uint8_t* sb = reinterpret_cast<const uint8_t*>(src);
+    // key codes of token t, channels l16 + 16 j: chunk (t, g), quad q, byte b
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int c = l16 + 16 * j;
+      const int g = c / (D / 4), cc = c % (D / 4);
+      const uint32_t* ch = reinterpret_cast<const uint32_t*>(sb + (g * 16 + t) * CB);
+      uint32_t dw[NDW];
+#pragma unroll
+      for (int k = 0; k < NDW; ++k) dw[k] = ch[k];
+      const uint32_t code = (quad_sel<NDW>(dw, cc >> 2) >> (8 * (cc & 3))) & 7u;
+      y[t * D + c] = lvl8[code];
+    }
+    __syncthreads();
+    for (int st = 1; st < D; st <<= 1) {
+      for (int b = l16; b < D / 2; b += 16) {
+        const int i = (b / st) * 2 * st + (b % st);
+        const int32_t a0 = y[t * D + i], a1 = y[t * D + i + st];
+        y[t * D + i] = a0 + a1;
+        y[t * D + i + st] = a0 - a1;
+      }
+      __syncthreads();
+    }
+    const double gam = f16_bits_to_f64(reinterpret_cast<const uint16_t*>(sb + 12 * D)[t]);
+    const double rd = sqrt((double)D);
+    float kx[NJ], vx[NJ];
+    float kmax = 0.0f, vmax = 0.0f;
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int c = l16 + 16 * j;
+      const double hc = (double)y[t * D + c] * 0.125;  // exact
+      const double a = (gam * (double)P.sigma[c]) * hc;
+      kx[j] = (float)(a / rd);
+      kmax = fmaxf(kmax, fabsf(kx[j]));
+      // value code of (t, c): V chunk (c / CL, t / 4), quad c % CL, byte t % 4
+      const uint32_t* ch = reinterpret_cast<const uint32_t*>(sb + 6 * D + ((t >> 2) * 16 + c / CL) * CB);
+      uint32_t dw[NDW];
+#pragma unroll
+      for (int k = 0; k < NDW; ++k) dw[k] = ch[k];
+      const uint32_t vc = (quad_sel<NDW>(dw, c % CL) >> (8 * (t & 3))) & 7u;
+      const double sc = f16_bits_to_f64(reinterpret_cast<const uint16_t*>(sb + 12 * D + 32)[c]);
+      const double zr = f16_bits_to_f64(reinterpret_cast<const uint16_t*>(sb + 14 * D + 32)[c]);
+      vx[j] = (float)(zr + sc * (double)vc);
+      vmax = fmaxf(vmax, fabsf(vx[j]));
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      kmax = fmaxf(kmax, __shfl_xor(kmax, o, 64));
+      vmax = fmaxf(vmax, __shfl_xor(vmax, o, 64));
+    }
+    if (lane == 0) {
+      s_red[0][wv] = kmax;
+      s_red[1][wv] = vmax;
+    }
+    __syncthreads();
+    const float ka = fmaxf(fmaxf(s_red[0][0], s_red[0][1]), fmaxf(s_red[0][2], s_red[0][3]));
+    const float va = fmaxf(fmaxf(s_red[1][0], s_red[1][1]), fmaxf(s_red[1][2], s_red[1][3]));
+    const float sK = ka / 448.0f, sV = va / 448.0f;
+    uint8_t* db = reinterpret_cast<uint8_t*>(dst);
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      const int c = l16 + 16 * j;
+      db[fp8_off<D>(0, t, c)] = (uint8_t)(sK > 0.0f ? f32_to_e4m3(kx[j] / sK) : 0u);
+      db[fp8_off<D>(1, t, c)] = (uint8_t)(sV > 0.0f ? f32_to_e4m3(vx[j] / sV) : 0u);
+    }
+    __syncthreads();
+    const int64_t ph = ((int64_t)layer * P.n_fp8 + did) * H + h;
+    uint32_t* reg8 = reinterpret_cast<uint32_t*>(P.fp8 + ph * fp8_region_bytes(D));
+    for (int w = tid; w < R8W; w += 256) reg8[w] = dst[w];
+    if (tid == 0) {
+      P.fp8_scales[ph * 2] = sK;
+      P.fp8_scales[ph * 2 + 1] = sV;
+    }
+    __syncthreads();
+  }
+}
+
+// Publish (Anchor, new FP8 id) and release the TQ3 ids, in list order.
+__global__ __launch_bounds__(1024) void promote_publish_kernel(int32_t* bt, uint8_t* tags,
+                                                               int max_pages, int32_t* ctrl,
+                                                               int32_t* tq3_stack,
+                                                               const int32_t* list) {
+  if (ctrl[CTRL_ABORT]) return;
+  const int n = ctrl[CTRL_NLIST];
+  const int top = ctrl[CTRL_TQ3_TOP];
+  for (int k = threadIdx.x; k < n; k += blockDim.x) {
+    const int32_t* le = list + 4LL * k;
+    const int64_t i = (int64_t)le[0] * max_pages + le[1];
+    bt[i] = le[3];
+    tags[i] = TAG_A;
+    tq3_stack[top + k] = le[2];
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) ctrl[CTRL_TQ3_TOP] = top + n;
+}
+
+// ===========================================================================
 // Compact per-format page lists
 // ===========================================================================
 __global__ __launch_bounds__(1024) void partition_kernel(const int32_t* bt, const uint8_t* tags,
@@ -875,6 +1097,23 @@ hipError_t launch_migrate(const PoolView& P, int n_req, int32_t* bt, uint8_t* ta
     hipLaunchKernelGGL(migrate_encode_kernel<128>, dim3(grid), dim3(256), 0, s, P);
   hipLaunchKernelGGL(migrate_publish_kernel, dim3(1), dim3(1024), 0, s, bt, tags, max_pages, P.ctrl,
                      P.fp8_stack, P.list);
+  return hipGetLastError();
+}
+
+hipError_t launch_promote(const PoolView& P, int n_req, int32_t* bt, uint8_t* tags, int max_pages,
+                          const uint8_t* mask, const int32_t* seq_lens, hipStream_t s) {
+  hipLaunchKernelGGL(promote_plan_kernel, dim3(1), dim3(MIG_NT), 0, s, n_req, bt, tags, max_pages,
+                     mask, seq_lens, P.ctrl, P.fp8_stack, P.list, P.n_tq3);
+  int64_t bound = (int64_t)n_req * max_pages;
+  if (bound > P.n_fp8) bound = P.n_fp8;
+  if (bound > P.n_tq3) bound = P.n_tq3;
+  const int grid = grid_for(bound * P.n_layers * P.n_kv_heads, 2048);
+  if (P.d == 256)
+    hipLaunchKernelGGL(promote_build_kernel<256>, dim3(grid), dim3(256), 0, s, P);
+  else
+    hipLaunchKernelGGL(promote_build_kernel<128>, dim3(grid), dim3(256), 0, s, P);
+  hipLaunchKernelGGL(promote_publish_kernel, dim3(1), dim3(1024), 0, s, bt, tags, max_pages, P.ctrl,
+                     P.tq3_stack, P.list);
   return hipGetLastError();
 }
 

@@ -107,6 +107,18 @@ class Twin:
             n = self.orc.migrate(self.obt, self.otags, am, sl)
             assert n >= 0
 
+    def promote(self, mask):
+        """Alg. 1 Promote of the Stale pages whose mask entry is set."""
+        import paper_2608_23834_amd as mk
+        torch = _torch()
+        sl = np.array(self.cur, np.int32)
+        mk.kv_promote_to_fp8(self.gpu, self.bt, self.tags, torch.from_numpy(mask).cuda(),
+                             torch.from_numpy(sl).cuda())
+        if self.orc is not None:
+            n = self.orc.promote(self.obt, self.otags, mask, sl)
+            assert n >= 0
+            return n
+
     def _ws(self, ws_fill):
         import paper_2608_23834_amd as mk
         ws = mk.workspace(self.gpu, self.n_req, self.max_pages)
