@@ -181,7 +181,7 @@ def cpu_baseline(w, budget_s=25.0, max_req=4):
 
 def chunk_bench(mk, torch, reps=5):
     """Chunked prefill (paged_attn_chunk) on the chunk workload at full size:
-    8 requests, each with a 512-query chunk appended after 65,024 context
+    8 requests, each with a 512-query chunk appended after 65,536 context
     tokens (mixed FP8/TQ3 pages), one layer.  HIP events on the current
     stream around `reps` calls; MFMA share = algorithmic causal-attention
     flops (4 d flops per query-key pair and head) / time / dense f16 peak."""

@@ -304,6 +304,18 @@ mkv_status paged_attn_last_times(mkv_pool* pool, float* scan_us, float* merge_us
 #define MKV_STREAM_PROBE_WORKGROUPS 2048
 mkv_status mkv_stream_read(const void* buf, size_t bytes, uint32_t* sink, hipStream_t stream);
 
+/* Arithmetic conformance probe for tests; correct use never needs it.  The
+ * bit-exact TQ3 metadata (gamma, V scale and zero; Sec. 4.1 FP16 key-norm
+ * correction and scale/zero) relies on the device's fp64 division and square
+ * root being correctly rounded and on the library's fp64 -> binary16
+ * rounding (nearest-even, saturating at 65504).  This runs exactly that
+ * compiled code: quot[i] = a[i] / b[i], root[i] = sqrt(a[i]), half[i] =
+ * binary16(a[i]) for i < n.  All five arrays are device memory (8-byte
+ * aligned; half 2-byte aligned).  Enqueued on stream; MKV_EINVAL on a null
+ * pointer or n < 0. */
+mkv_status mkv_fp64_probe(const double* a, const double* b, int64_t n, double* quot, double* root,
+                          uint16_t* half, hipStream_t stream);
+
 /* Read (and optionally clear) the device error word; synchronizes. */
 mkv_status kv_pool_check_errors(mkv_pool* pool, uint32_t* err_word, int32_t clear);
 

@@ -76,7 +76,7 @@ def workload(cfg_id: int) -> Workload:
                         _cfg4_lens(64, 20260004))
     if cfg_id == 5:
         return Workload(5, "chunk512-vs-65536-migrate", 1, 24, 4, 256, 1024, 4, 0.02, 8,
-                        (65536,) * 8, chunk=512)
+                        (65536 + 512,) * 8, chunk=512)
     raise ValueError(cfg_id)
 
 

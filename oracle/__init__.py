@@ -107,7 +107,7 @@ def _declare(L):
     L.orc_partition.argtypes = [i32, vp, vp, i32, vp, vp, vp, vp]
     L.orc_reconstruct.argtypes = [vp, i32, i32, i32, vp, vp, i32, i32, vp, vp]
     L.orc_decode.argtypes = [vp, i32, i32, i32, vp, vp, vp, i32, vp, vp, vp]
-    L.orc_chunk.argtypes = [vp, i32, i32, i32, vp, vp, vp, vp, i32, vp, vp, i64]
+    L.orc_chunk.argtypes = [vp, i32, i32, i32, vp, vp, vp, vp, i32, vp, vp, vp]
     L.orc_merge.argtypes = [i32, i32, vp, vp, vp, vp, vp]
     L.orc_num_threads.restype = i32
     L.orc_num_threads.argtypes = []
@@ -334,8 +334,9 @@ class Pool:
         cu = np.ascontiguousarray(cu_q, dtype=np.int32)
         sl = np.ascontiguousarray(seq_lens, dtype=np.int32)
         out = np.full((q.shape[0], self.n_q_heads, self.d), np.nan)
+        st = np.ascontiguousarray(np.broadcast_to(np.asarray(sample_stride, np.int32), (n_req,)))
         lib().orc_chunk(self._c(), layer, n_req, self.n_q_heads, _p(q), _p(cu), _p(block_table),
-                        _p(tags), max_pages, _p(sl), _p(out), int(sample_stride))
+                        _p(tags), max_pages, _p(sl), _p(out), _p(st))
         return out
 
 

@@ -906,32 +906,41 @@ void orc_decode(const orc_pool* P, int layer, int n_req, int n_q_heads, const ui
 /* Chunk (causal): request r has n_r = cu_q[r+1]-cu_q[r] queries; query i sits
  * at position seq_len - n_r + i and sees keys t <= that position.  The chunk's
  * own KV is read back from the pool (it was appended as FP8 beforehand).
- * q: bf16 [sum n_r][Hq][d]; out fp64 same shape. */
+ * q: bf16 [sum n_r][Hq][d]; out fp64 same shape.  strides (NULL: every
+ * query): only queries i with i % strides[r] == 0, and each request's last
+ * query, are computed; the other rows of out are left as they are. */
 void orc_chunk(const orc_pool* P, int layer, int n_req, int n_q_heads, const uint16_t* q,
                const int32_t* cu_q, const int32_t* bt, const uint8_t* tags, int max_pages,
-               const int32_t* seq_lens, double* out, int64_t sample_stride) {
+               const int32_t* seq_lens, double* out, const int32_t* strides) {
   int d = P->d, H = P->n_kv_heads, G = n_q_heads / H;
-  if (sample_stride < 1) sample_stride = 1;
+  /* one request at a time: its heads' reconstructed caches, then every
+   * sampled (head, query) row in parallel */
+  for (int r = 0; r < n_req; ++r) {
+    int n = seq_lens[r], nq = cu_q[r + 1] - cu_q[r];
+    int64_t stride = strides && strides[r] > 1 ? strides[r] : 1;
+    size_t per = (size_t)(n > 0 ? n : 1) * d;
+    double* kh = (double*)malloc(sizeof(double) * per * H);
+    double* vh = (double*)malloc(sizeof(double) * per * H);
+#pragma omp parallel for schedule(static)
+    for (int h = 0; h < H; ++h)
+      orc_reconstruct(P, layer, r, h, bt, tags, max_pages, n, kh + per * h, vh + per * h);
 #pragma omp parallel for collapse(2) schedule(dynamic)
-  for (int r = 0; r < n_req; ++r)
-    for (int h = 0; h < H; ++h) {
-      int n = seq_lens[r], nq = cu_q[r + 1] - cu_q[r];
-      double* kh = (double*)malloc(sizeof(double) * (size_t)(n > 0 ? n : 1) * d);
-      double* vh = (double*)malloc(sizeof(double) * (size_t)(n > 0 ? n : 1) * d);
-      double* qd = (double*)malloc(sizeof(double) * d);
-      orc_reconstruct(P, layer, r, h, bt, tags, max_pages, n, kh, vh);
+    for (int h = 0; h < H; ++h)
       for (int i = 0; i < nq; ++i) {
-        if (((int64_t)i % sample_stride) != 0 && i != nq - 1) continue;
+        if (((int64_t)i % stride) != 0 && i != nq - 1) continue;
         int pos = n - nq + i;
+        double* qd = (double*)malloc(sizeof(double) * d);
         for (int j = 0; j < G; ++j) {
           int hq = h * G + j;
           int64_t row = (int64_t)(cu_q[r] + i) * n_q_heads + hq;
           for (int c = 0; c < d; ++c) qd[c] = bf16_to_f64(q[row * d + c]);
-          attend(d, qd, kh, vh, pos + 1, out + row * d, 0);
+          attend(d, qd, kh + per * h, vh + per * h, pos + 1, out + row * d, 0);
         }
+        free(qd);
       }
-      free(kh); free(vh); free(qd);
-    }
+    free(kh);
+    free(vh);
+  }
 }
 
 /* Eq. (softmax-merge), Sec. 3.3: merge partials (m_j, l_j, Obar_j) into O.

@@ -28,7 +28,7 @@ EXPORTS = ["kv_pool_bytes", "kv_pool_create", "kv_pool_destroy", "kv_append_fp8"
            "kv_partition_pages", "kv_pool_free_counts",
            "kv_pool_read_free_lists", "kv_pool_counters", "kv_pool_check_errors",
            "paged_attn_set_timing", "paged_attn_last_times", "mkv_stream_read",
-           "paged_attn_decode_noalloc", "mkv_status_string"]
+           "paged_attn_decode_noalloc", "mkv_fp64_probe", "mkv_status_string"]
 
 _lib = None
 
@@ -91,6 +91,7 @@ def lib() -> ctypes.CDLL:
         L.paged_attn_set_timing.argtypes = [vp, i32]
         L.paged_attn_last_times.argtypes = [vp, vp, vp]
         L.mkv_stream_read.argtypes = [vp, sz, vp, vp]
+        L.mkv_fp64_probe.argtypes = [vp, vp, ctypes.c_int64, vp, vp, vp, vp]
         L.mkv_status_string.argtypes = [ctypes.c_int]
         _lib = L
     return _lib
@@ -305,6 +306,15 @@ def mkv_stream_read(buf, sink, stream=None):
     assert sink.numel() >= STREAM_PROBE_WORKGROUPS
     _check("mkv_stream_read", lib().mkv_stream_read(
         _ptr(buf), buf.numel() * buf.element_size(), _ptr(sink), _stream(stream)))
+
+
+def mkv_fp64_probe(a, b, quot, root, half, stream=None):
+    """Conformance probe (tests only): quot = a / b, root = sqrt(a), half =
+    binary16(a), by the library's own compiled fp64 code (device tensors)."""
+    n = a.numel()
+    assert b.numel() == n and quot.numel() == n and root.numel() == n and half.numel() == n
+    _check("mkv_fp64_probe", lib().mkv_fp64_probe(_ptr(a), _ptr(b), n, _ptr(quot), _ptr(root),
+                                                  _ptr(half), _stream(stream)))
 
 
 def kv_pool_check_errors(pool: Pool, clear=False) -> int:

@@ -382,6 +382,13 @@ mkv_status mkv_stream_read(const void* buf, size_t bytes, uint32_t* sink, hipStr
   return hip_status(launch_stream_read(buf, bytes, sink, MKV_STREAM_PROBE_WORKGROUPS, stream));
 }
 
+mkv_status mkv_fp64_probe(const double* a, const double* b, int64_t n, double* quot, double* root,
+                          uint16_t* half, hipStream_t stream) {
+  if (!a || !b || !quot || !root || !half || n < 0) return MKV_EINVAL;
+  if (n == 0) return MKV_OK;
+  return hip_status(launch_fp64_probe(a, b, n, quot, root, half, stream));
+}
+
 mkv_status kv_pool_check_errors(mkv_pool* pool, uint32_t* err_word, int32_t clear) {
   if (!pool) return MKV_EINVAL;
   if (hipDeviceSynchronize() != hipSuccess) return MKV_EHIP;

@@ -65,6 +65,8 @@ hipError_t launch_partition(int n_req, const int32_t* bt, const uint8_t* tags, i
                             const int32_t* seq_lens, int32_t* list8, int32_t* list3,
                             int32_t* counts, int32_t* err, hipStream_t s);
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
+hipError_t launch_fp64_probe(const double* a, const double* b, int64_t n, double* quot,
+                             double* root, uint16_t* half, hipStream_t s);
 
 // mkv_decode.hip
 struct DecodeShape {

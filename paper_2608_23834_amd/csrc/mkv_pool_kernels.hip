@@ -1117,6 +1117,28 @@ hipError_t launch_promote(const PoolView& P, int n_req, int32_t* bt, uint8_t* ta
   return hipGetLastError();
 }
 
+// Arithmetic conformance probe: the fp64 division, square root and binary16
+// rounding of this translation unit (the ones gamma and the V scale/zero rest
+// on), element by element.
+__global__ __launch_bounds__(256) void fp64_probe_kernel(const double* a, const double* b, int64_t n,
+                                                         double* quot, double* root,
+                                                         uint16_t* half) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) {
+    const double x = a[i], y = b[i];
+    quot[i] = x / y;
+    root[i] = sqrt(x);
+    half[i] = f64_to_f16_rne_sat(x);
+  }
+}
+
+hipError_t launch_fp64_probe(const double* a, const double* b, int64_t n, double* quot,
+                             double* root, uint16_t* half, hipStream_t s) {
+  hipLaunchKernelGGL(fp64_probe_kernel, dim3(grid_for((n + 255) / 256, 4096)), dim3(256), 0, s, a, b,
+                     n, quot, root, half);
+  return hipGetLastError();
+}
+
 hipError_t launch_partition(int n_req, const int32_t* bt, const uint8_t* tags, int max_pages,
                             const int32_t* seq_lens, int32_t* list8, int32_t* list3,
                             int32_t* counts, int32_t* err, hipStream_t s) {

@@ -204,7 +204,18 @@ class Twin:
         torch.cuda.synchronize()
         res = dict(out=out.cpu().numpy(), q=q, cu=cu, seq_lens=sl)
         if self.orc is not None:
-            res["ref_out"] = self.orc.chunk(layer, q, cu, self.obt, self.otags, sl, sample_stride)
+            if np.ndim(sample_stride) == 0:
+                res["ref_out"] = self.orc.chunk(layer, q, cu, self.obt, self.otags, sl, sample_stride)
+            else:  # per-request strides, one request per oracle call (progress lines)
+                ref = np.full(res["out"].shape, np.nan)
+                for r in range(self.n_req):
+                    st = np.full(self.n_req, 1 << 30, np.int32)
+                    st[r] = sample_stride[r]
+                    o = self.orc.chunk(layer, q, cu, self.obt, self.otags, sl, st)
+                    ref[cu[r]:cu[r + 1]] = o[cu[r]:cu[r + 1]]
+                    print(f"  oracle chunk rows of request {r} done (stride {sample_stride[r]})",
+                          flush=True)
+                res["ref_out"] = ref
         return res
 
     # -- comparisons -------------------------------------------------------

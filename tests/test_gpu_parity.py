@@ -67,9 +67,11 @@ def test_two_layers_chunked_fill(torch_cuda):
 
 
 def test_single_request_16k_config(torch_cuda):
-    """Config 2 shape (one 16K request, anchors 4 + 2%), one layer."""
+    """Config 2 at full size: one 16K request, anchors 4 + 2 %, all 16
+    layers appended, migrated and decoded."""
     w = wl.workload(2)
-    _run_decode_case(w, list(w.ctx))
+    assert w.n_layers == 16
+    _run_decode_case(w, list(w.ctx), n_layers=16)
 
 
 def test_long_pair_full_size(torch_cuda):
@@ -88,9 +90,9 @@ def test_batch64_config_full_size(torch_cuda):
     """Config 4 at full size: 64 requests with lengths drawn from U[4096,
     65536], pages of every request interleaved in one pool through shuffled
     free stacks, one layer, in the launch configuration of the benchmark's
-    decode call.  The GPU holds all 64 requests; the oracle models a sample
-    of them (the shortest, the longest and two others) from the same K/V
-    bytes, copied back from the device.  Physical ids differ between the two
+    decode call.  The GPU holds all 64 requests; the oracle models 16 of
+    them (the shortest, the longest and 14 others, most with a partly filled
+    last page) from the same K/V bytes, copied back from the device.  Physical ids differ between the two
     pools (the oracle does not see the other requests), so pages are
     compared bit for bit through each side's block table."""
     import oracle
@@ -125,7 +127,9 @@ def test_batch64_config_full_size(torch_cuda):
     g_bt, g_tags = bt.cpu().numpy(), tags.cpu().numpy()
     rng = np.random.default_rng(4)
     rest = [r for r in range(n_req) if r not in (int(np.argmin(lens)), int(np.argmax(lens)))]
-    sample = sorted({int(np.argmin(lens)), int(np.argmax(lens)), *rng.choice(rest, 2, replace=False).tolist()})
+    sample = sorted({int(np.argmin(lens)), int(np.argmax(lens)), *rng.choice(rest, 14, replace=False).tolist()})
+    assert len(sample) == 16
+    assert sum(lens[r] % 16 != 0 for r in sample) >= 8  # partly filled last pages
     s_lens = [lens[r] for r in sample]
     s_mp = max((L + 15) // 16 for L in s_lens)
     s_tot = sum((L + 15) // 16 for L in s_lens) + 8
@@ -536,13 +540,16 @@ def test_chunk_last_query_matches_decode(torch_cuda):
     assert err <= TOL, err
 
 
+@pytest.mark.timeout(900)
 def test_chunk_config5_full_size(torch_cuda):
-    """Config 5 at full size: 8 requests, a 512-query chunk each against
-    65,536 tokens of mixed pages (sampled queries: every 64th and the last),
-    then the migration of the pages the chunk pushed out of the Recent
-    window, bit-exact."""
+    """Config 5 at full size: 8 requests, a 512-query chunk each against a
+    65,536-token context of mixed pages (every query row of requests 0 and 1,
+    every 8th and the last of the others), then the migration of the pages
+    the chunk pushed out of the Recent window, bit-exact."""
     w = wl.workload(5)
-    tw, res = _run_chunk_case(w, list(w.ctx), [512] * 8, sample_stride=64, migrate_after=True)
+    assert all(L == 65536 + 512 for L in w.ctx)
+    tw, res = _run_chunk_case(w, list(w.ctx), [512] * 8, sample_stride=[1, 1] + [8] * 6,
+                              migrate_after=True)
     assert np.all(np.isfinite(res["out"]))
     # 512 new tokens push 32 pages per request out of the 1,024-token window;
     # anchors among them stay FP8
