@@ -84,8 +84,10 @@ def measured_traffic(workload_name: str):
     return int(kv["hbm_bytes_per_launch"])
 
 
-def build_state(w, n_layers, extra_tokens, mk, torch):
-    """Pool for `n_layers` layers filled with the workload's context, migrated."""
+def build_state(w, n_layers, extra_tokens, mk, torch, also=None):
+    """Pool for `n_layers` layers filled with the workload's context, migrated.
+    `also(layer, k, v, cu)`, if given, receives each layer's K/V (device bf16
+    bits) too, for the dense controls."""
     lens = list(w.ctx)
     n_req = len(lens)
     max_pages = (max(lens) + extra_tokens + PAGE - 1) // PAGE
@@ -113,6 +115,8 @@ def build_state(w, n_layers, extra_tokens, mk, torch):
             kt = torch.from_numpy(k.view(np.int16)).cuda()
             vt = torch.from_numpy(v.view(np.int16)).cuda()
             mk.kv_append_fp8(pool, l, bt, tags, sb, cu, kt, vt)
+            if also is not None:
+                also(l, kt, vt, cu)
             torch.cuda.synchronize()
             del kt, vt
     am = torch.from_numpy(wl.anchor_mask(w, max_pages)).cuda()
@@ -227,6 +231,106 @@ def chunk_bench(mk, torch, reps=5):
             "kernel": "chunk_kernel<256> (+ partition_kernel)"}
 
 
+class DenseControls:
+    """The same KV as the mixed pool held all-FP8 (a pool with no Retier: every
+    page stays FP8) and all-bf16 (the library's control pages), filled layer
+    by layer from the K/V build_state generates (the dense controls of the
+    paper's fused-decode canary, Sec. 6.3)."""
+
+    def __init__(self, w, n_layers, mk, torch):
+        lens = list(w.ctx)
+        self.w, self.lens, self.n_layers = w, lens, n_layers
+        self.mp = (max(lens) + PAGE - 1) // PAGE
+        n_pg = sum((L + PAGE - 1) // PAGE for L in lens)
+        self.fp8 = mk.Pool(n_layers, w.n_q_heads, w.n_kv_heads, w.head_dim, n_pg + 16, 1,
+                           w.recent, wl.rot_signs(w), wl.free_order(w, n_pg + 16, "fp8"), None)
+        self.bt8 = torch.full((len(lens), self.mp), -1, dtype=torch.int32, device="cuda")
+        self.tags8 = torch.full((len(lens), self.mp), 0xFF, dtype=torch.uint8, device="cuda")
+        self.bf16 = mk.ControlBf16(n_layers, w.n_q_heads, w.n_kv_heads, w.head_dim, n_pg)
+        ids = np.random.default_rng(w.seed).permutation(n_pg).astype(np.int32)
+        bt = np.full((len(lens), self.mp), -1, np.int32)
+        k0 = 0
+        for r, L in enumerate(lens):
+            npg = (L + PAGE - 1) // PAGE
+            bt[r, :npg] = ids[k0:k0 + npg]
+            k0 += npg
+        self.bt16 = torch.from_numpy(bt).cuda()
+        self.sb = torch.zeros(len(lens), dtype=torch.int32, device="cuda")
+        self.sl = torch.tensor(lens, dtype=torch.int32, device="cuda")
+        self.mk = mk
+
+    def add_layer(self, layer, k, v, cu):
+        self.mk.kv_append_fp8(self.fp8, layer, self.bt8, self.tags8, self.sb, cu, k, v)
+        self.bf16.write(layer, self.bt16, self.sb, cu, k, v)
+
+    def time(self, torch, q_all, mixed, reps):
+        """Decode-only sweeps of every layer (no append, no Retier) on the
+        mixed pool as it stands and on both controls; HIP events around
+        `reps` sweeps; us/layer, KV bytes per layer and GB/s for each."""
+        mk, w, n_layers = self.mk, self.w, self.n_layers
+        n_req, d, H = len(self.lens), w.head_dim, w.n_kv_heads
+        out = torch.zeros((n_req, w.n_q_heads, d), device="cuda")
+        stream = torch.cuda.current_stream()
+
+        def sweep_time(fn):
+            for _ in range(2):
+                for l in range(n_layers):
+                    fn(l)
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            for _ in range(reps):
+                for l in range(n_layers):
+                    fn(l)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            return e0.elapsed_time(e1) * 1e3 / (reps * n_layers)
+
+        pool, bt, tags, sl = mixed
+        ws_m = mk.workspace(pool, n_req, bt.shape[1])
+        t_mixed = sweep_time(lambda l: mk.paged_attn_decode(pool, l, q_all[l], bt, tags, sl, out,
+                                                            None, ws_m))
+        tg = tags.cpu().numpy()
+        sl_h = sl.cpu().numpy()
+        b_mixed = sum(kv_bytes_of(tg[r], int(sl_h[r]), d, H) for r in range(n_req))
+        ws8 = mk.workspace(self.fp8, n_req, self.mp)
+        t_fp8 = sweep_time(lambda l: mk.paged_attn_decode(self.fp8, l, q_all[l], self.bt8,
+                                                          self.tags8, self.sl, out, None, ws8))
+        tg8 = self.tags8.cpu().numpy()
+        assert (tg8[tg8 != 0xFF] == 0).all()
+        b_fp8 = sum(kv_bytes_of(tg8[r], L, d, H) for r, L in enumerate(self.lens))
+        ws16 = self.bf16.workspace(n_req, self.mp)
+        t_bf16 = sweep_time(lambda l: self.bf16.decode(l, q_all[l], self.bt16, self.sl, out, None,
+                                                       ws16))
+        b_bf16 = sum(2 * L * d * 2 for L in self.lens) * H
+        for pool_ in (pool, self.fp8):
+            if mk.kv_pool_check_errors(pool_):
+                raise RuntimeError("device error word set in the dense-control sweeps")
+
+        def row(t, b):
+            return {"us_per_layer": round(t, 3), "kv_bytes_per_layer": int(b),
+                    "kv_gb_per_s": round(b / (t * 1e-6) / 1e9, 1),
+                    "frac_of_hbm_peak": round(b / (t * 1e-6) / HBM_PEAK, 4)}
+
+        return {
+            "timing": f"decode only (decode + merge per layer, no append, no Retier), "
+                      f"{reps} sweeps of {n_layers} layers between two HIP events",
+            "mixed": {**row(t_mixed, b_mixed), "seq_len": int(sl_h[0]),
+                      "kernel": "decode_kernel<256, true, true, false> + decode_merge_kernel"},
+            "all_fp8": {**row(t_fp8, b_fp8), "seq_len": self.lens[0],
+                        "kernel": "the same kernels, every page FP8"},
+            "all_bf16": {**row(t_bf16, b_bf16), "seq_len": self.lens[0],
+                         "kernel": "bf16_decode_kernel<256, 8> + bf16_merge_kernel (control)"},
+            "mixed_vs_fp8_throughput": round(t_fp8 / t_mixed, 4),
+            "mixed_vs_bf16_throughput": round(t_bf16 / t_mixed, 4),
+            "fp8_over_mixed_kv_bytes": round(b_fp8 / b_mixed, 4),
+            "bf16_over_mixed_kv_bytes": round(b_bf16 / b_mixed, 4),
+            "paper_context": "the paper's canary on its Blackwell GPU: 0.9821x the dense FP8 "
+                             "route's throughput for the whole serving step while reading "
+                             "3.625x fewer KV bytes than its BF16-priced cache (Sec. 6.3)",
+        }
+
+
 def stream_probe(mk, torch, nbytes, achieved, reps=20):
     """A plain streaming read of `nbytes` (the library's probe kernel, 16-byte
     loads, each byte once), cycling through 16 buffers so no read is served
@@ -282,9 +386,11 @@ def main():
                     help="skip the chunked-prefill measurement")
     ap.add_argument("--copy-probe", action="store_true",
                     help="also run one 1 GiB device-to-device copy (calibrates HBM byte counters)")
-    ap.add_argument("--stream-probe", action="store_true",
-                    help="also time a plain streaming read of the decode's byte count (torch sum "
-                         "over cycled buffers) as a measured bandwidth ceiling")
+    ap.add_argument("--no-stream-probe", action="store_true",
+                    help="skip the streaming-read probe (a kernel that reads the decode's byte "
+                         "count once, over cycled buffers: the measured bandwidth ceiling)")
+    ap.add_argument("--no-controls", action="store_true",
+                    help="skip the dense controls (the same KV all-FP8 and all-bf16)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
@@ -301,7 +407,9 @@ def main():
     n_pass = 2 if args.no_unfused else 3
     n_steps = args.warmup + n_pass * args.steps  # warmup, pass A, pass B (, pass C)
     t_setup = time.perf_counter()
-    pool, bt, tags, am, max_pages = build_state(w, n_layers, n_steps + 16, mk, torch)
+    ctl = None if args.no_controls or args.cfg not in (2, 3) else DenseControls(w, n_layers, mk, torch)
+    pool, bt, tags, am, max_pages = build_state(w, n_layers, n_steps + 16, mk, torch,
+                                                None if ctl is None else ctl.add_layer)
     lens = list(w.ctx)
     n_req = len(lens)
     Hkv, d = w.n_kv_heads, w.head_dim
@@ -422,7 +530,10 @@ def main():
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f16",
+        "dtype": "fp8/f16 MFMA, fp32 accumulate",
+        "dtype_detail": "TQ3 scores on the fp8 MFMA (E4M3 codebook keys, rotated query as three "
+                        "E4M3 terms); FP8-page scores and all PV products on the f16 MFMA with "
+                        "hi + lo fp16 operands; softmax, scales and merge in fp32",
         "data": "synthetic",
         "config": {"workload": w.name, "n_req": n_req, "seq_len": lens[0], "layers": n_layers,
                    "q_heads": w.n_q_heads, "kv_heads": Hkv, "head_dim": d, "page_tokens": PAGE,
@@ -440,7 +551,9 @@ def main():
         "unfused_step": "third pass: the same steps with kv_append_fp8 and paged_attn_decode "
                         "as separate calls",
         "kv_bytes_per_layer": int(kv_bytes),
-        "effective_kv_gb_per_s": round(kv_bytes / (dec_us * 1e-6) / 1e9, 1),
+        "effective_kv_gb_per_s": round(kv_bytes / (ms_per_step * 1e-3 / n_layers) / 1e9, 1),
+        "effective_kv_note": "algorithmic KV bytes per layer / the headline step time per layer "
+                             "(decode, fused append, merge and the step's Retier share)",
         "roofline": {"bound": "hbm", "achieved": round(achieved / 1e9, 1), "peak": HBM_PEAK / 1e9,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK, 4), "traffic": traffic,
                      "kernel": "decode_kernel<256, true, true, true> (split scan with the "
@@ -448,7 +561,12 @@ def main():
         "counters": {k: int(v) for k, v in counters.items()},
         "setup_s": round(setup_s, 1),
     }
-    if args.stream_probe:
+    if ctl is not None:
+        print("[bench] dense controls", file=sys.stderr, flush=True)
+        res["dense_controls"] = ctl.time(torch, q_all, (pool, bt, tags, seq_after[n_steps - 1]), 5)
+        del ctl
+        torch.cuda.empty_cache()
+    if not args.no_stream_probe:
         res["stream_probe"] = stream_probe(mk, torch, int(kv_bytes), achieved)
     if args.copy_probe:
         a_ = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")

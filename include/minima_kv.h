@@ -304,6 +304,40 @@ mkv_status paged_attn_last_times(mkv_pool* pool, float* scan_us, float* merge_us
 #define MKV_STREAM_PROBE_WORKGROUPS 2048
 mkv_status mkv_stream_read(const void* buf, size_t bytes, uint32_t* sink, hipStream_t stream);
 
+/* Dense bf16 control for measurement tools; correct use never needs it.  The
+ * fused-decode canary of Sec. 6.3 times the mixed-format route against a
+ * dense control on the same KV; these calls hold that KV as bf16 pages and
+ * attend to it with a plain paged decode kernel, so the mixed path can be
+ * timed against an uncompressed cache of the same shape.
+ *  - pages: device, bf16 bits [n_layers][n_pages][n_kv_heads][2*16*head_dim]
+ *    (MKV_CONTROL_BF16_PAGE_HEAD_BYTES(head_dim) bytes per page-head: K
+ *    token-major, then V in 4-token groups per channel), 16-byte aligned.
+ *  - block_table: device int32 [n_req][max_pages] of page ids chosen by the
+ *    caller (no allocator, no tags: every page is bf16).
+ * mkv_control_bf16_write copies new rows of one layer (k, v: device bf16
+ * [n_new_total][n_kv_heads][head_dim]; request r's rows cu_new_tokens[r] ..
+ * cu_new_tokens[r+1]-1 land at positions seq_lens_before[r] ..) into their
+ * pages; rows whose page is unmapped are skipped.  mkv_control_bf16_decode
+ * computes out[r][hq] = sum_t softmax_t(q . k_t / sqrt(d)) v_t over t <
+ * seq_lens[r] (fp32 accumulate, lse as in paged_attn_decode), with ws of at
+ * least mkv_control_bf16_workspace_bytes().  Both enqueue on stream;
+ * EINVAL/EUNSUP/ERANGE/ENOMEM on bad arguments as the calls above. */
+#define MKV_CONTROL_BF16_PAGE_HEAD_BYTES(d) ((size_t)4 * 16 * (size_t)(d))
+mkv_status mkv_control_bf16_write(uint16_t* pages, int32_t n_pages, int32_t n_layers,
+                                  int32_t n_kv_heads, int32_t head_dim, int32_t layer,
+                                  int32_t n_req, const int32_t* block_table, int32_t max_pages,
+                                  const int32_t* seq_lens_before, const int32_t* cu_new_tokens,
+                                  int32_t n_new_total, const uint16_t* k, const uint16_t* v,
+                                  hipStream_t stream);
+mkv_status mkv_control_bf16_workspace_bytes(int32_t n_req, int32_t max_pages, int32_t n_kv_heads,
+                                            int32_t n_q_heads, int32_t head_dim, size_t* bytes);
+mkv_status mkv_control_bf16_decode(const uint16_t* pages, int32_t n_pages, int32_t n_layers,
+                                   int32_t n_kv_heads, int32_t n_q_heads, int32_t head_dim,
+                                   int32_t layer, int32_t n_req, const uint16_t* q,
+                                   const int32_t* block_table, int32_t max_pages,
+                                   const int32_t* seq_lens, float* out, float* lse, void* ws,
+                                   size_t ws_bytes, hipStream_t stream);
+
 /* Arithmetic conformance probe for tests; correct use never needs it.  The
  * bit-exact TQ3 metadata (gamma, V scale and zero; Sec. 4.1 FP16 key-norm
  * correction and scale/zero) relies on the device's fp64 division and square

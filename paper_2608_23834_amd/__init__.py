@@ -28,7 +28,8 @@ EXPORTS = ["kv_pool_bytes", "kv_pool_create", "kv_pool_destroy", "kv_append_fp8"
            "kv_partition_pages", "kv_pool_free_counts",
            "kv_pool_read_free_lists", "kv_pool_counters", "kv_pool_check_errors",
            "paged_attn_set_timing", "paged_attn_last_times", "mkv_stream_read",
-           "paged_attn_decode_noalloc", "mkv_fp64_probe", "mkv_status_string"]
+           "paged_attn_decode_noalloc", "mkv_fp64_probe", "mkv_control_bf16_write",
+           "mkv_control_bf16_workspace_bytes", "mkv_control_bf16_decode", "mkv_status_string"]
 
 _lib = None
 
@@ -92,6 +93,11 @@ def lib() -> ctypes.CDLL:
         L.paged_attn_last_times.argtypes = [vp, vp, vp]
         L.mkv_stream_read.argtypes = [vp, sz, vp, vp]
         L.mkv_fp64_probe.argtypes = [vp, vp, ctypes.c_int64, vp, vp, vp, vp]
+        L.mkv_control_bf16_write.argtypes = [vp, i32, i32, i32, i32, i32, i32, vp, i32, vp, vp, i32,
+                                             vp, vp, vp]
+        L.mkv_control_bf16_workspace_bytes.argtypes = [i32, i32, i32, i32, i32, vp]
+        L.mkv_control_bf16_decode.argtypes = [vp, i32, i32, i32, i32, i32, i32, i32, vp, vp, i32,
+                                              vp, vp, vp, vp, sz, vp]
         L.mkv_status_string.argtypes = [ctypes.c_int]
         _lib = L
     return _lib
@@ -315,6 +321,40 @@ def mkv_fp64_probe(a, b, quot, root, half, stream=None):
     assert b.numel() == n and quot.numel() == n and root.numel() == n and half.numel() == n
     _check("mkv_fp64_probe", lib().mkv_fp64_probe(_ptr(a), _ptr(b), n, _ptr(quot), _ptr(root),
                                                   _ptr(half), _stream(stream)))
+
+
+class ControlBf16:
+    """Dense bf16 control pages (measurement only): the same KV as the mixed
+    pool held as bf16, for timing the mixed path against an uncompressed
+    cache.  Page ids come from the caller's block table."""
+
+    def __init__(self, n_layers, n_q_heads, n_kv_heads, head_dim, n_pages, device="cuda"):
+        import torch
+        self.n_layers, self.n_q_heads, self.n_kv_heads, self.d = n_layers, n_q_heads, n_kv_heads, head_dim
+        self.n_pages = n_pages
+        self.pages = torch.zeros((n_layers, n_pages, n_kv_heads, 2 * PAGE * head_dim),
+                                 dtype=torch.int16, device=device)
+
+    def write(self, layer, block_table, seq_lens_before, cu_new_tokens, k, v, stream=None):
+        n_req, max_pages = block_table.shape
+        _check("mkv_control_bf16_write", lib().mkv_control_bf16_write(
+            _ptr(self.pages), self.n_pages, self.n_layers, self.n_kv_heads, self.d, layer, n_req,
+            _ptr(block_table), max_pages, _ptr(seq_lens_before), _ptr(cu_new_tokens),
+            int(k.shape[0]), _ptr(k), _ptr(v), _stream(stream)))
+
+    def workspace(self, n_req, max_pages, device="cuda"):
+        import torch
+        b = ctypes.c_size_t()
+        _check("mkv_control_bf16_workspace_bytes", lib().mkv_control_bf16_workspace_bytes(
+            n_req, max_pages, self.n_kv_heads, self.n_q_heads, self.d, ctypes.byref(b)))
+        return torch.empty(b.value, dtype=torch.uint8, device=device)
+
+    def decode(self, layer, q, block_table, seq_lens, out, lse, ws, stream=None):
+        n_req, max_pages = block_table.shape
+        _check("mkv_control_bf16_decode", lib().mkv_control_bf16_decode(
+            _ptr(self.pages), self.n_pages, self.n_layers, self.n_kv_heads, self.n_q_heads, self.d,
+            layer, n_req, _ptr(q), _ptr(block_table), max_pages, _ptr(seq_lens), _ptr(out),
+            _ptr(lse), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
 
 def kv_pool_check_errors(pool: Pool, clear=False) -> int:

@@ -29,7 +29,8 @@ EXACT = {"mkv_pool_kernels.hip"}
 # 128 output accumulators into VGPRs on every pass of the stage loop (for the
 # rarely taken rescale branch).
 EXTRA = {"mkv_chunk.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
-SOURCES = ["mkv_api.hip", "mkv_pool_kernels.hip", "mkv_decode.hip", "mkv_chunk.hip", "mkv_probe.hip"]
+SOURCES = ["mkv_api.hip", "mkv_pool_kernels.hip", "mkv_decode.hip", "mkv_chunk.hip", "mkv_probe.hip",
+           "mkv_control.hip"]
 
 
 def _compile(src: str) -> str:

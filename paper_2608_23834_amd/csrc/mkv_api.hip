@@ -382,6 +382,60 @@ mkv_status mkv_stream_read(const void* buf, size_t bytes, uint32_t* sink, hipStr
   return hip_status(launch_stream_read(buf, bytes, sink, MKV_STREAM_PROBE_WORKGROUPS, stream));
 }
 
+static mkv_status control_geometry(int32_t n_kv_heads, int32_t n_q_heads, int32_t head_dim) {
+  if (n_kv_heads < 1 || n_q_heads < 1 || n_q_heads % n_kv_heads) return MKV_EINVAL;
+  if (head_dim != 128 && head_dim != 256) return MKV_EUNSUP;
+  if (n_q_heads / n_kv_heads > 16) return MKV_EUNSUP;
+  return MKV_OK;
+}
+
+mkv_status mkv_control_bf16_write(uint16_t* pages, int32_t n_pages, int32_t n_layers,
+                                  int32_t n_kv_heads, int32_t head_dim, int32_t layer,
+                                  int32_t n_req, const int32_t* block_table, int32_t max_pages,
+                                  const int32_t* seq_lens_before, const int32_t* cu_new_tokens,
+                                  int32_t n_new_total, const uint16_t* k, const uint16_t* v,
+                                  hipStream_t stream) {
+  if (!pages || !block_table || !seq_lens_before || !cu_new_tokens) return MKV_EINVAL;
+  if (n_pages < 1 || n_layers < 1 || n_req < 1 || max_pages < 1 || n_new_total < 0) return MKV_EINVAL;
+  if (n_new_total > 0 && (!k || !v)) return MKV_EINVAL;
+  mkv_status st = control_geometry(n_kv_heads, n_kv_heads, head_dim);
+  if (st != MKV_OK) return st;
+  if (layer < 0 || layer >= n_layers || n_new_total > (1 << 30)) return MKV_ERANGE;
+  if (!aligned16(pages)) return MKV_EINVAL;
+  return hip_status(launch_control_bf16_write(pages, n_pages, n_kv_heads, head_dim, layer, n_req,
+                                              block_table, max_pages, seq_lens_before,
+                                              cu_new_tokens, n_new_total, k, v, stream));
+}
+
+mkv_status mkv_control_bf16_workspace_bytes(int32_t n_req, int32_t max_pages, int32_t n_kv_heads,
+                                            int32_t n_q_heads, int32_t head_dim, size_t* bytes) {
+  if (!bytes || n_req < 1 || max_pages < 1) return MKV_EINVAL;
+  mkv_status st = control_geometry(n_kv_heads, n_q_heads, head_dim);
+  if (st != MKV_OK) return st;
+  *bytes = control_bf16_ws_bytes(n_req, max_pages, n_kv_heads, n_q_heads / n_kv_heads, head_dim);
+  return MKV_OK;
+}
+
+mkv_status mkv_control_bf16_decode(const uint16_t* pages, int32_t n_pages, int32_t n_layers,
+                                   int32_t n_kv_heads, int32_t n_q_heads, int32_t head_dim,
+                                   int32_t layer, int32_t n_req, const uint16_t* q,
+                                   const int32_t* block_table, int32_t max_pages,
+                                   const int32_t* seq_lens, float* out, float* lse, void* ws,
+                                   size_t ws_bytes, hipStream_t stream) {
+  if (!pages || !q || !block_table || !seq_lens || !out || !ws) return MKV_EINVAL;
+  if (n_pages < 1 || n_layers < 1 || n_req < 1 || max_pages < 1) return MKV_EINVAL;
+  mkv_status st = control_geometry(n_kv_heads, n_q_heads, head_dim);
+  if (st != MKV_OK) return st;
+  if (layer < 0 || layer >= n_layers) return MKV_ERANGE;
+  if (n_req > 65535 || max_pages > 1024 * 256) return MKV_ERANGE;
+  if (!aligned16(pages) || !aligned16(q) || !aligned16(out) || !aligned16(ws)) return MKV_EINVAL;
+  if (ws_bytes < control_bf16_ws_bytes(n_req, max_pages, n_kv_heads, n_q_heads / n_kv_heads, head_dim))
+    return MKV_ENOMEM;
+  return hip_status(launch_control_bf16_decode(pages, n_pages, n_kv_heads, n_q_heads / n_kv_heads,
+                                               head_dim, layer, n_req, q, block_table, max_pages,
+                                               seq_lens, out, lse, ws, stream));
+}
+
 mkv_status mkv_fp64_probe(const double* a, const double* b, int64_t n, double* quot, double* root,
                           uint16_t* half, hipStream_t stream) {
   if (!a || !b || !quot || !root || !half || n < 0) return MKV_EINVAL;

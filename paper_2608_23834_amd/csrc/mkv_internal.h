@@ -85,6 +85,17 @@ hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t
                          const uint16_t* v_new = nullptr, int32_t* bt_w = nullptr,
                          uint8_t* tags_w = nullptr);
 
+// mkv_control.hip (dense bf16 control, measurement only)
+size_t control_bf16_ws_bytes(int n_req, int max_pages, int n_kv_heads, int group, int d);
+hipError_t launch_control_bf16_write(uint16_t* pages, int n_pages, int H, int d, int layer, int n_req,
+                                     const int32_t* bt, int max_pages, const int32_t* sb,
+                                     const int32_t* cu, int n_new, const uint16_t* k,
+                                     const uint16_t* v, hipStream_t s);
+hipError_t launch_control_bf16_decode(const uint16_t* pages, int n_pages, int H, int G, int d,
+                                      int layer, int n_req, const uint16_t* q, const int32_t* bt,
+                                      int max_pages, const int32_t* seq_lens, float* out,
+                                      float* lse, void* ws, hipStream_t s);
+
 // mkv_probe.hip
 hipError_t launch_stream_read(const void* buf, size_t bytes, uint32_t* sink, int n_wg, hipStream_t s);
 
