@@ -262,6 +262,27 @@ mkv_status paged_attn_chunk(mkv_pool* pool, int32_t layer, int32_t n_req, const 
                             const uint8_t* tags, int32_t max_pages, const int32_t* seq_lens,
                             float* out, void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* Graph eligibility of a decode step (Sec. 4.1: the graph path is gated on a
+ * homogeneous physical-cache cohort; other shapes, prefill or an
+ * inconsistent cache state fail closed to the generic path).  A decode step
+ * of this library -- paged_attn_decode or paged_attn_decode_append per layer,
+ * then kv_migrate_to_tq3 -- launches a fixed set of kernels whose grids and
+ * arguments depend only on the pool, n_req and max_pages; everything else it
+ * reads (queries, block table, tags, lengths) is read from device memory at
+ * run time, and it enqueues no memset and no host synchronization, so a step
+ * captured into a HIP graph replays correctly for any contents of the same
+ * buffers.  This returns a 64-bit key of everything such a capture bakes in:
+ * the pool (identity and geometry, page size, Recent window), n_req,
+ * max_pages, the split shape, the decode kernel instance (fused append or
+ * not) and the scoring flag (0: no attention scores; scoring runs another
+ * instance).  A caller replays a captured step only while the key it computes
+ * for the next step equals the captured one and the same device buffers are
+ * used, and launches the calls directly otherwise.  Errors: EINVAL;
+ * ESTATE when the pool is not a compressed cohort (no TQ3 pool) or kernel
+ * timing is on (its events are host objects, not graph nodes). */
+mkv_status paged_attn_decode_cohort_key(const mkv_pool* pool, int32_t n_req, int32_t max_pages,
+                                        int32_t fused_append, int32_t scoring, uint64_t* key);
+
 /* Compact per-format page lists (Sec. 4.1): the stable partition of logical
  * pages [0, ceil(seq_len/16)) into FP8 (tags R, A) and TQ3 (tag S), logical
  * order kept.  list8/list3: device int32 [n_req][max_pages][2] =

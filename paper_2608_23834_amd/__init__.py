@@ -29,7 +29,8 @@ EXPORTS = ["kv_pool_bytes", "kv_pool_create", "kv_pool_destroy", "kv_append_fp8"
            "kv_pool_read_free_lists", "kv_pool_counters", "kv_pool_check_errors",
            "paged_attn_set_timing", "paged_attn_last_times", "mkv_stream_read",
            "paged_attn_decode_noalloc", "mkv_fp64_probe", "mkv_control_bf16_write",
-           "mkv_control_bf16_workspace_bytes", "mkv_control_bf16_decode", "mkv_status_string"]
+           "mkv_control_bf16_workspace_bytes", "mkv_control_bf16_decode",
+           "paged_attn_decode_cohort_key", "mkv_status_string"]
 
 _lib = None
 
@@ -93,6 +94,7 @@ def lib() -> ctypes.CDLL:
         L.paged_attn_last_times.argtypes = [vp, vp, vp]
         L.mkv_stream_read.argtypes = [vp, sz, vp, vp]
         L.mkv_fp64_probe.argtypes = [vp, vp, ctypes.c_int64, vp, vp, vp, vp]
+        L.paged_attn_decode_cohort_key.argtypes = [vp, i32, i32, i32, i32, vp]
         L.mkv_control_bf16_write.argtypes = [vp, i32, i32, i32, i32, i32, i32, vp, i32, vp, vp, i32,
                                              vp, vp, vp]
         L.mkv_control_bf16_workspace_bytes.argtypes = [i32, i32, i32, i32, i32, vp]
@@ -321,6 +323,64 @@ def mkv_fp64_probe(a, b, quot, root, half, stream=None):
     assert b.numel() == n and quot.numel() == n and root.numel() == n and half.numel() == n
     _check("mkv_fp64_probe", lib().mkv_fp64_probe(_ptr(a), _ptr(b), n, _ptr(quot), _ptr(root),
                                                   _ptr(half), _stream(stream)))
+
+
+def paged_attn_decode_cohort_key(pool: Pool, n_req, max_pages, fused_append=True, scoring=False):
+    key = ctypes.c_uint64()
+    _check("paged_attn_decode_cohort_key", lib().paged_attn_decode_cohort_key(
+        pool.handle, n_req, max_pages, int(bool(fused_append)), int(bool(scoring)),
+        ctypes.byref(key)))
+    return key.value
+
+
+class DecodeStepGraph:
+    """A decode step (per layer paged_attn_decode_append, then
+    kv_migrate_to_tq3) captured once into a HIP graph and replayed for later
+    steps of the same cohort (Sec. 4.1 graph path gated on a homogeneous
+    cohort).  The step reads its inputs from fixed device buffers -- q
+    [n_layers][n_req][Hq][d], k_new / v_new [n_layers][n_req][Hkv][d],
+    seq_lens_before [n_req], seq_lens_after [n_req], anchor mask -- which the
+    caller refills before each run.  run(key) replays only when `key` (the
+    cohort key of the step about to run) equals the key captured; otherwise it
+    fails closed to launching the same calls directly.  Host orchestration
+    only: the work is the library's kernels either way."""
+
+    def __init__(self, pool: Pool, block_table, tags, bufs: dict, out, lse, ws):
+        self.pool, self.bt, self.tags, self.b, self.out, self.lse, self.ws = (
+            pool, block_table, tags, bufs, out, lse, ws)
+        n_req, max_pages = block_table.shape
+        self.key = paged_attn_decode_cohort_key(pool, n_req, max_pages, True, False)
+        self.graph = None
+        self.replays = 0
+        self.direct = 0
+
+    def _step(self):
+        b = self.b
+        for layer in range(self.pool.n_layers):
+            paged_attn_decode_append(self.pool, layer, b["q"][layer], b["k_new"][layer],
+                                     b["v_new"][layer], self.bt, self.tags, b["seq_before"],
+                                     self.out[layer], self.lse[layer], self.ws)
+        kv_migrate_to_tq3(self.pool, self.bt, self.tags, b["anchor"], b["seq_after"])
+
+    def capture(self):
+        """Capture one step (every kernel instance it uses must have run once
+        on this device before, so that no launch attribute is set inside)."""
+        import torch
+        g = torch.cuda.CUDAGraph()
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.graph(g, stream=s):
+            self._step()
+        torch.cuda.current_stream().wait_stream(s)
+        self.graph = g
+
+    def run(self, key):
+        if self.graph is not None and key == self.key:
+            self.graph.replay()
+            self.replays += 1
+        else:
+            self._step()
+            self.direct += 1
 
 
 class ControlBf16:

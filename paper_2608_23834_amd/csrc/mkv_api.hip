@@ -320,6 +320,29 @@ mkv_status paged_attn_chunk(mkv_pool* pool, int32_t layer, int32_t n_req, const 
   return st;
 }
 
+mkv_status paged_attn_decode_cohort_key(const mkv_pool* pool, int32_t n_req, int32_t max_pages,
+                                        int32_t fused_append, int32_t scoring, uint64_t* key) {
+  if (!pool || !key || n_req < 1 || max_pages < 1) return MKV_EINVAL;
+  if (n_req > 65535 || max_pages > 1024 * 256) return MKV_ERANGE;
+  if (pool->n_tq3 < 1 || pool->timing) return MKV_ESTATE;
+  const DecodeShape sh = decode_shape(n_req, max_pages, pool->n_kv_heads, pool->recent);
+  const uint64_t fields[] = {(uint64_t)(uintptr_t)pool, (uint64_t)(uintptr_t)pool->ctrl,
+                             (uint64_t)pool->n_layers, (uint64_t)pool->n_q_heads,
+                             (uint64_t)pool->n_kv_heads, (uint64_t)pool->d, (uint64_t)PAGE,
+                             (uint64_t)pool->n_fp8, (uint64_t)pool->n_tq3, (uint64_t)pool->recent,
+                             (uint64_t)n_req, (uint64_t)max_pages, (uint64_t)sh.cunits,
+                             (uint64_t)sh.max_chunks, (uint64_t)(fused_append != 0),
+                             (uint64_t)(scoring != 0), 0x4d4b5631ull /* key format */};
+  uint64_t h = 1469598103934665603ull;  // FNV-1a over the fields' bytes
+  for (uint64_t f : fields)
+    for (int b = 0; b < 8; ++b) {
+      h ^= (f >> (8 * b)) & 0xFFu;
+      h *= 1099511628211ull;
+    }
+  *key = h;
+  return MKV_OK;
+}
+
 mkv_status kv_partition_pages(int32_t n_req, const int32_t* block_table, const uint8_t* tags,
                               int32_t max_pages, const int32_t* seq_lens, int32_t* list8,
                               int32_t* list3, int32_t* counts, hipStream_t stream) {
