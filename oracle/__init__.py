@@ -16,6 +16,8 @@ Paper passages followed (by section / equation / algorithm):
   * Sec. 4.1: compact per-format lists, TQ3 page contents, the canary's
     active-cache byte counter (``canary_bytes``)
   * Sec. 4.3: FP8 -> TQ3 normalize-rotate-pack (``tq3_encode``)
+  * Sec. 3.1, Eqs. (score-partial), (score-global-weight), (attention-score):
+    page attention mass and its EWMA (``Pool.page_scores``)
 
 Every function is pinned by CPU tests against closed forms, library routines
 or brute force; none is "parity unpinned".
@@ -109,6 +111,7 @@ def _declare(L):
     L.orc_decode.argtypes = [vp, i32, i32, i32, vp, vp, vp, i32, vp, vp, vp]
     L.orc_chunk.argtypes = [vp, i32, i32, i32, vp, vp, vp, vp, i32, vp, vp, vp]
     L.orc_merge.argtypes = [i32, i32, vp, vp, vp, vp, vp]
+    L.orc_page_scores.argtypes = [vp, i32, i32, i32, vp, vp, vp, i32, vp, vp, f64, vp, vp, vp]
     L.orc_num_threads.restype = i32
     L.orc_num_threads.argtypes = []
 
@@ -327,6 +330,22 @@ class Pool:
         lib().orc_decode(self._c(), layer, n_req, self.n_q_heads, _p(q), _p(block_table), _p(tags),
                          max_pages, _p(sl), _p(out), _p(lse))
         return out, lse
+
+    def page_scores(self, layer, q_bf16, block_table, tags, seq_lens, head_mask, beta, a):
+        """Attention-score collector (Sec. 3.1 Eqs. score-partial ..
+        attention-score): updates `a` [n_req][max_pages] in place; returns
+        (q~ [n_req][max_pages][Hq], r [n_req][max_pages])."""
+        n_req, max_pages = block_table.shape
+        q = np.ascontiguousarray(q_bf16, dtype=np.uint16)
+        sl = np.ascontiguousarray(seq_lens, dtype=np.int32)
+        hm = np.ascontiguousarray(head_mask, dtype=np.uint8)
+        assert a.dtype == np.float64 and a.flags.c_contiguous and a.shape == (n_req, max_pages)
+        qn = np.full((n_req, max_pages, self.n_q_heads), np.nan)
+        rr = np.full((n_req, max_pages), np.nan)
+        lib().orc_page_scores(self._c(), layer, n_req, self.n_q_heads, _p(q), _p(block_table),
+                              _p(tags), max_pages, _p(sl), _p(hm), float(beta), _p(a), _p(qn),
+                              _p(rr))
+        return qn, rr
 
     def chunk(self, layer, q_bf16, cu_q, block_table, tags, seq_lens, sample_stride=1):
         n_req, max_pages = block_table.shape

@@ -903,6 +903,72 @@ void orc_decode(const orc_pool* P, int layer, int n_req, int n_q_heads, const ui
     }
 }
 
+/* Attention-score collector (Sec. 3.1, Eqs. score-partial, score-global-weight
+ * and attention-score).  For query head h of request r, the globally
+ * normalized mass of logical page p is the softmax weight of its tokens,
+ *   q_{h,p} = sum_{i in p} exp(s_i - m) / sum_i exp(s_i - m)
+ * (the partition form w_j rho_p^{(j)} of the equations is the same quantity
+ * for any partition j of the tokens).  The collector conditions on
+ * page-addressable mass, q~_{h,p} = q_{h,p} / sum_p' q_{h,p'}, averages it over
+ * the sampled heads (head_mask[hq] != 0), r_p = mean_h q~_{h,p}, and updates
+ * a_p = beta a_p + (1 - beta) r_p for the request's pages p < ceil(seq_len /
+ * 16) in place (other entries unchanged).  qn_out [n_req][max_pages][Hq]
+ * (q~, pages past the length left as they are) and r_out [n_req][max_pages]
+ * are written when non-null. */
+void orc_page_scores(const orc_pool* P, int layer, int n_req, int n_q_heads, const uint16_t* q,
+                     const int32_t* bt, const uint8_t* tags, int max_pages, const int32_t* seq_lens,
+                     const uint8_t* head_mask, double beta, double* a_inout, double* qn_out,
+                     double* r_out) {
+  int d = P->d, H = P->n_kv_heads, G = n_q_heads / H;
+  int n_sampled = 0;
+  for (int hq = 0; hq < n_q_heads; ++hq) n_sampled += head_mask[hq] != 0;
+#pragma omp parallel for schedule(dynamic)
+  for (int r = 0; r < n_req; ++r) {
+    int n = seq_lens[r], np = (n + ORC_PAGE - 1) / ORC_PAGE;
+    double* kh = (double*)malloc(sizeof(double) * (size_t)(n > 0 ? n : 1) * d);
+    double* vh = (double*)malloc(sizeof(double) * (size_t)(n > 0 ? n : 1) * d);
+    double* s = (double*)malloc(sizeof(double) * (size_t)(n > 0 ? n : 1));
+    double* qp = (double*)malloc(sizeof(double) * (size_t)(np > 0 ? np : 1));
+    double* racc = (double*)calloc((size_t)(np > 0 ? np : 1), sizeof(double));
+    double* qd = (double*)malloc(sizeof(double) * d);
+    for (int h = 0; h < H; ++h) {
+      orc_reconstruct(P, layer, r, h, bt, tags, max_pages, n, kh, vh);
+      for (int j = 0; j < G; ++j) {
+        int hq = h * G + j;
+        for (int c = 0; c < d; ++c) qd[c] = bf16_to_f64(q[((int64_t)r * n_q_heads + hq) * d + c]);
+        double m = -INFINITY;
+        for (int t = 0; t < n; ++t) {
+          double acc = 0.0;
+          for (int c = 0; c < d; ++c) acc += qd[c] * kh[(int64_t)t * d + c];
+          s[t] = acc / sqrt((double)d);
+          if (s[t] > m) m = s[t];
+        }
+        double l = 0.0;
+        for (int t = 0; t < n; ++t) l += exp(s[t] - m);
+        double z = 0.0;
+        for (int p = 0; p < np; ++p) {
+          double mass = 0.0;
+          for (int t = p * ORC_PAGE; t < n && t < (p + 1) * ORC_PAGE; ++t) mass += exp(s[t] - m);
+          qp[p] = mass / l;
+          z += qp[p];
+        }
+        for (int p = 0; p < np; ++p) {
+          double qn = qp[p] / z;
+          if (qn_out) qn_out[((int64_t)r * max_pages + p) * n_q_heads + hq] = qn;
+          if (head_mask[hq]) racc[p] += qn;
+        }
+      }
+    }
+    for (int p = 0; p < np; ++p) {
+      double rp = n_sampled ? racc[p] / n_sampled : 0.0;
+      if (r_out) r_out[(int64_t)r * max_pages + p] = rp;
+      double* ap = &a_inout[(int64_t)r * max_pages + p];
+      *ap = beta * *ap + (1.0 - beta) * rp;
+    }
+    free(kh); free(vh); free(s); free(qp); free(racc); free(qd);
+  }
+}
+
 /* Chunk (causal): request r has n_r = cu_q[r+1]-cu_q[r] queries; query i sits
  * at position seq_len - n_r + i and sees keys t <= that position.  The chunk's
  * own KV is read back from the pool (it was appended as FP8 beforehand).
