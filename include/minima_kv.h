@@ -262,6 +262,36 @@ mkv_status paged_attn_chunk(mkv_pool* pool, int32_t layer, int32_t n_req, const 
                             const uint8_t* tags, int32_t max_pages, const int32_t* seq_lens,
                             float* out, void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* Direct mixed-format attention-score collector (Sec. 3.1, Eqs.
+ * score-partial, score-global-weight and attention-score; Sec. 4.2: each
+ * split's local page mass is rescaled by its global softmax weight).
+ * paged_attn_decode_scores is paged_attn_decode (same arguments and outputs;
+ * lse is required) that also writes, for every logical page p <
+ * ceil(seq_lens[r] / 16) and query head hq, the page's local softmax mass and
+ * the reference exponent it was taken against:
+ *   page_mass[r][p][hq] = (sum_{i in p} 2^(s_i - m), m)  (fp32 pairs; s_i =
+ *   q.k_i log2(e) / sqrt(d), m the running maximum of the split that read the
+ *   page), other entries untouched.  page_mass: device float [n_req][max_pages]
+ *   [n_q_heads][2], 8-byte aligned.
+ * kv_page_scores_update then, for every request r and page p < ceil(seq_lens
+ * [r] / 16), forms the globally normalized mass q_{hq,p} = mass * 2^(m - lse
+ * [r][hq] / ln 2) (Eq. score-global-weight), conditions it on page-addressable
+ * mass, q~ = q / sum_p q, averages q~ over the sampled heads (head_mask
+ * [hq] != 0; device uint8 [n_q_heads]) into r_p, and updates scores[r][p] =
+ * beta * scores[r][p] + (1 - beta) * r_p in place (Eq. attention-score;
+ * device fp32 [n_req][max_pages]); r_out (same shape) and qn_out ([n_req]
+ * [max_pages][n_q_heads]) receive r and q~ when non-null.  seq_lens, lse
+ * and page_mass are those of the scoring decode; n_q_heads <= 256. */
+mkv_status paged_attn_decode_scores(mkv_pool* pool, int32_t layer, int32_t n_req,
+                                    const uint16_t* q, const int32_t* block_table,
+                                    const uint8_t* tags, int32_t max_pages,
+                                    const int32_t* seq_lens, float* out, float* lse, void* ws,
+                                    size_t ws_bytes, float* page_mass, hipStream_t stream);
+mkv_status kv_page_scores_update(const mkv_pool* pool, int32_t n_req, int32_t max_pages,
+                                 const int32_t* seq_lens, const float* lse,
+                                 const float* page_mass, const uint8_t* head_mask, float beta,
+                                 float* scores, float* r_out, float* qn_out, hipStream_t stream);
+
 /* Graph eligibility of a decode step (Sec. 4.1: the graph path is gated on a
  * homogeneous physical-cache cohort; other shapes, prefill or an
  * inconsistent cache state fail closed to the generic path).  A decode step

@@ -30,7 +30,8 @@ EXPORTS = ["kv_pool_bytes", "kv_pool_create", "kv_pool_destroy", "kv_append_fp8"
            "paged_attn_set_timing", "paged_attn_last_times", "mkv_stream_read",
            "paged_attn_decode_noalloc", "mkv_fp64_probe", "mkv_control_bf16_write",
            "mkv_control_bf16_workspace_bytes", "mkv_control_bf16_decode",
-           "paged_attn_decode_cohort_key", "mkv_status_string"]
+           "paged_attn_decode_cohort_key", "paged_attn_decode_scores", "kv_page_scores_update",
+           "mkv_status_string"]
 
 _lib = None
 
@@ -95,6 +96,10 @@ def lib() -> ctypes.CDLL:
         L.mkv_stream_read.argtypes = [vp, sz, vp, vp]
         L.mkv_fp64_probe.argtypes = [vp, vp, ctypes.c_int64, vp, vp, vp, vp]
         L.paged_attn_decode_cohort_key.argtypes = [vp, i32, i32, i32, i32, vp]
+        L.paged_attn_decode_scores.argtypes = [vp, i32, i32, vp, vp, vp, i32, vp, vp, vp, vp, sz,
+                                               vp, vp]
+        L.kv_page_scores_update.argtypes = [vp, i32, i32, vp, vp, vp, vp, ctypes.c_float, vp, vp,
+                                            vp, vp]
         L.mkv_control_bf16_write.argtypes = [vp, i32, i32, i32, i32, i32, i32, vp, i32, vp, vp, i32,
                                              vp, vp, vp]
         L.mkv_control_bf16_workspace_bytes.argtypes = [i32, i32, i32, i32, i32, vp]
@@ -231,6 +236,25 @@ def paged_attn_decode(pool: Pool, layer, q, block_table, tags, seq_lens, out, ls
         pool.handle, layer, n_req, _ptr(q), _ptr(block_table), _ptr(tags), max_pages,
         _ptr(seq_lens), _ptr(out), _ptr(lse), _ptr(ws), ws.numel() * ws.element_size(),
         _stream(stream)))
+
+
+def paged_attn_decode_scores(pool: Pool, layer, q, block_table, tags, seq_lens, out, lse, ws,
+                             page_mass, stream=None):
+    """paged_attn_decode that also writes each page's local mass and reference
+    exponent (page_mass: device float32 [n_req][max_pages][n_q_heads][2])."""
+    n_req, max_pages = block_table.shape
+    _check("paged_attn_decode_scores", lib().paged_attn_decode_scores(
+        pool.handle, layer, n_req, _ptr(q), _ptr(block_table), _ptr(tags), max_pages,
+        _ptr(seq_lens), _ptr(out), _ptr(lse), _ptr(ws), ws.numel() * ws.element_size(),
+        _ptr(page_mass), _stream(stream)))
+
+
+def kv_page_scores_update(pool: Pool, seq_lens, lse, page_mass, head_mask, beta, scores,
+                          r_out=None, qn_out=None, stream=None):
+    n_req, max_pages = scores.shape
+    _check("kv_page_scores_update", lib().kv_page_scores_update(
+        pool.handle, n_req, max_pages, _ptr(seq_lens), _ptr(lse), _ptr(page_mass),
+        _ptr(head_mask), float(beta), _ptr(scores), _ptr(r_out), _ptr(qn_out), _stream(stream)))
 
 
 DECODE_SCRATCH_BYTES = 32 * 1024 * 1024

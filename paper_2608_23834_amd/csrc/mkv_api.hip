@@ -217,6 +217,46 @@ mkv_status paged_attn_decode(mkv_pool* pool, int32_t layer, int32_t n_req, const
   return st;
 }
 
+mkv_status paged_attn_decode_scores(mkv_pool* pool, int32_t layer, int32_t n_req,
+                                    const uint16_t* q, const int32_t* block_table,
+                                    const uint8_t* tags, int32_t max_pages,
+                                    const int32_t* seq_lens, float* out, float* lse, void* ws,
+                                    size_t ws_bytes, float* page_mass, hipStream_t stream) {
+  if (!pool || !q || !block_table || !tags || !seq_lens || !out || !lse || !ws || !page_mass)
+    return MKV_EINVAL;
+  if (n_req < 1 || max_pages < 1) return MKV_EINVAL;
+  if (!aligned16(q) || !aligned16(out) || !aligned16(ws) || (reinterpret_cast<uintptr_t>(page_mass) & 7))
+    return MKV_EINVAL;
+  if (layer < 0 || layer >= pool->n_layers) return MKV_ERANGE;
+  if (n_req > 65535 || max_pages > 1024 * 256) return MKV_ERANGE;
+  if (ws_bytes < decode_ws_bytes(n_req, max_pages, pool->n_kv_heads, pool->group, pool->d, pool->recent))
+    return MKV_ENOMEM;
+  mkv_status st = hip_status(launch_decode(view_of(pool), layer, n_req, q, block_table, tags,
+                                           max_pages, seq_lens, out, lse, ws, stream,
+                                           pool->timing ? pool->timing_ev : nullptr, nullptr,
+                                           nullptr, nullptr, nullptr,
+                                           reinterpret_cast<float2*>(page_mass)));
+  if (st == MKV_OK) {
+    pool->decode_routes++;
+    if (pool->timing) pool->timed = 1;
+  }
+  return st;
+}
+
+mkv_status kv_page_scores_update(const mkv_pool* pool, int32_t n_req, int32_t max_pages,
+                                 const int32_t* seq_lens, const float* lse,
+                                 const float* page_mass, const uint8_t* head_mask, float beta,
+                                 float* scores, float* r_out, float* qn_out, hipStream_t stream) {
+  if (!pool || !seq_lens || !lse || !page_mass || !head_mask || !scores) return MKV_EINVAL;
+  if (n_req < 1 || max_pages < 1 || !(beta >= 0.0f && beta <= 1.0f)) return MKV_EINVAL;
+  if (reinterpret_cast<uintptr_t>(page_mass) & 7) return MKV_EINVAL;
+  if (pool->n_q_heads > 256) return MKV_EUNSUP;
+  if (n_req > 65535 || max_pages > 1024 * 256) return MKV_ERANGE;
+  return hip_status(launch_score_collect(n_req, pool->n_q_heads, max_pages, seq_lens, lse,
+                                         reinterpret_cast<const float2*>(page_mass), head_mask,
+                                         beta, scores, r_out, qn_out, stream));
+}
+
 mkv_status paged_attn_decode_noalloc(mkv_pool* pool, int32_t layer, int32_t n_req,
                                      const uint16_t* q, const int32_t* block_table,
                                      const uint8_t* tags, int32_t max_pages,

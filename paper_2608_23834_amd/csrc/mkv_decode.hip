@@ -89,6 +89,10 @@ struct DecodeArgs {
   // failed); then the FP8 free-list top after the call, or -1.  Written by
   // the scan, published by the merge kernel.
   int32_t* app_rec;
+  // SCORE instance: per (request, logical page, query head) the page's local
+  // softmax mass sum_i 2^(s_i - m) and the reference exponent m it was taken
+  // against (base 2, units of the scaled scores)
+  float2* page_mass;
 };
 
 // Cost of a request's pages: n_old pages wholly outside the Recent window and
@@ -220,8 +224,9 @@ __device__ __forceinline__ void p_operand(const float* p, bool row_is_b, half8& 
 // PAIR (query group of at most 8 heads): two pages share one score tile,
 // columns [0, 8) scoring page a and [8, 16) page b.  G6: at most six heads
 // (see head_of_col).
-template <int D, bool PAIR, bool G6, bool APP>
+template <int D, bool PAIR, bool G6, bool APP, bool SCORE = false>
 __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeArgs a) {
+  static_assert(!(APP && SCORE), "the scoring instance has no fused append");
   constexpr int NW = DecodeCfg<PAIR>::NW, NT = DecodeCfg<PAIR>::NT, SLOTS = DecodeCfg<PAIR>::SLOTS;
   constexpr int NCH = NCH_OF(PAIR);  // query heads a score tile holds
   constexpr int CL = D / 16, NDW = 3 * D / 128, CB = 3 * D / 32, NS = D / 32, QV = D / 64;
@@ -684,6 +689,16 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   };
   // TQ3 stages come first in the list, FP8 stages after them; the two loops
   // share the ring (a copy in flight may belong to either format).
+  // Score collector (SCORE instance, Sec. 3.1 Eq. score-partial): after the
+  // softmax step a lane's four weights are 2^(s - m_run) of tokens of the
+  // page its column scores; their sum over the column's 16 tokens is the
+  // page's local mass against m_run, stored with m_run for the collector,
+  // which rescales it by the global normalization (Eq. score-global-weight).
+  auto record_mass = [&](const float* w, int lp) {
+    const float ms = sum4rows((w[0] + w[1]) + (w[2] + w[3]));
+    if (lg == 0 && col_valid && lp < (S + PAGE - 1) / PAGE)
+      a.page_mass[((int64_t)r * mp + lp) * Hq + h * G + col_head] = make_float2(ms, st.m_run);
+  };
   int k_st = 0;  // stages begun by this wave; stage k sits in slot k % SLOTS
   while (jc < st3) {
     const int j = jc;
@@ -748,6 +763,7 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
     }
     STAGE_PRIO(2);
     softmax_step<D, NI>(st, sc, lg);
+    if constexpr (SCORE) record_mass(sc, col_b ? e.z : e.x);
     STAGE_PRIO(3);
     half8 pT, pTl;
     p_operand(sc, col_b, pT, pTl);
@@ -834,6 +850,7 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
     }
     STAGE_PRIO(2);
     softmax_step<D, NI>(st, sc, lg);
+    if constexpr (SCORE) record_mass(sc, col_b ? MASK_LP : e.x);
     STAGE_PRIO(3);
     half8 pT, pTl;
     p_operand(sc, col_b, pT, pTl);
@@ -1093,23 +1110,26 @@ static constexpr size_t lds_limit() {
   return 160 * 1024 - sizeof(int4) * MAX_CHUNK_PAGES - 3 * 16 * NW_MAX * sizeof(float) - 256;
 }
 
-template <bool APP>
+template <bool APP, bool SCORE = false>
 static const void* decode_instance(int d, bool pair, bool g6) {
   if (d == 256)
-    return g6 ? (const void*)decode_kernel<256, true, true, APP>
-                : pair ? (const void*)decode_kernel<256, true, false, APP>
-                       : (const void*)decode_kernel<256, false, false, APP>;
-  return g6 ? (const void*)decode_kernel<128, true, true, APP>
-              : pair ? (const void*)decode_kernel<128, true, false, APP>
-                     : (const void*)decode_kernel<128, false, false, APP>;
+    return g6 ? (const void*)decode_kernel<256, true, true, APP, SCORE>
+                : pair ? (const void*)decode_kernel<256, true, false, APP, SCORE>
+                       : (const void*)decode_kernel<256, false, false, APP, SCORE>;
+  return g6 ? (const void*)decode_kernel<128, true, true, APP, SCORE>
+              : pair ? (const void*)decode_kernel<128, true, false, APP, SCORE>
+                     : (const void*)decode_kernel<128, false, false, APP, SCORE>;
 }
 
 hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t* q,
                          const int32_t* bt, const uint8_t* tags, int max_pages,
                          const int32_t* seq_lens, float* out, float* lse, void* ws,
                          hipStream_t s, hipEvent_t* ev, const uint16_t* k_new,
-                         const uint16_t* v_new, int32_t* bt_w, uint8_t* tags_w) {
+                         const uint16_t* v_new, int32_t* bt_w, uint8_t* tags_w,
+                         float2* page_mass) {
   const bool app = k_new != nullptr;
+  const bool score = page_mass != nullptr;
+  if (app && score) return hipErrorInvalidValue;
   const DecodeShape sh = decode_shape(n_req, max_pages, P.n_kv_heads, P.recent);
   DecodeArgs a;
   a.P = P;
@@ -1130,6 +1150,7 @@ hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t
   a.v_new = v_new;
   a.bt_w = bt_w;
   a.tags_w = tags_w;
+  a.page_mass = page_mass;
   a.app_rec = app ? reinterpret_cast<int32_t*>(reinterpret_cast<uint8_t*>(ws) +
                                               decode_part_bytes(sh, n_req, P.n_kv_heads, P.group, P.d))
                   : nullptr;
@@ -1142,13 +1163,15 @@ hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t
   const size_t lds = qop_b + ring_b;  // the epilogue reuses each wave's ring slot
   if (lds > lds_limit()) return hipErrorInvalidValue;
   const bool g6 = pair && P.group <= 6;
-  const void* kern = app ? decode_instance<true>(P.d, pair, g6) : decode_instance<false>(P.d, pair, g6);
+  const void* kern = app     ? decode_instance<true>(P.d, pair, g6)
+                     : score ? decode_instance<false, true>(P.d, pair, g6)
+                             : decode_instance<false>(P.d, pair, g6);
   // the dynamic-LDS limit is raised once per kernel instance and device
   static std::atomic<uint32_t> attr_done[64];
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
-  const uint32_t bit = 1u << ((app ? 6 : 0) + (P.d == 256 ? 3 : 0) + (g6 ? 2 : pair ? 1 : 0));
+  const uint32_t bit = 1u << ((app ? 6 : score ? 12 : 0) + (P.d == 256 ? 3 : 0) + (g6 ? 2 : pair ? 1 : 0));
   if (dev < 0 || dev >= 64 || !(attr_done[dev].load() & bit)) {
     e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds_limit());
     if (e != hipSuccess) return e;
@@ -1171,6 +1194,79 @@ hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t
   const dim3 mblock(P.d / 4);
   return ev ? hipExtLaunchKernel(mk, mgrid, mblock, margs, 0, s, ev[2], ev[3], 0)
             : hipLaunchKernel(mk, mgrid, mblock, margs, 0, s);
+}
+
+// Attention-score collector (Sec. 3.1, Eqs. score-global-weight and
+// attention-score), after a scoring decode of the same call: one workgroup per
+// request.  The globally normalized mass of page p for query head hq is its
+// local mass rescaled by the global softmax normalization,
+// q = mass * 2^(m_ref - lse / ln 2) (lse of the merge); q~ = q / sum_p q over
+// the request's pages (page-addressable mass); r_p = the mean of q~ over the
+// sampled heads; a_p <- beta a_p + (1 - beta) r_p.  Pass 1 sums each sampled
+// head's masses (one wave per head, a pass over the pages); pass 2 forms r_p
+// and updates a_p (and writes q~ when asked).
+__global__ __launch_bounds__(256) void score_collect_kernel(int n_q_heads, int max_pages,
+                                                            const int32_t* seq_lens,
+                                                            const float* lse,
+                                                            const float2* page_mass,
+                                                            const uint8_t* head_mask, float beta,
+                                                            float* a_io, float* r_out,
+                                                            float* qn_out) {
+  constexpr int MAXH = 256;
+  __shared__ float s_inv[MAXH];  // 1 / sum_p q per head (0: not sampled)
+  __shared__ float s_l2[MAXH];   // lse in base 2 per head
+  __shared__ int s_ns;
+  const int r = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int S = seq_lens[r];
+  const int np = S >= 1 ? min((S + PAGE - 1) / PAGE, max_pages) : 0;
+  if (tid == 0) s_ns = 0;
+  __syncthreads();
+  const float kLog2e = 1.4426950408889634f;
+  for (int hq = tid; hq < n_q_heads; hq += 256) {
+    s_l2[hq] = lse[(int64_t)r * n_q_heads + hq] * kLog2e;
+    if (head_mask[hq]) atomicAdd(&s_ns, 1);
+  }
+  __syncthreads();
+  const bool want_q = qn_out != nullptr;
+  for (int hq = wv; hq < n_q_heads; hq += 4) {
+    float z = 0.0f;
+    if (head_mask[hq] || want_q) {
+      for (int p = lane; p < np; p += 64) {
+        const float2 mm = page_mass[((int64_t)r * max_pages + p) * n_q_heads + hq];
+        z += mm.x * exp2f(mm.y - s_l2[hq]);
+      }
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) z += __shfl_xor(z, o, 64);
+    }
+    if (lane == 0) s_inv[hq] = z > 0.0f ? 1.0f / z : 0.0f;
+  }
+  __syncthreads();
+  const int ns = s_ns;
+  for (int p = tid; p < np; p += 256) {
+    const float2* pm = page_mass + ((int64_t)r * max_pages + p) * n_q_heads;
+    float acc = 0.0f;
+    for (int hq = 0; hq < n_q_heads; ++hq) {
+      const bool smp = head_mask[hq] != 0;
+      if (!smp && !want_q) continue;
+      const float2 mm = pm[hq];
+      const float qn = mm.x * exp2f(mm.y - s_l2[hq]) * s_inv[hq];
+      if (want_q) qn_out[((int64_t)r * max_pages + p) * n_q_heads + hq] = qn;
+      if (smp) acc += qn;
+    }
+    const float rp = ns ? acc / (float)ns : 0.0f;
+    if (r_out) r_out[(int64_t)r * max_pages + p] = rp;
+    float* ap = a_io + (int64_t)r * max_pages + p;
+    *ap = beta * *ap + (1.0f - beta) * rp;
+  }
+}
+
+hipError_t launch_score_collect(int n_req, int n_q_heads, int max_pages, const int32_t* seq_lens,
+                                const float* lse, const float2* page_mass,
+                                const uint8_t* head_mask, float beta, float* a_io, float* r_out,
+                                float* qn_out, hipStream_t s) {
+  hipLaunchKernelGGL(score_collect_kernel, dim3(n_req), dim3(256), 0, s, n_q_heads, max_pages,
+                     seq_lens, lse, page_mass, head_mask, beta, a_io, r_out, qn_out);
+  return hipGetLastError();
 }
 
 }  // namespace mkv

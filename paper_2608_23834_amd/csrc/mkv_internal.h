@@ -83,7 +83,11 @@ hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t
                          const int32_t* seq_lens, float* out, float* lse, void* ws,
                          hipStream_t s, hipEvent_t* ev, const uint16_t* k_new = nullptr,
                          const uint16_t* v_new = nullptr, int32_t* bt_w = nullptr,
-                         uint8_t* tags_w = nullptr);
+                         uint8_t* tags_w = nullptr, float2* page_mass = nullptr);
+hipError_t launch_score_collect(int n_req, int n_q_heads, int max_pages, const int32_t* seq_lens,
+                                const float* lse, const float2* page_mass,
+                                const uint8_t* head_mask, float beta, float* a_io, float* r_out,
+                                float* qn_out, hipStream_t s);
 
 // mkv_control.hip (dense bf16 control, measurement only)
 size_t control_bf16_ws_bytes(int n_req, int max_pages, int n_kv_heads, int group, int d);
