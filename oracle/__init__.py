@@ -9,8 +9,9 @@ and shares no code with it.
 Paper passages followed (by section / equation / algorithm):
   * Sec. 2.1, Eq. (kv-per-token): bytes per live token (``kv_bytes_per_token``)
   * Sec. 3.1: tiers R/A/S, FP8 Recent/Anchor, 3-bit rotated Stale codec
-  * Alg. 1: Append, Retier and Promote transitions (``Pool.append``,
-    ``Pool.migrate``, ``Pool.promote``)
+  * Alg. 1: Append, Retier, Promote, SealPrefix and Finish transitions
+    (``Pool.append``, ``Pool.migrate``, ``Pool.promote``, ``Pool.acquire`` /
+    ``Pool.release``, ``Pool.finish``); Sec. 4.4 reference counts
   * Sec. 3.2, Eq. (effective-bits): effective rate (``effective_bits``)
   * Sec. 3.3, Eq. (softmax-merge): partials and merge (``merge``)
   * Sec. 4.1: compact per-format lists, TQ3 page contents, the canary's
@@ -103,6 +104,12 @@ def _declare(L):
     L.orc_append.argtypes = [vp, i32, i32, vp, vp, i32, vp, vp, vp, vp]
     L.orc_migrate.restype = i32
     L.orc_migrate.argtypes = [vp, i32, vp, vp, i32, vp, vp]
+    L.orc_pages_acquire.restype = i32
+    L.orc_pages_acquire.argtypes = [vp, i32, vp, vp]
+    L.orc_pages_release.restype = i32
+    L.orc_pages_release.argtypes = [vp, i32, vp, vp]
+    L.orc_request_finish.restype = i32
+    L.orc_request_finish.argtypes = [vp, i32, vp, vp, vp, i32]
     L.orc_promote.restype = i32
     L.orc_promote.argtypes = [vp, i32, vp, vp, i32, vp, vp]
     L.orc_tq3_reconstruct_f32.argtypes = [i32, vp, vp, vp, vp, vp, vp, vp, vp]
@@ -257,7 +264,8 @@ class _CPool(ctypes.Structure):
                 ("sigma", ctypes.c_void_p), ("fp8", ctypes.c_void_p),
                 ("fp8_scale", ctypes.c_void_p), ("tq3", ctypes.c_void_p),
                 ("fp8_stack", ctypes.c_void_p), ("fp8_top", ctypes.c_void_p),
-                ("tq3_stack", ctypes.c_void_p), ("tq3_top", ctypes.c_void_p)]
+                ("tq3_stack", ctypes.c_void_p), ("tq3_top", ctypes.c_void_p),
+                ("rc8", ctypes.c_void_p), ("rc3", ctypes.c_void_p)]
 
 
 class Pool:
@@ -280,12 +288,15 @@ class Pool:
         self.tq3_stack = np.ascontiguousarray(o3[::-1], dtype=np.int32)
         self.fp8_top = np.array([n_fp8], np.int32)
         self.tq3_top = np.array([n_tq3], np.int32)
+        self.rc8 = np.zeros(n_fp8, np.int32)  # references per page (0: free)
+        self.rc3 = np.zeros(max(n_tq3, 1), np.int32)
 
     def _c(self):
         s = _CPool(self.n_layers, self.n_kv_heads, self.d, self.n_fp8, self.n_tq3, self.recent,
                    self.sigma.ctypes.data, self.fp8.ctypes.data, self.fp8_scale.ctypes.data,
                    self.tq3.ctypes.data, self.fp8_stack.ctypes.data, self.fp8_top.ctypes.data,
-                   self.tq3_stack.ctypes.data, self.tq3_top.ctypes.data)
+                   self.tq3_stack.ctypes.data, self.tq3_top.ctypes.data,
+                   self.rc8.ctypes.data, self.rc3.ctypes.data)
         self._keep = s
         return ctypes.byref(s)
 
@@ -312,6 +323,25 @@ class Pool:
         pm = np.ascontiguousarray(promote_mask, dtype=np.uint8)
         return lib().orc_promote(self._c(), n_req, _p(block_table), _p(tags), max_pages, _p(pm),
                                  _p(sl))
+
+    def acquire(self, ids, tags) -> int:
+        """Alg. 1 SealPrefix / prefix attach: one more reference per listed page."""
+        ids = np.ascontiguousarray(ids, dtype=np.int32)
+        tg = np.ascontiguousarray(tags, dtype=np.uint8)
+        return lib().orc_pages_acquire(self._c(), len(ids), _p(ids), _p(tg))
+
+    def release(self, ids, tags) -> int:
+        """Prefix eviction: drop one reference per listed page (pages freed)."""
+        ids = np.ascontiguousarray(ids, dtype=np.int32)
+        tg = np.ascontiguousarray(tags, dtype=np.uint8)
+        return lib().orc_pages_release(self._c(), len(ids), _p(ids), _p(tg))
+
+    def finish(self, reqs, block_table, tags) -> int:
+        """Alg. 1 Finish of the listed requests (ascending): rows released, unmapped."""
+        n_req, max_pages = block_table.shape
+        rq = np.ascontiguousarray(reqs, dtype=np.int32)
+        return lib().orc_request_finish(self._c(), len(rq), _p(rq), _p(block_table), _p(tags),
+                                        max_pages)
 
     def reconstruct(self, layer, r, h, block_table, tags, n_tok):
         n_req, max_pages = block_table.shape

@@ -438,8 +438,12 @@ void orc_tq3_unpack(int d, const uint8_t* region, uint8_t* kcode, uint16_t* gamm
 }
 
 /* ------------------------------------------------------------------------ */
-/* Pool state machine (Alg. 1 Append / Retier; Sec. 3.1 tiers; Sec. 4.4 per- */
-/* kind free lists).                                                          */
+/* Pool state machine (Alg. 1 Append / Retier / Promote / SealPrefix /      */
+/* Finish; Sec. 3.1 tiers; Sec. 4.4 per-kind free lists, reference counts).  */
+/* Every mapped page carries a reference count: its block-table entries      */
+/* (request references) plus prefix-cache references.  A page with more     */
+/* than one reference is shared and immutable: Retier and Promote act on     */
+/* request-private pages (count 1) only.                                     */
 /* ------------------------------------------------------------------------ */
 typedef struct {
   int n_layers, n_kv_heads, d, n_fp8, n_tq3, recent;
@@ -451,6 +455,8 @@ typedef struct {
   int32_t* fp8_top;
   int32_t* tq3_stack;
   int32_t* tq3_top;
+  int32_t* rc8;       /* [n_fp8] references to each FP8 page (0: free) */
+  int32_t* rc3;       /* [n_tq3] references to each TQ3 page */
 } orc_pool;
 
 static uint8_t* fp8_region(const orc_pool* P, int layer, int id, int h) {
@@ -536,6 +542,7 @@ int orc_append(orc_pool* P, int layer, int n_req, int32_t* bt, uint8_t* tags, in
         *P->fp8_top -= 1;
         bt[i] = P->fp8_stack[*P->fp8_top];
         tags[i] = TAG_R;
+        P->rc8[bt[i]] = 1;
       }
     }
   }
@@ -617,7 +624,7 @@ int orc_migrate(orc_pool* P, int n_req, int32_t* bt, uint8_t* tags, int max_page
       int64_t i = (int64_t)r * max_pages + p;
       if (tags[i] != TAG_R) continue;
       int is_anchor = anchor ? anchor[i] != 0 : 0;
-      if (orc_tier(p, seq_lens[r], P->recent, is_anchor) == TAG_S) n_mig++;
+      if (orc_tier(p, seq_lens[r], P->recent, is_anchor) == TAG_S && P->rc8[bt[i]] == 1) n_mig++;
     }
   }
   if (n_mig > *P->tq3_top) return -1;
@@ -632,7 +639,8 @@ int orc_migrate(orc_pool* P, int n_req, int32_t* bt, uint8_t* tags, int max_page
       int is_anchor = anchor ? anchor[i] != 0 : 0;
       int z = orc_tier(p, seq_lens[r], P->recent, is_anchor);
       if (z == TAG_A) { tags[i] = TAG_A; continue; }
-      if (z != TAG_S) continue;
+      /* a shared (sealed) page stays as it is until it is private again */
+      if (z != TAG_S || P->rc8[bt[i]] != 1) continue;
       *P->tq3_top -= 1;
       mig[4 * k_mig] = r;
       mig[4 * k_mig + 1] = p;
@@ -675,6 +683,8 @@ int orc_migrate(orc_pool* P, int n_req, int32_t* bt, uint8_t* tags, int max_page
     int64_t i = (int64_t)mig[4 * j] * max_pages + mig[4 * j + 1];
     bt[i] = mig[4 * j + 3];
     tags[i] = TAG_S;
+    P->rc3[mig[4 * j + 3]] = 1;
+    P->rc8[mig[4 * j + 2]] = 0;
     P->fp8_stack[*P->fp8_top] = mig[4 * j + 2];
     *P->fp8_top += 1;
   }
@@ -730,7 +740,7 @@ int orc_promote(orc_pool* P, int n_req, int32_t* bt, uint8_t* tags, int max_page
     int np = (seq_lens[r] + ORC_PAGE - 1) / ORC_PAGE;
     for (int p = 0; p < np && p < max_pages; ++p) {
       int64_t i = (int64_t)r * max_pages + p;
-      if (tags[i] == TAG_S && promote[i]) n_pro++;
+      if (tags[i] == TAG_S && promote[i] && P->rc3[bt[i]] == 1) n_pro++;
     }
   }
   if (n_pro > *P->fp8_top) return -1;
@@ -740,7 +750,7 @@ int orc_promote(orc_pool* P, int n_req, int32_t* bt, uint8_t* tags, int max_page
     int np = (seq_lens[r] + ORC_PAGE - 1) / ORC_PAGE;
     for (int p = 0; p < np && p < max_pages; ++p) {
       int64_t i = (int64_t)r * max_pages + p;
-      if (!(tags[i] == TAG_S && promote[i])) continue;
+      if (!(tags[i] == TAG_S && promote[i] && P->rc3[bt[i]] == 1)) continue;
       *P->fp8_top -= 1;
       pro[4 * k] = r;
       pro[4 * k + 1] = p;
@@ -778,11 +788,99 @@ int orc_promote(orc_pool* P, int n_req, int32_t* bt, uint8_t* tags, int max_page
     int64_t i = (int64_t)pro[4 * j] * max_pages + pro[4 * j + 1];
     bt[i] = pro[4 * j + 3];
     tags[i] = TAG_A;
+    P->rc8[pro[4 * j + 3]] = 1;
+    P->rc3[pro[4 * j + 2]] = 0;
     P->tq3_stack[*P->tq3_top] = pro[4 * j + 2];
     *P->tq3_top += 1;
   }
   free(pro);
   return n_pro;
+}
+
+/* SealPrefix / prefix attach (Alg. 1 SealPrefix; Sec. 4.4): acquire one
+ * reference on each listed page, (id, tag) with tag R/A = FP8, S = TQ3.  Every
+ * listed page must be live (count >= 1) and its id in range; otherwise
+ * nothing changes and -1 is returned.  Duplicates acquire once each. */
+int orc_pages_acquire(orc_pool* P, int n, const int32_t* ids, const uint8_t* tg) {
+  for (int k = 0; k < n; ++k) {
+    int fp8 = tg[k] == TAG_R || tg[k] == TAG_A;
+    if (!fp8 && tg[k] != TAG_S) return -1;
+    int lim = fp8 ? P->n_fp8 : P->n_tq3;
+    if (ids[k] < 0 || ids[k] >= lim) return -1;
+    if ((fp8 ? P->rc8 : P->rc3)[ids[k]] < 1) return -1;
+  }
+  for (int k = 0; k < n; ++k) {
+    int fp8 = tg[k] == TAG_R || tg[k] == TAG_A;
+    (fp8 ? P->rc8 : P->rc3)[ids[k]] += 1;
+  }
+  return 0;
+}
+
+/* Release (Alg. 1 Finish / prefix eviction): drop one reference per listed
+ * entry, in list order; a page whose count reaches zero returns to the top
+ * of its free list at that moment (so a page listed twice is pushed at its
+ * second entry).  A page listed more often than it has references, a bad tag
+ * or id: nothing changes, -1.  Returns the number of pages freed. */
+int orc_pages_release(orc_pool* P, int n, const int32_t* ids, const uint8_t* tg) {
+  int32_t* need8 = (int32_t*)calloc((size_t)P->n_fp8 + 1, sizeof(int32_t));
+  int32_t* need3 = (int32_t*)calloc((size_t)P->n_tq3 + 1, sizeof(int32_t));
+  int bad = 0;
+  for (int k = 0; k < n && !bad; ++k) {
+    int fp8 = tg[k] == TAG_R || tg[k] == TAG_A;
+    if (!fp8 && tg[k] != TAG_S) { bad = 1; break; }
+    int lim = fp8 ? P->n_fp8 : P->n_tq3;
+    if (ids[k] < 0 || ids[k] >= lim) { bad = 1; break; }
+    int32_t* need = fp8 ? need8 : need3;
+    if (++need[ids[k]] > (fp8 ? P->rc8 : P->rc3)[ids[k]]) bad = 1;
+  }
+  free(need8);
+  free(need3);
+  if (bad) return -1;
+  int freed = 0;
+  for (int k = 0; k < n; ++k) {
+    int fp8 = tg[k] == TAG_R || tg[k] == TAG_A;
+    int32_t* rc = fp8 ? P->rc8 : P->rc3;
+    if (--rc[ids[k]] == 0) {
+      if (fp8) P->fp8_stack[(*P->fp8_top)++] = ids[k];
+      else P->tq3_stack[(*P->tq3_top)++] = ids[k];
+      freed++;
+    }
+  }
+  return freed;
+}
+
+/* Finish(q), Alg. 1: release every request reference of the listed requests'
+ * rows (each mapped entry, in ascending (request, page) order, as
+ * orc_pages_release), then unmap the rows (id -1, tag 0xFF).  reqs: the
+ * request indices, ascending.  Returns the pages freed, or -1 (nothing
+ * changed) on an inconsistent table. */
+int orc_request_finish(orc_pool* P, int n_fin, const int32_t* reqs, int32_t* bt, uint8_t* tags,
+                       int max_pages) {
+  int64_t n = 0;
+  for (int j = 0; j < n_fin; ++j)
+    for (int p = 0; p < max_pages; ++p) n += bt[(int64_t)reqs[j] * max_pages + p] >= 0;
+  int32_t* ids = (int32_t*)malloc(sizeof(int32_t) * (n + 1));
+  uint8_t* tg = (uint8_t*)malloc((size_t)n + 1);
+  int64_t k = 0;
+  for (int j = 0; j < n_fin; ++j)
+    for (int p = 0; p < max_pages; ++p) {
+      int64_t i = (int64_t)reqs[j] * max_pages + p;
+      if (bt[i] < 0) continue;
+      ids[k] = bt[i];
+      tg[k] = tags[i];
+      k++;
+    }
+  int freed = orc_pages_release(P, (int)n, ids, tg);
+  if (freed >= 0)
+    for (int j = 0; j < n_fin; ++j)
+      for (int p = 0; p < max_pages; ++p) {
+        int64_t i = (int64_t)reqs[j] * max_pages + p;
+        bt[i] = -1;
+        tags[i] = TAG_NONE;
+      }
+  free(ids);
+  free(tg);
+  return freed;
 }
 
 /* Compact per-format page lists (Sec. 4.1): stable partition of the logical
