@@ -57,6 +57,7 @@ typedef enum {
 #define MKV_DEVERR_NOT_RECENT 0x4u    /* append: tokens land in a mapped non-Recent page */
 #define MKV_DEVERR_RANGE 0x8u         /* a sequence length or page index is out of range */
 #define MKV_DEVERR_BAD_TAG 0x10u      /* attention found an unmapped page below seq_len */
+#define MKV_DEVERR_REFCOUNT 0x20u     /* acquire of a free page, release beyond its references */
 
 #define MKV_PAGE_SIZE 16
 #define MKV_ALL_LAYERS (-1)
@@ -171,6 +172,41 @@ mkv_status kv_migrate_to_tq3(mkv_pool* pool, int32_t n_req, int32_t* block_table
 mkv_status kv_promote_to_fp8(mkv_pool* pool, int32_t n_req, int32_t* block_table, uint8_t* tags,
                              int32_t max_pages, const uint8_t* promote_mask,
                              const int32_t* seq_lens, hipStream_t stream);
+
+/* Reference-counted pages and shared prefixes (Alg. 1 SealPrefix and Finish;
+ * Sec. 4.4 prefix reuse).  Every mapped page carries a count of the
+ * references to it: block-table entries of live requests plus prefix-cache
+ * references.  A page appended, migrated or promoted into has one reference
+ * (its request's).  A page with more than one reference is shared and
+ * immutable: kv_migrate_to_tq3 and kv_promote_to_fp8 leave it as it is (no
+ * re-encoding, no retag to Stale) until it is private again; decode reads it
+ * in place from every table that maps it.  Only full pages may be shared (the
+ * tail page a request still appends to must stay private).
+ *  - kv_pages_acquire: one more reference per listed page -- SealPrefix (the
+ *    cache's reference on a request's full pages) and attaching a cached
+ *    prefix to a new request (the caller writes the (id, tag) entries into
+ *    the request's block table, then acquires them).  ids: device int32 [n];
+ *    tags: device uint8 [n] (R or A: FP8 pool, S: TQ3 pool).  Every listed
+ *    page must be live; otherwise nothing changes and MKV_DEVERR_REFCOUNT is
+ *    set.
+ *  - kv_pages_release: one reference fewer per listed entry (prefix
+ *    eviction); a page whose count reaches zero returns to its free list, at
+ *    its last entry, pushes in entry order.  A page listed more often than it
+ *    has references, a bad tag or id: nothing changes, MKV_DEVERR_REFCOUNT.
+ *  - kv_request_finish: Finish(q) of the requests reqs (device int32
+ *    [n_fin], ascending, each < n_req): the mapped entries of their rows are
+ *    released as by kv_pages_release in ascending (request, page) order,
+ *    then the rows are unmapped (id -1, tag 0xFF).
+ *  - kv_pool_read_refcounts: the counts (host int32 [n_fp8_pages] and
+ *    [n_tq3_pages], either may be NULL); synchronizes. */
+mkv_status kv_pages_acquire(mkv_pool* pool, int32_t n, const int32_t* ids, const uint8_t* tags,
+                            hipStream_t stream);
+mkv_status kv_pages_release(mkv_pool* pool, int32_t n, const int32_t* ids, const uint8_t* tags,
+                            hipStream_t stream);
+mkv_status kv_request_finish(mkv_pool* pool, int32_t n_fin, const int32_t* reqs, int32_t n_req,
+                             int32_t* block_table, uint8_t* tags, int32_t max_pages,
+                             hipStream_t stream);
+mkv_status kv_pool_read_refcounts(mkv_pool* pool, int32_t* rc_fp8, int32_t* rc_tq3);
 
 /* Workspace bytes for paged_attn_decode and paged_attn_decode_append
  * (n_q_total = 0; the split partials, then n_req + 1 words the fused append

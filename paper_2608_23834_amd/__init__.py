@@ -21,9 +21,10 @@ TAG_R, TAG_A, TAG_S, TAG_NONE = 0, 1, 2, 0xFF
 STATUS = {0: "MKV_OK", 1: "MKV_EINVAL", 2: "MKV_EUNSUP", 3: "MKV_ENOMEM", 4: "MKV_ERANGE",
           5: "MKV_ESTATE", 6: "MKV_EHIP"}
 DEVERR = {"FP8_EXHAUSTED": 0x1, "TQ3_EXHAUSTED": 0x2, "NOT_RECENT": 0x4, "RANGE": 0x8,
-          "BAD_TAG": 0x10}
+          "BAD_TAG": 0x10, "REFCOUNT": 0x20}
 EXPORTS = ["kv_pool_bytes", "kv_pool_create", "kv_pool_destroy", "kv_append_fp8",
-           "kv_migrate_to_tq3", "kv_promote_to_fp8", "paged_attn_workspace_bytes", "paged_attn_workspace_init",
+           "kv_migrate_to_tq3", "kv_promote_to_fp8", "kv_pages_acquire", "kv_pages_release",
+           "kv_request_finish", "kv_pool_read_refcounts", "paged_attn_workspace_bytes", "paged_attn_workspace_init",
            "paged_attn_decode", "paged_attn_decode_append", "paged_attn_chunk",
            "kv_partition_pages", "kv_pool_free_counts",
            "kv_pool_read_free_lists", "kv_pool_counters", "kv_pool_check_errors",
@@ -79,6 +80,10 @@ def lib() -> ctypes.CDLL:
         L.kv_append_fp8.argtypes = [vp, i32, i32, vp, vp, i32, vp, vp, i32, vp, vp, vp]
         L.kv_migrate_to_tq3.argtypes = [vp, i32, vp, vp, i32, vp, vp, vp]
         L.kv_promote_to_fp8.argtypes = [vp, i32, vp, vp, i32, vp, vp, vp]
+        L.kv_pages_acquire.argtypes = [vp, i32, vp, vp, vp]
+        L.kv_pages_release.argtypes = [vp, i32, vp, vp, vp]
+        L.kv_request_finish.argtypes = [vp, i32, vp, i32, vp, vp, i32, vp]
+        L.kv_pool_read_refcounts.argtypes = [vp, vp, vp]
         L.paged_attn_workspace_bytes.argtypes = [vp, i32, i32, i32, vp]
         L.paged_attn_workspace_init.argtypes = [vp, sz, vp]
         L.paged_attn_decode.argtypes = [vp, i32, i32, vp, vp, vp, i32, vp, vp, vp, vp, sz, vp]
@@ -209,6 +214,34 @@ def kv_promote_to_fp8(pool: Pool, block_table, tags, promote_mask, seq_lens, str
     _check("kv_promote_to_fp8", lib().kv_promote_to_fp8(
         pool.handle, n_req, _ptr(block_table), _ptr(tags), max_pages, _ptr(promote_mask),
         _ptr(seq_lens), _stream(stream)))
+
+
+def kv_pages_acquire(pool: Pool, ids, tags, stream=None):
+    """SealPrefix / prefix attach: one more reference per listed page (device tensors)."""
+    _check("kv_pages_acquire", lib().kv_pages_acquire(pool.handle, int(ids.numel()), _ptr(ids),
+                                                      _ptr(tags), _stream(stream)))
+
+
+def kv_pages_release(pool: Pool, ids, tags, stream=None):
+    """Prefix eviction: one reference fewer per listed page (device tensors)."""
+    _check("kv_pages_release", lib().kv_pages_release(pool.handle, int(ids.numel()), _ptr(ids),
+                                                      _ptr(tags), _stream(stream)))
+
+
+def kv_request_finish(pool: Pool, reqs, block_table, tags, stream=None):
+    """Finish(q) of the requests in `reqs` (device int32, ascending)."""
+    n_req, max_pages = block_table.shape
+    _check("kv_request_finish", lib().kv_request_finish(
+        pool.handle, int(reqs.numel()), _ptr(reqs), n_req, _ptr(block_table), _ptr(tags),
+        max_pages, _stream(stream)))
+
+
+def kv_pool_read_refcounts(pool: Pool):
+    r8 = np.zeros(pool.n_fp8, np.int32)
+    r3 = np.zeros(max(pool.n_tq3, 1), np.int32)
+    _check("kv_pool_read_refcounts", lib().kv_pool_read_refcounts(pool.handle, r8.ctypes.data,
+                                                                  r3.ctypes.data))
+    return r8, r3[: pool.n_tq3]
 
 
 def paged_attn_workspace_bytes(pool: Pool, n_req, max_pages, n_q_total=0):

@@ -131,6 +131,8 @@ mkv_status kv_pool_create(const mkv_pool_desc* desc, mkv_pool** out) {
     img[(size_t)p->cl.tq3_stack + i] = desc->tq3_order ? desc->tq3_order[p->n_tq3 - 1 - i] : p->n_tq3 - 1 - i;
   std::memcpy(reinterpret_cast<uint8_t*>(img.data()) + p->cl.sigma_bytes, desc->rot_signs,
               (size_t)p->d);
+  for (int i = 0; i < p->n_fp8; ++i) img[(size_t)p->cl.last8 + i] = -1;
+  for (int i = 0; i < p->n_tq3; ++i) img[(size_t)p->cl.last3 + i] = -1;
   hipError_t e = hipMemcpy(p->ctrl, img.data(), img.size() * 4, hipMemcpyHostToDevice);
   int dev = -1;
   if (e == hipSuccess) e = hipGetDevice(&dev);
@@ -179,6 +181,42 @@ mkv_status kv_promote_to_fp8(mkv_pool* pool, int32_t n_req, int32_t* block_table
   if (n_req < 1 || max_pages < 1) return MKV_EINVAL;
   return hip_status(launch_promote(view_of(pool), n_req, block_table, tags, max_pages, promote_mask,
                                    seq_lens, stream));
+}
+
+mkv_status kv_pages_acquire(mkv_pool* pool, int32_t n, const int32_t* ids, const uint8_t* tags,
+                            hipStream_t stream) {
+  if (!pool || n < 0 || (n > 0 && (!ids || !tags))) return MKV_EINVAL;
+  return hip_status(launch_pages_acquire(view_of(pool), n, ids, tags, stream));
+}
+
+mkv_status kv_pages_release(mkv_pool* pool, int32_t n, const int32_t* ids, const uint8_t* tags,
+                            hipStream_t stream) {
+  if (!pool || n < 0 || (n > 0 && (!ids || !tags))) return MKV_EINVAL;
+  return hip_status(launch_pages_release(view_of(pool), n, ids, tags, 0, nullptr, 0, nullptr,
+                                         nullptr, 1, stream));
+}
+
+mkv_status kv_request_finish(mkv_pool* pool, int32_t n_fin, const int32_t* reqs, int32_t n_req,
+                             int32_t* block_table, uint8_t* tags, int32_t max_pages,
+                             hipStream_t stream) {
+  if (!pool || !reqs || !block_table || !tags || n_fin < 0 || n_req < 1 || max_pages < 1)
+    return MKV_EINVAL;
+  if ((int64_t)n_fin * max_pages > ((int64_t)1 << 31) - 1) return MKV_ERANGE;
+  return hip_status(launch_pages_release(view_of(pool), 0, nullptr, nullptr, n_fin, reqs, n_req,
+                                         block_table, tags, max_pages, stream));
+}
+
+mkv_status kv_pool_read_refcounts(mkv_pool* pool, int32_t* rc_fp8, int32_t* rc_tq3) {
+  if (!pool) return MKV_EINVAL;
+  if (hipDeviceSynchronize() != hipSuccess) return MKV_EHIP;
+  if (rc_fp8 && hipMemcpy(rc_fp8, pool->ctrl + pool->cl.rc8, (size_t)pool->n_fp8 * 4,
+                          hipMemcpyDeviceToHost) != hipSuccess)
+    return MKV_EHIP;
+  if (rc_tq3 && pool->n_tq3 > 0 &&
+      hipMemcpy(rc_tq3, pool->ctrl + pool->cl.rc3, (size_t)pool->n_tq3 * 4, hipMemcpyDeviceToHost) !=
+          hipSuccess)
+    return MKV_EHIP;
+  return MKV_OK;
 }
 
 mkv_status paged_attn_workspace_bytes(const mkv_pool* pool, int32_t n_req, int32_t max_pages,

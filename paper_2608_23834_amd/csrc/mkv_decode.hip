@@ -990,7 +990,7 @@ __global__ __launch_bounds__(D / 4) void decode_merge_kernel(int G, int H, int m
                                                             float* lse, const int32_t* app_rec,
                                                             int32_t* bt_w, uint8_t* tags_w,
                                                             int max_pages, const int32_t* seq_lens,
-                                                            int32_t* ctrl) {
+                                                            int32_t* ctrl, int32_t* rc8) {
   constexpr int B = 32;
   static_assert(D / 4 >= B && D / 4 <= 64, "one wave; lane j holds slot j's (m, l)");
   const int n = blockIdx.x, h = blockIdx.y, r = blockIdx.z, c4 = threadIdx.x;
@@ -1001,6 +1001,7 @@ __global__ __launch_bounds__(D / 4) void decode_merge_kernel(int G, int H, int m
       const int64_t ix = (int64_t)r * max_pages + seq_lens[r] / PAGE;
       bt_w[ix] = id;
       tags_w[ix] = TAG_R;
+      rc8[id] = 1;  // one request reference
     }
     if (r == 0 && app_rec[gridDim.z] >= 0) ctrl[CTRL_FP8_TOP] = app_rec[gridDim.z];
   }
@@ -1189,7 +1190,8 @@ hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t
   const float* pa = a.partials;
   const int32_t* rec = a.app_rec;
   int32_t* ctrl = P.ctrl;
-  void* margs[] = {&G, &H, &mc, &pa, &out, &lse, &rec, &bt_w, &tags_w, &mpg, &seq_lens, &ctrl};
+  int32_t* rc8 = P.rc8;
+  void* margs[] = {&G, &H, &mc, &pa, &out, &lse, &rec, &bt_w, &tags_w, &mpg, &seq_lens, &ctrl, &rc8};
   const void* mk = P.d == 256 ? (const void*)decode_merge_kernel<256> : (const void*)decode_merge_kernel<128>;
   const dim3 mblock(P.d / 4);
   return ev ? hipExtLaunchKernel(mk, mgrid, mblock, margs, 0, s, ev[2], ev[3], 0)

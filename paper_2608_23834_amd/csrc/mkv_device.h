@@ -32,10 +32,13 @@ enum CtrlSlot {
 };
 constexpr int MIG_BLOCKS = 256;  // most workgroups of a migration plan
 struct CtrlLayout {
-  int64_t fp8_stack, tq3_stack, list, sigma_bytes, mig, total_words;
+  int64_t fp8_stack, tq3_stack, list, sigma_bytes, mig, rc8, rc3, occ8, occ3, last8, last3,
+      total_words;
 };
 // mig: migration-plan scratch, per-workgroup counts [MIG_BLOCKS], per-workgroup
-// error bits [MIG_BLOCKS], the TQ3 free-list top the plan started from
+// error bits [MIG_BLOCKS], the TQ3 free-list top the plan started from.
+// rc8 / rc3: references per FP8 / TQ3 page (0: free).  occ* / last*: release
+// scratch per page (occurrences in the call, last list index), 0 / -1 at rest.
 __host__ __device__ inline CtrlLayout ctrl_layout(int n_fp8, int n_tq3, int d) {
   CtrlLayout c;
   c.fp8_stack = CTRL_HEADER;
@@ -43,7 +46,13 @@ __host__ __device__ inline CtrlLayout ctrl_layout(int n_fp8, int n_tq3, int d) {
   c.list = c.tq3_stack + n_tq3;
   c.sigma_bytes = (c.list + 4LL * n_fp8) * 4;  // byte offset of int8 sigma[d]
   c.mig = c.list + 4LL * n_fp8 + (d + 3) / 4;
-  c.total_words = c.mig + 2LL * MIG_BLOCKS + 1;
+  c.rc8 = c.mig + 2LL * MIG_BLOCKS + 1;
+  c.rc3 = c.rc8 + n_fp8;
+  c.occ8 = c.rc3 + n_tq3;
+  c.occ3 = c.occ8 + n_fp8;
+  c.last8 = c.occ3 + n_tq3;
+  c.last3 = c.last8 + n_fp8;
+  c.total_words = c.last3 + n_tq3;
   return c;
 }
 

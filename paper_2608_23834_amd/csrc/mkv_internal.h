@@ -30,6 +30,12 @@ struct PoolView {
   int32_t* fp8_stack;
   int32_t* tq3_stack;
   int32_t* list;
+  int32_t* rc8;  // references per FP8 page
+  int32_t* rc3;  // references per TQ3 page
+  int32_t* occ8;
+  int32_t* occ3;
+  int32_t* last8;
+  int32_t* last3;
   int n_layers, n_kv_heads, d, group, n_fp8, n_tq3, recent;
 };
 
@@ -43,6 +49,12 @@ inline PoolView view_of(const mkv_pool* p) {
   v.fp8_stack = p->ctrl + p->cl.fp8_stack;
   v.tq3_stack = p->ctrl + p->cl.tq3_stack;
   v.list = p->ctrl + p->cl.list;
+  v.rc8 = p->ctrl + p->cl.rc8;
+  v.rc3 = p->ctrl + p->cl.rc3;
+  v.occ8 = p->ctrl + p->cl.occ8;
+  v.occ3 = p->ctrl + p->cl.occ3;
+  v.last8 = p->ctrl + p->cl.last8;
+  v.last3 = p->ctrl + p->cl.last3;
   v.n_layers = p->n_layers;
   v.n_kv_heads = p->n_kv_heads;
   v.d = p->d;
@@ -67,6 +79,12 @@ hipError_t launch_partition(int n_req, const int32_t* bt, const uint8_t* tags, i
 hipError_t launch_fill_zero(void* p, size_t bytes, hipStream_t s);
 hipError_t launch_fp64_probe(const double* a, const double* b, int64_t n, double* quot,
                              double* root, uint16_t* half, hipStream_t s);
+
+hipError_t launch_pages_acquire(const PoolView& P, int n, const int32_t* ids, const uint8_t* tags,
+                                hipStream_t s);
+hipError_t launch_pages_release(const PoolView& P, int n, const int32_t* ids, const uint8_t* tags,
+                                int n_fin, const int32_t* reqs, int n_req, int32_t* bt,
+                                uint8_t* bt_tags, int max_pages, hipStream_t s);
 
 // mkv_decode.hip
 struct DecodeShape {

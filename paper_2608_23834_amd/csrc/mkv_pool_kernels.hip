@@ -29,7 +29,7 @@ __global__ __launch_bounds__(1024) void append_plan_kernel(int n_req, int32_t* b
                                                            int max_pages, const int32_t* sb,
                                                            const int32_t* cu, int32_t* ctrl,
                                                            const int32_t* fp8_stack, int32_t* list,
-                                                           int n_fp8, int n_new_total) {
+                                                           int n_fp8, int n_new_total, int32_t* rc8) {
   __shared__ int scratch[32];
   __shared__ int s_err, s_need, s_touch;
   const int tid = threadIdx.x;
@@ -95,6 +95,7 @@ __global__ __launch_bounds__(1024) void append_plan_kernel(int n_req, int32_t* b
           id = fp8_stack[top - 1 - (base_alloc + rank)];
           bt[i] = id;
           tags[i] = TAG_R;
+          rc8[id] = 1;  // one request reference
         } else {
           id = bt[i];
         }
@@ -438,6 +439,7 @@ __global__ __launch_bounds__(64) void append_step_kernel(PoolView P, int layer_s
       const int64_t i = (int64_t)r * max_pages + p;
       bt[i] = ent_id[j];
       tags[i] = TAG_R;
+      P.rc8[ent_id[j]] = 1;
     }
   }
   if (lane == 0) P.ctrl[CTRL_FP8_TOP] = top - n_fresh;
@@ -465,8 +467,24 @@ constexpr int MIG_NT = 1024;
 constexpr int64_t MIG_BATCH = (int64_t)MIG_NT * MIG_KB;
 struct MigBatch {
   uint8_t tg[MIG_KB], an[MIG_KB];
-  int32_t id[MIG_KB], sl[MIG_KB], rq[MIG_KB], pg[MIG_KB];
+  int32_t id[MIG_KB], sl[MIG_KB], rq[MIG_KB], pg[MIG_KB], rc[MIG_KB];
 };
+// references of the entries' pages (shared pages are left alone by Retier and
+// Promote); 0 where the tag or id names no page
+struct RcView {
+  const int32_t* rc8;
+  const int32_t* rc3;
+  int n_fp8, n_tq3;
+};
+__device__ __forceinline__ void mig_load_rc(MigBatch& m, const RcView& v) {
+#pragma unroll
+  for (int j = 0; j < MIG_KB; ++j) {
+    const bool f8 = m.tg[j] == TAG_R || m.tg[j] == TAG_A, f3 = m.tg[j] == TAG_S;
+    const int id = m.id[j];
+    const bool ok = m.rq[j] >= 0 && id >= 0 && ((f8 && id < v.n_fp8) || (f3 && id < v.n_tq3));
+    m.rc[j] = ok ? (f8 ? v.rc8 : v.rc3)[id] : 0;
+  }
+}
 // entries f0 .. f0 + MIG_KB - 1: (request, page) stepped from one division
 __device__ __forceinline__ void mig_load(MigBatch& m, int64_t f0, int64_t N, int max_pages,
                                          const int32_t* bt, const uint8_t* tags,
@@ -490,7 +508,8 @@ __device__ __forceinline__ int mig_kind(const MigBatch& m, int j, int W) {
   if (m.rq[j] < 0) return 0;
   const int p = m.pg[j], S = m.sl[j];
   if (m.tg[j] != TAG_R || p >= (S + PAGE - 1) / PAGE || (p + 1) * PAGE > S - W) return 0;
-  return m.an[j] ? 2 : 1;
+  if (m.an[j]) return 2;
+  return m.rc[j] == 1 ? 1 : 0;  // a shared (sealed) page stays until it is private
 }
 
 // Count and validate the entries [e0, e1) (the whole workgroup); workgroup 0
@@ -499,7 +518,7 @@ __device__ __forceinline__ void mig_count_range(int b, int n_req, const int32_t*
                                                 const uint8_t* tags, int max_pages,
                                                 const uint8_t* anchor, const int32_t* seq_lens,
                                                 int W, int64_t e0, int64_t e1, int n_fp8,
-                                                int* s_cnt, int* s_err) {
+                                                int* s_cnt, int* s_err, const RcView& rv) {
   const int tid = threadIdx.x;
   int err = 0, cnt = 0;
   if (b == 0) {
@@ -511,12 +530,14 @@ __device__ __forceinline__ void mig_count_range(int b, int n_req, const int32_t*
   for (int64_t b0 = e0; b0 < e1; b0 += MIG_BATCH) {
     MigBatch m;
     mig_load(m, b0 + (int64_t)tid * MIG_KB, e1, max_pages, bt, tags, anchor, seq_lens);
+    mig_load_rc(m, rv);
 #pragma unroll
     for (int j = 0; j < MIG_KB; ++j) {
-      if (mig_kind(m, j, W) == 1) {
-        cnt++;
-        if (m.id[j] < 0 || m.id[j] >= n_fp8) err |= MKV_DEVERR_RANGE;
-      }
+      const int p = m.pg[j], S = m.sl[j];
+      const bool old_r = m.rq[j] >= 0 && m.tg[j] == TAG_R && p < (S + PAGE - 1) / PAGE &&
+                         (p + 1) * PAGE <= S - W && !m.an[j];
+      if (old_r && (m.id[j] < 0 || m.id[j] >= n_fp8)) err |= MKV_DEVERR_RANGE;
+      if (mig_kind(m, j, W) == 1) cnt++;
     }
   }
   if (cnt) atomicAdd(s_cnt, cnt);
@@ -525,7 +546,8 @@ __device__ __forceinline__ void mig_count_range(int b, int n_req, const int32_t*
 
 __global__ __launch_bounds__(MIG_NT) void migrate_count_kernel(
     int n_req, const int32_t* bt, const uint8_t* tags, int max_pages, const uint8_t* anchor,
-    const int32_t* seq_lens, int W, int32_t* ctrl, int32_t* mig, int64_t per_blk, int n_fp8) {
+    const int32_t* seq_lens, int W, int32_t* ctrl, int32_t* mig, int64_t per_blk, int n_fp8,
+    RcView rv) {
   __shared__ int s_err, s_cnt;
   const int tid = threadIdx.x, b = blockIdx.x;
   if (tid == 0) { s_err = 0; s_cnt = 0; }
@@ -533,7 +555,8 @@ __global__ __launch_bounds__(MIG_NT) void migrate_count_kernel(
   const int64_t N = (int64_t)n_req * max_pages;
   const int64_t e0 = (int64_t)b * per_blk, e1 = min(N, e0 + per_blk);
   __syncthreads();
-  mig_count_range(b, n_req, bt, tags, max_pages, anchor, seq_lens, W, e0, e1, n_fp8, &s_cnt, &s_err);
+  mig_count_range(b, n_req, bt, tags, max_pages, anchor, seq_lens, W, e0, e1, n_fp8, &s_cnt, &s_err,
+                  rv);
   __syncthreads();
   if (tid == 0) {
     mig[b] = s_cnt;
@@ -547,7 +570,7 @@ template <bool ONE>
 __global__ __launch_bounds__(MIG_NT) void migrate_list_kernel(
     int n_req, const int32_t* bt, uint8_t* tags, int max_pages, const uint8_t* anchor,
     const int32_t* seq_lens, int W, int32_t* ctrl, const int32_t* tq3_stack, int32_t* list,
-    const int32_t* mig, int64_t per_blk, int nb, int n_fp8) {
+    const int32_t* mig, int64_t per_blk, int nb, int n_fp8, RcView rv) {
   __shared__ int scratch[32];
   __shared__ int s_err, s_tot, s_pre;
   const int tid = threadIdx.x, b = blockIdx.x;
@@ -556,7 +579,7 @@ __global__ __launch_bounds__(MIG_NT) void migrate_list_kernel(
   const int top3 = ONE ? ctrl[CTRL_TQ3_TOP] : mig[2 * MIG_BLOCKS];
   if constexpr (ONE) {
     mig_count_range(0, n_req, bt, tags, max_pages, anchor, seq_lens, W, 0,
-                    (int64_t)n_req * max_pages, n_fp8, &s_tot, &s_err);
+                    (int64_t)n_req * max_pages, n_fp8, &s_tot, &s_err, rv);
   } else if (tid < nb) {
     const int c = mig[tid], e = mig[MIG_BLOCKS + tid];
     if (c) atomicAdd(&s_tot, c);
@@ -582,6 +605,7 @@ __global__ __launch_bounds__(MIG_NT) void migrate_list_kernel(
   for (int64_t b0 = e0; b0 < e1; b0 += MIG_BATCH) {
     MigBatch m;
     mig_load(m, b0 + (int64_t)tid * MIG_KB, e1, max_pages, bt, tags, anchor, seq_lens);
+    mig_load_rc(m, rv);
     int k[MIG_KB], c = 0;
 #pragma unroll
     for (int j = 0; j < MIG_KB; ++j) {
@@ -742,7 +766,8 @@ __global__ __launch_bounds__(256) void migrate_encode_kernel(PoolView P) {
 __global__ __launch_bounds__(1024) void migrate_publish_kernel(int32_t* bt, uint8_t* tags,
                                                                int max_pages, int32_t* ctrl,
                                                                int32_t* fp8_stack,
-                                                               const int32_t* list) {
+                                                               const int32_t* list, int32_t* rc8,
+                                                               int32_t* rc3) {
   if (ctrl[CTRL_ABORT]) return;
   const int n = ctrl[CTRL_NLIST];
   const int top = ctrl[CTRL_FP8_TOP];
@@ -751,6 +776,8 @@ __global__ __launch_bounds__(1024) void migrate_publish_kernel(int32_t* bt, uint
     const int64_t i = (int64_t)r * max_pages + p;
     bt[i] = dst;
     tags[i] = TAG_S;
+    rc3[dst] = 1;  // the request's reference moves to the new page
+    rc8[src] = 0;
     fp8_stack[top + k] = src;
   }
   __syncthreads();
@@ -769,13 +796,14 @@ __global__ __launch_bounds__(1024) void migrate_publish_kernel(int32_t* bt, uint
 // nothing.  The FP8 ids are popped here; the pages are built by the build
 // kernel and published after it (copy before publish).
 __device__ __forceinline__ bool pro_hit(const MigBatch& m, int j) {
-  if (m.rq[j] < 0 || m.tg[j] != TAG_S || !m.an[j]) return false;
+  if (m.rq[j] < 0 || m.tg[j] != TAG_S || !m.an[j] || m.rc[j] != 1) return false;
   return m.pg[j] < (m.sl[j] + PAGE - 1) / PAGE;
 }
 
 __global__ __launch_bounds__(MIG_NT) void promote_plan_kernel(
     int n_req, const int32_t* bt, const uint8_t* tags, int max_pages, const uint8_t* mask,
-    const int32_t* seq_lens, int32_t* ctrl, const int32_t* fp8_stack, int32_t* list, int n_tq3) {
+    const int32_t* seq_lens, int32_t* ctrl, const int32_t* fp8_stack, int32_t* list, int n_tq3,
+    RcView rv) {
   __shared__ int scratch[32];
   __shared__ int s_err, s_tot;
   const int tid = threadIdx.x;
@@ -790,11 +818,14 @@ __global__ __launch_bounds__(MIG_NT) void promote_plan_kernel(
   for (int64_t b0 = 0; b0 < N; b0 += MIG_BATCH) {
     MigBatch m;
     mig_load(m, b0 + (int64_t)tid * MIG_KB, N, max_pages, bt, tags, mask, seq_lens);
+    mig_load_rc(m, rv);
 #pragma unroll
     for (int j = 0; j < MIG_KB; ++j) {
+      if (m.rq[j] >= 0 && m.tg[j] == TAG_S && m.an[j] && m.pg[j] < (m.sl[j] + PAGE - 1) / PAGE &&
+          (m.id[j] < 0 || m.id[j] >= n_tq3))
+        err |= MKV_DEVERR_RANGE;
       if (pro_hit(m, j)) {
         cnt++;
-        if (m.id[j] < 0 || m.id[j] >= n_tq3) err |= MKV_DEVERR_RANGE;
       }
     }
   }
@@ -818,6 +849,7 @@ __global__ __launch_bounds__(MIG_NT) void promote_plan_kernel(
     MigBatch m;
     const int64_t f0 = b0 + (int64_t)tid * MIG_KB;
     mig_load(m, f0, N, max_pages, bt, tags, mask, seq_lens);
+    mig_load_rc(m, rv);
     bool hit[MIG_KB];
     int c = 0;
 #pragma unroll
@@ -963,7 +995,8 @@ __global__ __launch_bounds__(256) void promote_build_kernel(PoolView P) {
 __global__ __launch_bounds__(1024) void promote_publish_kernel(int32_t* bt, uint8_t* tags,
                                                                int max_pages, int32_t* ctrl,
                                                                int32_t* tq3_stack,
-                                                               const int32_t* list) {
+                                                               const int32_t* list, int32_t* rc8,
+                                                               int32_t* rc3) {
   if (ctrl[CTRL_ABORT]) return;
   const int n = ctrl[CTRL_NLIST];
   const int top = ctrl[CTRL_TQ3_TOP];
@@ -972,10 +1005,194 @@ __global__ __launch_bounds__(1024) void promote_publish_kernel(int32_t* bt, uint
     const int64_t i = (int64_t)le[0] * max_pages + le[1];
     bt[i] = le[3];
     tags[i] = TAG_A;
+    rc8[le[3]] = 1;
+    rc3[le[2]] = 0;
     tq3_stack[top + k] = le[2];
   }
   __syncthreads();
   if (threadIdx.x == 0) ctrl[CTRL_TQ3_TOP] = top + n;
+}
+
+// ===========================================================================
+// Reference counts: SealPrefix / prefix attach (acquire), eviction and Finish
+// (release)
+// ===========================================================================
+
+// (format, id) of a tagged entry: 0 FP8 (tags R, A), 1 TQ3 (tag S); false when
+// the tag names no pool or the id is out of range.
+__device__ __forceinline__ bool ref_of(uint8_t tag, int id, int n_fp8, int n_tq3, int& fmt) {
+  fmt = tag == TAG_S ? 1 : 0;
+  if (tag != TAG_R && tag != TAG_A && tag != TAG_S) return false;
+  return id >= 0 && id < (fmt ? n_tq3 : n_fp8);
+}
+
+// One workgroup: every listed page must be live (one reference or more);
+// otherwise nothing changes.  Then one more reference per entry.
+__global__ __launch_bounds__(1024) void pages_acquire_kernel(int n, const int32_t* ids,
+                                                             const uint8_t* tags, PoolView P) {
+  __shared__ int s_err;
+  const int tid = threadIdx.x;
+  if (tid == 0) s_err = 0;
+  __syncthreads();
+  for (int k = tid; k < n; k += blockDim.x) {
+    int fmt;
+    const int id = ids[k];
+    if (!ref_of(tags[k], id, P.n_fp8, P.n_tq3, fmt) || (fmt ? P.rc3 : P.rc8)[id] < 1)
+      atomicOr(&s_err, (int)MKV_DEVERR_REFCOUNT);
+  }
+  __syncthreads();
+  if (s_err) {
+    if (tid == 0) atomicOr(&P.ctrl[CTRL_ERR], s_err);
+    return;
+  }
+  for (int k = tid; k < n; k += blockDim.x) {
+    int fmt;
+    const int id = ids[k];
+    (void)ref_of(tags[k], id, P.n_fp8, P.n_tq3, fmt);
+    atomicAdd(&(fmt ? P.rc3 : P.rc8)[id], 1);
+  }
+}
+
+// One workgroup.  Entries: an explicit list (reqs == nullptr: ids/tags[n]) or
+// the rows of the listed requests (entry j * max_pages + p = row reqs[j], page
+// p, mapped entries only).  Each entry drops one reference, in entry order: a
+// page whose count reaches zero is pushed onto its free list at its last
+// entry.  Pass 1 counts each page's entries and finds its last one (scratch
+// occ / last, 0 / -1 at rest); a page with more entries than references, a
+// bad tag or id, or a bad request list fails the call (scratch restored,
+// nothing else changed).  Pass 2 walks the entries in order, ranks the
+// freeing ones with a block scan and applies the counts; table rows are then
+// unmapped.
+__global__ __launch_bounds__(1024) void pages_release_kernel(int n, const int32_t* ids,
+                                                             const uint8_t* tags, int n_fin,
+                                                             const int32_t* reqs, int n_req,
+                                                             int32_t* bt, uint8_t* bt_tags,
+                                                             int max_pages, PoolView P) {
+  __shared__ int scratch[32];
+  __shared__ int s_err;
+  const int tid = threadIdx.x;
+  const bool table = reqs != nullptr;
+  const int64_t N = table ? (int64_t)n_fin * max_pages : n;
+  if (tid == 0) s_err = 0;
+  __syncthreads();
+  if (table) {
+    for (int j = tid; j < n_fin; j += blockDim.x) {
+      const int r = reqs[j];
+      if (r < 0 || r >= n_req || (j > 0 && reqs[j - 1] >= r)) atomicOr(&s_err, (int)MKV_DEVERR_RANGE);
+    }
+    __syncthreads();
+    if (s_err) {
+      if (tid == 0) atomicOr(&P.ctrl[CTRL_ERR], s_err);
+      return;
+    }
+  }
+  // entry k -> (mapped, fmt, id); false for an unmapped table entry
+  auto entry = [&](int64_t k, int& fmt, int& id, bool& ok) {
+    uint8_t tg;
+    if (table) {
+      const int64_t i = (int64_t)reqs[k / max_pages] * max_pages + k % max_pages;
+      id = bt[i];
+      tg = bt_tags[i];
+      if (id < 0) {
+        ok = false;
+        return false;
+      }
+    } else {
+      id = ids[k];
+      tg = tags[k];
+    }
+    ok = ref_of(tg, id, P.n_fp8, P.n_tq3, fmt);
+    return true;
+  };
+  for (int64_t k = tid; k < N; k += blockDim.x) {
+    int fmt, id;
+    bool ok;
+    if (!entry(k, fmt, id, ok)) continue;
+    if (!ok) {
+      atomicOr(&s_err, (int)MKV_DEVERR_REFCOUNT);
+      continue;
+    }
+    atomicAdd(&(fmt ? P.occ3 : P.occ8)[id], 1);
+    atomicMax(&(fmt ? P.last3 : P.last8)[id], (int)k);
+  }
+  __syncthreads();
+  for (int64_t k = tid; k < N; k += blockDim.x) {
+    int fmt, id;
+    bool ok;
+    if (!entry(k, fmt, id, ok) || !ok) continue;
+    if ((fmt ? P.occ3 : P.occ8)[id] > (fmt ? P.rc3 : P.rc8)[id]) atomicOr(&s_err, (int)MKV_DEVERR_REFCOUNT);
+  }
+  __syncthreads();
+  const int err = s_err;
+  if (err) {
+    for (int64_t k = tid; k < N; k += blockDim.x) {
+      int fmt, id;
+      bool ok;
+      if (!entry(k, fmt, id, ok) || !ok) continue;
+      (fmt ? P.occ3 : P.occ8)[id] = 0;
+      (fmt ? P.last3 : P.last8)[id] = -1;
+    }
+    if (tid == 0) atomicOr(&P.ctrl[CTRL_ERR], err);
+    return;
+  }
+  const int top8 = P.ctrl[CTRL_FP8_TOP], top3 = P.ctrl[CTRL_TQ3_TOP];
+  int base8 = 0, base3 = 0;
+  for (int64_t b0 = 0; b0 < N; b0 += blockDim.x) {
+    const int64_t k = b0 + tid;
+    int fmt = 0, id = 0;
+    bool ok = false;
+    bool last = false, freed = false;
+    if (k < N && entry(k, fmt, id, ok) && ok) {
+      int32_t* lastv = fmt ? P.last3 : P.last8;
+      last = lastv[id] == (int)k;
+      if (last) {
+        int32_t* rc = fmt ? P.rc3 : P.rc8;
+        int32_t* occ = fmt ? P.occ3 : P.occ8;
+        const int left = rc[id] - occ[id];
+        freed = left == 0;
+        rc[id] = left;
+        occ[id] = 0;
+        lastv[id] = -1;
+      }
+    }
+    // ranks of the freeing entries, FP8 in the low and TQ3 in the high half
+    const int v = freed ? (fmt ? (1 << 16) : 1) : 0;
+    int tot;
+    const int pre = block_excl_scan(v, scratch, &tot);
+    if (freed) {
+      if (fmt) P.tq3_stack[top3 + base3 + (pre >> 16)] = id;
+      else P.fp8_stack[top8 + base8 + (pre & 0xFFFF)] = id;
+    }
+    base8 += tot & 0xFFFF;
+    base3 += tot >> 16;
+  }
+  __syncthreads();
+  if (table)
+    for (int64_t k = tid; k < N; k += blockDim.x) {
+      const int64_t i = (int64_t)reqs[k / max_pages] * max_pages + k % max_pages;
+      bt[i] = -1;
+      bt_tags[i] = TAG_NONE;
+    }
+  if (tid == 0) {
+    P.ctrl[CTRL_FP8_TOP] = top8 + base8;
+    P.ctrl[CTRL_TQ3_TOP] = top3 + base3;
+  }
+}
+
+hipError_t launch_pages_acquire(const PoolView& P, int n, const int32_t* ids, const uint8_t* tags,
+                                hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(pages_acquire_kernel, dim3(1), dim3(1024), 0, s, n, ids, tags, P);
+  return hipGetLastError();
+}
+
+hipError_t launch_pages_release(const PoolView& P, int n, const int32_t* ids, const uint8_t* tags,
+                                int n_fin, const int32_t* reqs, int n_req, int32_t* bt,
+                                uint8_t* bt_tags, int max_pages, hipStream_t s) {
+  if ((reqs ? n_fin : n) == 0) return hipSuccess;
+  hipLaunchKernelGGL(pages_release_kernel, dim3(1), dim3(1024), 0, s, n, ids, tags, n_fin, reqs,
+                     n_req, bt, bt_tags, max_pages, P);
+  return hipGetLastError();
 }
 
 // ===========================================================================
@@ -1055,7 +1272,7 @@ hipError_t launch_append(const PoolView& P, int layer, int n_req, int32_t* bt, u
     return hipGetLastError();
   }
   hipLaunchKernelGGL(append_plan_kernel, dim3(1), dim3(1024), 0, s, n_req, bt, tags, max_pages, sb,
-                     cu, P.ctrl, P.fp8_stack, P.list, P.n_fp8, n_new_total);
+                     cu, P.ctrl, P.fp8_stack, P.list, P.n_fp8, n_new_total, P.rc8);
   // upper bound on listed pages: new tokens / 16 + one partial page per request
   const int64_t pages_bound = (int64_t)n_new_total / PAGE + n_req + 1;
   const int grid = grid_for((pages_bound * n_lcall * P.n_kv_heads * 2 + 3) / 4, 8192);
@@ -1077,16 +1294,17 @@ hipError_t launch_migrate(const PoolView& P, int n_req, int32_t* bt, uint8_t* ta
   const int nb = (int)((n_bat + bat_per - 1) / bat_per);
   const int64_t per_blk = bat_per * MIG_BATCH;
   int32_t* mig = P.ctrl + ctrl_layout(P.n_fp8, P.n_tq3, P.d).mig;
+  const RcView rv = {P.rc8, P.rc3, P.n_fp8, P.n_tq3};
   if (nb == 1) {
     hipLaunchKernelGGL(migrate_list_kernel<true>, dim3(1), dim3(MIG_NT), 0, s, n_req, bt, tags,
                        max_pages, anchor, seq_lens, P.recent, P.ctrl, P.tq3_stack, P.list, mig,
-                       per_blk, nb, P.n_fp8);
+                       per_blk, nb, P.n_fp8, rv);
   } else {
     hipLaunchKernelGGL(migrate_count_kernel, dim3(nb), dim3(MIG_NT), 0, s, n_req, bt, tags,
-                       max_pages, anchor, seq_lens, P.recent, P.ctrl, mig, per_blk, P.n_fp8);
+                       max_pages, anchor, seq_lens, P.recent, P.ctrl, mig, per_blk, P.n_fp8, rv);
     hipLaunchKernelGGL(migrate_list_kernel<false>, dim3(nb), dim3(MIG_NT), 0, s, n_req, bt, tags,
                        max_pages, anchor, seq_lens, P.recent, P.ctrl, P.tq3_stack, P.list, mig,
-                       per_blk, nb, P.n_fp8);
+                       per_blk, nb, P.n_fp8, rv);
   }
   int64_t bound = (int64_t)n_req * max_pages;
   if (bound > P.n_fp8) bound = P.n_fp8;
@@ -1096,14 +1314,15 @@ hipError_t launch_migrate(const PoolView& P, int n_req, int32_t* bt, uint8_t* ta
   else
     hipLaunchKernelGGL(migrate_encode_kernel<128>, dim3(grid), dim3(256), 0, s, P);
   hipLaunchKernelGGL(migrate_publish_kernel, dim3(1), dim3(1024), 0, s, bt, tags, max_pages, P.ctrl,
-                     P.fp8_stack, P.list);
+                     P.fp8_stack, P.list, P.rc8, P.rc3);
   return hipGetLastError();
 }
 
 hipError_t launch_promote(const PoolView& P, int n_req, int32_t* bt, uint8_t* tags, int max_pages,
                           const uint8_t* mask, const int32_t* seq_lens, hipStream_t s) {
   hipLaunchKernelGGL(promote_plan_kernel, dim3(1), dim3(MIG_NT), 0, s, n_req, bt, tags, max_pages,
-                     mask, seq_lens, P.ctrl, P.fp8_stack, P.list, P.n_tq3);
+                     mask, seq_lens, P.ctrl, P.fp8_stack, P.list, P.n_tq3,
+                     RcView{P.rc8, P.rc3, P.n_fp8, P.n_tq3});
   int64_t bound = (int64_t)n_req * max_pages;
   if (bound > P.n_fp8) bound = P.n_fp8;
   if (bound > P.n_tq3) bound = P.n_tq3;
@@ -1113,7 +1332,7 @@ hipError_t launch_promote(const PoolView& P, int n_req, int32_t* bt, uint8_t* ta
   else
     hipLaunchKernelGGL(promote_build_kernel<128>, dim3(grid), dim3(256), 0, s, P);
   hipLaunchKernelGGL(promote_publish_kernel, dim3(1), dim3(1024), 0, s, bt, tags, max_pages, P.ctrl,
-                     P.tq3_stack, P.list);
+                     P.tq3_stack, P.list, P.rc8, P.rc3);
   return hipGetLastError();
 }
 

@@ -119,6 +119,52 @@ class Twin:
             assert n >= 0
             return n
 
+    # -- reference counts and shared prefixes (Alg. 1 SealPrefix / Finish) --
+    def acquire(self, ids, tags):
+        import paper_2608_23834_amd as mk
+        torch = _torch()
+        ids = np.ascontiguousarray(ids, np.int32)
+        tags = np.ascontiguousarray(tags, np.uint8)
+        mk.kv_pages_acquire(self.gpu, torch.from_numpy(ids).cuda(), torch.from_numpy(tags).cuda())
+        if self.orc is not None:
+            assert self.orc.acquire(ids, tags) == 0
+
+    def release(self, ids, tags):
+        import paper_2608_23834_amd as mk
+        torch = _torch()
+        ids = np.ascontiguousarray(ids, np.int32)
+        tags = np.ascontiguousarray(tags, np.uint8)
+        mk.kv_pages_release(self.gpu, torch.from_numpy(ids).cuda(), torch.from_numpy(tags).cuda())
+        if self.orc is not None:
+            return self.orc.release(ids, tags)
+
+    def finish(self, reqs):
+        import paper_2608_23834_amd as mk
+        torch = _torch()
+        rq = np.ascontiguousarray(reqs, np.int32)
+        mk.kv_request_finish(self.gpu, torch.from_numpy(rq).cuda(), self.bt, self.tags)
+        if self.orc is not None:
+            n = self.orc.finish(rq, self.obt, self.otags)
+            assert n >= 0
+        for r in reqs:
+            self.cur[r] = 0
+
+    def set_rows(self, r, pages, ids, tags):
+        """Write block-table entries of request r (both sides), e.g. a cached prefix."""
+        torch = _torch()
+        self.bt[r, pages] = torch.tensor(np.asarray(ids, np.int32), device="cuda")
+        self.tags[r, pages] = torch.tensor(np.asarray(tags, np.uint8), device="cuda")
+        if self.orc is not None:
+            self.obt[r, pages] = ids
+            self.otags[r, pages] = tags
+
+    def check_refcounts(self):
+        import paper_2608_23834_amd as mk
+        r8, r3 = mk.kv_pool_read_refcounts(self.gpu)
+        assert np.array_equal(r8, self.orc.rc8[: self.n_fp8]), "fp8 reference counts"
+        assert np.array_equal(r3, self.orc.rc3[: self.n_tq3]), "tq3 reference counts"
+        return r8, r3
+
     def _ws(self, ws_fill):
         import paper_2608_23834_amd as mk
         ws = mk.workspace(self.gpu, self.n_req, self.max_pages)
