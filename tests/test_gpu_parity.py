@@ -264,6 +264,37 @@ def test_decode_append_fused_full_size(torch_cuda):
     assert (tw.otags == 0).sum() == 2 * 129
 
 
+def test_decode_append_many_requests(torch_cuda):
+    """The fused decode step with many requests: 24 ragged requests (d = 256,
+    two layers; fresh pages opened for several requests in one launch)
+    against the oracle's separate append and decode, bit-exact state; and the
+    fail-closed contract (zero outputs, lse -inf, no state change) for 20
+    requests when the free list cannot hold their fresh pages."""
+    import paper_2608_23834_amd as mk
+    torch = torch_cuda
+    rng = np.random.default_rng(24)
+    lens = [int(x) for x in rng.integers(0, 900, 24)]
+    lens[:3] = [0, 1, 16]
+    tw = _fused_steps(wl.workload(2), lens, n_layers=2, n_steps=6, recent=64, check_every=3)
+    assert tw.n_req > 16
+    # free list too short for the fresh pages of one step: nothing changes
+    d, Hq, n = 128, 2, 20
+    gp = mk.Pool(1, Hq, 1, d, 8, 2, 16, np.ones(d, np.int8))
+    bt = torch.full((n, 4), -1, dtype=torch.int32, device="cuda")
+    tg = torch.full((n, 4), 0xFF, dtype=torch.uint8, device="cuda")
+    ws = mk.workspace(gp, n, 4)
+    q = torch.from_numpy(rng.integers(0x3c00, 0x3f00, (n, Hq, d)).astype(np.int16)).cuda()
+    kv = torch.from_numpy(rng.integers(0x3c00, 0x3f00, (n, 1, d)).astype(np.int16)).cuda()
+    out = torch.full((n, Hq, d), 7.0, device="cuda")
+    lse = torch.full((n, Hq), 7.0, device="cuda")
+    mk.paged_attn_decode_append(gp, 0, q, kv, kv, bt, tg, torch.zeros(n, dtype=torch.int32,
+                                                                      device="cuda"), out, lse, ws)
+    torch.cuda.synchronize()
+    assert mk.kv_pool_check_errors(gp, clear=True) & mk.DEVERR["FP8_EXHAUSTED"]
+    assert (out.cpu().numpy() == 0).all() and np.isneginf(lse.cpu().numpy()).all()
+    assert (bt.cpu().numpy() == -1).all() and mk.kv_pool_free_counts(gp) == (8, 2)
+
+
 def test_decode_append_fails_closed(torch_cuda):
     """A fused step that cannot append as a whole (free list exhausted, a
     length out of range, a page that is not Recent) changes no state, sets
