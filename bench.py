@@ -11,7 +11,8 @@ paged_attn_decode_append (the new token of each request appended inside the
 decode launch, then attention over the grown context); after the last layer
 kv_migrate_to_tq3 (pages leaving the Recent window).  The same steps with the
 append as its own call (kv_append_fp8, then paged_attn_decode) are timed too,
-for comparison.  All inputs
+for comparison, and the same KV held all-FP8 and all-bf16 is timed as dense
+controls (decode-only sweeps of every layer on the three caches).  All inputs
 are resident in HBM before the timed region.  The headline value is the step
 time per layer (us/layer, lower is better); the decode kernel's own time, its
 effective KV bandwidth and its fraction of the 8 TB/s HBM peak are reported
@@ -316,7 +317,7 @@ class DenseControls:
             "timing": f"decode only (decode + merge per layer, no append, no Retier), "
                       f"{reps} sweeps of {n_layers} layers between two HIP events",
             "mixed": {**row(t_mixed, b_mixed), "seq_len": int(sl_h[0]),
-                      "kernel": "decode_kernel<256, true, true, false> + decode_merge_kernel"},
+                      "kernel": "decode_kernel<256, true, true, false, false> + decode_merge_kernel"},
             "all_fp8": {**row(t_fp8, b_fp8), "seq_len": self.lens[0],
                         "kernel": "the same kernels, every page FP8"},
             "all_bf16": {**row(t_bf16, b_bf16), "seq_len": self.lens[0],
@@ -559,8 +560,8 @@ def main():
                              "(decode, fused append, merge and the step's Retier share)",
         "roofline": {"bound": "hbm", "achieved": round(achieved / 1e9, 1), "peak": HBM_PEAK / 1e9,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK, 4), "traffic": traffic,
-                     "kernel": "decode_kernel<256, true, true, true> (split scan with the "
-                               "fused append, one launch per layer)"},
+                     "kernel": "decode_kernel<256, true, true, true, false> (split scan with "
+                               "the fused append, one launch per layer)"},
         "counters": {k: int(v) for k, v in counters.items()},
         "setup_s": round(setup_s, 1),
     }

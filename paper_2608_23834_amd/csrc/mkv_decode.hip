@@ -1,32 +1,39 @@
 // Mixed-format paged decode attention (Sec. 3.3, Eq. softmax-merge; Sec. 4.1
 // direct fused decode) for gfx950.
 //
-// One launch per layer.  Grid (chunk, KV head, request); one workgroup of
-// 12 (or 8) wave64s per CU.  Chunks are ranges of logical pages of equal
-// cost: a page wholly outside the Recent window (a TQ3 page unless it is an
-// anchor) costs 2 units, a Recent (FP8) page 5 units -- an FP8 page carries
-// twice the bytes of a TQ3 page, and its scattered 16-byte copies make it
-// cost the scan about 2.5 times as much (measured); the unit count per chunk
-// is chosen so that the launch is about one workgroup per CU.  Each workgroup
-//  1. loads the GQA group's queries and builds two fp16 MFMA operands in LDS:
-//     the plain queries for FP8 pages and the rotated ones for TQ3 pages
-//     (q_rot = R q, exact algebra since k_hat = gamma R^T mu_c, so keys are
-//     never de-rotated), the Hadamard transform done in registers;
+// One launch per layer.  Grid (chunk, KV head, request); one workgroup per CU:
+// 12 wave64s with one ring slot each when a KV head's query group has at most
+// 8 heads (two pages share a score tile), else 8 waves with two slots.  Chunks
+// are ranges of logical pages of equal cost: a page wholly outside the Recent
+// window costs 2 units, a Recent (FP8) page 5 (its scattered 16-byte copies
+// make it cost the scan about 2.5 times a TQ3 page, measured); the unit count
+// per chunk is chosen so that the launch is about one workgroup per CU.  Each
+// workgroup
+//  1. loads its chunk's tags and page ids and the request's length together,
+//     and meanwhile builds the query operands in LDS: the plain query as fp16
+//     (FP8 pages) and the rotated query q_rot = R q (exact algebra: k_hat =
+//     gamma R^T mu_c, so keys are never de-rotated) times the softmax scale,
+//     as three E4M3 terms under a power-of-two head scale (TQ3 pages), the
+//     Hadamard transform done with DPP / permlane butterflies;
 //  2. splits its pages by format into compact lists in logical order (Sec.
-//     4.1 per-format lists, built per chunk with wave ballots) and turns them
-//     into stages of equal size: a pair of TQ3 pages or one FP8 page;
-//  3. each wave streams its run of stages through a two-slot LDS ring fed by
-//     direct HBM -> LDS copies, two stages in flight behind the one computed:
-//     QK^T on MFMA 16x16x32 f16 (M = 16 tokens, N = query heads, K = 32
-//     channels), 3-bit codes turned into E4M3 codebook bytes by one v_perm per
-//     4 codes and into fp16 by the hardware converter; online softmax in base
-//     2; PV on MFMA with M = 16 channels, N = heads, K = 32 tokens, the TQ3
-//     values entering as exact integer codes with the per-channel scale and
-//     zero applied in fp32;
-//  4. the eight waves merge in LDS into one (m_j, l_j, O_j) partial per chunk.
+//     4.1 per-format lists, per chunk, with wave ballots) and turns them into
+//     stages of equal size: a pair of TQ3 pages or one FP8 page; waves claim
+//     stages from an LDS counter and raise their priority as they progress;
+//  3. each wave streams its stages through its ring slot, fed by direct HBM ->
+//     LDS copies (global_load_lds_dwordx4): QK^T of TQ3 pages on
+//     v_mfma_scale_f32_16x16x128_f8f6f4 (3-bit codes -> E4M3 codebook bytes by
+//     one v_perm per 4 codes, against the three query terms; M = 16 tokens, N
+//     = 16 columns = the group's heads against page a and page b), of FP8
+//     pages on v_mfma_f32_16x16x32_f16; online softmax in base 2 with a lazy
+//     reference max; PV on the f16 MFMA with block-diagonal page rows, the
+//     weights as an fp16 hi + lo pair, TQ3 value codes as exact integers and
+//     the per-channel scale and zero applied in fp32 to the MFMA output;
+//  4. merges its waves' rows in LDS into one (m_j, l_j, O_j) partial per chunk.
 // A second kernel merges all partials of a request and query head (Eq.
 // softmax-merge).  The workspace holds O(chunks x heads x d) partials, never
-// anything the size of the cache.
+// anything the size of the cache.  Instances: APP fuses the decode-step append
+// of one token per request into the launch; SCORE also records every page's
+// local softmax mass for the attention-score collector.
 #include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
