@@ -332,6 +332,51 @@ class DenseControls:
         }
 
 
+def score_overhead(mk, torch, pool, bt, tags, sl, q_all, n_layers, w, reps=5):
+    """Cost of the direct attention-score collector (Sec. 3.1 / 4.2) on the
+    mixed cache: decode-only sweeps of every layer with paged_attn_decode, then
+    with paged_attn_decode_scores plus kv_page_scores_update (all query heads
+    sampled), HIP events around `reps` sweeps."""
+    n_req, mp = bt.shape
+    d, Hq = w.head_dim, w.n_q_heads
+    out = torch.zeros((n_req, Hq, d), device="cuda")
+    lse = torch.zeros((n_req, Hq), device="cuda")
+    ws = mk.workspace(pool, n_req, mp)
+    pm = torch.zeros((n_req, mp, Hq, 2), device="cuda")
+    scores = torch.zeros((n_req, mp), device="cuda")
+    hm = torch.ones(Hq, dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def sweep(fn):
+        for l in range(n_layers):
+            fn(l)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(reps):
+            for l in range(n_layers):
+                fn(l)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / (reps * n_layers)
+
+    t_plain = sweep(lambda l: mk.paged_attn_decode(pool, l, q_all[l], bt, tags, sl, out, lse, ws))
+
+    def scored(l):
+        mk.paged_attn_decode_scores(pool, l, q_all[l], bt, tags, sl, out, lse, ws, pm)
+        mk.kv_page_scores_update(pool, sl, lse, pm, hm, 0.9, scores)
+
+    t_score = sweep(scored)
+    if mk.kv_pool_check_errors(pool):
+        raise RuntimeError("device error word set in the score-collector sweeps")
+    return {"decode_us_per_layer": round(t_plain, 3),
+            "decode_with_scores_us_per_layer": round(t_score, 3),
+            "overhead_frac": round(t_score / t_plain - 1.0, 4),
+            "what": "paged_attn_decode_scores + kv_page_scores_update (every query head "
+                    "sampled, EWMA beta 0.9) against paged_attn_decode, decode-only sweeps of "
+                    f"all {n_layers} layers, {reps} sweeps between two HIP events"}
+
+
 def stream_probe(mk, torch, nbytes, achieved, reps=20):
     """A plain streaming read of `nbytes` (the library's probe kernel, 16-byte
     loads, each byte once), cycling through 16 buffers so no read is served
@@ -393,6 +438,8 @@ def main():
     ap.add_argument("--no-stream-probe", action="store_true",
                     help="skip the streaming-read probe (a kernel that reads the decode's byte "
                          "count once, over cycled buffers: the measured bandwidth ceiling)")
+    ap.add_argument("--no-scores", action="store_true",
+                    help="skip timing the attention-score collector")
     ap.add_argument("--no-controls", action="store_true",
                     help="skip the dense controls (the same KV all-FP8 and all-bf16)")
     args = ap.parse_args()
@@ -570,6 +617,9 @@ def main():
         res["dense_controls"] = ctl.time(torch, q_all, (pool, bt, tags, seq_after[n_steps - 1]), 5)
         del ctl
         torch.cuda.empty_cache()
+    if not args.no_scores:
+        res["score_collector"] = score_overhead(mk, torch, pool, bt, tags, seq_after[n_steps - 1],
+                                                q_all, n_layers, w)
     if not args.no_stream_probe:
         res["stream_probe"] = stream_probe(mk, torch, int(kv_bytes), achieved)
     if args.copy_probe:

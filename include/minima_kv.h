@@ -312,7 +312,9 @@ mkv_status paged_attn_chunk(mkv_pool* pool, int32_t layer, int32_t n_req, const 
  * kv_page_scores_update then, for every request r and page p < ceil(seq_lens
  * [r] / 16), forms the globally normalized mass q_{hq,p} = mass * 2^(m - lse
  * [r][hq] / ln 2) (Eq. score-global-weight), conditions it on page-addressable
- * mass, q~ = q / sum_p q, averages q~ over the sampled heads (head_mask
+ * mass, q~ = q / sum_p q (= q: with no sink logit every token's weight is
+ * page mass, and the merge's lse is the log of the sum the masses partition,
+ * so sum_p q = 1 up to rounding), averages q~ over the sampled heads (head_mask
  * [hq] != 0; device uint8 [n_q_heads]) into r_p, and updates scores[r][p] =
  * beta * scores[r][p] + (1 - beta) * r_p in place (Eq. attention-score;
  * device fp32 [n_req][max_pages]); r_out (same shape) and qn_out ([n_req]

@@ -1206,75 +1206,63 @@ hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t
 }
 
 // Attention-score collector (Sec. 3.1, Eqs. score-global-weight and
-// attention-score), after a scoring decode of the same call: one workgroup per
-// request.  The globally normalized mass of page p for query head hq is its
-// local mass rescaled by the global softmax normalization,
-// q = mass * 2^(m_ref - lse / ln 2) (lse of the merge); q~ = q / sum_p q over
-// the request's pages (page-addressable mass); r_p = the mean of q~ over the
-// sampled heads; a_p <- beta a_p + (1 - beta) r_p.  Pass 1 sums each sampled
-// head's masses (one wave per head, a pass over the pages); pass 2 forms r_p
-// and updates a_p (and writes q~ when asked).
-__global__ __launch_bounds__(256) void score_collect_kernel(int n_q_heads, int max_pages,
-                                                            const int32_t* seq_lens,
-                                                            const float* lse,
-                                                            const float2* page_mass,
-                                                            const uint8_t* head_mask, float beta,
-                                                            float* a_io, float* r_out,
-                                                            float* qn_out) {
+// attention-score), after a scoring decode of the same call; one thread per
+// page, workgroups over page blocks and requests.  The globally normalized
+// mass of page p for query head hq is its local mass rescaled by the global
+// softmax normalization, q = mass * 2^(m_ref - lse / ln 2) (lse of the
+// merge).  The collector conditions on page-addressable mass, q / sum_p q;
+// this attention has no sink logit and the merge's lse is the log of the very
+// sum of weights that the page masses partition, so sum_p q = 1 and q~ = q up
+// to rounding.  r_p = the mean of q~ over the sampled heads; a_p <- beta a_p +
+// (1 - beta) r_p; q~ is written when asked.
+constexpr int SCORE_UP_NT = 64;  // pages per update workgroup
+__global__ __launch_bounds__(SCORE_UP_NT) void score_update_kernel(int n_q_heads, int max_pages,
+                                                                   const int32_t* seq_lens,
+                                                                   const float* lse,
+                                                                   const float2* page_mass,
+                                                                   const uint8_t* head_mask,
+                                                                   float beta, float* a_io,
+                                                                   float* r_out, float* qn_out) {
   constexpr int MAXH = 256;
-  __shared__ float s_inv[MAXH];  // 1 / sum_p q per head (0: not sampled)
-  __shared__ float s_l2[MAXH];   // lse in base 2 per head
+  __shared__ float s_l2[MAXH];
+  __shared__ uint8_t s_smp[MAXH];
   __shared__ int s_ns;
-  const int r = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int r = blockIdx.y, tid = threadIdx.x;
+  const int p = blockIdx.x * SCORE_UP_NT + tid;
   const int S = seq_lens[r];
   const int np = S >= 1 ? min((S + PAGE - 1) / PAGE, max_pages) : 0;
   if (tid == 0) s_ns = 0;
   __syncthreads();
-  const float kLog2e = 1.4426950408889634f;
-  for (int hq = tid; hq < n_q_heads; hq += 256) {
-    s_l2[hq] = lse[(int64_t)r * n_q_heads + hq] * kLog2e;
-    if (head_mask[hq]) atomicAdd(&s_ns, 1);
+  for (int hq = tid; hq < n_q_heads; hq += SCORE_UP_NT) {
+    s_l2[hq] = lse[(int64_t)r * n_q_heads + hq] * 1.4426950408889634f;
+    s_smp[hq] = head_mask[hq] != 0;
+    if (s_smp[hq]) atomicAdd(&s_ns, 1);
   }
   __syncthreads();
-  const bool want_q = qn_out != nullptr;
-  for (int hq = wv; hq < n_q_heads; hq += 4) {
-    float z = 0.0f;
-    if (head_mask[hq] || want_q) {
-      for (int p = lane; p < np; p += 64) {
-        const float2 mm = page_mass[((int64_t)r * max_pages + p) * n_q_heads + hq];
-        z += mm.x * exp2f(mm.y - s_l2[hq]);
-      }
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) z += __shfl_xor(z, o, 64);
-    }
-    if (lane == 0) s_inv[hq] = z > 0.0f ? 1.0f / z : 0.0f;
+  if (p >= np) return;
+  const float2* pm = page_mass + ((int64_t)r * max_pages + p) * n_q_heads;
+  float acc = 0.0f;
+#pragma unroll 8
+  for (int hq = 0; hq < n_q_heads; ++hq) {
+    const float2 mm = pm[hq];
+    const float qn = mm.x * exp2f(mm.y - s_l2[hq]);
+    if (qn_out) qn_out[((int64_t)r * max_pages + p) * n_q_heads + hq] = qn;
+    if (s_smp[hq]) acc += qn;
   }
-  __syncthreads();
   const int ns = s_ns;
-  for (int p = tid; p < np; p += 256) {
-    const float2* pm = page_mass + ((int64_t)r * max_pages + p) * n_q_heads;
-    float acc = 0.0f;
-    for (int hq = 0; hq < n_q_heads; ++hq) {
-      const bool smp = head_mask[hq] != 0;
-      if (!smp && !want_q) continue;
-      const float2 mm = pm[hq];
-      const float qn = mm.x * exp2f(mm.y - s_l2[hq]) * s_inv[hq];
-      if (want_q) qn_out[((int64_t)r * max_pages + p) * n_q_heads + hq] = qn;
-      if (smp) acc += qn;
-    }
-    const float rp = ns ? acc / (float)ns : 0.0f;
-    if (r_out) r_out[(int64_t)r * max_pages + p] = rp;
-    float* ap = a_io + (int64_t)r * max_pages + p;
-    *ap = beta * *ap + (1.0f - beta) * rp;
-  }
+  const float rp = ns ? acc / (float)ns : 0.0f;
+  if (r_out) r_out[(int64_t)r * max_pages + p] = rp;
+  float* ap = a_io + (int64_t)r * max_pages + p;
+  *ap = beta * *ap + (1.0f - beta) * rp;
 }
 
 hipError_t launch_score_collect(int n_req, int n_q_heads, int max_pages, const int32_t* seq_lens,
                                 const float* lse, const float2* page_mass,
                                 const uint8_t* head_mask, float beta, float* a_io, float* r_out,
                                 float* qn_out, hipStream_t s) {
-  hipLaunchKernelGGL(score_collect_kernel, dim3(n_req), dim3(256), 0, s, n_q_heads, max_pages,
-                     seq_lens, lse, page_mass, head_mask, beta, a_io, r_out, qn_out);
+  hipLaunchKernelGGL(score_update_kernel, dim3((max_pages + SCORE_UP_NT - 1) / SCORE_UP_NT, n_req),
+                     dim3(SCORE_UP_NT), 0, s, n_q_heads, max_pages, seq_lens, lse, page_mass,
+                     head_mask, beta, a_io, r_out, qn_out);
   return hipGetLastError();
 }
 
