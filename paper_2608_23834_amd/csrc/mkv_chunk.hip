@@ -43,8 +43,10 @@
 
 namespace mkv {
 
-constexpr int CW = 4;        // waves per chunk workgroup
-constexpr int CSLOTS = 7;    // stages in the shared ring
+constexpr int NSW = 4;       // score waves per chunk workgroup (one PV wave each)
+constexpr int CW = 2 * NSW;  // waves per chunk workgroup
+constexpr int CSLOTS = 8;    // raw stages in the shared ring (copies of scattered pages
+                             // take several microseconds to land)
 constexpr int CMASK_LP = 0x3FFFFFFF / PAGE;
 
 struct ChunkArgs {
@@ -91,43 +93,59 @@ __device__ __forceinline__ half8 h8u(uint32_t a, uint32_t b, uint32_t c, uint32_
 }
 constexpr float CM_INIT = -1.0e30f;  // running max before the first score (finite: no inf - inf)
 
-// Byte selector of the codes of quad 2 mb + h of a chunk (h = 0 or 1, per
-// lane): quad_sel with the quad's low bit taken from a lane value.
-template <int NDW>
-__device__ __forceinline__ uint32_t quad_pair_sel(const uint32_t* Dw, int mb, int h) {
-  if (mb < NDW) return (Dw[mb] >> (3 * h)) & 0x07070707u;
-  const int p = mb - NDW;
-  const uint32_t q0 = ((Dw[3 * p] >> 6) & 0x03030303u) | ((Dw[3 * p + 1] >> 4) & 0x04040404u);
-  const uint32_t q1 = ((Dw[3 * p + 1] >> 7) & 0x01010101u) | ((Dw[3 * p + 2] >> 5) & 0x06060606u);
-  return h ? q1 : q0;
-}
-// half h of x broadcast to both halves
-__device__ __forceinline__ half2v bcast_half(half2v x, int h) {
-  const uint32_t b = __builtin_bit_cast(uint32_t, x);
-  return __builtin_bit_cast(half2v, __builtin_amdgcn_perm(b, b, h ? 0x03020302u : 0x01000100u));
-}
+// LDS of a chunk workgroup (bytes): the ring of raw stages, two buffers of
+// unpacked key operands, three of unpacked value operands, two of the
+// weights the score waves hand to the PV waves, and the rows' softmax
+// denominators for the final normalization.
+template <int D>
+struct ChunkLds {
+  static constexpr int NK8 = D / 64, NMB = D / 32;
+  static constexpr int STAGE = 2 * (int)tq3_region_bytes(D);
+  static constexpr int KX = NK8 * 64 * 32;            // key bytes [k-step][lane][32]
+  static constexpr int KB = KX + 64;                  // + gamma fp16 [page][16]
+  static constexpr int VX = 2 * NMB * 64 * 8;         // value codes [page][block][lane][8]
+  static constexpr int SX = 2 * NMB * 32 * 4;         // V scale (hi, lo) fp16 [page][block][row]
+  static constexpr int VB = VX + SX + 2 * NMB * 32 * 2;  // + V zero fp16 [page][block][row]
+  // weights of one stage from one score wave: 5 half8 operands per lane
+  // ([field][lane][16]: page a hi, lo, page b hi, lo, zero term), the
+  // rescale factor per lane and the wave's moved flag
+  static constexpr int WF_ALPHA = 5 * 1024, WF_FLAG = WF_ALPHA + 256, WPW = WF_FLAG + 16;
+  static constexpr int KB0 = CSLOTS * STAGE;
+  static constexpr int VB0 = KB0 + 2 * KB;
+  static constexpr int WB0 = VB0 + 3 * VB;
+  static constexpr int LB0 = WB0 + 2 * NSW * WPW;     // row denominators [score wave][32]
+  static constexpr int TOTAL = LB0 + NSW * 32 * 4;
+  static_assert(KB % 16 == 0 && VB % 16 == 0 && STAGE % 16 == 0 && WPW % 16 == 0,
+                "16-byte aligned buffers");
+  static_assert(TOTAL <= 160 * 1024, "one workgroup's LDS");
+};
 
 template <int D>
 __global__ __launch_bounds__(64 * CW, 1) void chunk_kernel(ChunkArgs a) {
   constexpr int NDW = 3 * D / 128, CL = D / 16, QQ = D / 4;
-  constexpr int NKS = D / 16;   // k-steps of the score product (16 channels each)
+  constexpr int NKS = D / 16;   // k-steps of the FP8-page score product (16 channels each)
+  constexpr int NK8 = D / 64;   // k-steps of the TQ3 score product (64 channels each)
   constexpr int NMB = D / 32;   // 32-channel blocks of the output
-  constexpr int KPC = QQ / 8;   // k-steps per key chunk (a chunk holds QQ channels)
+  constexpr int KPC = QQ / 8;   // FP8-page k-steps per channel quarter
   constexpr int R3 = (int)tq3_region_bytes(D);
   constexpr int R8 = (int)fp8_region_bytes(D);
   constexpr int STAGE = 2 * R3;       // a TQ3 page pair, or one FP8 page + its two scales
   constexpr int MAIN_KB = 16 * D / 1024;  // whole KiB of a TQ3 page (its last 32 bytes aside)
-  constexpr int OPS_W = 2 * MAIN_KB / CW;  // 1-KiB copies per wave per stage
-  constexpr int NI = D / 64;               // 1-KiB copies per half of an FP8 page
-  static_assert(2 * MAIN_KB % CW == 0 && 2 * NI == CW * OPS_W, "copies split evenly");
+  constexpr int OPS_W = 2 * MAIN_KB / NSW;  // 1-KiB copies per score wave per stage
+  constexpr int NI = D / 64;                // 1-KiB copies per half of an FP8 page
+  using LY = ChunkLds<D>;
+  static_assert(2 * MAIN_KB % NSW == 0 && 2 * NI == NSW * OPS_W, "copies split evenly");
   static_assert(R3 == 1024 * MAIN_KB + 32, "TQ3 page = whole KiB + a 32-byte tail");
   static_assert(R8 + 8 <= STAGE, "an FP8 page and its scales fit one stage");
-  static_assert(CL == 2 * NMB, "a lane's chunk row covers two channels per block");
+  static_assert(CL == 2 * NMB, "a chunk row of V covers two channels per block");
+  static_assert(CW == 2 * NSW, "one PV wave per score wave");
   extern __shared__ __align__(16) uint8_t smem[];
   const PoolView& P = a.P;
   const int r = blockIdx.z, h = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool score_wave = wid < NSW;
+  const int sw = wid % NSW;  // the score wave (and its rows) this wave belongs to
   // MFMA lane roles: li = lane % 32 (row of A, column of B and of the
   // output), lg = lane / 32 (k-slot group)
   const int li = lane & 31, lg = lane >> 5;
@@ -135,468 +153,668 @@ __global__ __launch_bounds__(64 * CW, 1) void chunk_kernel(ChunkArgs a) {
   const int G = P.group, H = P.n_kv_heads, Hq = H * G;
   const int mp = a.max_pages;
 
-  // ---- request and rows of this wave
+  // ---- request and rows of this wave pair
   const int q0 = a.cu_q[r], q1 = a.cu_q[r + 1];
   const int nq = q1 - q0;
   const int S = a.seq_lens[r];
   const bool range_ok = q0 >= 0 && nq >= 0 && q1 <= a.n_q_total;
   const int rows_r = range_ok ? nq * G : 0;
-  const int rb = blockIdx.x * (CW * 32) + wid * 32;
+  const int rb = blockIdx.x * (NSW * 32) + sw * 32;
   if (!range_ok || nq < 1 || S < nq || S > mp * PAGE) {  // workgroup-uniform
     if (blockIdx.x == 0 && tid == 0) atomicOr(&P.ctrl[CTRL_ERR], (int)MKV_DEVERR_RANGE);
     // rows that can be located get zeros
     const int rho = rb + li;
-    if (rho < rows_r) {
+    if (score_wave && rho < rows_r) {
       float* o = a.out + ((int64_t)(q0 + rho / G) * Hq + h * G + rho % G) * D;
       for (int c = lg; c < D; c += 2) o[c] = 0.0f;
     }
     return;
   }
-  if (blockIdx.x * (CW * 32) >= rows_r) return;  // whole workgroup past the rows
-  // Waves whose rows all lie past the request's rows still take part in the
-  // copies and barriers; their scores are all masked.
+  if (blockIdx.x * (NSW * 32) >= rows_r) return;  // whole workgroup past the rows
+  // Wave pairs whose rows all lie past the request's rows still take part
+  // in the copies, the unpacking and the barriers; their scores are all
+  // masked.
   const int P0 = S - nq;  // position of the chunk's first query
   // this lane's query row rb + li: last token it may see, min(S - 1,
   // position); -1 for rows past the request's rows (all masked)
   const int rho_l = rb + li;
   const int lim = rho_l < rows_r ? min(S - 1, P0 + rho_l / G) : -1;
+  const int n8 = a.counts[2 * r], n3 = a.counts[2 * r + 1];
+  const int st3 = (n3 + 1) / 2, n_st = st3 + n8;
+  uint8_t* const kbuf = smem + LY::KB0;
+  uint8_t* const vbuf = smem + LY::VB0;
+  uint8_t* const wbuf = smem + LY::WB0;
+  float* const lbuf = reinterpret_cast<float*>(smem + LY::LB0);
+  auto barrier = [&]() {
+    wait_lgkm0();  // this wave's LDS reads and writes are done
+    __builtin_amdgcn_s_barrier();
+    __asm__ __volatile__("" ::: "memory");
+  };
+  struct TqW {
+    half8 ha, la, hb, lb, z;  // weights of pages a and b (hi, lo); zero-term operand
+  };
+  // this pair's weight slot of stage j
+  auto wslot = [&](int j) { return wbuf + ((j & 1) * NSW + sw) * LY::WPW; };
 
-  // ---- query operand: B of S^T = K Q^T.  Lane (li, lg) holds, for k-step s,
-  // channels (D/2) lg + 8 s + b (b < 8) of query row rb + li (the MFMA pairs
-  // slot b of lane group lg in A and B; the key operands use the same
-  // channel order).  TQ3 pages use q_rot = R q (R = d^-1/2 H diag(sigma)) as
-  // an fp16 pair hi + lo (fp32 accuracy: two MFMAs), FP8 pages the plain q
-  // (bf16 -> fp16 is exact: one MFMA).  Keys enter as fp16 too: the fp8 MFMA
-  // adds its products in groups aligned to the group's largest one and keeps
-  // only about 15 bits there, which moved chunk outputs by up to 2e-3 where
-  // keys carry large norms.
-  half8 qop[NKS];
-  // the rotated query's fp16 low part lives in this wave's LDS area after the
-  // ring: [k-step][lane]
-  half8* qlo = reinterpret_cast<half8*>(smem + CSLOTS * STAGE) + wid * NKS * 64;
-  auto build_q = [&](bool rotated) {
-    const int rho = min(rho_l, rows_r - 1);
-    const uint16_t* qrow = a.q + ((int64_t)(q0 + rho / G) * Hq + h * G + rho % G) * D + (D / 2) * lg;
-    float x[NKS][8];
+  // Stage j of the loops below is a TQ3 pair for j < st3, else an FP8 page.
+  // Pass i (one barrier each, i = 0 .. n_st): the score waves take stage i
+  // (scores, softmax, weights into LDS; for a TQ3 pair also the unpacking
+  // of pair i + 1) while the PV waves take stage i - 1 with the weights
+  // handed over in pass i - 1.
+  if (score_wave) {
+    // ======================= score waves =======================
+    const int rho_c = min(rho_l, rows_r - 1);  // a valid row to load for masked lanes
+    const uint16_t* qrow_ptr = a.q + ((int64_t)(q0 + rho_c / G) * Hq + h * G + rho_c % G) * D;
+    const int2* l3 = reinterpret_cast<const int2*>(a.list3) + (int64_t)r * mp;
+    const int2* l8 = reinterpret_cast<const int2*>(a.list8) + (int64_t)r * mp;
+    // (logical page, physical id) of a list entry; out-of-range ids read
+    // page 0 with every token masked and are reported after the loop (no
+    // memory writes while copies are in flight)
+    bool bad_id = false;
+    auto checked = [&](int2 e, int n_ids) {
+      if (e.y < 0 || e.y >= n_ids) {
+        bad_id = true;
+        return make_int2(CMASK_LP, 0);
+      }
+      return e;
+    };
+    // List entries are wave-uniform: scalar loads through the constant
+    // address space (tracked by lgkmcnt, so waiting for them never drains
+    // the page copies in flight), each issued one pass before its use.
+    typedef __attribute__((address_space(4))) const int cint;
+    cint* l3c = (cint*)(uintptr_t)l3;
+    cint* l8c = (cint*)(uintptr_t)l8;
+    auto ent = [&](cint* l, int k) { return make_int2(l[2 * k], l[2 * k + 1]); };
+    // stage j -> {lp_a, id_a, lp_b, id_b}; id_b < 0 marks an FP8 stage
+    auto stage_at = [&](int j) {
+      j = __builtin_amdgcn_readfirstlane(j);
+      if (j >= n_st) return make_int4(CMASK_LP, 0, CMASK_LP, 0);  // past the list: never used
+      if (j < st3) {
+        const int2 ea = checked(ent(l3c, 2 * j), P.n_tq3);
+        const int2 eb = 2 * j + 1 < n3 ? checked(ent(l3c, 2 * j + 1), P.n_tq3) : make_int2(CMASK_LP, ea.y);
+        return make_int4(ea.x, ea.y, eb.x, eb.y);
+      }
+      const int2 e = checked(ent(l8c, j - st3), P.n_fp8);
+      return make_int4(e.x, e.y, 0, -1);
+    };
+    const int layer = a.layer;
+    const uint8_t* tq3_l = P.tq3 + (int64_t)layer * P.n_tq3 * H * R3;
+    const uint8_t* fp8_l = P.fp8 + (int64_t)layer * P.n_fp8 * H * R8;
+    const uint8_t* scl_l = reinterpret_cast<const uint8_t*>(P.fp8_scales + (int64_t)layer * P.n_fp8 * H * 2);
+    const uint32_t ring_lds = __builtin_amdgcn_readfirstlane(
+        (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)smem);
+    // FP8 pages land block-permuted (see dma_fp8_page): per-lane source offsets
+    const uint32_t vk = 16u * (uint32_t)(ln * (D / 16) + l4 * NI);
+    const uint32_t vv = 16u * (uint32_t)((ln * 4 + l4) * NI);
+    // This wave's share of stage e's copies into ring slot `slot`: OPS_W
+    // whole KiB (TQ3: KiB w OPS_W .. of the two pages laid end to end; FP8:
+    // copies w OPS_W .. of the page's 2 NI), and for waves 0 and 1 one small
+    // copy (TQ3: the 32-byte tail of page a resp. b; FP8: the two scales,
+    // copied by both so that every stage costs each wave the same number of
+    // copies).  Only the score waves copy.
+    auto issue = [&](int4 e, int slot) {
+      // wave-uniform by construction; said so for the scalar operands of the copies
+      slot = __builtin_amdgcn_readfirstlane(slot);
+      e.y = __builtin_amdgcn_readfirstlane(e.y);
+      e.w = __builtin_amdgcn_readfirstlane(e.w);
+      const uint32_t dst = ring_lds + slot * STAGE;
+      if (e.w >= 0) {
 #pragma unroll
-    for (int s = 0; s < NKS; ++s) {
-      const uint4 raw = *reinterpret_cast<const uint4*>(qrow + 8 * s);
-      const uint16_t* hb = reinterpret_cast<const uint16_t*>(&raw);
+        for (int i = 0; i < OPS_W; ++i) {
+          const int g = wid * OPS_W + i, pg = g / MAIN_KB, kb = g % MAIN_KB;
+          const int id = pg ? e.w : e.y;
+          dma16<0>(16u * lane + 1024u * kb, tq3_l + ((int64_t)id * H + h) * R3,
+                   dst + pg * R3 + 1024 * kb);
+        }
+        if (wid < 2) {
+          const int id = wid ? e.w : e.y;
+          if (lane < 8) dma4(16 * D + 4 * lane, tq3_l + ((int64_t)id * H + h) * R3, dst + wid * R3 + 16 * D);
+        }
+      } else {
+        const uint8_t* src = fp8_l + ((int64_t)e.y * H + h) * R8;
 #pragma unroll
-      for (int j = 0; j < 8; ++j) x[s][j] = bf16_to_f32(hb[j]);
-    }
-    if (rotated) {
-      const int8_t* sg = P.sigma + (D / 2) * lg;
+        for (int i = 0; i < OPS_W; ++i) {
+          const int op = wid * OPS_W + i;
+          if (op < NI)
+            dma16<0>(vk, src + 16 * op, dst + 1024 * op);
+          else
+            dma16<0>(vv, src + 16 * D + 16 * (op - NI), dst + 16 * D + 1024 * (op - NI));
+        }
+        if (wid < 2 && lane < 2) dma4(4 * lane, scl_l + ((int64_t)e.y * H + h) * 8, dst + R8);
+      }
+    };
+    // Ring bookkeeping: stage s sits in slot s % CSLOTS; `issued` stages have
+    // been copied so far.  The slot of a TQ3 pair s is free from pass s on
+    // (its raw bytes were unpacked in pass s - 1), that of an FP8 page s
+    // from pass s + 2 on (read by the score waves in pass s, by the PV
+    // waves in pass s + 1).  A wait for stage s lets the copies of the
+    // stages after it stay in flight (every stage costs a wave the same
+    // copies).
+    int issued = 0;
+    int4 e_iss = stage_at(0);  // the entries of stage `issued`
+    auto refill = [&](int pass) {
+      bool fresh = true;  // e_iss holds stage `issued`
+      while (issued < n_st) {
+        const int prev = issued - CSLOTS;
+        if (prev >= 0 && (prev < st3 ? prev : prev + 2) > pass) break;
+        if (!fresh) e_iss = stage_at(issued);
+        issue(e_iss, issued % CSLOTS);
+        ++issued;
+        fresh = false;
+      }
+    };
+    // entries of the next stage to copy, loaded at the end of a pass (the
+    // barrier's wait covers their latency)
+    auto prefetch_iss = [&]() { e_iss = stage_at(issued); };
+    auto wait_for = [&](int s) {
+      const int later = max(0, min(issued - 1 - s, CSLOTS - 1));
+#define MKV_CHUNK_WAIT(n)                                   \
+  case n:                                                  \
+    if (wid < 2) wait_vmcnt<(n) * (OPS_W + 1)>();          \
+    else wait_vmcnt<(n) * OPS_W>();                        \
+    break;
+      switch (later) {
+        MKV_CHUNK_WAIT(1)
+        MKV_CHUNK_WAIT(2)
+        MKV_CHUNK_WAIT(3)
+        MKV_CHUNK_WAIT(4)
+        MKV_CHUNK_WAIT(5)
+        MKV_CHUNK_WAIT(6)
+        MKV_CHUNK_WAIT(7)
+        default: wait_vmcnt<0>(); break;
+      }
+#undef MKV_CHUNK_WAIT
+    };
+    static_assert(CSLOTS <= 8 && (CSLOTS - 1) * (OPS_W + 1) < 64,
+                  "wait_for covers up to seven stages in flight");
+    refill(-1);
+    prefetch_iss();
+
+    // ---- rotated query of this lane's row, q_rot = R q (R = d^-1/2 H
+    // diag(sigma)), times the softmax scale log2(e)/sqrt(d) (scores come out
+    // in base 2) and a power-of-two row scale qsc that puts the row's
+    // largest entry in [128, 256), as three E4M3 terms t0 + t1 + t2 (each
+    // the E4M3 rounding of what the earlier ones left; the remainder sits
+    // below E4M3's subnormal step, about 2^-17 of the largest entry).  B
+    // operand of the 32x32x64 fp8 MFMA: lane (li, lg) holds, for k-step s,
+    // channels 64 s + 32 lg + j (j < 32) of row rb + li; the key operand
+    // uses the same order.
+    v8i qt[3][NK8];
+    float qinv;
+    {
+      float x[NK8][32];
 #pragma unroll
-      for (int s = 0; s < NKS; ++s)
+      for (int s = 0; s < NK8; ++s)
 #pragma unroll
-        for (int j = 0; j < 8; ++j) x[s][j] *= (float)sg[8 * s + j];
-      // Walsh-Hadamard butterflies over the channel bits: j (strides 1-4)
-      // and s (strides 8 .. D/4) inside the lane, lg (stride D/2) across
-      // lanes l ^ 32; the stages commute
+        for (int v = 0; v < 4; ++v) {
+          const uint4 raw = *reinterpret_cast<const uint4*>(qrow_ptr + 64 * s + 32 * lg + 8 * v);
+          const uint16_t* hb = reinterpret_cast<const uint16_t*>(&raw);
+          // the signs sit 4-byte aligned in the control buffer
+          const uint32_t* sgw = reinterpret_cast<const uint32_t*>(P.sigma + 64 * s + 32 * lg + 8 * v);
+          const uint2 sg2 = make_uint2(sgw[0], sgw[1]);
+          const int8_t* sg = reinterpret_cast<const int8_t*>(&sg2);
 #pragma unroll
-      for (int st = 1; st < 8; st <<= 1)
+          for (int j = 0; j < 8; ++j) x[s][8 * v + j] = bf16_to_f32(hb[j]) * (float)sg[j];
+        }
+      // Walsh-Hadamard butterflies over the channel bits: j (strides 1-16)
+      // and s (strides 64 ..) inside the lane, lg (stride 32) across lanes
+      // l ^ 32; the stages commute
 #pragma unroll
-        for (int s = 0; s < NKS; ++s)
+      for (int st = 1; st < 32; st <<= 1)
 #pragma unroll
-          for (int j = 0; j < 8; ++j)
+        for (int s = 0; s < NK8; ++s)
+#pragma unroll
+          for (int j = 0; j < 32; ++j)
             if (!(j & st)) {
               const float x0 = x[s][j], x1 = x[s][j + st];
               x[s][j] = x0 + x1;
               x[s][j + st] = x0 - x1;
             }
 #pragma unroll
-      for (int st = 1; st < NKS; st <<= 1)
+      for (int st = 1; st < NK8; st <<= 1)
 #pragma unroll
-        for (int s = 0; s < NKS; ++s)
+        for (int s = 0; s < NK8; ++s)
           if (!(s & st)) {
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
+            for (int j = 0; j < 32; ++j) {
               const float x0 = x[s][j], x1 = x[s + st][j];
               x[s][j] = x0 + x1;
               x[s + st][j] = x0 - x1;
             }
           }
       const float sgn32 = (lane & 32) ? -1.0f : 1.0f;
-      const float qscale = rsqrtf((float)D);
+      const float qscale = rsqrtf((float)D) * a.sm_log2;
+      float amax = 0.0f;
 #pragma unroll
-      for (int s = 0; s < NKS; ++s)
+      for (int s = 0; s < NK8; ++s)
 #pragma unroll
-        for (int j = 0; j < 8; ++j)
+        for (int j = 0; j < 32; ++j) {
           x[s][j] = fmaf(sgn32, x[s][j], lane_xor<32>(x[s][j], lane)) * qscale;
-    }
+          amax = fmaxf(amax, fabsf(x[s][j]));
+        }
+      amax = fmaxf(amax, lane_xor<32>(amax, lane));
+      int ex = 0;
+      (void)frexpf(amax, &ex);  // amax in [2^(ex-1), 2^ex)
+      const bool ok = rho_l < rows_r && amax > 0.0f;
+      const float qsc = ok ? ldexpf(1.0f, 8 - ex) : 0.0f;
+      qinv = ok ? ldexpf(1.0f, ex - 8) : 0.0f;
 #pragma unroll
-    for (int s = 0; s < NKS; ++s) {
-      half8 lo;
+      for (int s = 0; s < NK8; ++s)
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        qop[s][j] = (_Float16)x[s][j];
-        lo[j] = (_Float16)(x[s][j] - (float)qop[s][j]);
-      }
-      if (rotated) qlo[s * 64 + lane] = lo;
+        for (int w = 0; w < 8; ++w) {
+          uint32_t b0 = 0, b1 = 0, b2 = 0;
+#pragma unroll
+          for (int k = 0; k < 4; ++k) {
+            float v = x[s][4 * w + k] * qsc;
+            const uint32_t e0 = f32_to_e4m3(v);
+            v -= e4m3_to_f32(e0);
+            const uint32_t e1 = f32_to_e4m3(v);
+            v -= e4m3_to_f32(e1);
+            const uint32_t e2 = f32_to_e4m3(v);
+            b0 |= e0 << (8 * k);
+            b1 |= e1 << (8 * k);
+            b2 |= e2 << (8 * k);
+          }
+          qt[0][s][w] = (int)b0;
+          qt[1][s][w] = (int)b1;
+          qt[2][s][w] = (int)b2;
+        }
     }
-  };
 
-  // ---- stage list: TQ3 pairs (list3 entries 2k, 2k+1), then FP8 pages
-  const int n8 = a.counts[2 * r], n3 = a.counts[2 * r + 1];
-  const int st3 = (n3 + 1) / 2, n_st = st3 + n8;
-  const int2* l3 = reinterpret_cast<const int2*>(a.list3) + (int64_t)r * mp;
-  const int2* l8 = reinterpret_cast<const int2*>(a.list8) + (int64_t)r * mp;
-  // (logical page, physical id) of a list entry; out-of-range ids read page 0
-  // with every token masked and are reported after the loop (no memory
-  // writes while copies are in flight)
-  bool bad_id = false;
-  auto checked = [&](int2 e, int n_ids) {
-    if (e.y < 0 || e.y >= n_ids) {
-      bad_id = true;
-      return make_int2(CMASK_LP, 0);
-    }
-    return e;
-  };
-  // List entries reach the wave 64 at a time (lane k holds entry base + k)
-  // and are read out with v_readlane: one vector load per 64 entries (its
-  // wait also drains the copies in flight).  Two caches: one for the stage
-  // being copied, one for the stage being computed, which lags it.
-  struct ListCache {
-    int2 v;
-    int tag;  // 2 * base + list (0: TQ3, 1: FP8)
-  };
-  ListCache c_iss{make_int2(0, 0), -1}, c_cmp{make_int2(0, 0), -1};
-  auto entry = [&](ListCache& c, int list, int k) {
-    const int base = k & ~63, tag = 2 * base + list;
-    if (tag != c.tag) {
-      const int2* l = list ? l8 : l3;
-      const int n = list ? n8 : n3;
-      c.v = l[min(base + lane, n - 1)];
-      c.tag = tag;
-    }
-    return make_int2(__builtin_amdgcn_readlane(c.v.x, k - base),
-                     __builtin_amdgcn_readlane(c.v.y, k - base));
-  };
-  // stage j -> {lp_a, id_a, lp_b, id_b}; id_b < 0 marks an FP8 stage
-  auto stage_at = [&](ListCache& c, int j) {
-    if (j < st3) {
-      const int2 ea = checked(entry(c, 0, 2 * j), P.n_tq3);
-      int2 eb = 2 * j + 1 < n3 ? checked(entry(c, 0, 2 * j + 1), P.n_tq3) : make_int2(CMASK_LP, ea.y);
-      return make_int4(ea.x, ea.y, eb.x, eb.y);
-    }
-    const int2 e = checked(entry(c, 1, j - st3), P.n_fp8);
-    return make_int4(e.x, e.y, 0, -1);
-  };
-  const int layer = a.layer;
-  const uint8_t* tq3_l = P.tq3 + (int64_t)layer * P.n_tq3 * H * R3;
-  const uint8_t* fp8_l = P.fp8 + (int64_t)layer * P.n_fp8 * H * R8;
-  const uint8_t* scl_l = reinterpret_cast<const uint8_t*>(P.fp8_scales + (int64_t)layer * P.n_fp8 * H * 2);
-  const uint32_t ring_lds = __builtin_amdgcn_readfirstlane(
-      (uint32_t)(uintptr_t)(__attribute__((address_space(3))) void*)smem);
-  // FP8 pages land block-permuted (see dma_fp8_page): per-lane source offsets
-  const uint32_t vk = 16u * (uint32_t)(ln * (D / 16) + l4 * NI);
-  const uint32_t vv = 16u * (uint32_t)((ln * 4 + l4) * NI);
-  // This wave's share of stage e's copies into ring slot `slot`: OPS_W whole
-  // KiB (TQ3: KiB w OPS_W .. of the two pages laid end to end; FP8: copies
-  // w OPS_W .. of the page's 2 NI), and for waves 0 and 1 one small copy
-  // (TQ3: the 32-byte tail of page a resp. b; FP8: the two scales, copied by
-  // both so that every stage costs each wave the same number of copies).
-  auto issue = [&](const int4& e, int slot) {
-    const uint32_t dst = ring_lds + slot * STAGE;
-    if (e.w >= 0) {
+    float m_run = CM_INIT, l_run = 0.0f;  // this lane's row; l_run over its tokens
+    const float smk = a.sm_log2;
+    // Online softmax over the base-2 scores sc[16] of this lane's query row
+    // (its 16 tokens of the tile; the other 16 sit in lane l ^ 32).  The
+    // reference max moves (lazily, when a score passes it by 2^8): alpha is
+    // the factor the PV accumulators still owe, 1 where the reference
+    // stayed; the return value says whether any row of the wave moved.
+    auto softmax = [&](float* sc, float& alpha) {
+      float mx = sc[0];
 #pragma unroll
-      for (int i = 0; i < OPS_W; ++i) {
-        const int g = wid * OPS_W + i, pg = g / MAIN_KB, kb = g % MAIN_KB;
-        const int id = pg ? e.w : e.y;
-        dma16<0>(16u * lane + 1024u * kb, tq3_l + ((int64_t)id * H + h) * R3,
-                 dst + pg * R3 + 1024 * kb);
+      for (int k = 1; k < 16; ++k) mx = fmaxf(mx, sc[k]);
+      mx = fmaxf(mx, lane_xor<32>(mx, lane));
+      const bool need = mx > m_run + 8.0f;
+      const float m_new = need ? mx : m_run;
+      alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      m_run = m_new;
+      float lsum = 0.0f;
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        sc[k] = __builtin_amdgcn_exp2f(sc[k] - m_new);  // -inf -> 0
+        lsum += sc[k];
       }
-      if (wid < 2) {
-        const int id = wid ? e.w : e.y;
-        if (lane < 8) dma4(16 * D + 4 * lane, tq3_l + ((int64_t)id * H + h) * R3, dst + wid * R3 + 16 * D);
+      l_run = fmaf(l_run, alpha, lsum);
+      return __any(need);
+    };
+    // weights p[0..7] as an fp16 hi + lo pair (one token can carry most of
+    // a row's mass, and its weight, taken against a lagging reference max,
+    // is then not a power of two; a single fp16 rounding of it moves the
+    // output by up to 2^-12 of that token's value)
+    auto split8 = [&](const float* p, half8& hi, half8& lo) {
+      uint32_t hh4[4], ll4[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) split2(p[2 * k], p[2 * k + 1], hh4[k], ll4[k]);
+      hi = h8u(hh4[0], hh4[1], hh4[2], hh4[3]);
+      lo = h8u(ll4[0], ll4[1], ll4[2], ll4[3]);
+    };
+    // hand the weights of stage j (and the rescale the PV accumulators owe
+    // before them) to the PV wave of this pair
+    auto put_weights = [&](int j, const TqW& w, float alpha, bool moved) {
+      uint8_t* ws = wslot(j);
+      *reinterpret_cast<half8*>(ws + 0 * 1024 + 16 * lane) = w.ha;
+      *reinterpret_cast<half8*>(ws + 1 * 1024 + 16 * lane) = w.la;
+      *reinterpret_cast<half8*>(ws + 2 * 1024 + 16 * lane) = w.hb;
+      *reinterpret_cast<half8*>(ws + 3 * 1024 + 16 * lane) = w.lb;
+      *reinterpret_cast<half8*>(ws + 4 * 1024 + 16 * lane) = w.z;
+      reinterpret_cast<float*>(ws + LY::WF_ALPHA)[lane] = alpha;
+      if (lane == 0) *reinterpret_cast<int*>(ws + LY::WF_FLAG) = moved ? 1 : 0;
+    };
+
+    // ---- unpacking of a TQ3 pair (the 256 threads of the score waves, from
+    // the raw stage at rs):
+    //  keys: threads 0-127, one code chunk (token, channel quarter) each:
+    //    codes -> E4M3 codebook bytes (one v_perm per 4 codes) in the score
+    //    product's A layout, kb[k-step][lane (32 lg + token of the pair)][32];
+    //  values: threads 128-255, one code chunk (16 channels, 4 tokens) each:
+    //    code bytes in the PV product's A layout, vb[page][block][lane][8]
+    //    (lane 32 hk + rr: channel CL (rr % 16) + 2 mb + rr / 16, tokens 4
+    //    hk .. 4 hk + 3 then 8 + 4 hk .. 8 + 4 hk + 3, the order in which
+    //    the score tile hands each lane its weights);
+    //  per (page, block, row rr): the V scale split as (hi, lo) fp16 (hi
+    //    keeps 8 significant bits, so code x hi is exact in fp16) and the V
+    //    zero; gamma of both pages after the key bytes.
+    auto unpack = [&](const uint8_t* rs, uint8_t* kb, uint8_t* vb) {
+      if (tid < 128) {
+        const int p = tid >> 6, tok = tid & 15, g = (tid >> 4) & 3;
+        uint32_t dw[NDW];
+        read_chunk<NDW>(dw, rs + p * R3, 16 * g + tok);
+#pragma unroll
+        for (int q8 = 0; q8 < CL / 8; ++q8) {
+          uint32_t o[8];
+#pragma unroll
+          for (int w = 0; w < 8; ++w) o[w] = __builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(dw, 8 * q8 + w));
+          const int c0 = g * QQ + 32 * q8;  // first channel of these 32 bytes
+          uint4* dst = reinterpret_cast<uint4*>(kb + ((c0 / 64) * 64 + 32 * ((c0 / 32) & 1) + 16 * p + tok) * 32);
+          dst[0] = make_uint4(o[0], o[1], o[2], o[3]);
+          dst[1] = make_uint4(o[4], o[5], o[6], o[7]);
+        }
+      } else {
+        const int u = tid - 128;
+        const int p = u >> 6, r0 = u & 15, g = (u >> 4) & 3;
+        uint32_t dw[NDW];
+        read_chunk<NDW>(dw, rs + p * R3 + 6 * D, 16 * g + r0);
+        uint8_t* base = vb + (p * NMB * 64 + 32 * (g & 1) + r0) * 8 + 4 * (g >> 1);
+#pragma unroll
+        for (int q = 0; q < CL; ++q)
+          *reinterpret_cast<uint32_t*>(base + ((q >> 1) * 64 + 16 * (q & 1)) * 8) = quad_sel<NDW>(dw, q);
       }
-    } else {
-      const uint8_t* src = fp8_l + ((int64_t)e.y * H + h) * R8;
+      if (tid < NMB * 32) {
+        const int mb = tid >> 5, rr = tid & 31, ch = CL * (rr & 15) + 2 * mb + (rr >> 4);
 #pragma unroll
-      for (int i = 0; i < OPS_W; ++i) {
-        const int op = wid * OPS_W + i;
-        if (op < NI)
-          dma16<0>(vk, src + 16 * op, dst + 1024 * op);
-        else
-          dma16<0>(vv, src + 16 * D + 16 * (op - NI), dst + 16 * D + 1024 * (op - NI));
+        for (int p = 0; p < 2; ++p) {
+          const half2v s1 = bcast(*reinterpret_cast<const _Float16*>(rs + p * R3 + 12 * D + 32 + 2 * ch));
+          const half2v sh = hi8x2(s1);
+          const half2v sp = {sh[0], s1[0] - sh[0]};  // exact split
+          *reinterpret_cast<half2v*>(vb + LY::VX + ((p * NMB + mb) * 32 + rr) * 4) = sp;
+          *reinterpret_cast<_Float16*>(vb + LY::VX + LY::SX + ((p * NMB + mb) * 32 + rr) * 2) =
+              *reinterpret_cast<const _Float16*>(rs + p * R3 + 14 * D + 32 + 2 * ch);
+        }
       }
-      if (wid < 2 && lane < 2) dma4(4 * lane, scl_l + ((int64_t)e.y * H + h) * 8, dst + R8);
-    }
-  };
+      if (tid < 16)
+        *reinterpret_cast<uint32_t*>(kb + LY::KX + 4 * tid) =
+            *reinterpret_cast<const uint32_t*>(rs + (tid >> 3) * R3 + 12 * D + 4 * (tid & 7));
+    };
 
-  // ---- accumulators: O^T tile (32 channels x the 32 query rows) per block
-  // mb.  Lane (li, lg), element e holds query row rb + li and tile row rr =
-  // 8 (e / 4) + 4 lg + e % 4, which is channel CL (rr % 16) + 2 mb + rr / 16
-  // (a lane's V chunk row rr % 16 then serves every block).
-  float16v acc[NMB];
+    // Scores and weights of the TQ3 pair e from its unpacked keys kb.  The
+    // score tile's rows are the pair's 32 tokens (page a, then page b); lane
+    // (li, lg) receives tokens 4 lg .. 4 lg + 3 and 8 + 4 lg .. of each page,
+    // which are exactly the k-slots of its weight operand.
+    // (the products are issued first; the rest of the pass's issue work
+    // runs while they execute)
+    auto tq3_qk = [&](const uint8_t* kb, float16v& st0, float16v& st1) {
+      st0 = float16v{};
+      st1 = float16v{};  // even and odd k-steps: two MFMA chains
 #pragma unroll
-  for (int mb = 0; mb < NMB; ++mb) acc[mb] = float16v{};
-  float m_run = CM_INIT, l_run = 0.0f;  // this lane's row; l_run over its tokens
-  const float smk = a.sm_log2;
-  const int hh = li >> 4;   // which of the block's two channels of the chunk row
-  const int rrow = li & 15; // this lane's chunk row (A operands of PV)
-
-  // Online softmax over the scores sc[16] of this lane's query row (its 16
-  // tokens of the tile; the other 16 sit in lane l ^ 32), given before the
-  // softmax scale log2(e)/sqrt(d), which enters with the max subtraction.  The reference max
-  // moves (lazily, when a score passes it by 2^8) without a branch: alpha is
-  // the factor the accumulators still owe, 1 where the reference stayed; the
-  // return value says whether any row of the wave moved.
-  auto softmax = [&](float* sc, float& alpha) {
-    float mx = sc[0];
+      for (int s = 0; s < NK8; ++s) {
+        const v8i A = *reinterpret_cast<const v8i*>(kb + (s * 64 + lane) * 32);
+        float16v& st = (s & 1) ? st1 : st0;
 #pragma unroll
-    for (int k = 1; k < 16; ++k) mx = fmaxf(mx, sc[k]);
-    mx = fmaxf(mx, lane_xor<32>(mx, lane)) * smk;
-    const bool need = mx > m_run + 8.0f;
-    const float m_new = need ? mx : m_run;
-    alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-    m_run = m_new;
-    float lsum = 0.0f;
-#pragma unroll
-    for (int k = 0; k < 16; ++k) {
-      sc[k] = __builtin_amdgcn_exp2f(fmaf(sc[k], smk, -m_new));  // -inf -> 0
-      lsum += sc[k];
-    }
-    l_run = fmaf(l_run, alpha, lsum);
-    return __any(need);
-  };
-  // weights p[0..7] as an fp16 hi + lo pair (one token can carry most of a
-  // row's mass, and its weight, taken against a lagging reference max, is
-  // then not a power of two; a single fp16 rounding of it moves the output
-  // by up to 2^-12 of that token's value)
-  auto split8 = [&](const float* p, half8& hi, half8& lo) {
-    uint32_t hh4[4], ll4[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) split2(p[2 * k], p[2 * k + 1], hh4[k], ll4[k]);
-    hi = h8u(hh4[0], hh4[1], hh4[2], hh4[3]);
-    lo = h8u(ll4[0], ll4[1], ll4[2], ll4[3]);
-  };
-  struct TqW {
-    half8 ha, la, hb, lb, z;  // weights of pages a and b (hi, lo); zero-term operand
-  };
-
-  // Scores and weights of the TQ3 pair e in ring slot ra.  The score tile's
-  // rows are the pair's 32 tokens (page a, then page b); lane (li, lg)
-  // receives tokens 4 lg .. 4 lg + 3 and 8 + 4 lg .. of each page, which are
-  // exactly the k-slots of its weight operand.
-  auto tq3_scores = [&](const uint8_t* ra, const int4& e, TqW& w, float& alpha) {
-    const uint8_t* pg = ra + (li >= 16 ? R3 : 0);
-    uint32_t kc0[NDW], kc1[NDW];
-    read_chunk<NDW>(kc0, pg, 16 * (2 * lg) + rrow);
-    read_chunk<NDW>(kc1, pg, 16 * (2 * lg + 1) + rrow);
-    const uint2 ga0 = *reinterpret_cast<const uint2*>(ra + 12 * D + 8 * lg);
-    const uint2 ga1 = *reinterpret_cast<const uint2*>(ra + 12 * D + 16 + 8 * lg);
-    const uint2 gb0 = *reinterpret_cast<const uint2*>(ra + R3 + 12 * D + 8 * lg);
-    const uint2 gb1 = *reinterpret_cast<const uint2*>(ra + R3 + 12 * D + 16 + 8 * lg);
-    float16v st = {};
-#pragma unroll
-    for (int s = 0; s < NKS; ++s) {
-      const uint32_t* kc = s < KPC ? kc0 : kc1;
-      const int qd = 2 * (s % KPC);
-      const uint32_t c0 = __builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(kc, qd));
-      const uint32_t c1 = __builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(kc, qd + 1));
-      const half8 K = h8(cvt_lo(c0), cvt_hi(c0), cvt_lo(c1), cvt_hi(c1));
-      st = __builtin_amdgcn_mfma_f32_32x32x16_f16(K, qop[s], st, 0, 0, 0);
-      st = __builtin_amdgcn_mfma_f32_32x32x16_f16(K, qlo[s * 64 + lane], st, 0, 0, 0);
-    }
-    // element e: token 8 (e / 4) + 4 lg + e % 4 of the pair (page a below 16)
-    const _Float16* gam[4] = {reinterpret_cast<const _Float16*>(&ga0), reinterpret_cast<const _Float16*>(&ga1),
-                              reinterpret_cast<const _Float16*>(&gb0), reinterpret_cast<const _Float16*>(&gb1)};
-    float sc[16];
-    if ((max(e.x, e.z) + 1) * PAGE <= P0 + 1) {
-      // the pair lies wholly before the chunk's first query: no mask
-#pragma unroll
-      for (int e4 = 0; e4 < 4; ++e4)
-#pragma unroll
-        for (int u = 0; u < 4; ++u) sc[4 * e4 + u] = st[4 * e4 + u] * (float)gam[e4][u];
-    } else {
-#pragma unroll
-      for (int e4 = 0; e4 < 4; ++e4) {
-        const int t0 = (e4 < 2 ? e.x : e.z) * PAGE + 8 * (e4 & 1) + 4 * lg;
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-          sc[4 * e4 + u] = t0 + u <= lim ? st[4 * e4 + u] * (float)gam[e4][u] : -INFINITY;
+        for (int t = 0; t < 3; ++t)
+          st = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(A, qt[t][s], st, 0, 0, 0, 0, 0, 0);
       }
-    }
-    const bool moved = softmax(sc, alpha);
-    split8(sc, w.ha, w.la);
-    split8(sc + 8, w.hb, w.lb);
-    const float ra_ = ((sc[0] + sc[1]) + (sc[2] + sc[3])) + ((sc[4] + sc[5]) + (sc[6] + sc[7]));
-    const float rb_ = ((sc[8] + sc[9]) + (sc[10] + sc[11])) + ((sc[12] + sc[13]) + (sc[14] + sc[15]));
-    uint32_t zh, zl;
-    split2(ra_, rb_, zh, zl);
-    w.z = h8u(zh, zl, 0u, 0u);  // (R_a, R_b) hi, then lo
-    return moved;
-  };
-  // O^T += V^T P^T for the TQ3 pair in ring slot ra, with exact V operands:
-  // v = zero + scale * code is split as scale_hi * code + scale_lo * code +
-  // zero, scale_hi keeping 8 significant bits of the fp16 scale (so 3-bit
-  // codes times it are exact in fp16) and scale_lo the remaining 3.  The
-  // products that reach fp32 accuracy: (hi + lo weights) x scale_hi term, hi
-  // weights x scale_lo term (lo x scale_lo sits below 2^-19 of the value), and
-  // the zero term as zero_a (sum of weights over page a) + zero_b (same for
-  // b), whose sums the MFMA completes across the two lane groups.
-  auto tq3_pv = [&](const uint8_t* ra, const TqW& w) {
-    uint32_t va0[NDW], va2[NDW], vb0[NDW], vb2[NDW];
-    read_chunk<NDW>(va0, ra + 6 * D, 16 * lg + rrow);
-    read_chunk<NDW>(va2, ra + 6 * D, 16 * (lg + 2) + rrow);
-    read_chunk<NDW>(vb0, ra + R3 + 6 * D, 16 * lg + rrow);
-    read_chunk<NDW>(vb2, ra + R3 + 6 * D, 16 * (lg + 2) + rrow);
-    const half2v* sca = reinterpret_cast<const half2v*>(ra + 12 * D + 32 + 2 * CL * rrow);
-    const half2v* zra = reinterpret_cast<const half2v*>(ra + 14 * D + 32 + 2 * CL * rrow);
-    const half2v* scb = reinterpret_cast<const half2v*>(ra + R3 + 12 * D + 32 + 2 * CL * rrow);
-    const half2v* zrb = reinterpret_cast<const half2v*>(ra + R3 + 14 * D + 32 + 2 * CL * rrow);
+    };
+    auto tq3_scores = [&](const uint8_t* kb, const float16v& st0, const float16v& st1, const int4& e,
+                          TqW& w, float& alpha) {
+      const float16v st = st0 + st1;
+      // element e: token 8 (e / 4) + 4 lg + e % 4 of the pair (page a below 16)
+      uint2 gw[4];
 #pragma unroll
-    for (int mb = 0; mb < NMB; ++mb) {
-      const half2v s2a = sca[mb], s2b = scb[mb];
-      const half2v sha = hi8x2(s2a), shb = hi8x2(s2b);
-      const half2v sah = bcast_half(sha, hh), sal = bcast_half(s2a - sha, hh);  // exact split
-      const half2v sbh = bcast_half(shb, hh), sbl = bcast_half(s2b - shb, hh);
-      const uint32_t ua0 = quad_pair_sel<NDW>(va0, mb, hh), ua2 = quad_pair_sel<NDW>(va2, mb, hh);
-      const uint32_t ub0 = quad_pair_sel<NDW>(vb0, mb, hh), ub2 = quad_pair_sel<NDW>(vb2, mb, hh);
-      const half2v a01 = cvt_code<false>(ua0), a23 = cvt_code<true>(ua0);
-      const half2v a45 = cvt_code<false>(ua2), a67 = cvt_code<true>(ua2);
-      const half2v b01 = cvt_code<false>(ub0), b23 = cvt_code<true>(ub0);
-      const half2v b45 = cvt_code<false>(ub2), b67 = cvt_code<true>(ub2);
-      const half8 A1a = h8(a01 * sah, a23 * sah, a45 * sah, a67 * sah);
-      const half8 A2a = h8(a01 * sal, a23 * sal, a45 * sal, a67 * sal);
-      const half8 A1b = h8(b01 * sbh, b23 * sbh, b45 * sbh, b67 * sbh);
-      const half8 A2b = h8(b01 * sbl, b23 * sbl, b45 * sbl, b67 * sbl);
-      const _Float16 za = bcast_half(zra[mb], hh)[0], zb = bcast_half(zrb[mb], hh)[0];
-      const half8 Az = half8{za, zb, za, zb, (_Float16)0.0f, (_Float16)0.0f, (_Float16)0.0f,
-                             (_Float16)0.0f};
-      acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(A1a, w.ha, acc[mb], 0, 0, 0);
-      acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(A2a, w.ha, acc[mb], 0, 0, 0);
-      acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(A1a, w.la, acc[mb], 0, 0, 0);
-      acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(A1b, w.hb, acc[mb], 0, 0, 0);
-      acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(A2b, w.hb, acc[mb], 0, 0, 0);
-      acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(A1b, w.lb, acc[mb], 0, 0, 0);
-      acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(Az, w.z, acc[mb], 0, 0, 0);
-    }
-  };
-  auto rescale = [&](float alpha) {
+      for (int e4 = 0; e4 < 4; ++e4) gw[e4] = *reinterpret_cast<const uint2*>(kb + LY::KX + 16 * e4 + 8 * lg);
+      float sc[16];
+      if ((max(e.x, e.z) + 1) * PAGE <= P0 + 1) {
+        // the pair lies wholly before the chunk's first query: no mask
 #pragma unroll
-    for (int mb = 0; mb < NMB; ++mb) acc[mb] *= alpha;  // column = this lane's row
-  };
+        for (int e4 = 0; e4 < 4; ++e4)
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            sc[4 * e4 + u] = st[4 * e4 + u] * qinv * (float)reinterpret_cast<const _Float16*>(&gw[e4])[u];
+      } else {
+#pragma unroll
+        for (int e4 = 0; e4 < 4; ++e4) {
+          const int t0 = (e4 < 2 ? e.x : e.z) * PAGE + 8 * (e4 & 1) + 4 * lg;
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            sc[4 * e4 + u] = t0 + u <= lim
+                                 ? st[4 * e4 + u] * qinv * (float)reinterpret_cast<const _Float16*>(&gw[e4])[u]
+                                 : -INFINITY;
+        }
+      }
+      const bool moved = softmax(sc, alpha);
+      split8(sc, w.ha, w.la);
+      split8(sc + 8, w.hb, w.lb);
+      const float ra_ = ((sc[0] + sc[1]) + (sc[2] + sc[3])) + ((sc[4] + sc[5]) + (sc[6] + sc[7]));
+      const float rb_ = ((sc[8] + sc[9]) + (sc[10] + sc[11])) + ((sc[12] + sc[13]) + (sc[14] + sc[15]));
+      uint32_t zh, zl;
+      split2(ra_, rb_, zh, zl);
+      w.z = h8u(zh, zl, 0u, 0u);  // (R_a, R_b) hi, then lo
+      return moved;
+    };
 
-  // ---- the stage loop.  The TQ3 phase is software-pipelined: pass j runs the
-  // PV product of stage j - 1 and the scores and softmax of stage j in one
-  // straight-line block.  A pass reads two ring slots (j - 1 and j); the
-  // barrier at its start frees the slot of stage j - 2 for stage j + CSLOTS - 2.
-  const int n_pre = min(CSLOTS - 2, n_st);
-  for (int k = 0; k < n_pre; ++k) issue(stage_at(c_iss, k), k);
-  build_q(true);
-  // Stage j's copies have landed (this wave's by its vmcnt, everyone's by the
-  // barrier); every wave is done with stage j - 2.
-  auto next_stage = [&](int j) {
-    if (j + CSLOTS - 2 <= n_st) {
-      if (wid < 2)
-        wait_vmcnt<(CSLOTS - 3) * (OPS_W + 1)>();
-      else
-        wait_vmcnt<(CSLOTS - 3) * OPS_W>();
-    } else {
-      wait_vmcnt<0>();
-    }
-    wait_lgkm0();  // this wave's reads of earlier stages are done
-    __builtin_amdgcn_s_barrier();
-    __asm__ __volatile__("" ::: "memory");
-    if (j + CSLOTS - 2 < n_st) issue(stage_at(c_iss, j + CSLOTS - 2), (j + CSLOTS - 2) % CSLOTS);
-  };
-  {
-    TqW w;  // weights of the stage whose PV is pending
-    if (st3 > 0) {
-      next_stage(0);
+    // ---- passes over the TQ3 pairs
+    if (st3 > 0) wait_for(0);
+    barrier();
+    if (st3 > 0) unpack(smem, kbuf, vbuf);
+    int4 e_cmp = stage_at(0);  // the entries of the stage being scored
+    for (int j = 0; j < st3; ++j) {
+      if (j + 1 < st3) wait_for(j + 1);
+      barrier();  // pair j unpacked; its raw slot is free
+      float16v st0, st1;
+      tq3_qk(kbuf + (j & 1) * LY::KB, st0, st1);
+      refill(j);
+      const int4 e = e_cmp;
+      TqW w;
       float alpha;
-      (void)tq3_scores(smem, stage_at(c_cmp, 0), w, alpha);  // accumulators still zero
+      const bool moved = tq3_scores(kbuf + (j & 1) * LY::KB, st0, st1, e, w, alpha);
+      put_weights(j, w, alpha, moved);
+      if (j + 1 < st3)
+        unpack(smem + ((j + 1) % CSLOTS) * STAGE, kbuf + ((j + 1) & 1) * LY::KB,
+               vbuf + ((j + 1) % 3) * LY::VB);
+      e_cmp = stage_at(j + 1);
+      prefetch_iss();
     }
-    for (int j = 1; j < st3; ++j) {
-      next_stage(j);
-      const int4 e = stage_at(c_cmp, j);
-      tq3_pv(smem + ((j - 1) % CSLOTS) * STAGE, w);
-      TqW wn;
-      float alpha;
-      if (tq3_scores(smem + (j % CSLOTS) * STAGE, e, wn, alpha)) rescale(alpha);
-      w = wn;
-    }
-    if (st3 > 0) tq3_pv(smem + ((st3 - 1) % CSLOTS) * STAGE, w);
-  }
-  if (st3 < n_st) build_q(false);  // plain queries for the FP8 pages
-  for (int j = st3; j < n_st; ++j) {
-    next_stage(j);
-    const int4 e = stage_at(c_cmp, j);
-    const uint8_t* ra = smem + (j % CSLOTS) * STAGE;
-    // ---------------- one FP8 page: score rows 0-15 are its tokens, 16-31 zero
-    // block-permuted page (see dma_fp8_page): 16-byte block 64 w + 16 Q + t
-    // holds bytes 16 w .. of token t's channel quarter Q (K), and of the
-    // lane-chunk (t, Q) (V)
-    const uint2* pk = reinterpret_cast<const uint2*>(ra);
-    const float2 ksv = *reinterpret_cast<const float2*>(ra + R8);
-    float16v st = {};
+    // ---- passes over the FP8 pages: plain queries as fp16 (bf16 -> fp16 is
+    // exact for the query range) against FP8 keys, straight from the ring.
+    // Lane (li, lg) holds, for k-step s, channels (D/2) lg + 8 s + b (b < 8)
+    // of its row.
+    if (st3 < n_st) {
+      half8 qop[NKS];
+      {
+        const uint16_t* qrow = qrow_ptr + (D / 2) * lg;
 #pragma unroll
-    for (int s = 0; s < NKS; ++s) {
-      const int Q = 2 * lg + s / KPC, off = 8 * (s % KPC);
-      half8 K = {};
-      if (li < 16) {
-        const uint2 kw = pk[2 * (64 * (off / 16) + 16 * Q + li) + (off / 8) % 2];
-        K = h8(cvt_lo(kw.x), cvt_hi(kw.x), cvt_lo(kw.y), cvt_hi(kw.y));
+        for (int s = 0; s < NKS; ++s) {
+          const uint4 raw = *reinterpret_cast<const uint4*>(qrow + 8 * s);
+          const uint16_t* hb = reinterpret_cast<const uint16_t*>(&raw);
+#pragma unroll
+          for (int j = 0; j < 8; ++j) qop[s][j] = (_Float16)bf16_to_f32(hb[j]);
+        }
       }
-      st = __builtin_amdgcn_mfma_f32_32x32x16_f16(K, qop[s], st, 0, 0, 0);
-    }
-    float sc[16];
-    {
-      const float kk = ksv.x;
+      for (int j = st3; j < n_st; ++j) {
+        wait_for(j);
+        barrier();  // page j visible
+        refill(j);
+        const int4 e = e_cmp;
+        e_cmp = stage_at(j + 1);
+        prefetch_iss();
+        const uint8_t* ra = smem + (j % CSLOTS) * STAGE;
+        // block-permuted page (see dma_fp8_page): 16-byte block 64 w + 16 Q
+        // + t holds bytes 16 w .. of token t's channel quarter Q (K); score
+        // rows 0-15 are the page's tokens, 16-31 zero
+        const uint2* pk = reinterpret_cast<const uint2*>(ra);
+        const float2 ksv = *reinterpret_cast<const float2*>(ra + R8);
+        float16v st = {};
 #pragma unroll
-      for (int e4 = 0; e4 < 4; ++e4) {
-        const int t0 = e.x * PAGE + 8 * (e4 & 1) + 4 * lg;
+        for (int s = 0; s < NKS; ++s) {
+          const int Q = 2 * lg + s / KPC, off = 8 * (s % KPC);
+          half8 K = {};
+          if (li < 16) {
+            const uint2 kw = pk[2 * (64 * (off / 16) + 16 * Q + li) + (off / 8) % 2];
+            K = h8(cvt_lo(kw.x), cvt_hi(kw.x), cvt_lo(kw.y), cvt_hi(kw.y));
+          }
+          st = __builtin_amdgcn_mfma_f32_32x32x16_f16(K, qop[s], st, 0, 0, 0);
+        }
+        float sc[16];
+        const float kk = ksv.x * smk;
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
-          sc[4 * e4 + u] = (e4 < 2 && t0 + u <= lim) ? st[4 * e4 + u] * kk : -INFINITY;
+        for (int e4 = 0; e4 < 4; ++e4) {
+          const int t0 = e.x * PAGE + 8 * (e4 & 1) + 4 * lg;
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            sc[4 * e4 + u] = (e4 < 2 && t0 + u <= lim) ? st[4 * e4 + u] * kk : -INFINITY;
+        }
+        float alpha;
+        const bool moved = softmax(sc, alpha);
+        // the page's V scale folded into the weights
+        float pw[8];
+#pragma unroll
+        for (int k = 0; k < 8; ++k) pw[k] = sc[k] * ksv.y;
+        TqW w;
+        split8(pw, w.ha, w.la);
+        w.hb = w.la;
+        w.lb = w.la;
+        w.z = w.la;
+        put_weights(j, w, alpha, moved);
       }
     }
-    float alpha;
-    if (softmax(sc, alpha)) rescale(alpha);
-    // the page's V scale folded into the weights
-    float pw[8];
+    barrier();  // the PV waves' last pass
+    if (__any(bad_id) && lane == 0) atomicOr(&P.ctrl[CTRL_ERR], (int)MKV_DEVERR_RANGE);
+    const float L = l_run + lane_xor<32>(l_run, lane);
+    if (lg == 0) lbuf[sw * 32 + li] = L;
+    barrier();
+  } else {
+    // ========================= PV waves =========================
+    // accumulators: O^T tile (32 channels x the 32 query rows) per block mb.
+    // Lane (li, lg), element e holds query row rb + li and tile row rr = 8
+    // (e / 4) + 4 lg + e % 4, which is channel CL (rr % 16) + 2 mb + rr / 16
+    // (the value unpacking lays its operands out for this order).
+    float16v acc[NMB];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) pw[k] = sc[k] * ksv.y;
-    half8 pH, pL;
-    split8(pw, pH, pL);
-    // lane-chunks (rrow, lg) and (rrow, lg + 2) of V: dword m = tokens
-    // 4 g' .. 4 g' + 3 of channel CL rrow + m
-    const uint2* pv = reinterpret_cast<const uint2*>(ra + PAGE * D);
+    for (int mb = 0; mb < NMB; ++mb) acc[mb] = float16v{};
+    // the weights of stage j, after the rescale they carry
+    auto get_weights = [&](int j, TqW& w) {
+      const uint8_t* ws = wslot(j);
+      if (*reinterpret_cast<const int*>(ws + LY::WF_FLAG)) {
+        const float alpha = reinterpret_cast<const float*>(ws + LY::WF_ALPHA)[lane];
 #pragma unroll
-    for (int mb = 0; mb < NMB; ++mb) {
-      const int blk = 64 * (mb / 2);
-      const uint2 v0 = pv[2 * (blk + 16 * lg + rrow) + (mb & 1)];
-      const uint2 v2 = pv[2 * (blk + 16 * (lg + 2) + rrow) + (mb & 1)];
-      const uint32_t w0 = hh ? v0.y : v0.x, w2 = hh ? v2.y : v2.x;
-      const half8 Av = h8(cvt_lo(w0), cvt_hi(w0), cvt_lo(w2), cvt_hi(w2));
-      acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(Av, pH, acc[mb], 0, 0, 0);
-      acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(Av, pL, acc[mb], 0, 0, 0);
-    }
-  }
-
-  if (__any(bad_id) && lane == 0) atomicOr(&P.ctrl[CTRL_ERR], (int)MKV_DEVERR_RANGE);
-  // ---- normalize and store: tile row rr = 8 kk + 4 lg + u (kk, u: the
-  // lane's elements 4 kk + u and 8 + 4 kk + u) is chunk row rr % 16 = rr
-  // for both halves hh = 0, 1 of every block, so channels CL rr .. CL rr + CL
-  // - 1 are contiguous: channel CL rr + 2 mb + hh <- acc[mb][4 kk + 8 hh + u]
-  const float L = l_run + lane_xor<32>(l_run, lane);
-  if (rho_l < rows_r) {
-    const float inv = L > 0.0f ? 1.0f / L : 0.0f;
-    float* o = a.out + ((int64_t)(q0 + rho_l / G) * Hq + h * G + rho_l % G) * D;
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int rr = 8 * kk + 4 * lg + u;
-#pragma unroll
-        for (int v = 0; v < NMB / 2; ++v)
-          *reinterpret_cast<float4*>(o + CL * rr + 4 * v) =
-              make_float4(acc[2 * v][4 * kk + u] * inv, acc[2 * v][4 * kk + 8 + u] * inv,
-                          acc[2 * v + 1][4 * kk + u] * inv, acc[2 * v + 1][4 * kk + 8 + u] * inv);
+        for (int mb = 0; mb < NMB; ++mb) acc[mb] *= alpha;  // column = this lane's row
       }
+      w.ha = *reinterpret_cast<const half8*>(ws + 0 * 1024 + 16 * lane);
+      w.la = *reinterpret_cast<const half8*>(ws + 1 * 1024 + 16 * lane);
+      w.hb = *reinterpret_cast<const half8*>(ws + 2 * 1024 + 16 * lane);
+      w.lb = *reinterpret_cast<const half8*>(ws + 3 * 1024 + 16 * lane);
+      w.z = *reinterpret_cast<const half8*>(ws + 4 * 1024 + 16 * lane);
+    };
+    // O^T += V^T P^T for the TQ3 pair unpacked in vb, with exact V operands:
+    // v = zero + scale * code is split as scale_hi * code + scale_lo * code
+    // + zero.  The products that reach fp32 accuracy: (hi + lo weights) x
+    // scale_hi term, hi weights x scale_lo term (lo x scale_lo sits below
+    // 2^-19 of the value), and the zero term as zero_a (sum of weights over
+    // page a) + zero_b (same for b), whose sums the MFMA completes across
+    // the two lane groups.
+    auto tq3_pv = [&](const uint8_t* vb, const TqW& w) {
+      const _Float16* zx = reinterpret_cast<const _Float16*>(vb + LY::VX + LY::SX);
+      // software pipeline over the blocks: the LDS reads of block mb + 2 and
+      // the operand building of block mb + 1 run between the MFMAs of block mb
+      struct Raw {
+        uint2 cw[2];
+        half2v s2[2];
+        _Float16 za, zb;
+      };
+      struct Ops {
+        half8 A1[2], A2[2], Az;
+      };
+      auto load = [&](int mb, Raw& x) {
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+          x.cw[p] = *reinterpret_cast<const uint2*>(vb + ((p * NMB + mb) * 64 + lane) * 8);
+          x.s2[p] = *reinterpret_cast<const half2v*>(vb + LY::VX + ((p * NMB + mb) * 32 + li) * 4);
+        }
+        x.za = zx[mb * 32 + li];
+        x.zb = zx[(NMB + mb) * 32 + li];
+      };
+      auto build = [&](const Raw& x, Ops& o) {
+#pragma unroll
+        for (int p = 0; p < 2; ++p) {
+          const half2v sh = bcast(x.s2[p][0]), sl = bcast(x.s2[p][1]);
+          const half2v c01 = cvt_code<false>(x.cw[p].x), c23 = cvt_code<true>(x.cw[p].x);
+          const half2v c45 = cvt_code<false>(x.cw[p].y), c67 = cvt_code<true>(x.cw[p].y);
+          o.A1[p] = h8(c01 * sh, c23 * sh, c45 * sh, c67 * sh);
+          o.A2[p] = h8(c01 * sl, c23 * sl, c45 * sl, c67 * sl);
+        }
+        o.Az = half8{x.za, x.zb, x.za, x.zb, (_Float16)0.0f, (_Float16)0.0f, (_Float16)0.0f,
+                     (_Float16)0.0f};
+      };
+      Raw xr[2];
+      Ops op[2];
+      load(0, xr[0]);
+      if (NMB > 1) load(1, xr[1]);
+      build(xr[0], op[0]);
+#pragma unroll
+      for (int mb = 0; mb < NMB; ++mb) {
+        const Ops& o = op[mb & 1];
+        if (mb + 1 < NMB) build(xr[(mb + 1) & 1], op[(mb + 1) & 1]);
+        if (mb + 2 < NMB) load(mb + 2, xr[mb & 1]);
+        acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(o.A1[0], w.ha, acc[mb], 0, 0, 0);
+        acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(o.A2[0], w.ha, acc[mb], 0, 0, 0);
+        acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(o.A1[0], w.la, acc[mb], 0, 0, 0);
+        acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(o.A1[1], w.hb, acc[mb], 0, 0, 0);
+        acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(o.A2[1], w.hb, acc[mb], 0, 0, 0);
+        acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(o.A1[1], w.lb, acc[mb], 0, 0, 0);
+        acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(o.Az, w.z, acc[mb], 0, 0, 0);
+        // one MFMA, then a share of the next block's VALU and LDS work
+        if (mb + 1 < NMB) {
+#pragma unroll
+          for (int k = 0; k < 7; ++k) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+            __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);  // VALU
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+          }
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    };
+    // O^T += V^T P^T for the FP8 page in ring slot ra (weights hi + lo, the
+    // page's V scale already folded in): lane-chunks (rrow, lg) and (rrow,
+    // lg + 2) of V, dword m = tokens 4 g' .. 4 g' + 3 of channel CL rrow + m
+    auto fp8_pv = [&](const uint8_t* ra, const TqW& w) {
+      const int rrow = li & 15, hh = li >> 4;
+      const uint2* pv = reinterpret_cast<const uint2*>(ra + PAGE * D);
+#pragma unroll
+      for (int mb = 0; mb < NMB; ++mb) {
+        const int blk = 64 * (mb / 2);
+        const uint2 v0 = pv[2 * (blk + 16 * lg + rrow) + (mb & 1)];
+        const uint2 v2 = pv[2 * (blk + 16 * (lg + 2) + rrow) + (mb & 1)];
+        const uint32_t w0 = hh ? v0.y : v0.x, w2 = hh ? v2.y : v2.x;
+        const half8 Av = h8(cvt_lo(w0), cvt_hi(w0), cvt_lo(w2), cvt_hi(w2));
+        acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(Av, w.ha, acc[mb], 0, 0, 0);
+        acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(Av, w.la, acc[mb], 0, 0, 0);
+      }
+    };
+    barrier();  // the score waves' first unpacking
+    barrier();  // pass 0: the weights of stage 0
+    for (int j = 0; j < st3; ++j) {  // pass j + 1
+      barrier();
+      TqW w;
+      get_weights(j, w);
+      tq3_pv(vbuf + (j % 3) * LY::VB, w);
+    }
+    for (int j = st3; j < n_st; ++j) {
+      barrier();
+      TqW w;
+      get_weights(j, w);
+      fp8_pv(smem + (j % CSLOTS) * STAGE, w);
+    }
+    barrier();  // the rows' denominators
+    // ---- normalize and store: tile row rr = 8 kk + 4 lg + u (kk, u: the
+    // lane's elements 4 kk + u and 8 + 4 kk + u) is chunk row rr % 16 = rr
+    // for both halves hh = 0, 1 of every block, so channels CL rr .. CL rr +
+    // CL - 1 are contiguous: channel CL rr + 2 mb + hh <- acc[mb][4 kk + 8
+    // hh + u]
+    if (rho_l < rows_r) {
+      const float L = lbuf[sw * 32 + li];
+      const float inv = L > 0.0f ? 1.0f / L : 0.0f;
+      float* o = a.out + ((int64_t)(q0 + rho_l / G) * Hq + h * G + rho_l % G) * D;
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int rr = 8 * kk + 4 * lg + u;
+#pragma unroll
+          for (int v = 0; v < NMB / 2; ++v)
+            *reinterpret_cast<float4*>(o + CL * rr + 4 * v) =
+                make_float4(acc[2 * v][4 * kk + u] * inv, acc[2 * v][4 * kk + 8 + u] * inv,
+                            acc[2 * v + 1][4 * kk + u] * inv, acc[2 * v + 1][4 * kk + 8 + u] * inv);
+        }
+    }
   }
 }
 
@@ -626,14 +844,13 @@ hipError_t launch_chunk(const PoolView& P, int layer, int n_req, const uint16_t*
   hipError_t e = launch_partition(n_req, bt, tags, max_pages, seq_lens, list8, list3, counts,
                                   P.ctrl + CTRL_ERR, s);
   if (e != hipSuccess) return e;
-  const size_t lds = (size_t)CSLOTS * 2 * tq3_region_bytes(P.d) +  // the shared ring
-                     (size_t)CW * (P.d / 16) * 64 * 16;              // rotated-query low parts
+  const size_t lds = P.d == 256 ? (size_t)ChunkLds<256>::TOTAL : (size_t)ChunkLds<128>::TOTAL;
   const void* kern = P.d == 256 ? (const void*)chunk_kernel<256> : (const void*)chunk_kernel<128>;
   e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
   // rows of one request: at most n_q_total queries x group heads
   const int64_t rows = (int64_t)n_q_total * P.group;
-  const int wg_rows = CW * 32;
+  const int wg_rows = NSW * 32;
   const int blocks = (int)((rows + wg_rows - 1) / wg_rows);
   dim3 grid(blocks, P.n_kv_heads, n_req);
   void* args[] = {&a};
