@@ -5,32 +5,34 @@
 // rotated queries against TQ3 key codes times the FP16 key-norm correction,
 // plain queries against FP8 keys, one online softmax per query row.
 //
-// Launch: one partition kernel (compact per-format lists, Sec. 4.1) and one
-// attention kernel.  Grid (row block, KV head, request); 256 threads = 4
-// waves, one workgroup per CU.  A query row is a (query token, head of the
-// GQA group) pair; each wave owns one tile of 32 rows.  The workgroup streams
-// every page of its request, TQ3 pairs first and FP8 pages after, through one
-// LDS ring shared by its waves: each wave issues a quarter of every stage's
-// direct HBM -> LDS copies, and one barrier per stage both publishes the
-// stage and frees the slot read two stages before.  All products run on
-// v_mfma_f32_32x32x16_f16 (on gfx950 it sustains about 1.7x the rate of the
-// 16x16x32 shape):
-//   S^T = K Q^T: M = 32 tokens (the two pages of a TQ3 pair; one FP8 page
-//                and 16 zero rows), N = the 32 query rows, K = 16 channels;
-//                TQ3 codes -> E4M3 codebook bytes (one v_perm per 4 codes)
-//                -> fp16 against the rotated query as an fp16 hi + lo pair
-//                (two MFMAs), FP8 keys -> fp16 against the plain query (exact
-//                in fp16, one MFMA);
-//   online softmax per query row in base 2 (lazy rescale, threshold 2^8),
-//                causal mask token <= position of the query;
-//   O^T += V^T P^T: M = 32 channels, N = the 32 query rows, K = the 16
-//                tokens of one page: a lane's score outputs are exactly the 8
-//                tokens per page its weight operand holds, so the weights
-//                never move between lanes.  Weights as an fp16 hi + lo pair;
-//                TQ3 values as exact fp16 operands (high and low parts of
-//                scale * code) with the zero term as one rank-2 product of
-//                the pages' zeros and weight sums per stage; FP8 values
-//                exact, the page's V scale folded into the weights.
+// Launch: the partition kernel (compact per-format lists, Sec. 4.1), a stage
+// table kernel (per request: the TQ3 pages in pairs, then the FP8 pages) and
+// the attention kernel.  Grid (row block, KV head, request); 512 threads =
+// 8 waves, one workgroup per CU, two waves per SIMD.  A query row is a
+// (query token, head of the GQA group) pair; a workgroup owns 128 rows, and
+// its waves come in pairs over 32 rows each:
+//  * a score wave holds its rows' rotated queries as three E4M3 terms in
+//    registers, copies its share of every stage (direct HBM -> LDS copies
+//    into a ring of eight stages) and of the stage table, unpacks its share
+//    of the next TQ3 pair into MFMA operand layouts in LDS (key codes ->
+//    E4M3 codebook bytes, value codes as bytes, the V scale split for exact
+//    fp16 products), and computes S^T = K Q^T on
+//    v_mfma_f32_32x32x64_f8f6f4 (M = the pair's 32 tokens, N = the 32 rows,
+//    K = 64 channels; three MFMAs per k-step, one per query term), the
+//    causal mask, the online softmax in base 2 (lazy rescale, threshold 2^8)
+//    and the weights as fp16 hi + lo pairs, which it hands over in LDS;
+//  * a PV wave holds the rows' O^T accumulators (32 channels x 32 rows per
+//    block) and computes O^T += V^T P^T on v_mfma_f32_32x32x16_f16 (M = 32
+//    channels, N = the 32 rows, K = the 16 tokens of one page; a lane's
+//    score outputs are exactly the 8 tokens per page its weight operand
+//    holds): values as exact fp16 operands (scale_hi * code, scale_lo *
+//    code), the zero term as one rank-2 product of the pages' zeros and
+//    weight sums, applying the rescale the score wave passed along first.
+// Pass i (one barrier): the score waves take stage i while the PV waves take
+// stage i - 1.  FP8 pages: the score wave scores them on the f16 MFMA against
+// the plain query (the fp8 MFMA keeps too few bits where FP8 keys carry
+// large norms) with one zero-padded half of the tile, and folds the page's V
+// scale into the weights; the PV wave reads the page's values from the ring.
 // The workgroups of one (request, KV head) read the same pages at about the
 // same time, so the page bytes come from L2 after the first reader.
 #include <hip/hip_runtime.h>
@@ -45,8 +47,7 @@ namespace mkv {
 
 constexpr int NSW = 4;       // score waves per chunk workgroup (one PV wave each)
 constexpr int CW = 2 * NSW;  // waves per chunk workgroup
-constexpr int CSLOTS = 8;    // raw stages in the shared ring (copies of scattered pages
-                             // take several microseconds to land)
+constexpr int CSLOTS = 8;    // raw stages in the shared ring
 constexpr int CMASK_LP = 0x3FFFFFFF / PAGE;
 
 struct ChunkArgs {
@@ -59,16 +60,68 @@ struct ChunkArgs {
   const int32_t* list8;   // [n_req][max_pages][2] (logical page, physical id)
   const int32_t* list3;
   const int32_t* counts;  // [n_req][2] (n_fp8, n_tq3)
+  const int4* stages;     // [n_req][max_pages] stage table (chunk_stages_kernel)
   float sm_log2;          // log2(e) / sqrt(d)
 };
 
 static size_t al256(size_t b) { return (b + 255) / 256 * 256; }
 
-// workspace: the two compact lists and their counts
+// workspace: the two compact lists, their counts and the stage table (one
+// int4 per stage; the chunk kernel copies it in 1 KiB blocks, so 1 KiB of
+// slack after it keeps the last block inside the workspace)
+struct ChunkWs {
+  size_t list8, list3, counts, stages, total;
+};
+static ChunkWs chunk_ws(int n_req, int max_pages) {
+  ChunkWs w;
+  const size_t lb = al256((size_t)n_req * max_pages * 2 * sizeof(int32_t));
+  w.list8 = 0;
+  w.list3 = lb;
+  w.counts = 2 * lb;
+  w.stages = w.counts + al256((size_t)n_req * 2 * sizeof(int32_t));
+  w.total = w.stages + al256((size_t)n_req * max_pages * sizeof(int4) + 1024);
+  return w;
+}
 size_t chunk_ws_bytes(int n_req, int max_pages, int n_q_total, int n_kv_heads, int group, int d) {
   (void)n_q_total; (void)n_kv_heads; (void)group; (void)d;
-  return 2 * al256((size_t)n_req * max_pages * 2 * sizeof(int32_t)) +
-         al256((size_t)n_req * 2 * sizeof(int32_t));
+  return chunk_ws(n_req, max_pages).total;
+}
+
+// Stage table of a chunk call: per request, stage j -> {lp_a, id_a, lp_b,
+// id_b}: the TQ3 pages in pairs (list entries 2 j, 2 j + 1; a missing page b
+// is masked) first, then the FP8 pages one per stage (id_b = -1).  Ids
+// outside the pool become page 0 with every token masked, and set the range
+// error bit.
+__global__ __launch_bounds__(256) void chunk_stages_kernel(int max_pages, int n_tq3, int n_fp8,
+                                                           const int32_t* list8,
+                                                           const int32_t* list3,
+                                                           const int32_t* counts, int4* stages,
+                                                           int32_t* err) {
+  const int r = blockIdx.y, j = blockIdx.x * 256 + threadIdx.x;
+  const int n8 = counts[2 * r], n3 = counts[2 * r + 1];
+  const int st3 = (n3 + 1) / 2, n_st = st3 + n8;  // at most the request's pages
+  if (j >= n_st) return;
+  const int2* l3 = reinterpret_cast<const int2*>(list3) + (int64_t)r * max_pages;
+  const int2* l8 = reinterpret_cast<const int2*>(list8) + (int64_t)r * max_pages;
+  bool bad = false;
+  auto checked = [&](int2 e, int n_ids) {
+    if (e.y < 0 || e.y >= n_ids) {
+      bad = true;
+      return make_int2(CMASK_LP, 0);
+    }
+    return e;
+  };
+  int4 st;
+  if (j < st3) {
+    const int2 ea = checked(l3[2 * j], n_tq3);
+    const int2 eb = 2 * j + 1 < n3 ? checked(l3[2 * j + 1], n_tq3) : make_int2(CMASK_LP, ea.y);
+    st = make_int4(ea.x, ea.y, eb.x, eb.y);
+  } else {
+    const int2 e = checked(l8[j - st3], n_fp8);
+    st = make_int4(e.x, e.y, 0, -1);
+  }
+  stages[(int64_t)r * max_pages + j] = st;
+  if (bad) atomicOr(err, (int)MKV_DEVERR_RANGE);
 }
 
 // fp16 value with its low 3 significand bits cleared (8 significant bits left)
@@ -95,8 +148,9 @@ constexpr float CM_INIT = -1.0e30f;  // running max before the first score (fini
 
 // LDS of a chunk workgroup (bytes): the ring of raw stages, two buffers of
 // unpacked key operands, three of unpacked value operands, two of the
-// weights the score waves hand to the PV waves, and the rows' softmax
-// denominators for the final normalization.
+// weights the score waves hand to the PV waves, the rows' softmax
+// denominators for the final normalization, and three blocks of the stage
+// table.
 template <int D>
 struct ChunkLds {
   static constexpr int NK8 = D / 64, NMB = D / 32;
@@ -114,7 +168,8 @@ struct ChunkLds {
   static constexpr int VB0 = KB0 + 2 * KB;
   static constexpr int WB0 = VB0 + 3 * VB;
   static constexpr int LB0 = WB0 + 2 * NSW * WPW;     // row denominators [score wave][32]
-  static constexpr int TOTAL = LB0 + NSW * 32 * 4;
+  static constexpr int LS0 = LB0 + NSW * 32 * 4;      // stage-table blocks [3][64 stages][16]
+  static constexpr int TOTAL = LS0 + 3 * 1024;
   static_assert(KB % 16 == 0 && VB % 16 == 0 && STAGE % 16 == 0 && WPW % 16 == 0,
                 "16-byte aligned buffers");
   static_assert(TOTAL <= 160 * 1024, "one workgroup's LDS");
@@ -203,39 +258,25 @@ __global__ __launch_bounds__(64 * CW, 1) void chunk_kernel(ChunkArgs a) {
   // handed over in pass i - 1.
   if (score_wave) {
     // ======================= score waves =======================
+    // The score waves are the critical path of every pass (their weights
+    // feed the next one; the PV waves have slack): the SIMD's arbiter takes
+    // their instructions first and fills the gaps with the PV waves'.
+    __builtin_amdgcn_s_setprio(2);
     const int rho_c = min(rho_l, rows_r - 1);  // a valid row to load for masked lanes
     const uint16_t* qrow_ptr = a.q + ((int64_t)(q0 + rho_c / G) * Hq + h * G + rho_c % G) * D;
-    const int2* l3 = reinterpret_cast<const int2*>(a.list3) + (int64_t)r * mp;
-    const int2* l8 = reinterpret_cast<const int2*>(a.list8) + (int64_t)r * mp;
-    // (logical page, physical id) of a list entry; out-of-range ids read
-    // page 0 with every token masked and are reported after the loop (no
-    // memory writes while copies are in flight)
-    bool bad_id = false;
-    auto checked = [&](int2 e, int n_ids) {
-      if (e.y < 0 || e.y >= n_ids) {
-        bad_id = true;
-        return make_int2(CMASK_LP, 0);
-      }
-      return e;
-    };
-    // List entries are wave-uniform: scalar loads through the constant
-    // address space (tracked by lgkmcnt, so waiting for them never drains
-    // the page copies in flight), each issued one pass before its use.
-    typedef __attribute__((address_space(4))) const int cint;
-    cint* l3c = (cint*)(uintptr_t)l3;
-    cint* l8c = (cint*)(uintptr_t)l8;
-    auto ent = [&](cint* l, int k) { return make_int2(l[2 * k], l[2 * k + 1]); };
+    const uint8_t* stab = reinterpret_cast<const uint8_t*>(a.stages + (int64_t)r * mp);
+    // The stage table reaches LDS in blocks of 64 stages (1 KiB), three
+    // buffers, copied by every score wave itself with the counted copies of
+    // the pages (so its own wait for a page makes the block visible to it);
+    // block k + 1 is copied just before the first page of block k.
+    const uint8_t* lsb = smem + LY::LS0;
     // stage j -> {lp_a, id_a, lp_b, id_b}; id_b < 0 marks an FP8 stage
     auto stage_at = [&](int j) {
       j = __builtin_amdgcn_readfirstlane(j);
       if (j >= n_st) return make_int4(CMASK_LP, 0, CMASK_LP, 0);  // past the list: never used
-      if (j < st3) {
-        const int2 ea = checked(ent(l3c, 2 * j), P.n_tq3);
-        const int2 eb = 2 * j + 1 < n3 ? checked(ent(l3c, 2 * j + 1), P.n_tq3) : make_int2(CMASK_LP, ea.y);
-        return make_int4(ea.x, ea.y, eb.x, eb.y);
-      }
-      const int2 e = checked(ent(l8c, j - st3), P.n_fp8);
-      return make_int4(e.x, e.y, 0, -1);
+      const int4 v = *reinterpret_cast<const int4*>(lsb + ((j >> 6) % 3) * 1024 + (j & 63) * 16);
+      return make_int4(__builtin_amdgcn_readfirstlane(v.x), __builtin_amdgcn_readfirstlane(v.y),
+                       __builtin_amdgcn_readfirstlane(v.z), __builtin_amdgcn_readfirstlane(v.w));
     };
     const int layer = a.layer;
     const uint8_t* tq3_l = P.tq3 + (int64_t)layer * P.n_tq3 * H * R3;
@@ -290,7 +331,15 @@ __global__ __launch_bounds__(64 * CW, 1) void chunk_kernel(ChunkArgs a) {
     // waves in pass s + 1).  A wait for stage s lets the copies of the
     // stages after it stay in flight (every stage costs a wave the same
     // copies).
+    const uint32_t lst_lds = ring_lds + LY::LS0;
+    auto issue_list = [&](int k) {  // block k of the stage table -> buffer k % 3
+      dma16<0>(16u * lane, stab + 1024 * k, lst_lds + (k % 3) * 1024);
+    };
+    const int n_blk = (n_st + 63) / 64;
     int issued = 0;
+    issue_list(0);
+    if (n_blk > 1) issue_list(1);
+    wait_vmcnt<0>();
     int4 e_iss = stage_at(0);  // the entries of stage `issued`
     auto refill = [&](int pass) {
       bool fresh = true;  // e_iss holds stage `issued`
@@ -298,6 +347,7 @@ __global__ __launch_bounds__(64 * CW, 1) void chunk_kernel(ChunkArgs a) {
         const int prev = issued - CSLOTS;
         if (prev >= 0 && (prev < st3 ? prev : prev + 2) > pass) break;
         if (!fresh) e_iss = stage_at(issued);
+        if ((issued & 63) == 0 && issued > 0 && (issued >> 6) + 1 < n_blk) issue_list((issued >> 6) + 1);
         issue(e_iss, issued % CSLOTS);
         ++issued;
         fresh = false;
@@ -483,32 +533,33 @@ __global__ __launch_bounds__(64 * CW, 1) void chunk_kernel(ChunkArgs a) {
     //  per (page, block, row rr): the V scale split as (hi, lo) fp16 (hi
     //    keeps 8 significant bits, so code x hi is exact in fp16) and the V
     //    zero; gamma of both pages after the key bytes.
-    auto unpack = [&](const uint8_t* rs, uint8_t* kb, uint8_t* vb) {
-      if (tid < 128) {
-        const int p = tid >> 6, tok = tid & 15, g = (tid >> 4) & 3;
-        uint32_t dw[NDW];
-        read_chunk<NDW>(dw, rs + p * R3, 16 * g + tok);
+    auto unpack_k = [&](const uint8_t* rs, uint8_t* kb) {  // threads 0-127
+      const int p = tid >> 6, tok = tid & 15, g = (tid >> 4) & 3;
+      uint32_t dw[NDW];
+      read_chunk<NDW>(dw, rs + p * R3, 16 * g + tok);
 #pragma unroll
-        for (int q8 = 0; q8 < CL / 8; ++q8) {
-          uint32_t o[8];
+      for (int q8 = 0; q8 < CL / 8; ++q8) {
+        uint32_t o[8];
 #pragma unroll
-          for (int w = 0; w < 8; ++w) o[w] = __builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(dw, 8 * q8 + w));
-          const int c0 = g * QQ + 32 * q8;  // first channel of these 32 bytes
-          uint4* dst = reinterpret_cast<uint4*>(kb + ((c0 / 64) * 64 + 32 * ((c0 / 32) & 1) + 16 * p + tok) * 32);
-          dst[0] = make_uint4(o[0], o[1], o[2], o[3]);
-          dst[1] = make_uint4(o[4], o[5], o[6], o[7]);
-        }
-      } else {
-        const int u = tid - 128;
-        const int p = u >> 6, r0 = u & 15, g = (u >> 4) & 3;
-        uint32_t dw[NDW];
-        read_chunk<NDW>(dw, rs + p * R3 + 6 * D, 16 * g + r0);
-        uint8_t* base = vb + (p * NMB * 64 + 32 * (g & 1) + r0) * 8 + 4 * (g >> 1);
-#pragma unroll
-        for (int q = 0; q < CL; ++q)
-          *reinterpret_cast<uint32_t*>(base + ((q >> 1) * 64 + 16 * (q & 1)) * 8) = quad_sel<NDW>(dw, q);
+        for (int w = 0; w < 8; ++w) o[w] = __builtin_amdgcn_perm(KLUT_HI, KLUT_LO, quad_sel<NDW>(dw, 8 * q8 + w));
+        const int c0 = g * QQ + 32 * q8;  // first channel of these 32 bytes
+        uint4* dst = reinterpret_cast<uint4*>(kb + ((c0 / 64) * 64 + 32 * ((c0 / 32) & 1) + 16 * p + tok) * 32);
+        dst[0] = make_uint4(o[0], o[1], o[2], o[3]);
+        dst[1] = make_uint4(o[4], o[5], o[6], o[7]);
       }
-      if (tid < NMB * 32) {
+    };
+    auto unpack_v = [&](const uint8_t* rs, uint8_t* vb) {  // threads 128-255
+      const int u = tid - 128;
+      const int p = u >> 6, r0 = u & 15, g = (u >> 4) & 3;
+      uint32_t dw[NDW];
+      read_chunk<NDW>(dw, rs + p * R3 + 6 * D, 16 * g + r0);
+      uint8_t* base = vb + (p * NMB * 64 + 32 * (g & 1) + r0) * 8 + 4 * (g >> 1);
+#pragma unroll
+      for (int q = 0; q < CL; ++q)
+        *reinterpret_cast<uint32_t*>(base + ((q >> 1) * 64 + 16 * (q & 1)) * 8) = quad_sel<NDW>(dw, q);
+    };
+    auto unpack_side = [&](const uint8_t* rs, uint8_t* kb, uint8_t* vb) {
+      if (tid < NMB * 32) {  // whole waves
         const int mb = tid >> 5, rr = tid & 31, ch = CL * (rr & 15) + 2 * mb + (rr >> 4);
 #pragma unroll
         for (int p = 0; p < 2; ++p) {
@@ -524,6 +575,13 @@ __global__ __launch_bounds__(64 * CW, 1) void chunk_kernel(ChunkArgs a) {
         *reinterpret_cast<uint32_t*>(kb + LY::KX + 4 * tid) =
             *reinterpret_cast<const uint32_t*>(rs + (tid >> 3) * R3 + 12 * D + 4 * (tid & 7));
     };
+    auto unpack = [&](const uint8_t* rs, uint8_t* kb, uint8_t* vb) {
+      if (wid < 2)
+        unpack_k(rs, kb);
+      else
+        unpack_v(rs, vb);
+      unpack_side(rs, kb, vb);
+    };
 
     // Scores and weights of the TQ3 pair e from its unpacked keys kb.  The
     // score tile's rows are the pair's 32 tokens (page a, then page b); lane
@@ -531,16 +589,48 @@ __global__ __launch_bounds__(64 * CW, 1) void chunk_kernel(ChunkArgs a) {
     // which are exactly the k-slots of its weight operand.
     // (the products are issued first; the rest of the pass's issue work
     // runs while they execute)
-    auto tq3_qk = [&](const uint8_t* kb, float16v& st0, float16v& st1) {
+    auto tq3_qk = [&](const uint8_t* kb, float16v& st0, float16v& st1, auto rev) {
       st0 = float16v{};
       st1 = float16v{};  // even and odd k-steps: two MFMA chains
 #pragma unroll
-      for (int s = 0; s < NK8; ++s) {
+      for (int s_ = 0; s_ < NK8; ++s_) {
+        const int s = decltype(rev)::value ? NK8 - 1 - s_ : s_;
         const v8i A = *reinterpret_cast<const v8i*>(kb + (s * 64 + lane) * 32);
         float16v& st = (s & 1) ? st1 : st0;
 #pragma unroll
         for (int t = 0; t < 3; ++t)
           st = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(A, qt[t][s], st, 0, 0, 0, 0, 0, 0);
+      }
+    };
+    // the score products of the pair in kb_cur with the unpacking of the next
+    // pair (raw stage rs) between them: one straight block per wave kind, so
+    // the unpacking's VALU work fills the MFMA latencies
+    auto qk_unpack = [&](const uint8_t* kb_cur, float16v& st0, float16v& st1, const uint8_t* rs,
+                         uint8_t* kb, uint8_t* vb) {
+      // (the two kinds take the k-steps in opposite orders, which keeps the
+      // compiler from hoisting the shared products out of both blocks)
+      if (wid < 2) {
+        tq3_qk(kb_cur, st0, st1, std::false_type{});
+        unpack_k(rs, kb);
+        unpack_side(rs, kb, vb);
+#pragma unroll
+        for (int k = 0; k < 3 * NK8; ++k) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+          __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);  // VALU
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+          __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // DS write
+        }
+      } else {
+        tq3_qk(kb_cur, st0, st1, std::true_type{});
+        unpack_v(rs, vb);
+        unpack_side(rs, kb, vb);
+#pragma unroll
+        for (int k = 0; k < 3 * NK8; ++k) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
+          __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);  // VALU
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+          __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // DS write
+        }
       }
     };
     auto tq3_scores = [&](const uint8_t* kb, const float16v& st0, const float16v& st1, const int4& e,
@@ -588,17 +678,17 @@ __global__ __launch_bounds__(64 * CW, 1) void chunk_kernel(ChunkArgs a) {
     for (int j = 0; j < st3; ++j) {
       if (j + 1 < st3) wait_for(j + 1);
       barrier();  // pair j unpacked; its raw slot is free
+      // (in the last pass the unpacking reads a slot that holds no pair and
+      // writes buffers nobody reads any more)
       float16v st0, st1;
-      tq3_qk(kbuf + (j & 1) * LY::KB, st0, st1);
+      qk_unpack(kbuf + (j & 1) * LY::KB, st0, st1, smem + ((j + 1) % CSLOTS) * STAGE,
+                kbuf + ((j + 1) & 1) * LY::KB, vbuf + ((j + 1) % 3) * LY::VB);
       refill(j);
       const int4 e = e_cmp;
       TqW w;
       float alpha;
       const bool moved = tq3_scores(kbuf + (j & 1) * LY::KB, st0, st1, e, w, alpha);
       put_weights(j, w, alpha, moved);
-      if (j + 1 < st3)
-        unpack(smem + ((j + 1) % CSLOTS) * STAGE, kbuf + ((j + 1) & 1) * LY::KB,
-               vbuf + ((j + 1) % 3) * LY::VB);
       e_cmp = stage_at(j + 1);
       prefetch_iss();
     }
@@ -666,7 +756,6 @@ __global__ __launch_bounds__(64 * CW, 1) void chunk_kernel(ChunkArgs a) {
       }
     }
     barrier();  // the PV waves' last pass
-    if (__any(bad_id) && lane == 0) atomicOr(&P.ctrl[CTRL_ERR], (int)MKV_DEVERR_RANGE);
     const float L = l_run + lane_xor<32>(l_run, lane);
     if (lg == 0) lbuf[sw * 32 + li] = L;
     barrier();
@@ -833,16 +922,22 @@ hipError_t launch_chunk(const PoolView& P, int layer, int n_req, const uint16_t*
   a.seq_lens = seq_lens;
   a.out = out;
   uint8_t* w = reinterpret_cast<uint8_t*>(ws);
-  const size_t lb = al256((size_t)n_req * max_pages * 2 * sizeof(int32_t));
-  int32_t* list8 = reinterpret_cast<int32_t*>(w);
-  int32_t* list3 = reinterpret_cast<int32_t*>(w + lb);
-  int32_t* counts = reinterpret_cast<int32_t*>(w + 2 * lb);
+  const ChunkWs wl = chunk_ws(n_req, max_pages);
+  int32_t* list8 = reinterpret_cast<int32_t*>(w + wl.list8);
+  int32_t* list3 = reinterpret_cast<int32_t*>(w + wl.list3);
+  int32_t* counts = reinterpret_cast<int32_t*>(w + wl.counts);
+  int4* stages = reinterpret_cast<int4*>(w + wl.stages);
   a.list8 = list8;
   a.list3 = list3;
   a.counts = counts;
+  a.stages = stages;
   a.sm_log2 = 1.4426950408889634f / sqrtf((float)P.d);
   hipError_t e = launch_partition(n_req, bt, tags, max_pages, seq_lens, list8, list3, counts,
                                   P.ctrl + CTRL_ERR, s);
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(chunk_stages_kernel, dim3((max_pages + 255) / 256, n_req), dim3(256), 0, s,
+                     max_pages, P.n_tq3, P.n_fp8, list8, list3, counts, stages, P.ctrl + CTRL_ERR);
+  e = hipGetLastError();
   if (e != hipSuccess) return e;
   const size_t lds = P.d == 256 ? (size_t)ChunkLds<256>::TOTAL : (size_t)ChunkLds<128>::TOTAL;
   const void* kern = P.d == 256 ? (const void*)chunk_kernel<256> : (const void*)chunk_kernel<128>;
