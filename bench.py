@@ -38,6 +38,7 @@ sys.path.insert(0, ROOT)
 import mkv_workloads as wl  # noqa: E402
 
 HBM_PEAK = 8.0e12  # MI355X HBM3E, bytes/s
+MFMA_FP8_PEAK = 5.0e15  # dense fp8 MFMA, MI355X
 MFMA_F16_PEAK = 2.5e15  # MI355X dense f16 MFMA, flop/s
 PAGE = 16
 
@@ -229,7 +230,10 @@ def chunk_bench(mk, torch, reps=5):
             "us_per_call": round(us, 1), "algorithmic_tflop": round(flops / 1e12, 3),
             "tflop_per_s": round(tf, 1), "mfma_peak_tflop_per_s": MFMA_F16_PEAK / 1e12,
             "mfma_frac": round(tf * 1e12 / MFMA_F16_PEAK, 4),
-            "kernel": "chunk_kernel<256> (+ partition_kernel)"}
+            "mfma_frac_of_fp8_peak": round(tf * 1e12 / MFMA_FP8_PEAK, 4),
+            "mfma_dtypes": "TQ3 scores on fp8 MFMA (3-term E4M3 query), PV and FP8-page scores "
+                           "on f16 MFMA (hi + lo operands), fp32 accumulate",
+            "kernel": "chunk_kernel<256> (+ partition_kernel, chunk_stages_kernel)"}
 
 
 class DenseControls:

@@ -223,25 +223,33 @@ __global__ __launch_bounds__(64 * CW_WAVES, 2) void bf16_decode_kernel(CtlArgs a
 }
 
 // Eq. softmax-merge over every wave partial of a (request, KV head): one
-// 64-thread workgroup per (query head of the group, KV head, request).  Per
+// 4-wave workgroup per (query head of the group, KV head, request); each wave
+// merges a quarter of the slots and the four results are merged in LDS.  Per
 // batch of 64 slots the (m_j, l_j) are read at once (one per lane), the batch
 // maximum and weights 2^(m_j - M) l_j come from wave reductions, and each
-// thread folds its channels of the weighted O rows with independent loads;
-// empty slots (l_j = 0) are skipped, their O rows never read.
+// thread folds its channels of the weighted O rows of 16 slots at a time with
+// independent loads; empty slots (l_j = 0) are skipped, their O rows never
+// read.
 template <int D, int GMAX>
-__global__ __launch_bounds__(64) void bf16_merge_kernel(int G, int H, int n_slots, const float* part,
-                                                       float* out, float* lse) {
+__global__ __launch_bounds__(256) void bf16_merge_kernel(int G, int H, int n_slots, const float* part,
+                                                        float* out, float* lse) {
   constexpr int CPT = D / 64;  // channels per thread
-  const int n = blockIdx.x, h = blockIdx.y, r = blockIdx.z, lane = threadIdx.x;
+  constexpr int GRP = 16;      // slots whose O rows one lane loads at once
+  __shared__ float s_m[4], s_l[4], s_o[4][D];
+  const int n = blockIdx.x, h = blockIdx.y, r = blockIdx.z;
+  const int wv = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const float* base = part + ((int64_t)r * H + h) * n_slots * ctl_part_floats<GMAX>(D);
+  // wave wv merges the slots [k_lo, k_hi), 64 at a time
+  const int quarter = (n_slots + 3) / 4;
+  const int k_lo = wv * quarter, k_hi = min(n_slots, k_lo + quarter);
   float M = -INFINITY, L = 0.0f;
   float o[CPT];
 #pragma unroll
   for (int i = 0; i < CPT; ++i) o[i] = 0.0f;
-  for (int k0 = 0; k0 < n_slots; k0 += 64) {
+  for (int k0 = k_lo; k0 < k_hi; k0 += 64) {
     const int k = k0 + lane;
     const float* pk = base + (int64_t)min(k, n_slots - 1) * ctl_part_floats<GMAX>(D);
-    const float lj = k < n_slots ? pk[GMAX * D + GMAX + n] : 0.0f;
+    const float lj = k < k_hi ? pk[GMAX * D + GMAX + n] : 0.0f;
     const float mj = lj > 0.0f ? pk[GMAX * D + n] : -INFINITY;
     float mb = mj;
 #pragma unroll
@@ -256,28 +264,51 @@ __global__ __launch_bounds__(64) void bf16_merge_kernel(int G, int H, int n_slot
     L = L * f + ws;
 #pragma unroll
     for (int i = 0; i < CPT; ++i) o[i] *= f;
-    const int nb = min(64, n_slots - k0);
-    for (int j0 = 0; j0 < nb; j0 += 8) {
-      float w8[8], x8[8][CPT];
+    const int nb = min(64, k_hi - k0);
+    for (int j0 = 0; j0 < nb; j0 += GRP) {
+      float w8[GRP], x8[GRP][CPT];
 #pragma unroll
-      for (int j = 0; j < 8; ++j) {
+      for (int j = 0; j < GRP; ++j) {
         w8[j] = __shfl(wj, min(j0 + j, 63), 64);
         const float* pj = base + (int64_t)(k0 + min(j0 + j, nb - 1)) * ctl_part_floats<GMAX>(D) + n * D;
 #pragma unroll
         for (int i = 0; i < CPT; ++i) x8[j][i] = w8[j] != 0.0f && j0 + j < nb ? pj[lane + 64 * i] : 0.0f;
       }
 #pragma unroll
-      for (int j = 0; j < 8; ++j)
+      for (int j = 0; j < GRP; ++j)
 #pragma unroll
         for (int i = 0; i < CPT; ++i) o[i] = fmaf(w8[j], x8[j][i], o[i]);
     }
     M = Mn;
   }
-  const int64_t row = (int64_t)r * H * G + h * G + n;
-  const float inv = L > 0.0f ? 1.0f / L : 0.0f;
+  // the four waves' (M, L, O) into one
+  if (lane == 0) {
+    s_m[wv] = M;
+    s_l[wv] = L;
+  }
 #pragma unroll
-  for (int i = 0; i < CPT; ++i) out[row * D + lane + 64 * i] = L > 0.0f ? o[i] * inv : 0.0f;
-  if (lse && lane == 0) lse[row] = L > 0.0f ? (M + log2f(L)) * 0.69314718055994531f : -INFINITY;
+  for (int i = 0; i < CPT; ++i) s_o[wv][lane + 64 * i] = o[i];
+  __syncthreads();
+  if (wv != 0) return;
+  float Mt = -INFINITY;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) Mt = fmaxf(Mt, s_l[w] > 0.0f ? s_m[w] : -INFINITY);
+  float Lt = 0.0f, ot[CPT];
+#pragma unroll
+  for (int i = 0; i < CPT; ++i) ot[i] = 0.0f;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    if (!(s_l[w] > 0.0f)) continue;  // an empty wave's O is zero, but skip it anyway
+    const float f = exp2f(s_m[w] - Mt);
+    Lt = fmaf(s_l[w], f, Lt);
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) ot[i] = fmaf(f, s_o[w][lane + 64 * i], ot[i]);
+  }
+  const int64_t row = (int64_t)r * H * G + h * G + n;
+  const float inv = Lt > 0.0f ? 1.0f / Lt : 0.0f;
+#pragma unroll
+  for (int i = 0; i < CPT; ++i) out[row * D + lane + 64 * i] = Lt > 0.0f ? ot[i] * inv : 0.0f;
+  if (lse && lane == 0) lse[row] = Lt > 0.0f ? (Mt + log2f(Lt)) * 0.69314718055994531f : -INFINITY;
 }
 
 // Scatter new bf16 K/V rows into their pages: one workgroup of d threads per
@@ -354,16 +385,16 @@ hipError_t launch_control_bf16_decode(const uint16_t* pages, int n_pages, int H,
   const float* part = a.part;
   if (d == 256 && G <= 8) {
     hipLaunchKernelGGL((bf16_decode_kernel<256, 8>), grid, block, 0, s, a);
-    hipLaunchKernelGGL((bf16_merge_kernel<256, 8>), mgrid, dim3(64), 0, s, G, H, n_slots, part, out, lse);
+    hipLaunchKernelGGL((bf16_merge_kernel<256, 8>), mgrid, dim3(256), 0, s, G, H, n_slots, part, out, lse);
   } else if (d == 256) {
     hipLaunchKernelGGL((bf16_decode_kernel<256, 16>), grid, block, 0, s, a);
-    hipLaunchKernelGGL((bf16_merge_kernel<256, 16>), mgrid, dim3(64), 0, s, G, H, n_slots, part, out, lse);
+    hipLaunchKernelGGL((bf16_merge_kernel<256, 16>), mgrid, dim3(256), 0, s, G, H, n_slots, part, out, lse);
   } else if (G <= 8) {
     hipLaunchKernelGGL((bf16_decode_kernel<128, 8>), grid, block, 0, s, a);
-    hipLaunchKernelGGL((bf16_merge_kernel<128, 8>), mgrid, dim3(64), 0, s, G, H, n_slots, part, out, lse);
+    hipLaunchKernelGGL((bf16_merge_kernel<128, 8>), mgrid, dim3(256), 0, s, G, H, n_slots, part, out, lse);
   } else {
     hipLaunchKernelGGL((bf16_decode_kernel<128, 16>), grid, block, 0, s, a);
-    hipLaunchKernelGGL((bf16_merge_kernel<128, 16>), mgrid, dim3(64), 0, s, G, H, n_slots, part, out, lse);
+    hipLaunchKernelGGL((bf16_merge_kernel<128, 16>), mgrid, dim3(256), 0, s, G, H, n_slots, part, out, lse);
   }
   return hipGetLastError();
 }
