@@ -371,14 +371,22 @@ def score_overhead(mk, torch, pool, bt, tags, sl, q_all, n_layers, w, reps=5):
         mk.kv_page_scores_update(pool, sl, lse, pm, hm, 0.9, scores)
 
     t_score = sweep(scored)
+    # the same plain sweeps with the fixed (deterministic) stage schedule
+    mk.paged_attn_set_deterministic(pool, True)
+    try:
+        t_det = sweep(lambda l: mk.paged_attn_decode(pool, l, q_all[l], bt, tags, sl, out, lse, ws))
+    finally:
+        mk.paged_attn_set_deterministic(pool, False)
     if mk.kv_pool_check_errors(pool):
         raise RuntimeError("device error word set in the score-collector sweeps")
     return {"decode_us_per_layer": round(t_plain, 3),
             "decode_with_scores_us_per_layer": round(t_score, 3),
             "overhead_frac": round(t_score / t_plain - 1.0, 4),
+            "deterministic_decode_us_per_layer": round(t_det, 3),
             "what": "paged_attn_decode_scores + kv_page_scores_update (every query head "
                     "sampled, EWMA beta 0.9) against paged_attn_decode, decode-only sweeps of "
-                    f"all {n_layers} layers, {reps} sweeps between two HIP events"}
+                    f"all {n_layers} layers, {reps} sweeps between two HIP events; and "
+                    "paged_attn_decode with paged_attn_set_deterministic on"}
 
 
 def stream_probe(mk, torch, nbytes, achieved, reps=20):

@@ -371,6 +371,16 @@ mkv_status kv_pool_read_free_lists(mkv_pool* pool, int32_t* fp8_ids, int32_t* n_
 /* Route / fallback / dense-shadow / physical-byte counters (synchronizes). */
 mkv_status kv_pool_counters(mkv_pool* pool, mkv_counters* out);
 
+/* Deterministic decode: with enable != 0, paged_attn_decode, its fused-append
+ * and scoring forms and paged_attn_decode_noalloc on this pool give every
+ * wave of a split a fixed list of stages (wave w: stages w, w + NW, ...)
+ * instead of claiming them at run time, so out and lse are bit-identical from
+ * call to call for the same inputs (otherwise they can differ in the last
+ * bits, by fp32 summation order).  Off by default: the fixed schedule balances
+ * the waves of a SIMD less well.  Takes effect for calls enqueued after it;
+ * part of the cohort key. */
+mkv_status paged_attn_set_deterministic(mkv_pool* pool, int32_t enable);
+
 /* Kernel timing for measurement tools; correct use never needs it.  When
  * enabled, each paged_attn_decode or paged_attn_decode_append call on this
  * pool launches its split-scan and merge kernels with HIP events that track

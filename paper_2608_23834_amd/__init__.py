@@ -28,7 +28,8 @@ EXPORTS = ["kv_pool_bytes", "kv_pool_create", "kv_pool_destroy", "kv_append_fp8"
            "paged_attn_decode", "paged_attn_decode_append", "paged_attn_chunk",
            "kv_partition_pages", "kv_pool_free_counts",
            "kv_pool_read_free_lists", "kv_pool_counters", "kv_pool_check_errors",
-           "paged_attn_set_timing", "paged_attn_last_times", "mkv_stream_read",
+           "paged_attn_set_timing", "paged_attn_set_deterministic", "paged_attn_last_times",
+           "mkv_stream_read",
            "paged_attn_decode_noalloc", "mkv_fp64_probe", "mkv_control_bf16_write",
            "mkv_control_bf16_workspace_bytes", "mkv_control_bf16_decode",
            "paged_attn_decode_cohort_key", "paged_attn_decode_scores", "kv_page_scores_update",
@@ -97,6 +98,7 @@ def lib() -> ctypes.CDLL:
         L.kv_pool_counters.argtypes = [vp, vp]
         L.kv_pool_check_errors.argtypes = [vp, vp, i32]
         L.paged_attn_set_timing.argtypes = [vp, i32]
+        L.paged_attn_set_deterministic.argtypes = [vp, i32]
         L.paged_attn_last_times.argtypes = [vp, vp, vp]
         L.mkv_stream_read.argtypes = [vp, sz, vp, vp]
         L.mkv_fp64_probe.argtypes = [vp, vp, ctypes.c_int64, vp, vp, vp, vp]
@@ -348,6 +350,11 @@ def kv_pool_counters(pool: Pool) -> dict:
     c = Counters()
     _check("kv_pool_counters", lib().kv_pool_counters(pool.handle, ctypes.byref(c)))
     return {n: getattr(c, n) for n, _ in Counters._fields_}
+
+
+def paged_attn_set_deterministic(pool: Pool, enable: bool) -> None:
+    _check("paged_attn_set_deterministic",
+           lib().paged_attn_set_deterministic(pool.handle, int(bool(enable))))
 
 
 def paged_attn_set_timing(pool: Pool, enable: bool) -> None:

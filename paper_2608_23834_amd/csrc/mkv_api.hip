@@ -121,6 +121,7 @@ mkv_status kv_pool_create(const mkv_pool_desc* desc, mkv_pool** out) {
   p->cl = ctrl_layout(p->n_fp8, p->n_tq3, p->d);
   p->decode_routes = p->chunk_routes = 0;
   p->timing = p->timed = 0;
+  p->deterministic = 0;
   // host image of ctrl: header, stacks (next id handed out = last element)
   std::vector<int32_t> img((size_t)p->cl.total_words, 0);
   img[CTRL_FP8_TOP] = p->n_fp8;
@@ -347,6 +348,12 @@ mkv_status paged_attn_decode_append(mkv_pool* pool, int32_t layer, int32_t n_req
   return st;
 }
 
+mkv_status paged_attn_set_deterministic(mkv_pool* pool, int32_t enable) {
+  if (!pool) return MKV_EINVAL;
+  pool->deterministic = enable != 0;
+  return MKV_OK;
+}
+
 mkv_status paged_attn_set_timing(mkv_pool* pool, int32_t enable) {
   if (!pool) return MKV_EINVAL;
   if (enable && !pool->timing) {
@@ -410,7 +417,8 @@ mkv_status paged_attn_decode_cohort_key(const mkv_pool* pool, int32_t n_req, int
                              (uint64_t)pool->n_fp8, (uint64_t)pool->n_tq3, (uint64_t)pool->recent,
                              (uint64_t)n_req, (uint64_t)max_pages, (uint64_t)sh.cunits,
                              (uint64_t)sh.max_chunks, (uint64_t)(fused_append != 0),
-                             (uint64_t)(scoring != 0), 0x4d4b5631ull /* key format */};
+                             (uint64_t)(scoring != 0), (uint64_t)pool->deterministic,
+                             0x4d4b5632ull /* key format */};
   uint64_t h = 1469598103934665603ull;  // FNV-1a over the fields' bytes
   for (uint64_t f : fields)
     for (int b = 0; b < 8; ++b) {

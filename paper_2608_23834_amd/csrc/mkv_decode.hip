@@ -522,7 +522,16 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   // 12-wave workgroup get most of their SIMD, waves 8-11 what is left.  Near
   // the end of the stage list the younger waves stop claiming (a stage they
   // take would finish last), so the last stages run on the faster waves.
+  // With the deterministic schedule wave w takes stages w, w + NW, w + 2 NW,
+  // ..., so every call folds the same pages in the same order and the outputs
+  // are bit-identical from call to call.
+  int det_next = wid + NW;
   auto claim = [&]() {
+    if (a.P.deterministic) {
+      const int v = min(det_next, n_st);
+      det_next += NW;
+      return v;
+    }
     int v = 0;
     if (lane == 0) {
       const int rank = wid / 4;

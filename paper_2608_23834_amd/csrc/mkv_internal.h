@@ -17,6 +17,7 @@ struct mkv_pool {
   uint64_t decode_routes, chunk_routes;
   hipEvent_t timing_ev[4];  // scan start and end, merge start and end (timing on)
   int timing, timed;
+  int deterministic;  // decode with a fixed stage schedule
 };
 
 namespace mkv {
@@ -37,6 +38,7 @@ struct PoolView {
   int32_t* last8;
   int32_t* last3;
   int n_layers, n_kv_heads, d, group, n_fp8, n_tq3, recent;
+  int deterministic;  // decode: fixed stage schedule instead of run-time claiming
 };
 
 inline PoolView view_of(const mkv_pool* p) {
@@ -62,6 +64,7 @@ inline PoolView view_of(const mkv_pool* p) {
   v.n_fp8 = p->n_fp8;
   v.n_tq3 = p->n_tq3;
   v.recent = p->recent;
+  v.deterministic = p->deterministic;
   return v;
 }
 
