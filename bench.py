@@ -336,7 +336,7 @@ class DenseControls:
         }
 
 
-def score_overhead(mk, torch, pool, bt, tags, sl, q_all, n_layers, w, reps=5):
+def score_overhead(mk, torch, pool, bt, tags, sl, q_all, n_layers, w, reps=5, det_after=False):
     """Cost of the direct attention-score collector (Sec. 3.1 / 4.2) on the
     mixed cache: decode-only sweeps of every layer with paged_attn_decode, then
     with paged_attn_decode_scores plus kv_page_scores_update (all query heads
@@ -350,6 +350,7 @@ def score_overhead(mk, torch, pool, bt, tags, sl, q_all, n_layers, w, reps=5):
     scores = torch.zeros((n_req, mp), device="cuda")
     hm = torch.ones(Hq, dtype=torch.uint8, device="cuda")
     stream = torch.cuda.current_stream()
+    mk.paged_attn_set_deterministic(pool, False)
 
     def sweep(fn):
         for l in range(n_layers):
@@ -376,7 +377,7 @@ def score_overhead(mk, torch, pool, bt, tags, sl, q_all, n_layers, w, reps=5):
     try:
         t_det = sweep(lambda l: mk.paged_attn_decode(pool, l, q_all[l], bt, tags, sl, out, lse, ws))
     finally:
-        mk.paged_attn_set_deterministic(pool, False)
+        mk.paged_attn_set_deterministic(pool, det_after)
     if mk.kv_pool_check_errors(pool):
         raise RuntimeError("device error word set in the score-collector sweeps")
     return {"decode_us_per_layer": round(t_plain, 3),
@@ -454,6 +455,8 @@ def main():
                     help="skip timing the attention-score collector")
     ap.add_argument("--no-controls", action="store_true",
                     help="skip the dense controls (the same KV all-FP8 and all-bf16)")
+    ap.add_argument("--deterministic", action="store_true",
+                    help="decode with the fixed stage schedule (bit-identical outputs call to call)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
@@ -494,6 +497,8 @@ def main():
     cu1 = torch.arange(n_req + 1, dtype=torch.int32, device="cuda")
     out = torch.zeros((n_req, w.n_q_heads, d), device="cuda")
     ws = mk.workspace(pool, n_req, max_pages)
+    if args.deterministic:
+        mk.paged_attn_set_deterministic(pool, True)
     torch.cuda.synchronize()
     setup_s = time.perf_counter() - t_setup
     print(f"[bench] {w.name}: state built in {setup_s:.1f} s", file=sys.stderr, flush=True)
@@ -602,7 +607,8 @@ def main():
                    "q_heads": w.n_q_heads, "kv_heads": Hkv, "head_dim": d, "page_tokens": PAGE,
                    "recent_tokens": w.recent, "kv_formats": "fp8-e4m3 (R,A) + tq3 (S)",
                    "step": "per layer: decode with the append of 1 token/request fused "
-                           "(paged_attn_decode_append); then migrate"},
+                           "(paged_attn_decode_append); then migrate",
+                   "stage_schedule": "fixed (deterministic)" if args.deterministic else "run-time"},
         "decode_attn_us_per_layer": round(dec_us, 3),
         "decode_scan_us": round(scan_mean, 3),
         "decode_merge_us": round(float(merge_us.mean()), 3),
@@ -631,7 +637,7 @@ def main():
         torch.cuda.empty_cache()
     if not args.no_scores:
         res["score_collector"] = score_overhead(mk, torch, pool, bt, tags, seq_after[n_steps - 1],
-                                                q_all, n_layers, w)
+                                                q_all, n_layers, w, det_after=args.deterministic)
     if not args.no_stream_probe:
         res["stream_probe"] = stream_probe(mk, torch, int(kv_bytes), achieved)
     if args.copy_probe:
