@@ -595,6 +595,10 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   // bits, and the workgroup's partial is marked so that the merge writes
   // zeros for the call.
   auto append_token = [&]() {
+    // the append waves are the youngest of their SIMDs: without a raised
+    // priority the streaming waves starve them and the appended page's stage,
+    // which waits for them, runs last
+    STAGE_PRIO(3);
     int bad = 0, n_fresh = 0, rank = 0;
     bool fresh = false;  // this request's page is fresh
     const int top = P.ctrl[CTRL_FP8_TOP];
@@ -899,21 +903,29 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
     lrow[i] = __shfl(l_col, 4 * lg + i, 64);
   }
   if (pair) {
+    // Merge the two page parities.  Rows of page b sit in lanes l + 32; one
+    // permlane32 swap of acc[m] with acc[m + CL/2] puts both parities of
+    // acc[m] (channel CL ln + m) in lanes l < 32 and both of acc[m + CL/2]
+    // in lanes l + 32, so the merged value of acc[m] lands in the low half of
+    // one register and that of acc[m + CL/2] in the high half (the factors
+    // of lane l are copied to lane l + 32 first)
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
-      // rows of page b sit in lanes l + 32; only lanes l < 32 keep the result
       const float m2 = upper_half(mrow[i]), l2 = upper_half(lrow[i]);
       const float M = fmaxf(lrow[i] > 0.0f ? mrow[i] : -INFINITY, l2 > 0.0f ? m2 : -INFINITY);
-      const float f1 = lrow[i] > 0.0f ? exp2f(mrow[i] - M) : 0.0f;
-      const float f2 = l2 > 0.0f ? exp2f(m2 - M) : 0.0f;
-#pragma unroll
-      for (int m = 0; m < CL; ++m) {
-        const float o2 = upper_half(st.acc[m][i]);
-        st.acc[m][i] = f1 * st.acc[m][i] + f2 * o2;
-        asm volatile("" : "+v"(st.acc[m][i]));  // merged here, not sunk past the barriers
-      }
+      const float f1 = lrow[i] > 0.0f ? __builtin_amdgcn_exp2f(mrow[i] - M) : 0.0f;
+      const float f2 = l2 > 0.0f ? __builtin_amdgcn_exp2f(m2 - M) : 0.0f;
       lrow[i] = f1 * lrow[i] + f2 * l2;
       mrow[i] = M;
+      const float g1 = __uint_as_float(swap32(f1).x), g2 = __uint_as_float(swap32(f2).x);
+#pragma unroll
+      for (int m = 0; m < CL / 2; ++m) {
+        const auto p = __builtin_amdgcn_permlane32_swap(__float_as_uint(st.acc[m][i]),
+                                                        __float_as_uint(st.acc[m + CL / 2][i]), false, false);
+        float z = g1 * __uint_as_float(p[0]) + g2 * __uint_as_float(p[1]);
+        asm volatile("" : "+v"(z));  // merged here, not sunk past the barriers
+        st.acc[m][i] = z;
+      }
     }
   }
   // Each wave writes its merged rows into its own ring slot as soon as its
@@ -921,22 +933,26 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   // needed before the store and the merge work overlaps the other waves'
   // scans.  Row (wave, head) keeps channel c = CL ln + 4 k + t at position
   // (16 k + ln) 4 + t: every lane stores float4s and the 16 lanes of a row
-  // store consecutive 16-byte words (no bank conflicts).
+  // store consecutive 16-byte words (no bank conflicts).  With the page-pair
+  // layout the lanes l < 32 store k < CL / 8 and the lanes l + 32 the rest.
   float* mm = s_mlf[0];  // [G][NW]
   float* ml = s_mlf[1];  // [G][NW]
   float* fw = s_mlf[2];  // [G][NW]
-  if (!row_b) {
+  {
     float* macc = reinterpret_cast<float*>(wring);  // [G][D]
+    const int rg = pair ? (lg & 1) : lg;             // accumulator row group of this lane's values
+    const int k0 = pair ? (lg >> 1) * (CL / 8) : 0;  // first float4 of the row this lane stores
+    constexpr int NK = pair ? CL / 8 : CL / 4;
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
-      const int head = head_of_col<G6>(4 * lg + i);
+      const int head = head_of_col<G6>(4 * rg + i);
       if (head >= 0 && head < G) {
         float4* row = reinterpret_cast<float4*>(macc + head * D);
 #pragma unroll
-        for (int k = 0; k < CL / 4; ++k)
-          row[16 * k + ln] = make_float4(st.acc[4 * k][i], st.acc[4 * k + 1][i], st.acc[4 * k + 2][i],
-                                         st.acc[4 * k + 3][i]);
-        if (ln == 0) {
+        for (int k = 0; k < NK; ++k)
+          row[16 * (k0 + k) + ln] = make_float4(st.acc[4 * k][i], st.acc[4 * k + 1][i], st.acc[4 * k + 2][i],
+                                                st.acc[4 * k + 3][i]);
+        if (ln == 0 && lg == rg) {
           mm[head * NW + wid] = mrow[i];
           ml[head * NW + wid] = lrow[i];
         }
@@ -960,11 +976,13 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
 #pragma unroll
     for (int w4 = 0; w4 < NW / 4; ++w4) {
       const float4 a4 = m4[w4], b4 = l4[w4];
-      L += (b4.x > 0.0f ? exp2f(a4.x - M) * b4.x : 0.0f) + (b4.y > 0.0f ? exp2f(a4.y - M) * b4.y : 0.0f) +
-           (b4.z > 0.0f ? exp2f(a4.z - M) * b4.z : 0.0f) + (b4.w > 0.0f ? exp2f(a4.w - M) * b4.w : 0.0f);
+      L += (b4.x > 0.0f ? __builtin_amdgcn_exp2f(a4.x - M) * b4.x : 0.0f) +
+           (b4.y > 0.0f ? __builtin_amdgcn_exp2f(a4.y - M) * b4.y : 0.0f) +
+           (b4.z > 0.0f ? __builtin_amdgcn_exp2f(a4.z - M) * b4.z : 0.0f) +
+           (b4.w > 0.0f ? __builtin_amdgcn_exp2f(a4.w - M) * b4.w : 0.0f);
     }
     const float lw = ml[tid];
-    fw[tid] = lw > 0.0f ? exp2f(mm[tid] - M) / L : 0.0f;
+    fw[tid] = lw > 0.0f ? __builtin_amdgcn_exp2f(mm[tid] - M) / L : 0.0f;
     if (tid % NW == 0) {
       part[G * D + head] = M;
       part[G * D + G + head] = (APP && s_app_bad) ? -1.0f : L;  // -1: the merge writes zeros
