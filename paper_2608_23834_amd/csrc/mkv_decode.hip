@@ -249,8 +249,8 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   __shared__ int4 s_stage[MAX_CHUNK_PAGES];  // {lp_a, id_a, lp_b, id_b}; id_b < 0: FP8 stage
   __shared__ int s_next;  // next unclaimed stage (one-slot schedule)
   __shared__ int s_app, s_app_bad;  // fused append: append waves done, error flag
-  // per (head, wave): running max, denominator, combine weight (epilogue)
-  __shared__ __align__(16) float s_mlf[3][16 * NW_MAX];
+  // per (head, wave): running max and denominator (epilogue)
+  __shared__ __align__(16) float s_mlf[2][16 * NW_MAX];
   static_assert(NCH_OF(PAIR) * D * 4 <= SLOTS * 2 * (int)tq3_region_bytes(D),
                 "a wave's merged rows fit its own ring slot");
   const PoolView& P = a.P;
@@ -937,7 +937,6 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   // layout the lanes l < 32 store k < CL / 8 and the lanes l + 32 the rest.
   float* mm = s_mlf[0];  // [G][NW]
   float* ml = s_mlf[1];  // [G][NW]
-  float* fw = s_mlf[2];  // [G][NW]
   {
     float* macc = reinterpret_cast<float*>(wring);  // [G][D]
     const int rg = pair ? (lg & 1) : lg;             // accumulator row group of this lane's values
@@ -959,49 +958,48 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
       }
     }
   }
-  __syncthreads();
-  // combine weights f_w = 2^(m_w - M) / L, one thread per (head, wave); rows
-  // with l_w = 0 take no part
-  if (tid < G * NW) {
-    const int head = tid / NW;
-    const float4* m4 = reinterpret_cast<const float4*>(mm + head * NW);
-    const float4* l4 = reinterpret_cast<const float4*>(ml + head * NW);
-    float M = -INFINITY, L = 0.0f;
-#pragma unroll
-    for (int w4 = 0; w4 < NW / 4; ++w4) {
-      const float4 a4 = m4[w4], b4 = l4[w4];
-      M = fmaxf(M, fmaxf(fmaxf(b4.x > 0.0f ? a4.x : -INFINITY, b4.y > 0.0f ? a4.y : -INFINITY),
-                         fmaxf(b4.z > 0.0f ? a4.z : -INFINITY, b4.w > 0.0f ? a4.w : -INFINITY)));
-    }
-#pragma unroll
-    for (int w4 = 0; w4 < NW / 4; ++w4) {
-      const float4 a4 = m4[w4], b4 = l4[w4];
-      L += (b4.x > 0.0f ? __builtin_amdgcn_exp2f(a4.x - M) * b4.x : 0.0f) +
-           (b4.y > 0.0f ? __builtin_amdgcn_exp2f(a4.y - M) * b4.y : 0.0f) +
-           (b4.z > 0.0f ? __builtin_amdgcn_exp2f(a4.z - M) * b4.z : 0.0f) +
-           (b4.w > 0.0f ? __builtin_amdgcn_exp2f(a4.w - M) * b4.w : 0.0f);
-    }
-    const float lw = ml[tid];
-    fw[tid] = lw > 0.0f ? __builtin_amdgcn_exp2f(mm[tid] - M) / L : 0.0f;
-    if (tid % NW == 0) {
-      part[G * D + head] = M;
-      part[G * D + G + head] = (APP && s_app_bad) ? -1.0f : L;  // -1: the merge writes zeros
-    }
-  }
-  __syncthreads();
-  // four consecutive positions of a macc row are four consecutive channels
+  __syncthreads();  // every wave's rows and (m, l) are in LDS
+  // Each thread folds the waves' rows of one head into four channels of the
+  // partial, with the head's combine weights f_w = 2^(m_w - M) (M the largest
+  // m_w of the rows with l_w > 0; rows with l_w = 0 take no part):
+  // O_j = sum_w f_w O_w / L_j, L_j = sum_w f_w l_w.  Every thread of a head
+  // computes the same weights, so no further barrier is needed.  Four
+  // consecutive positions of a macc row are four consecutive channels.
   for (int it = tid; it < G * D / 4; it += NT) {
     const int n = it / (D / 4), pos = 4 * (it % (D / 4));
     const int c = CL * ((pos >> 2) & 15) + 4 * (pos >> 6);
+    const float4* m4 = reinterpret_cast<const float4*>(mm + n * NW);
+    const float4* l4 = reinterpret_cast<const float4*>(ml + n * NW);
+    float mw[NW], lw[NW];
+#pragma unroll
+    for (int w4 = 0; w4 < NW / 4; ++w4) {
+      const float4 a4 = m4[w4], b4 = l4[w4];
+      mw[4 * w4] = a4.x, mw[4 * w4 + 1] = a4.y, mw[4 * w4 + 2] = a4.z, mw[4 * w4 + 3] = a4.w;
+      lw[4 * w4] = b4.x, lw[4 * w4 + 1] = b4.y, lw[4 * w4 + 2] = b4.z, lw[4 * w4 + 3] = b4.w;
+    }
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) M = fmaxf(M, lw[w] > 0.0f ? mw[w] : -INFINITY);
+    float L = 0.0f;
     float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
     for (int w = 0; w < NW; ++w) {
-      const float f = fw[n * NW + w];
+      const float f = lw[w] > 0.0f ? __builtin_amdgcn_exp2f(mw[w] - M) : 0.0f;
       const float4 x = *reinterpret_cast<const float4*>(ring + w * SLOTS * STAGE + (n * D + pos) * 4);
-      o.x += f * x.x;
-      o.y += f * x.y;
-      o.z += f * x.z;
-      o.w += f * x.w;
+      L = fmaf(f, lw[w], L);
+      o.x = fmaf(f, x.x, o.x);
+      o.y = fmaf(f, x.y, o.y);
+      o.z = fmaf(f, x.z, o.z);
+      o.w = fmaf(f, x.w, o.w);
+    }
+    const float inv = L > 0.0f ? 1.0f / L : 0.0f;
+    o.x *= inv;
+    o.y *= inv;
+    o.z *= inv;
+    o.w *= inv;
+    if (pos == 0) {
+      part[G * D + n] = M;
+      part[G * D + G + n] = (APP && s_app_bad) ? -1.0f : L;  // -1: the merge writes zeros
     }
     *reinterpret_cast<float4*>(part + n * D + c) = o;
   }
@@ -1142,7 +1140,7 @@ hipError_t decode_scratch(int dev, void** ptr) {
 // dynamic LDS a decode workgroup may use: 160 KiB per CU minus the static arrays
 static constexpr size_t lds_limit() {
   // s_stage, s_mlf; s_next and slack
-  return 160 * 1024 - sizeof(int4) * MAX_CHUNK_PAGES - 3 * 16 * NW_MAX * sizeof(float) - 256;
+  return 160 * 1024 - sizeof(int4) * MAX_CHUNK_PAGES - 2 * 16 * NW_MAX * sizeof(float) - 256;
 }
 
 template <bool APP, bool SCORE = false>
