@@ -260,6 +260,12 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   const int G = P.group, H = P.n_kv_heads, Hq = H * G;
   const int mp = a.max_pages;
   constexpr bool pair = PAIR;
+  // The arguments the prologue needs come in one batch of loads from the
+  // argument segment: otherwise the compiler fetches some of them (the chunk
+  // size, the pool and partial pointers) only after the first batch has
+  // returned, and the page-table loads wait for a second round trip.
+  asm volatile("" ::"s"(a.cunits), "s"(a.bt), "s"(a.tags), "s"(a.seq_lens), "s"(a.q), "s"(P.sigma),
+               "s"(P.recent), "s"(mp), "s"(a.n_req), "s"(P.tq3), "s"(P.fp8), "s"(a.partials));
   // LDS: [rotated query as E4M3 terms][plain-query operand][page ring | wave merge]
   uint8_t* qf8 = smem;  // [term][step][lane][32 bytes], see the query build below
   half8* qpl = reinterpret_cast<half8*>(smem + QF8_TERMS * NK8 * 64 * 32);  // plain query (bf16 -> fp16 is exact)
