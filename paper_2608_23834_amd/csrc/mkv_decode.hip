@@ -2,7 +2,7 @@
 // direct fused decode) for gfx950.
 //
 // One launch per layer.  Grid (chunk, KV head, request); one workgroup per CU:
-// 12 wave64s with one ring slot each when a KV head's query group has at most
+// 8 wave64s with one ring slot each when a KV head's query group has at most
 // 8 heads (two pages share a score tile), else 8 waves with two slots.  Chunks
 // are ranges of logical pages of equal cost: a page wholly outside the Recent
 // window costs 2 units, a Recent (FP8) page 5 (its scattered 16-byte copies
@@ -48,12 +48,16 @@
 
 namespace mkv {
 
-// Workgroup shape per instance: with the paired score layout (G <= 8) 12
+// Workgroup shape per instance: with the paired score layout (G <= 8) 8
 // waves, each with a one-stage ring slot (a stage is moved into registers as
 // soon as it lands and the slot refilled at once); otherwise 8 waves with two
-// slots.  Either way one workgroup fills a CU's LDS.
+// slots.  One workgroup per CU either way.  Eight one-slot waves beat twelve
+// on the long pair (29.7 against 31.0 us per scan): the stage loop is not
+// issue-bound with two waves per SIMD, and fewer copies in flight per CU let
+// the memory system deliver more (a further L2 prefetch of later stages, or
+// four waves, were slower still).
 #ifndef MKV_PAIR_NW
-#define MKV_PAIR_NW 12
+#define MKV_PAIR_NW 8
 #define MKV_PAIR_SLOTS 1
 #endif
 template <bool PAIR> struct DecodeCfg {
@@ -61,7 +65,7 @@ template <bool PAIR> struct DecodeCfg {
   static constexpr int SLOTS = PAIR ? MKV_PAIR_SLOTS : 2;  // ring slots per wave
   static constexpr int NT = 64 * NW;
 };
-constexpr int NW_MAX = 12;
+constexpr int NW_MAX = MKV_PAIR_NW > 8 ? MKV_PAIR_NW : 8;
 // Wave priority by progress through a stage (claimed -> 1, scores done -> 2,
 // weights done -> 3): among the waves of a SIMD the one furthest into its
 // stage issues first, so stages finish roughly in the order they were claimed.
@@ -524,10 +528,10 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   // together (stages differ in cost and the waves of a SIMD do not get equal
   // issue shares).  With two slots per wave the claimed stage after the
   // current one is already in flight.
-  // A SIMD issues the instructions of its oldest wave first: waves 0-3 of a
-  // 12-wave workgroup get most of their SIMD, waves 8-11 what is left.  Near
-  // the end of the stage list the younger waves stop claiming (a stage they
-  // take would finish last), so the last stages run on the faster waves.
+  // A SIMD issues the instructions of its oldest wave first: waves 0-3 get
+  // most of their SIMD, the later ones what is left.  Near the end of the
+  // stage list the younger waves stop claiming (a stage they take would
+  // finish last), so the last stages run on the faster waves.
   // With the deterministic schedule wave w takes stages w, w + NW, w + 2 NW,
   // ..., so every call folds the same pages in the same order and the outputs
   // are bit-identical from call to call.
