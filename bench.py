@@ -455,6 +455,8 @@ def main():
                     help="skip timing the attention-score collector")
     ap.add_argument("--no-controls", action="store_true",
                     help="skip the dense controls (the same KV all-FP8 and all-bf16)")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="skip the pass that replays the same steps as captured HIP graphs")
     ap.add_argument("--deterministic", action="store_true",
                     help="decode with the fixed stage schedule (bit-identical outputs call to call)")
     args = ap.parse_args()
@@ -470,8 +472,8 @@ def main():
     torch.cuda.init()
     w = wl.workload(args.cfg)
     n_layers = args.layers or w.n_layers
-    n_pass = 2 if args.no_unfused else 3
-    n_steps = args.warmup + n_pass * args.steps  # warmup, pass A, pass B (, pass C)
+    n_pass = 2 + (not args.no_unfused) + (not args.no_graph)
+    n_steps = args.warmup + n_pass * args.steps  # warmup, pass A, pass B (, pass C) (, pass D)
     t_setup = time.perf_counter()
     ctl = None if args.no_controls or args.cfg not in (2, 3) else DenseControls(w, n_layers, mk, torch)
     pool, bt, tags, am, max_pages = build_state(w, n_layers, n_steps + 16, mk, torch,
@@ -567,7 +569,7 @@ def main():
         c1 = torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
         c0.record(stream)
-        for s in range(args.warmup + 2 * args.steps, n_steps):
+        for s in range(args.warmup + 2 * args.steps, args.warmup + 3 * args.steps):
             step_unfused(s)
         c1.record(stream)
         torch.cuda.synchronize()
@@ -575,6 +577,34 @@ def main():
         err = mk.kv_pool_check_errors(pool)
         if err:
             raise RuntimeError(f"device error word {err:#x} during the benchmark")
+    # pass D: the same whole steps (fused append, decode, Retier) captured once
+    # each into a HIP graph -- the serving loop's graph path (Sec. 4.1) -- and
+    # replayed in order; the same kernels, without the per-launch host gaps
+    graph_ms = None
+    if not args.no_graph:
+        s_first = args.warmup + (3 if not args.no_unfused else 2) * args.steps
+        graphs = []
+        cap = torch.cuda.Stream()
+        cap.wait_stream(stream)
+        for s in range(s_first, s_first + args.steps):
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=cap):
+                step(s)
+            graphs.append(g)
+        stream.wait_stream(cap)
+        torch.cuda.synchronize()
+        g0 = torch.cuda.Event(enable_timing=True)
+        g1 = torch.cuda.Event(enable_timing=True)
+        g0.record(stream)
+        for g in graphs:
+            g.replay()
+        g1.record(stream)
+        torch.cuda.synchronize()
+        graph_ms = g0.elapsed_time(g1) / args.steps
+        err = mk.kv_pool_check_errors(pool)
+        if err:
+            raise RuntimeError(f"device error word {err:#x} in the graph pass")
+        del graphs
     sl0 = [L + args.warmup + args.steps + 1 for L in lens]
     sl1 = [L + args.warmup + 2 * args.steps for L in lens]
     kvb0 = sum(kv_bytes_of(tags_mid[r], sl0[r], d, Hkv) for r in range(n_req))
@@ -617,6 +647,8 @@ def main():
                          "around the split-scan (with the fused append) and merge kernels of "
                          "each step's last call",
         "unfused_us_per_layer": None if unfused_ms is None else round(unfused_ms * 1e3 / n_layers, 3),
+        "graph_us_per_layer": None if graph_ms is None else round(graph_ms * 1e3 / n_layers, 3),
+        "graph_step": "last pass: the same whole steps, each captured into a HIP graph and replayed in order",
         "unfused_step": "third pass: the same steps with kv_append_fp8 and paged_attn_decode "
                         "as separate calls",
         "kv_bytes_per_layer": int(kv_bytes),

@@ -545,7 +545,7 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
     int v = 0;
     if (lane == 0) {
       const int rank = wid / 4;
-      const int keep = rank == 0 ? 0 : rank == 1 ? 6 : 24;  // stages left for older waves
+      const int keep = rank == 0 ? 0 : rank == 1 ? 3 : 24;  // stages left for older waves
       const int seen = __atomic_load_n(&s_next, __ATOMIC_RELAXED);
       v = (n_st - seen <= keep) ? n_st : atomicAdd(&s_next, 1);
     }
