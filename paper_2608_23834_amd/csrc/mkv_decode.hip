@@ -1240,17 +1240,22 @@ hipError_t launch_decode(const PoolView& P, int layer, int n_req, const uint16_t
 }
 
 // Attention-score collector (Sec. 3.1, Eqs. score-global-weight and
-// attention-score), after a scoring decode of the same call; one thread per
-// page, workgroups over page blocks and requests.  The globally normalized
-// mass of page p for query head hq is its local mass rescaled by the global
-// softmax normalization, q = mass * 2^(m_ref - lse / ln 2) (lse of the
-// merge).  The collector conditions on page-addressable mass, q / sum_p q;
-// this attention has no sink logit and the merge's lse is the log of the very
-// sum of weights that the page masses partition, so sum_p q = 1 and q~ = q up
-// to rounding.  r_p = the mean of q~ over the sampled heads; a_p <- beta a_p +
-// (1 - beta) r_p; q~ is written when asked.
-constexpr int SCORE_UP_NT = 64;  // pages per update workgroup
-__global__ __launch_bounds__(SCORE_UP_NT) void score_update_kernel(int n_q_heads, int max_pages,
+// attention-score), after a scoring decode of the same call; workgroups over
+// blocks of pages and requests.  The globally normalized mass of page p for
+// query head hq is its local mass rescaled by the global softmax
+// normalization, q = mass * 2^(m_ref - lse / ln 2) (lse of the merge).  The
+// collector conditions on page-addressable mass, q / sum_p q; this attention
+// has no sink logit and the merge's lse is the log of the very sum of weights
+// that the page masses partition, so sum_p q = 1 and q~ = q up to rounding.
+// r_p = the mean of q~ over the sampled heads; a_p <- beta a_p + (1 - beta)
+// r_p; q~ is written when asked.
+// Every load goes out at the start (the length, the block's page masses --
+// consecutive terms to consecutive threads, four per thread -- the scores,
+// lse and the head mask): one memory round trip.  Each page's sum over the
+// sampled heads runs in head order from LDS.
+constexpr int SCORE_UP_NT = 256;  // threads per update workgroup
+constexpr int SCORE_UP_EPT = 4;   // (page, head) terms per thread
+__global__ __launch_bounds__(SCORE_UP_NT) void score_update_kernel(int n_q_heads, int max_pages, int ppb,
                                                                    const int32_t* seq_lens,
                                                                    const float* lse,
                                                                    const float2* page_mass,
@@ -1259,12 +1264,23 @@ __global__ __launch_bounds__(SCORE_UP_NT) void score_update_kernel(int n_q_heads
                                                                    float* r_out, float* qn_out) {
   constexpr int MAXH = 256;
   __shared__ float s_l2[MAXH];
-  __shared__ uint8_t s_smp[MAXH];
+  __shared__ bool s_smp[MAXH];
+  __shared__ float s_q[SCORE_UP_NT * SCORE_UP_EPT];
   __shared__ int s_ns;
   const int r = blockIdx.y, tid = threadIdx.x;
-  const int p = blockIdx.x * SCORE_UP_NT + tid;
+  const int p0 = blockIdx.x * ppb;
+  const int npb = min(ppb, max_pages - p0);  // pages of this block inside the table
+  const int64_t e0 = ((int64_t)r * max_pages + p0) * n_q_heads;  // the block's first (page, head) term
+  const int ne = npb * n_q_heads;  // at most SCORE_UP_NT * SCORE_UP_EPT
   const int S = seq_lens[r];
-  const int np = S >= 1 ? min((S + PAGE - 1) / PAGE, max_pages) : 0;
+  float2 mm[SCORE_UP_EPT];
+#pragma unroll
+  for (int k = 0; k < SCORE_UP_EPT; ++k) {
+    const int e = tid + k * SCORE_UP_NT;
+    mm[k] = e < ne ? page_mass[e0 + e] : make_float2(0.0f, 0.0f);
+  }
+  float a_old = 0.0f;
+  if (tid < npb) a_old = a_io[(int64_t)r * max_pages + p0 + tid];
   if (tid == 0) s_ns = 0;
   __syncthreads();
   for (int hq = tid; hq < n_q_heads; hq += SCORE_UP_NT) {
@@ -1273,30 +1289,38 @@ __global__ __launch_bounds__(SCORE_UP_NT) void score_update_kernel(int n_q_heads
     if (s_smp[hq]) atomicAdd(&s_ns, 1);
   }
   __syncthreads();
-  if (p >= np) return;
-  const float2* pm = page_mass + ((int64_t)r * max_pages + p) * n_q_heads;
-  float acc = 0.0f;
-#pragma unroll 8
-  for (int hq = 0; hq < n_q_heads; ++hq) {
-    const float2 mm = pm[hq];
-    const float qn = mm.x * exp2f(mm.y - s_l2[hq]);
-    if (qn_out) qn_out[((int64_t)r * max_pages + p) * n_q_heads + hq] = qn;
-    if (s_smp[hq]) acc += qn;
+  const int np = S >= 1 ? min((S + PAGE - 1) / PAGE, max_pages) : 0;
+#pragma unroll
+  for (int k = 0; k < SCORE_UP_EPT; ++k) {
+    const int e = tid + k * SCORE_UP_NT;
+    if (e >= ne) break;
+    const int pl = e / n_q_heads, hq = e - pl * n_q_heads;
+    const float qn = mm[k].x * exp2f(mm[k].y - s_l2[hq]);
+    const bool live = p0 + pl < np;  // masses past the request's end were never written
+    if (qn_out && live) qn_out[e0 + e] = qn;
+    s_q[e] = (live && s_smp[hq]) ? qn : 0.0f;
   }
+  __syncthreads();
+  if (tid >= npb || p0 + tid >= np) return;
+  float acc = 0.0f;
+  for (int hq = 0; hq < n_q_heads; ++hq) acc += s_q[tid * n_q_heads + hq];
   const int ns = s_ns;
   const float rp = ns ? acc / (float)ns : 0.0f;
-  if (r_out) r_out[(int64_t)r * max_pages + p] = rp;
-  float* ap = a_io + (int64_t)r * max_pages + p;
-  *ap = beta * *ap + (1.0f - beta) * rp;
+  const int64_t pi = (int64_t)r * max_pages + p0 + tid;
+  if (r_out) r_out[pi] = rp;
+  a_io[pi] = beta * a_old + (1.0f - beta) * rp;
 }
 
 hipError_t launch_score_collect(int n_req, int n_q_heads, int max_pages, const int32_t* seq_lens,
                                 const float* lse, const float2* page_mass,
                                 const uint8_t* head_mask, float beta, float* a_io, float* r_out,
                                 float* qn_out, hipStream_t s) {
-  hipLaunchKernelGGL(score_update_kernel, dim3((max_pages + SCORE_UP_NT - 1) / SCORE_UP_NT, n_req),
-                     dim3(SCORE_UP_NT), 0, s, n_q_heads, max_pages, seq_lens, lse, page_mass,
-                     head_mask, beta, a_io, r_out, qn_out);
+  if (n_q_heads < 1 || n_q_heads > 256) return hipErrorInvalidValue;
+  // pages per workgroup: every thread stages at most SCORE_UP_EPT terms
+  const int ppb = max(1, min(SCORE_UP_NT, SCORE_UP_NT * SCORE_UP_EPT / n_q_heads));
+  hipLaunchKernelGGL(score_update_kernel, dim3((max_pages + ppb - 1) / ppb, n_req), dim3(SCORE_UP_NT), 0, s,
+                     n_q_heads, max_pages, ppb, seq_lens, lse, page_mass, head_mask, beta, a_io, r_out,
+                     qn_out);
   return hipGetLastError();
 }
 
