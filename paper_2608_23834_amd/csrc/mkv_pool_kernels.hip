@@ -564,8 +564,9 @@ __global__ __launch_bounds__(MIG_NT) void migrate_count_kernel(
   }
 }
 
-// ONE: a single workgroup that owns the whole table counts it itself first
-// (one launch instead of two).
+// ONE: a single workgroup owns the whole table (at most one batch): it loads
+// the batch once, counts and validates it, and lists it after one scan (one
+// launch instead of two, one pass over the table instead of two).
 template <bool ONE>
 __global__ __launch_bounds__(MIG_NT) void migrate_list_kernel(
     int n_req, const int32_t* bt, uint8_t* tags, int max_pages, const uint8_t* anchor,
@@ -578,8 +579,57 @@ __global__ __launch_bounds__(MIG_NT) void migrate_list_kernel(
   __syncthreads();
   const int top3 = ONE ? ctrl[CTRL_TQ3_TOP] : mig[2 * MIG_BLOCKS];
   if constexpr (ONE) {
-    mig_count_range(0, n_req, bt, tags, max_pages, anchor, seq_lens, W, 0,
-                    (int64_t)n_req * max_pages, n_fp8, &s_tot, &s_err, rv);
+    const int64_t N = (int64_t)n_req * max_pages;  // <= MIG_BATCH
+    MigBatch m;
+    mig_load(m, (int64_t)tid * MIG_KB, N, max_pages, bt, tags, anchor, seq_lens);
+    mig_load_rc(m, rv);
+    int err = 0, k[MIG_KB], c = 0;
+    for (int r = tid; r < n_req; r += MIG_NT) {
+      const int S = seq_lens[r];
+      if (S < 0 || (S + PAGE - 1) / PAGE > max_pages) err |= MKV_DEVERR_RANGE;
+    }
+#pragma unroll
+    for (int j = 0; j < MIG_KB; ++j) {
+      const int p = m.pg[j], S = m.sl[j];
+      const bool old_r = m.rq[j] >= 0 && m.tg[j] == TAG_R && p < (S + PAGE - 1) / PAGE &&
+                         (p + 1) * PAGE <= S - W && !m.an[j];
+      if (old_r && (m.id[j] < 0 || m.id[j] >= n_fp8)) err |= MKV_DEVERR_RANGE;
+      k[j] = mig_kind(m, j, W);
+      c += k[j] == 1;
+    }
+    if (err) atomicOr(&s_err, err);
+    int total;
+    int e = block_excl_scan(c, scratch, &total);  // its barriers also publish s_err
+    err = s_err;
+    if (err == 0 && total > top3) err |= MKV_DEVERR_TQ3_EXHAUSTED;
+    if (err == 0 && total > n_fp8) err |= MKV_DEVERR_RANGE;
+    if (err) {
+      if (tid == 0) {
+        atomicOr(&ctrl[CTRL_ERR], err);
+        ctrl[CTRL_ABORT] = 1;
+        ctrl[CTRL_NLIST] = 0;
+      }
+      return;
+    }
+    const int64_t f0 = (int64_t)tid * MIG_KB;
+#pragma unroll
+    for (int j = 0; j < MIG_KB; ++j) {
+      if (k[j] == 2) tags[f0 + j] = TAG_A;  // Anchor: tag only, stays FP8
+      if (k[j] == 1) {
+        int32_t* le = list + 4LL * e;
+        le[0] = m.rq[j];
+        le[1] = m.pg[j];
+        le[2] = m.id[j];
+        le[3] = tq3_stack[top3 - 1 - e];
+        e++;
+      }
+    }
+    if (tid == 0) {
+      ctrl[CTRL_TQ3_TOP] = top3 - total;
+      ctrl[CTRL_NLIST] = total;
+      ctrl[CTRL_ABORT] = 0;
+    }
+    return;
   } else if (tid < nb) {
     const int c = mig[tid], e = mig[MIG_BLOCKS + tid];
     if (c) atomicAdd(&s_tot, c);
