@@ -326,20 +326,21 @@ __global__ __launch_bounds__(DecodeCfg<PAIR>::NT, 1) void decode_kernel(DecodeAr
   }
   const int s_in = a.seq_lens[r];
   // with the fused append the request's new token sits at position s_in
-  const int S0 = !APP ? s_in : (s_in >= 0 && s_in < mp * PAGE ? s_in + 1 : -1);
-  const bool bad_len = S0 < 1 || S0 > mp * PAGE;
-  if (bad_len) {
+  const int S = !APP ? s_in : (s_in >= 0 && s_in < mp * PAGE ? s_in + 1 : -1);
+  if (S < 1 || S > mp * PAGE) {
     if (chunk == 0 && h == 0 && tid == 0) atomicOr(&P.ctrl[CTRL_ERR], (int)MKV_DEVERR_RANGE);
     if (APP && chunk == 0 && h == 0 && tid == 0) {  // no workgroup holds this request's token
       a.app_rec[r] = -1;
       if (r == 0) a.app_rec[a.n_req] = -1;
     }
+    if (tid < G) part[G * D + G + tid] = 0.0f;  // empty partial: the merge writes zeros
+    return;
   }
-  // no early return: a branch here would let the compiler sink the page-table
-  // loads below it, behind the length load's round trip; an invalid length
-  // or a chunk past the request's end simply has no stages
-  const int S = bad_len ? 0 : S0;
-  const int n_pg = bad_len ? 0 : min(p1, (S + PAGE - 1) / PAGE) - p0;  // pages of the chunk before the end
+  const int n_pg = min(p1, (S + PAGE - 1) / PAGE) - p0;  // pages of the chunk before the end
+  if (n_pg <= 0) {
+    if (tid < G) part[G * D + G + tid] = 0.0f;  // slot past the request's end
+    return;
+  }
   // ---- query operands, built while the page-table loads are in flight, in MFMA
   // lane order (ln = lane % 16 the score column, lg = lane / 16):
   //  qpl[s][lane] holds channels (D/4) lg + 8 s + j, j < 8 (fp16, FP8 pages);
