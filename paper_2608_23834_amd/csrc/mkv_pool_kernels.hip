@@ -503,6 +503,18 @@ __device__ __forceinline__ void mig_load(MigBatch& m, int64_t f0, int64_t N, int
     if (++p == max_pages) { p = 0; ++r; }
   }
 }
+// The reference counts a migration plan needs: only a Recent page that has
+// left the window and is not an anchor can migrate, and only then does its
+// count decide (a shared page stays FP8); every other entry skips the gather.
+__device__ __forceinline__ void mig_load_rc_candidates(MigBatch& m, const RcView& v, int W) {
+#pragma unroll
+  for (int j = 0; j < MIG_KB; ++j) {
+    const int p = m.pg[j], S = m.sl[j], id = m.id[j];
+    const bool cand = m.rq[j] >= 0 && m.tg[j] == TAG_R && !m.an[j] && p < (S + PAGE - 1) / PAGE &&
+                      (p + 1) * PAGE <= S - W && id >= 0 && id < v.n_fp8;
+    m.rc[j] = cand ? v.rc8[id] : 0;
+  }
+}
 // 1: migrating page, 2: Anchor to retag, 0: neither
 __device__ __forceinline__ int mig_kind(const MigBatch& m, int j, int W) {
   if (m.rq[j] < 0) return 0;
@@ -530,7 +542,7 @@ __device__ __forceinline__ void mig_count_range(int b, int n_req, const int32_t*
   for (int64_t b0 = e0; b0 < e1; b0 += MIG_BATCH) {
     MigBatch m;
     mig_load(m, b0 + (int64_t)tid * MIG_KB, e1, max_pages, bt, tags, anchor, seq_lens);
-    mig_load_rc(m, rv);
+    mig_load_rc_candidates(m, rv, W);
 #pragma unroll
     for (int j = 0; j < MIG_KB; ++j) {
       const int p = m.pg[j], S = m.sl[j];
@@ -582,7 +594,7 @@ __global__ __launch_bounds__(MIG_NT) void migrate_list_kernel(
     const int64_t N = (int64_t)n_req * max_pages;  // <= MIG_BATCH
     MigBatch m;
     mig_load(m, (int64_t)tid * MIG_KB, N, max_pages, bt, tags, anchor, seq_lens);
-    mig_load_rc(m, rv);
+    mig_load_rc_candidates(m, rv, W);
     int err = 0, k[MIG_KB], c = 0;
     for (int r = tid; r < n_req; r += MIG_NT) {
       const int S = seq_lens[r];
@@ -655,7 +667,7 @@ __global__ __launch_bounds__(MIG_NT) void migrate_list_kernel(
   for (int64_t b0 = e0; b0 < e1; b0 += MIG_BATCH) {
     MigBatch m;
     mig_load(m, b0 + (int64_t)tid * MIG_KB, e1, max_pages, bt, tags, anchor, seq_lens);
-    mig_load_rc(m, rv);
+    mig_load_rc_candidates(m, rv, W);
     int k[MIG_KB], c = 0;
 #pragma unroll
     for (int j = 0; j < MIG_KB; ++j) {
