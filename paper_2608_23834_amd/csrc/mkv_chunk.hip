@@ -61,6 +61,7 @@ struct ChunkArgs {
   const int32_t* list3;
   const int32_t* counts;  // [n_req][2] (n_fp8, n_tq3)
   const int4* stages;     // [n_req][max_pages] stage table (chunk_stages_kernel)
+  const int32_t* rbo;     // [n_req + 1] first row block of each request (chunk_rows_kernel)
   float sm_log2;          // log2(e) / sqrt(d)
 };
 
@@ -70,7 +71,7 @@ static size_t al256(size_t b) { return (b + 255) / 256 * 256; }
 // int4 per stage; the chunk kernel copies it in 1 KiB blocks, so 1 KiB of
 // slack after it keeps the last block inside the workspace)
 struct ChunkWs {
-  size_t list8, list3, counts, stages, total;
+  size_t list8, list3, counts, stages, rbo, total;
 };
 static ChunkWs chunk_ws(int n_req, int max_pages) {
   ChunkWs w;
@@ -79,7 +80,8 @@ static ChunkWs chunk_ws(int n_req, int max_pages) {
   w.list3 = lb;
   w.counts = 2 * lb;
   w.stages = w.counts + al256((size_t)n_req * 2 * sizeof(int32_t));
-  w.total = w.stages + al256((size_t)n_req * max_pages * sizeof(int4) + 1024);
+  w.rbo = w.stages + al256((size_t)n_req * max_pages * sizeof(int4) + 1024);
+  w.total = w.rbo + al256((size_t)(n_req + 1) * sizeof(int32_t));
   return w;
 }
 size_t chunk_ws_bytes(int n_req, int max_pages, int n_q_total, int n_kv_heads, int group, int d) {
@@ -147,26 +149,24 @@ __device__ __forceinline__ half8 h8u(uint32_t a, uint32_t b, uint32_t c, uint32_
 constexpr float CM_INIT = -1.0e30f;  // running max before the first score (finite: no inf - inf)
 
 // LDS of a chunk workgroup (bytes): the ring of raw stages, two buffers of
-// unpacked key operands, three of unpacked value operands, two of the
-// weights the score waves hand to the PV waves, the rows' softmax
-// denominators for the final normalization, and three blocks of the stage
-// table.
+// unpacked key operands, two of unpacked value operands, two of the weights
+// the score waves hand to the PV waves, the rows' softmax denominators for
+// the final normalization, and three blocks of the stage table.
 template <int D>
 struct ChunkLds {
   static constexpr int NK8 = D / 64, NMB = D / 32;
   static constexpr int STAGE = 2 * (int)tq3_region_bytes(D);
-  static constexpr int KX = NK8 * 64 * 32;            // key bytes [k-step][lane][32]
-  static constexpr int KB = KX + 64;                  // + gamma fp16 [page][16]
+  static constexpr int KB = NK8 * 64 * 32;            // key bytes [k-step][lane][32]
   static constexpr int VX = 2 * NMB * 64 * 8;         // value codes [page][block][lane][8]
   static constexpr int SX = 2 * NMB * 32 * 4;         // V scale (hi, lo) fp16 [page][block][row]
   static constexpr int VB = VX + SX + 2 * NMB * 32 * 2;  // + V zero fp16 [page][block][row]
   // weights of one stage from one score wave: 5 half8 operands per lane
-  // ([field][lane][16]: page a hi, lo, page b hi, lo, zero term), the
-  // rescale factor per lane and the wave's moved flag
-  static constexpr int WF_ALPHA = 5 * 1024, WF_FLAG = WF_ALPHA + 256, WPW = WF_FLAG + 16;
+  // ([field][lane][16]: page a hi, lo, page b hi, lo, zero term) and the
+  // rescale factor per lane
+  static constexpr int WF_ALPHA = 5 * 1024, WPW = WF_ALPHA + 256;
   static constexpr int KB0 = CSLOTS * STAGE;
   static constexpr int VB0 = KB0 + 2 * KB;
-  static constexpr int WB0 = VB0 + 3 * VB;
+  static constexpr int WB0 = VB0 + 2 * VB;
   static constexpr int LB0 = WB0 + 2 * NSW * WPW;     // row denominators [score wave][32]
   static constexpr int LS0 = LB0 + NSW * 32 * 4;      // stage-table blocks [3][64 stages][16]
   static constexpr int TOTAL = LS0 + 3 * 1024;
@@ -175,8 +175,10 @@ struct ChunkLds {
   static_assert(TOTAL <= 160 * 1024, "one workgroup's LDS");
 };
 
+// One 128-row block xb of request r and KV head h (the body of a chunk
+// workgroup; every wave of the workgroup runs it).
 template <int D>
-__global__ __launch_bounds__(64 * CW, 1) void chunk_kernel(ChunkArgs a) {
+__device__ __forceinline__ void chunk_block(const ChunkArgs& a, int r, int h, int xb, uint8_t* smem) {
   constexpr int NDW = 3 * D / 128, CL = D / 16, QQ = D / 4;
   constexpr int NKS = D / 16;   // k-steps of the FP8-page score product (16 channels each)
   constexpr int NK8 = D / 64;   // k-steps of the TQ3 score product (64 channels each)
@@ -194,9 +196,7 @@ __global__ __launch_bounds__(64 * CW, 1) void chunk_kernel(ChunkArgs a) {
   static_assert(R8 + 8 <= STAGE, "an FP8 page and its scales fit one stage");
   static_assert(CL == 2 * NMB, "a chunk row of V covers two channels per block");
   static_assert(CW == 2 * NSW, "one PV wave per score wave");
-  extern __shared__ __align__(16) uint8_t smem[];
   const PoolView& P = a.P;
-  const int r = blockIdx.z, h = blockIdx.y;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const bool score_wave = wid < NSW;
@@ -214,9 +214,9 @@ __global__ __launch_bounds__(64 * CW, 1) void chunk_kernel(ChunkArgs a) {
   const int S = a.seq_lens[r];
   const bool range_ok = q0 >= 0 && nq >= 0 && q1 <= a.n_q_total;
   const int rows_r = range_ok ? nq * G : 0;
-  const int rb = blockIdx.x * (NSW * 32) + sw * 32;
+  const int rb = xb * (NSW * 32) + sw * 32;
   if (!range_ok || nq < 1 || S < nq || S > mp * PAGE) {  // workgroup-uniform
-    if (blockIdx.x == 0 && tid == 0) atomicOr(&P.ctrl[CTRL_ERR], (int)MKV_DEVERR_RANGE);
+    if (xb == 0 && tid == 0) atomicOr(&P.ctrl[CTRL_ERR], (int)MKV_DEVERR_RANGE);
     // rows that can be located get zeros
     const int rho = rb + li;
     if (score_wave && rho < rows_r) {
@@ -225,7 +225,7 @@ __global__ __launch_bounds__(64 * CW, 1) void chunk_kernel(ChunkArgs a) {
     }
     return;
   }
-  if (blockIdx.x * (NSW * 32) >= rows_r) return;  // whole workgroup past the rows
+  if (xb * (NSW * 32) >= rows_r) return;  // whole workgroup past the rows (not with the row-block table)
   // Wave pairs whose rows all lie past the request's rows still take part
   // in the copies, the unpacking and the barriers; their scores are all
   // masked.
@@ -270,13 +270,23 @@ __global__ __launch_bounds__(64 * CW, 1) void chunk_kernel(ChunkArgs a) {
     // the pages (so its own wait for a page makes the block visible to it);
     // block k + 1 is copied just before the first page of block k.
     const uint8_t* lsb = smem + LY::LS0;
-    // stage j -> {lp_a, id_a, lp_b, id_b}; id_b < 0 marks an FP8 stage
-    auto stage_at = [&](int j) {
+    // stage j -> {lp_a, id_a, lp_b, id_b}; id_b < 0 marks an FP8 stage.  Two
+    // readers (c = 0: the stage being scored, c = 1: the next stage to copy)
+    // each keep one block in registers, lane l holding stage 64 k + l, and
+    // take an entry with lane reads: one LDS read per 64 stages.
+    int4 blk_v[2] = {make_int4(0, 0, 0, 0), make_int4(0, 0, 0, 0)};
+    int blk_k[2] = {-1, -1};
+    auto stage_at = [&](int j, int c) {
       j = __builtin_amdgcn_readfirstlane(j);
       if (j >= n_st) return make_int4(CMASK_LP, 0, CMASK_LP, 0);  // past the list: never used
-      const int4 v = *reinterpret_cast<const int4*>(lsb + ((j >> 6) % 3) * 1024 + (j & 63) * 16);
-      return make_int4(__builtin_amdgcn_readfirstlane(v.x), __builtin_amdgcn_readfirstlane(v.y),
-                       __builtin_amdgcn_readfirstlane(v.z), __builtin_amdgcn_readfirstlane(v.w));
+      if ((j >> 6) != blk_k[c]) {
+        blk_k[c] = j >> 6;
+        blk_v[c] = *reinterpret_cast<const int4*>(lsb + ((j >> 6) % 3) * 1024 + lane * 16);
+        wait_lgkm0();  // here, so that the lane reads after the join wait for nothing
+      }
+      const int l = j & 63;
+      return make_int4(__builtin_amdgcn_readlane(blk_v[c].x, l), __builtin_amdgcn_readlane(blk_v[c].y, l),
+                       __builtin_amdgcn_readlane(blk_v[c].z, l), __builtin_amdgcn_readlane(blk_v[c].w, l));
     };
     const int layer = a.layer;
     const uint8_t* tq3_l = P.tq3 + (int64_t)layer * P.n_tq3 * H * R3;
@@ -325,10 +335,11 @@ __global__ __launch_bounds__(64 * CW, 1) void chunk_kernel(ChunkArgs a) {
       }
     };
     // Ring bookkeeping: stage s sits in slot s % CSLOTS; `issued` stages have
-    // been copied so far.  The slot of a TQ3 pair s is free from pass s on
-    // (its raw bytes were unpacked in pass s - 1), that of an FP8 page s
-    // from pass s + 2 on (read by the score waves in pass s, by the PV
-    // waves in pass s + 1).  A wait for stage s lets the copies of the
+    // been copied so far.  The slot of a TQ3 pair s is free from pass s + 2
+    // on (its keys are unpacked in pass s - 1, its values and key-norm
+    // corrections read in pass s + 1), that of an FP8 page s from pass s + 3
+    // on (read by the score waves in pass s, by the PV waves in pass
+    // s + 2).  A wait for stage s lets the copies of the
     // stages after it stay in flight (every stage costs a wave the same
     // copies).
     const uint32_t lst_lds = ring_lds + LY::LS0;
@@ -340,13 +351,13 @@ __global__ __launch_bounds__(64 * CW, 1) void chunk_kernel(ChunkArgs a) {
     issue_list(0);
     if (n_blk > 1) issue_list(1);
     wait_vmcnt<0>();
-    int4 e_iss = stage_at(0);  // the entries of stage `issued`
+    int4 e_iss = stage_at(0, 1);  // the entries of stage `issued`
     auto refill = [&](int pass) {
       bool fresh = true;  // e_iss holds stage `issued`
       while (issued < n_st) {
         const int prev = issued - CSLOTS;
-        if (prev >= 0 && (prev < st3 ? prev : prev + 2) > pass) break;
-        if (!fresh) e_iss = stage_at(issued);
+        if (prev >= 0 && (prev < st3 ? prev + 2 : prev + 3) > pass) break;
+        if (!fresh) e_iss = stage_at(issued, 1);
         if ((issued & 63) == 0 && issued > 0 && (issued >> 6) + 1 < n_blk) issue_list((issued >> 6) + 1);
         issue(e_iss, issued % CSLOTS);
         ++issued;
@@ -355,7 +366,7 @@ __global__ __launch_bounds__(64 * CW, 1) void chunk_kernel(ChunkArgs a) {
     };
     // entries of the next stage to copy, loaded at the end of a pass (the
     // barrier's wait covers their latency)
-    auto prefetch_iss = [&]() { e_iss = stage_at(issued); };
+    auto prefetch_iss = [&]() { e_iss = stage_at(issued, 1); };
     auto wait_for = [&](int s) {
       const int later = max(0, min(issued - 1 - s, CSLOTS - 1));
 #define MKV_CHUNK_WAIT(n)                                   \
@@ -476,15 +487,15 @@ __global__ __launch_bounds__(64 * CW, 1) void chunk_kernel(ChunkArgs a) {
     // Online softmax over the base-2 scores sc[16] of this lane's query row
     // (its 16 tokens of the tile; the other 16 sit in lane l ^ 32).  The
     // reference max moves (lazily, when a score passes it by 2^8): alpha is
-    // the factor the PV accumulators still owe, 1 where the reference
-    // stayed; the return value says whether any row of the wave moved.
+    // the factor the PV accumulators still owe, exactly 1 where the
+    // reference stayed (the PV wave skips the rescale when no row of its
+    // tile moved).
     auto softmax = [&](float* sc, float& alpha) {
       float mx = sc[0];
 #pragma unroll
       for (int k = 1; k < 16; ++k) mx = fmaxf(mx, sc[k]);
       mx = fmaxf(mx, lane_xor<32>(mx, lane));
-      const bool need = mx > m_run + 8.0f;
-      const float m_new = need ? mx : m_run;
+      const float m_new = mx > m_run + 8.0f ? mx : m_run;
       alpha = __builtin_amdgcn_exp2f(m_run - m_new);
       m_run = m_new;
       float lsum = 0.0f;
@@ -494,7 +505,6 @@ __global__ __launch_bounds__(64 * CW, 1) void chunk_kernel(ChunkArgs a) {
         lsum += sc[k];
       }
       l_run = fmaf(l_run, alpha, lsum);
-      return __any(need);
     };
     // weights p[0..7] as an fp16 hi + lo pair (one token can carry most of
     // a row's mass, and its weight, taken against a lagging reference max,
@@ -509,7 +519,7 @@ __global__ __launch_bounds__(64 * CW, 1) void chunk_kernel(ChunkArgs a) {
     };
     // hand the weights of stage j (and the rescale the PV accumulators owe
     // before them) to the PV wave of this pair
-    auto put_weights = [&](int j, const TqW& w, float alpha, bool moved) {
+    auto put_weights = [&](int j, const TqW& w, float alpha) {
       uint8_t* ws = wslot(j);
       *reinterpret_cast<half8*>(ws + 0 * 1024 + 16 * lane) = w.ha;
       *reinterpret_cast<half8*>(ws + 1 * 1024 + 16 * lane) = w.la;
@@ -517,7 +527,6 @@ __global__ __launch_bounds__(64 * CW, 1) void chunk_kernel(ChunkArgs a) {
       *reinterpret_cast<half8*>(ws + 3 * 1024 + 16 * lane) = w.lb;
       *reinterpret_cast<half8*>(ws + 4 * 1024 + 16 * lane) = w.z;
       reinterpret_cast<float*>(ws + LY::WF_ALPHA)[lane] = alpha;
-      if (lane == 0) *reinterpret_cast<int*>(ws + LY::WF_FLAG) = moved ? 1 : 0;
     };
 
     // ---- unpacking of a TQ3 pair (the 256 threads of the score waves, from
@@ -532,7 +541,9 @@ __global__ __launch_bounds__(64 * CW, 1) void chunk_kernel(ChunkArgs a) {
     //    the score tile hands each lane its weights);
     //  per (page, block, row rr): the V scale split as (hi, lo) fp16 (hi
     //    keeps 8 significant bits, so code x hi is exact in fp16) and the V
-    //    zero; gamma of both pages after the key bytes.
+    //    zero.
+    // The keys of a pair are unpacked one pass before its score product, its
+    // values one pass after it (with its scores).
     auto unpack_k = [&](const uint8_t* rs, uint8_t* kb) {  // threads 0-127
       const int p = tid >> 6, tok = tid & 15, g = (tid >> 4) & 3;
       uint32_t dw[NDW];
@@ -558,8 +569,8 @@ __global__ __launch_bounds__(64 * CW, 1) void chunk_kernel(ChunkArgs a) {
       for (int q = 0; q < CL; ++q)
         *reinterpret_cast<uint32_t*>(base + ((q >> 1) * 64 + 16 * (q & 1)) * 8) = quad_sel<NDW>(dw, q);
     };
-    auto unpack_side = [&](const uint8_t* rs, uint8_t* kb, uint8_t* vb) {
-      if (tid < NMB * 32) {  // whole waves
+    auto unpack_side = [&](const uint8_t* rs, uint8_t* vb) {
+      if (NMB * 32 >= 64 * NSW || tid < NMB * 32) {  // whole waves (every score wave at d = 256)
         const int mb = tid >> 5, rr = tid & 31, ch = CL * (rr & 15) + 2 * mb + (rr >> 4);
 #pragma unroll
         for (int p = 0; p < 2; ++p) {
@@ -571,95 +582,48 @@ __global__ __launch_bounds__(64 * CW, 1) void chunk_kernel(ChunkArgs a) {
               *reinterpret_cast<const _Float16*>(rs + p * R3 + 14 * D + 32 + 2 * ch);
         }
       }
-      if (tid < 16)
-        *reinterpret_cast<uint32_t*>(kb + LY::KX + 4 * tid) =
-            *reinterpret_cast<const uint32_t*>(rs + (tid >> 3) * R3 + 12 * D + 4 * (tid & 7));
-    };
-    auto unpack = [&](const uint8_t* rs, uint8_t* kb, uint8_t* vb) {
-      if (wid < 2)
-        unpack_k(rs, kb);
-      else
-        unpack_v(rs, vb);
-      unpack_side(rs, kb, vb);
     };
 
-    // Scores and weights of the TQ3 pair e from its unpacked keys kb.  The
-    // score tile's rows are the pair's 32 tokens (page a, then page b); lane
-    // (li, lg) receives tokens 4 lg .. 4 lg + 3 and 8 + 4 lg .. of each page,
-    // which are exactly the k-slots of its weight operand.
-    // (the products are issued first; the rest of the pass's issue work
-    // runs while they execute)
-    auto tq3_qk = [&](const uint8_t* kb, float16v& st0, float16v& st1, auto rev) {
-      st0 = float16v{};
-      st1 = float16v{};  // even and odd k-steps: two MFMA chains
+    // S^T = K Q^T of the pair whose keys are unpacked in kb: M = the pair's
+    // 32 tokens (page a, then page b), N = the wave's 32 rows, one chain of
+    // three MFMAs (one per query term) per k-step
+    auto tq3_qk = [&](const uint8_t* kb, float16v& st, auto rev) {
+      st = float16v{};
 #pragma unroll
       for (int s_ = 0; s_ < NK8; ++s_) {
         const int s = decltype(rev)::value ? NK8 - 1 - s_ : s_;
         const v8i A = *reinterpret_cast<const v8i*>(kb + (s * 64 + lane) * 32);
-        float16v& st = (s & 1) ? st1 : st0;
 #pragma unroll
         for (int t = 0; t < 3; ++t)
           st = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(A, qt[t][s], st, 0, 0, 0, 0, 0, 0);
       }
     };
-    // the score products of the pair in kb_cur with the unpacking of the next
-    // pair (raw stage rs) between them: one straight block per wave kind, so
-    // the unpacking's VALU work fills the MFMA latencies
-    auto qk_unpack = [&](const uint8_t* kb_cur, float16v& st0, float16v& st1, const uint8_t* rs,
-                         uint8_t* kb, uint8_t* vb) {
-      // (the two kinds take the k-steps in opposite orders, which keeps the
-      // compiler from hoisting the shared products out of both blocks)
-      if (wid < 2) {
-        tq3_qk(kb_cur, st0, st1, std::false_type{});
-        unpack_k(rs, kb);
-        unpack_side(rs, kb, vb);
-#pragma unroll
-        for (int k = 0; k < 3 * NK8; ++k) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-          __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);  // VALU
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
-          __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // DS write
-        }
-      } else {
-        tq3_qk(kb_cur, st0, st1, std::true_type{});
-        unpack_v(rs, vb);
-        unpack_side(rs, kb, vb);
-#pragma unroll
-        for (int k = 0; k < 3 * NK8; ++k) {
-          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-          __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);  // VALU
-          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
-          __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // DS write
-        }
-      }
-    };
-    auto tq3_scores = [&](const uint8_t* kb, const float16v& st0, const float16v& st1, const int4& e,
-                          TqW& w, float& alpha) {
-      const float16v st = st0 + st1;
+    // Scores and weights of the TQ3 pair e from its score product st and the
+    // key-norm corrections gamma in its raw stage rs.  Lane (li, lg)
+    // receives tokens 4 lg .. 4 lg + 3 and 8 + 4 lg .. of each page, which
+    // are exactly the k-slots of its weight operand.  `masked`: some token
+    // of the pair lies past the chunk's first query.
+    auto tq3_scores = [&](const uint8_t* rs, const float16v& st, const int4& e, TqW& w, float& alpha,
+                          auto masked) {
       // element e: token 8 (e / 4) + 4 lg + e % 4 of the pair (page a below 16)
       uint2 gw[4];
 #pragma unroll
-      for (int e4 = 0; e4 < 4; ++e4) gw[e4] = *reinterpret_cast<const uint2*>(kb + LY::KX + 16 * e4 + 8 * lg);
+      for (int e4 = 0; e4 < 4; ++e4)
+        gw[e4] = *reinterpret_cast<const uint2*>(rs + (e4 >> 1) * R3 + 12 * D + 16 * (e4 & 1) + 8 * lg);
       float sc[16];
-      if ((max(e.x, e.z) + 1) * PAGE <= P0 + 1) {
-        // the pair lies wholly before the chunk's first query: no mask
 #pragma unroll
-        for (int e4 = 0; e4 < 4; ++e4)
+      for (int e4 = 0; e4 < 4; ++e4) {
+        const int t0 = (e4 < 2 ? e.x : e.z) * PAGE + 8 * (e4 & 1) + 4 * lg;
 #pragma unroll
-          for (int u = 0; u < 4; ++u)
-            sc[4 * e4 + u] = st[4 * e4 + u] * qinv * (float)reinterpret_cast<const _Float16*>(&gw[e4])[u];
-      } else {
-#pragma unroll
-        for (int e4 = 0; e4 < 4; ++e4) {
-          const int t0 = (e4 < 2 ? e.x : e.z) * PAGE + 8 * (e4 & 1) + 4 * lg;
-#pragma unroll
-          for (int u = 0; u < 4; ++u)
-            sc[4 * e4 + u] = t0 + u <= lim
-                                 ? st[4 * e4 + u] * qinv * (float)reinterpret_cast<const _Float16*>(&gw[e4])[u]
-                                 : -INFINITY;
+        for (int u = 0; u < 4; ++u) {
+          const float v = st[4 * e4 + u] * qinv * (float)reinterpret_cast<const _Float16*>(&gw[e4])[u];
+          if constexpr (decltype(masked)::value)
+            sc[4 * e4 + u] = t0 + u <= lim ? v : -INFINITY;
+          else
+            sc[4 * e4 + u] = v;
         }
       }
-      const bool moved = softmax(sc, alpha);
+      softmax(sc, alpha);
       split8(sc, w.ha, w.la);
       split8(sc + 8, w.hb, w.lb);
       const float ra_ = ((sc[0] + sc[1]) + (sc[2] + sc[3])) + ((sc[4] + sc[5]) + (sc[6] + sc[7]));
@@ -667,38 +631,170 @@ __global__ __launch_bounds__(64 * CW, 1) void chunk_kernel(ChunkArgs a) {
       uint32_t zh, zl;
       split2(ra_, rb_, zh, zl);
       w.z = h8u(zh, zl, 0u, 0u);  // (R_a, R_b) hi, then lo
-      return moved;
     };
+    // a pair whose pages both end before the chunk's first query needs no mask
+    auto unmasked = [&](const int4& e) { return (max(e.x, e.z) + 1) * PAGE <= P0 + 1; };
 
-    // ---- passes over the TQ3 pairs
+    // ---- passes over the TQ3 pairs.  Pass p (after barrier p + 1) issues
+    // the score product of pair p (keys unpacked in pass p - 1) and, while
+    // the matrix unit works on it, finishes pair p - 1 (scores from the
+    // product issued in pass p - 1, softmax, weights into LDS) and unpacks
+    // the keys of pair p + 1 and the values of pair p - 1; the PV waves take
+    // pair p - 2.  One straight block per wave kind, so that the VALU and LDS
+    // work fills the MFMA latencies.
+    float16v st_prev = {};                // score product of stage p - 1
+    int4 e_prev = make_int4(0, 0, 0, 0);  // entries of stage p - 1
+    auto tq3_pass = [&](int p, float16v& st, auto masked, auto key_kind) {
+      constexpr bool KK = decltype(key_kind)::value;  // this wave unpacks keys (else values)
+      const uint8_t* kb = kbuf + (p & 1) * LY::KB;
+      uint8_t* kb_next = kbuf + ((p + 1) & 1) * LY::KB;
+      uint8_t* vb_prev = vbuf + ((p + 1) & 1) * LY::VB;  // buffer (p - 1) & 1
+      const uint8_t* rs_prev = smem + ((p + CSLOTS - 1) % CSLOTS) * STAGE;
+      const uint8_t* rs_next = smem + ((p + 1) % CSLOTS) * STAGE;
+      // k-step of the i-th step of the product (the two kinds take the
+      // k-steps in opposite orders, which keeps the compiler from merging
+      // the two blocks' products)
+      auto kstep = [&](int i) { return KK ? i : NK8 - 1 - i; };
+      auto ld_a = [&](int i) { return *reinterpret_cast<const v8i*>(kb + (kstep(i) * 64 + lane) * 32); };
+      v8i A[2];
+      A[0] = ld_a(0);
+      A[1] = ld_a(1);
+      uint2 gw[4];
+#pragma unroll
+      for (int e4 = 0; e4 < 4; ++e4)
+        gw[e4] = *reinterpret_cast<const uint2*>(rs_prev + (e4 >> 1) * R3 + 12 * D + 16 * (e4 & 1) + 8 * lg);
+      st = float16v{};
+      // MFMA m of the product (k-step m / 3, query term m % 3); the operand of
+      // the k-step after next is read once the last MFMA of a k-step is issued
+      auto mf = [&](int m) {
+        const int i = m / 3, t = m % 3;
+        if (i >= NK8) return;  // d = 128: six MFMAs
+        st = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(A[i & 1], qt[t][kstep(i)], st, 0, 0, 0, 0, 0,
+                                                             0);
+        if (t == 2 && i + 2 < NK8) A[i & 1] = ld_a(i + 2);
+        __builtin_amdgcn_sched_barrier(0);
+      };
+      // pair p - 1: scores, softmax and weights, between the MFMAs
+      float sc[16];
+      auto scores = [&](int e4) {
+        const int t0 = (e4 < 2 ? e_prev.x : e_prev.z) * PAGE + 8 * (e4 & 1) + 4 * lg;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const float v = st_prev[4 * e4 + u] * qinv * (float)reinterpret_cast<const _Float16*>(&gw[e4])[u];
+          if constexpr (decltype(masked)::value)
+            sc[4 * e4 + u] = t0 + u <= lim ? v : -INFINITY;
+          else
+            sc[4 * e4 + u] = v;
+        }
+      };
+      float m_new, alpha, lsum = 0.0f;
+      auto ex = [&](int k0, int k1) {
+#pragma unroll
+        for (int k = k0; k < k1; ++k) {
+          sc[k] = __builtin_amdgcn_exp2f(sc[k] - m_new);  // -inf -> 0
+          lsum += sc[k];
+        }
+      };
+      TqW w;
+      mf(0);
+      scores(0);
+      scores(1);
+      __builtin_amdgcn_sched_barrier(0);
+      mf(1);
+      scores(2);
+      scores(3);
+      __builtin_amdgcn_sched_barrier(0);
+      mf(2);
+      {
+        float mx = sc[0];
+#pragma unroll
+        for (int k = 1; k < 16; ++k) mx = fmaxf(mx, sc[k]);
+        mx = fmaxf(mx, lane_xor<32>(mx, lane));
+        m_new = mx > m_run + 8.0f ? mx : m_run;
+        alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+        m_run = m_new;
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      mf(3);
+      ex(0, 6);
+      __builtin_amdgcn_sched_barrier(0);
+      mf(4);
+      ex(6, 11);
+      __builtin_amdgcn_sched_barrier(0);
+      mf(5);
+      ex(11, 16);
+      l_run = fmaf(l_run, alpha, lsum);
+      __builtin_amdgcn_sched_barrier(0);
+      mf(6);
+      split8(sc, w.ha, w.la);
+      __builtin_amdgcn_sched_barrier(0);
+      mf(7);
+      split8(sc + 8, w.hb, w.lb);
+      __builtin_amdgcn_sched_barrier(0);
+      mf(8);
+      {
+        const float ra_ = ((sc[0] + sc[1]) + (sc[2] + sc[3])) + ((sc[4] + sc[5]) + (sc[6] + sc[7]));
+        const float rb_ = ((sc[8] + sc[9]) + (sc[10] + sc[11])) + ((sc[12] + sc[13]) + (sc[14] + sc[15]));
+        uint32_t zh, zl;
+        split2(ra_, rb_, zh, zl);
+        w.z = h8u(zh, zl, 0u, 0u);  // (R_a, R_b) hi, then lo
+      }
+      put_weights(p - 1, w, alpha);
+      __builtin_amdgcn_sched_barrier(0);
+      // then this wave's share of the unpacking: keys of pair p + 1 or
+      // values of pair p - 1, and the values' side data of pair p - 1
+      mf(9);
+      if constexpr (KK)
+        unpack_k(rs_next, kb_next);
+      else
+        unpack_v(rs_prev, vb_prev);
+      __builtin_amdgcn_sched_barrier(0);
+      mf(10);
+      unpack_side(rs_prev, vb_prev);
+      __builtin_amdgcn_sched_barrier(0);
+      mf(11);
+    };
     if (st3 > 0) wait_for(0);
     barrier();
-    if (st3 > 0) unpack(smem, kbuf, vbuf);
-    int4 e_cmp = stage_at(0);  // the entries of the stage being scored
-    for (int j = 0; j < st3; ++j) {
-      if (j + 1 < st3) wait_for(j + 1);
-      barrier();  // pair j unpacked; its raw slot is free
-      // (in the last pass the unpacking reads a slot that holds no pair and
-      // writes buffers nobody reads any more)
-      float16v st0, st1;
-      qk_unpack(kbuf + (j & 1) * LY::KB, st0, st1, smem + ((j + 1) % CSLOTS) * STAGE,
-                kbuf + ((j + 1) & 1) * LY::KB, vbuf + ((j + 1) % 3) * LY::VB);
-      refill(j);
-      const int4 e = e_cmp;
-      TqW w;
-      float alpha;
-      const bool moved = tq3_scores(kbuf + (j & 1) * LY::KB, st0, st1, e, w, alpha);
-      put_weights(j, w, alpha, moved);
-      e_cmp = stage_at(j + 1);
+    if (st3 > 0 && wid < 2) unpack_k(smem, kbuf);
+    for (int p = 0; p < st3; ++p) {
+      if (p + 1 < st3) wait_for(p + 1);
+      barrier();  // keys of pair p unpacked; raw pair p + 1 landed
+      // (in the last pass the key unpacking reads a slot that holds no pair
+      // and writes a buffer nobody reads any more)
+      float16v st;
+      if (p == 0) {
+        if (wid < 2) {
+          tq3_qk(kbuf, st, std::false_type{});
+          unpack_k(smem + (1 % CSLOTS) * STAGE, kbuf + LY::KB);
+        } else {
+          tq3_qk(kbuf, st, std::true_type{});
+        }
+      } else if (unmasked(e_prev)) {
+        if (wid < 2)
+          tq3_pass(p, st, std::false_type{}, std::true_type{});
+        else
+          tq3_pass(p, st, std::false_type{}, std::false_type{});
+      } else {
+        if (wid < 2)
+          tq3_pass(p, st, std::true_type{}, std::true_type{});
+        else
+          tq3_pass(p, st, std::true_type{}, std::false_type{});
+      }
+      refill(p);
+      st_prev = st;
+      e_prev = stage_at(p, 0);
       prefetch_iss();
     }
-    // ---- passes over the FP8 pages: plain queries as fp16 (bf16 -> fp16 is
-    // exact for the query range) against FP8 keys, straight from the ring.
-    // Lane (li, lg) holds, for k-step s, channels (D/2) lg + 8 s + b (b < 8)
-    // of its row.
-    if (st3 < n_st) {
+    // ---- passes over the FP8 pages: pass p scores page p with plain
+    // queries as fp16 (bf16 -> fp16 is exact for the query range) against
+    // its FP8 keys, straight from the ring, and finishes the weights of
+    // stage p - 1 (for p = st3 the last TQ3 pair, whose values it also
+    // unpacks); the last pass only finishes.  Lane (li, lg) holds, for
+    // k-step s, channels (D/2) lg + 8 s + b (b < 8) of its row.
+    {
       half8 qop[NKS];
-      {
+      if (st3 < n_st) {
         const uint16_t* qrow = qrow_ptr + (D / 2) * lg;
 #pragma unroll
         for (int s = 0; s < NKS; ++s) {
@@ -708,51 +804,69 @@ __global__ __launch_bounds__(64 * CW, 1) void chunk_kernel(ChunkArgs a) {
           for (int j = 0; j < 8; ++j) qop[s][j] = (_Float16)bf16_to_f32(hb[j]);
         }
       }
-      for (int j = st3; j < n_st; ++j) {
-        wait_for(j);
-        barrier();  // page j visible
-        refill(j);
-        const int4 e = e_cmp;
-        e_cmp = stage_at(j + 1);
-        prefetch_iss();
-        const uint8_t* ra = smem + (j % CSLOTS) * STAGE;
-        // block-permuted page (see dma_fp8_page): 16-byte block 64 w + 16 Q
-        // + t holds bytes 16 w .. of token t's channel quarter Q (K); score
-        // rows 0-15 are the page's tokens, 16-31 zero
-        const uint2* pk = reinterpret_cast<const uint2*>(ra);
-        const float2 ksv = *reinterpret_cast<const float2*>(ra + R8);
+      float2 ks_prev = make_float2(0.0f, 0.0f);  // key and value scales of FP8 stage p - 1
+      for (int p = st3; p <= n_st; ++p) {
+        if (p < n_st) wait_for(p);
+        barrier();  // page p visible
+        refill(p);
         float16v st = {};
+        float2 ksv = make_float2(0.0f, 0.0f);
+        if (p < n_st) {
+          const uint8_t* ra = smem + (p % CSLOTS) * STAGE;
+          // block-permuted page (see dma_fp8_page): 16-byte block 64 w + 16
+          // Q + t holds bytes 16 w .. of token t's channel quarter Q (K);
+          // score rows 0-15 are the page's tokens, 16-31 zero
+          const uint2* pk = reinterpret_cast<const uint2*>(ra);
+          ksv = *reinterpret_cast<const float2*>(ra + R8);
 #pragma unroll
-        for (int s = 0; s < NKS; ++s) {
-          const int Q = 2 * lg + s / KPC, off = 8 * (s % KPC);
-          half8 K = {};
-          if (li < 16) {
-            const uint2 kw = pk[2 * (64 * (off / 16) + 16 * Q + li) + (off / 8) % 2];
-            K = h8(cvt_lo(kw.x), cvt_hi(kw.x), cvt_lo(kw.y), cvt_hi(kw.y));
+          for (int s = 0; s < NKS; ++s) {
+            const int Q = 2 * lg + s / KPC, off = 8 * (s % KPC);
+            half8 K = {};
+            if (li < 16) {
+              const uint2 kw = pk[2 * (64 * (off / 16) + 16 * Q + li) + (off / 8) % 2];
+              K = h8(cvt_lo(kw.x), cvt_hi(kw.x), cvt_lo(kw.y), cvt_hi(kw.y));
+            }
+            st = __builtin_amdgcn_mfma_f32_32x32x16_f16(K, qop[s], st, 0, 0, 0);
           }
-          st = __builtin_amdgcn_mfma_f32_32x32x16_f16(K, qop[s], st, 0, 0, 0);
         }
-        float sc[16];
-        const float kk = ksv.x * smk;
+        if (p > 0) {
+          TqW w;
+          float alpha;
+          if (p == st3) {  // the last TQ3 pair
+            const uint8_t* rs_prev = smem + ((p + CSLOTS - 1) % CSLOTS) * STAGE;
+            uint8_t* vb_prev = vbuf + ((p + 1) & 1) * LY::VB;
+            if (unmasked(e_prev))
+              tq3_scores(rs_prev, st_prev, e_prev, w, alpha, std::false_type{});
+            else
+              tq3_scores(rs_prev, st_prev, e_prev, w, alpha, std::true_type{});
+            if (wid >= 2) unpack_v(rs_prev, vb_prev);
+            unpack_side(rs_prev, vb_prev);
+          } else {
+            float sc[16];
+            const float kk = ks_prev.x * smk;
 #pragma unroll
-        for (int e4 = 0; e4 < 4; ++e4) {
-          const int t0 = e.x * PAGE + 8 * (e4 & 1) + 4 * lg;
+            for (int e4 = 0; e4 < 4; ++e4) {
+              const int t0 = e_prev.x * PAGE + 8 * (e4 & 1) + 4 * lg;
 #pragma unroll
-          for (int u = 0; u < 4; ++u)
-            sc[4 * e4 + u] = (e4 < 2 && t0 + u <= lim) ? st[4 * e4 + u] * kk : -INFINITY;
+              for (int u = 0; u < 4; ++u)
+                sc[4 * e4 + u] = (e4 < 2 && t0 + u <= lim) ? st_prev[4 * e4 + u] * kk : -INFINITY;
+            }
+            softmax(sc, alpha);
+            // the page's V scale folded into the weights
+            float pw[8];
+#pragma unroll
+            for (int k = 0; k < 8; ++k) pw[k] = sc[k] * ks_prev.y;
+            split8(pw, w.ha, w.la);
+            w.hb = w.la;
+            w.lb = w.la;
+            w.z = w.la;
+          }
+          put_weights(p - 1, w, alpha);
         }
-        float alpha;
-        const bool moved = softmax(sc, alpha);
-        // the page's V scale folded into the weights
-        float pw[8];
-#pragma unroll
-        for (int k = 0; k < 8; ++k) pw[k] = sc[k] * ksv.y;
-        TqW w;
-        split8(pw, w.ha, w.la);
-        w.hb = w.la;
-        w.lb = w.la;
-        w.z = w.la;
-        put_weights(j, w, alpha, moved);
+        st_prev = st;
+        ks_prev = ksv;
+        e_prev = stage_at(p, 0);
+        prefetch_iss();
       }
     }
     barrier();  // the PV waves' last pass
@@ -761,150 +875,230 @@ __global__ __launch_bounds__(64 * CW, 1) void chunk_kernel(ChunkArgs a) {
     barrier();
   } else {
     // ========================= PV waves =========================
-    // accumulators: O^T tile (32 channels x the 32 query rows) per block mb.
-    // Lane (li, lg), element e holds query row rb + li and tile row rr = 8
-    // (e / 4) + 4 lg + e % 4, which is channel CL (rr % 16) + 2 mb + rr / 16
-    // (the value unpacking lays its operands out for this order).
-    float16v acc[NMB];
+    // PV wave v owns the 32-channel blocks mb = NBW v .. NBW v + NBW - 1 of
+    // the output for all 128 rows of the workgroup (the rows of every score
+    // wave g), so each value operand is built once per workgroup.
+    // Accumulators: O^T tile (32 channels x the 32 rows of score wave g) per
+    // (block, g).  Lane (li, lg), element e holds row 32 g + li and tile row
+    // rr = 8 (e / 4) + 4 lg + e % 4, which is channel CL (rr % 16) + 2 mb +
+    // rr / 16 (the value unpacking lays its operands out for this order).
+    constexpr int NBW = NMB / NSW;
+    static_assert(NMB % NSW == 0 && NBW <= 2, "whole blocks per PV wave");
+    const int pv = wid - NSW;
+    float16v acc[NBW][NSW];
 #pragma unroll
-    for (int mb = 0; mb < NMB; ++mb) acc[mb] = float16v{};
-    // the weights of stage j, after the rescale they carry
-    auto get_weights = [&](int j, TqW& w) {
-      const uint8_t* ws = wslot(j);
-      if (*reinterpret_cast<const int*>(ws + LY::WF_FLAG)) {
-        const float alpha = reinterpret_cast<const float*>(ws + LY::WF_ALPHA)[lane];
+    for (int b = 0; b < NBW; ++b)
 #pragma unroll
-        for (int mb = 0; mb < NMB; ++mb) acc[mb] *= alpha;  // column = this lane's row
+      for (int g = 0; g < NSW; ++g) acc[b][g] = float16v{};
+    // weights of stage j from score wave g
+    auto wsl = [&](int j, int g) { return wbuf + ((j & 1) * NSW + g) * LY::WPW; };
+    // the rescales the weights of stage j carry, one per score wave (skipped
+    // when every factor is 1: no reference max moved)
+    auto rescale = [&](int j) {
+      float al[NSW];
+      bool any = false;
+#pragma unroll
+      for (int g = 0; g < NSW; ++g) {
+        al[g] = reinterpret_cast<const float*>(wsl(j, g) + LY::WF_ALPHA)[lane];
+        any |= al[g] != 1.0f;
       }
+      if (__any(any)) {
+#pragma unroll
+        for (int b = 0; b < NBW; ++b)
+#pragma unroll
+          for (int g = 0; g < NSW; ++g) acc[b][g] *= al[g];  // column = this lane's row
+      }
+    };
+    auto ld_w = [&](int j, int g, TqW& w) {
+      const uint8_t* ws = wsl(j, g);
       w.ha = *reinterpret_cast<const half8*>(ws + 0 * 1024 + 16 * lane);
       w.la = *reinterpret_cast<const half8*>(ws + 1 * 1024 + 16 * lane);
       w.hb = *reinterpret_cast<const half8*>(ws + 2 * 1024 + 16 * lane);
       w.lb = *reinterpret_cast<const half8*>(ws + 3 * 1024 + 16 * lane);
       w.z = *reinterpret_cast<const half8*>(ws + 4 * 1024 + 16 * lane);
     };
-    // O^T += V^T P^T for the TQ3 pair unpacked in vb, with exact V operands:
-    // v = zero + scale * code is split as scale_hi * code + scale_lo * code
-    // + zero.  The products that reach fp32 accuracy: (hi + lo weights) x
-    // scale_hi term, hi weights x scale_lo term (lo x scale_lo sits below
-    // 2^-19 of the value), and the zero term as zero_a (sum of weights over
-    // page a) + zero_b (same for b), whose sums the MFMA completes across
-    // the two lane groups.
-    auto tq3_pv = [&](const uint8_t* vb, const TqW& w) {
+    // O^T += V^T P^T for the TQ3 pair of stage j (values unpacked in vb),
+    // with exact V operands: v = zero + scale * code is split as scale_hi *
+    // code + scale_lo * code + zero.  The products that reach fp32 accuracy:
+    // (hi + lo weights) x scale_hi term, hi weights x scale_lo term (lo x
+    // scale_lo sits below 2^-19 of the value), and the zero term as zero_a
+    // (sum of weights over page a) + zero_b (same for b), whose sums the
+    // MFMA completes across the two lane groups.
+    auto tq3_pv = [&](int j) {
+      const uint8_t* vb = vbuf + (j & 1) * LY::VB;
       const _Float16* zx = reinterpret_cast<const _Float16*>(vb + LY::VX + LY::SX);
-      // software pipeline over the blocks: the LDS reads of block mb + 2 and
-      // the operand building of block mb + 1 run between the MFMAs of block mb
-      struct Raw {
-        uint2 cw[2];
-        half2v s2[2];
-        _Float16 za, zb;
-      };
       struct Ops {
         half8 A1[2], A2[2], Az;
       };
-      auto load = [&](int mb, Raw& x) {
+      // the weights of score wave g + 1 are read while the products of g run
+      TqW wb[2];
+      ld_w(j, 0, wb[0]);
+      Ops op[NBW];
+#pragma unroll
+      for (int b = 0; b < NBW; ++b) {
+        const int mb = NBW * pv + b;
 #pragma unroll
         for (int p = 0; p < 2; ++p) {
-          x.cw[p] = *reinterpret_cast<const uint2*>(vb + ((p * NMB + mb) * 64 + lane) * 8);
-          x.s2[p] = *reinterpret_cast<const half2v*>(vb + LY::VX + ((p * NMB + mb) * 32 + li) * 4);
+          const uint2 cw = *reinterpret_cast<const uint2*>(vb + ((p * NMB + mb) * 64 + lane) * 8);
+          const half2v s2 = *reinterpret_cast<const half2v*>(vb + LY::VX + ((p * NMB + mb) * 32 + li) * 4);
+          const half2v sh = bcast(s2[0]), sl = bcast(s2[1]);
+          const half2v c01 = cvt_code<false>(cw.x), c23 = cvt_code<true>(cw.x);
+          const half2v c45 = cvt_code<false>(cw.y), c67 = cvt_code<true>(cw.y);
+          op[b].A1[p] = h8(c01 * sh, c23 * sh, c45 * sh, c67 * sh);
+          op[b].A2[p] = h8(c01 * sl, c23 * sl, c45 * sl, c67 * sl);
         }
-        x.za = zx[mb * 32 + li];
-        x.zb = zx[(NMB + mb) * 32 + li];
-      };
-      auto build = [&](const Raw& x, Ops& o) {
+        const _Float16 za = zx[mb * 32 + li], zb = zx[(NMB + mb) * 32 + li];
+        op[b].Az = half8{za, zb, za, zb, (_Float16)0.0f, (_Float16)0.0f, (_Float16)0.0f, (_Float16)0.0f};
+      }
+      rescale(j);
 #pragma unroll
-        for (int p = 0; p < 2; ++p) {
-          const half2v sh = bcast(x.s2[p][0]), sl = bcast(x.s2[p][1]);
-          const half2v c01 = cvt_code<false>(x.cw[p].x), c23 = cvt_code<true>(x.cw[p].x);
-          const half2v c45 = cvt_code<false>(x.cw[p].y), c67 = cvt_code<true>(x.cw[p].y);
-          o.A1[p] = h8(c01 * sh, c23 * sh, c45 * sh, c67 * sh);
-          o.A2[p] = h8(c01 * sl, c23 * sl, c45 * sl, c67 * sl);
-        }
-        o.Az = half8{x.za, x.zb, x.za, x.zb, (_Float16)0.0f, (_Float16)0.0f, (_Float16)0.0f,
-                     (_Float16)0.0f};
-      };
-      Raw xr[2];
-      Ops op[2];
-      load(0, xr[0]);
-      if (NMB > 1) load(1, xr[1]);
-      build(xr[0], op[0]);
-#pragma unroll
-      for (int mb = 0; mb < NMB; ++mb) {
-        const Ops& o = op[mb & 1];
-        if (mb + 1 < NMB) build(xr[(mb + 1) & 1], op[(mb + 1) & 1]);
-        if (mb + 2 < NMB) load(mb + 2, xr[mb & 1]);
-        acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(o.A1[0], w.ha, acc[mb], 0, 0, 0);
-        acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(o.A2[0], w.ha, acc[mb], 0, 0, 0);
-        acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(o.A1[0], w.la, acc[mb], 0, 0, 0);
-        acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(o.A1[1], w.hb, acc[mb], 0, 0, 0);
-        acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(o.A2[1], w.hb, acc[mb], 0, 0, 0);
-        acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(o.A1[1], w.lb, acc[mb], 0, 0, 0);
-        acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(o.Az, w.z, acc[mb], 0, 0, 0);
-        // one MFMA, then a share of the next block's VALU and LDS work
-        if (mb + 1 < NMB) {
-#pragma unroll
-          for (int k = 0; k < 7; ++k) {
-            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // MFMA
-            __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);  // VALU
-            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
-          }
-        }
+      for (int g = 0; g < NSW; ++g) {
+        if (g + 1 < NSW) ld_w(j, g + 1, wb[(g + 1) & 1]);
         __builtin_amdgcn_sched_barrier(0);
+        const TqW& w = wb[g & 1];
+        // the blocks' chains interleaved
+#define MKV_PV(A, B)                                                                     \
+  _Pragma("unroll") for (int b = 0; b < NBW; ++b) acc[b][g] =                            \
+      __builtin_amdgcn_mfma_f32_32x32x16_f16(op[b].A, w.B, acc[b][g], 0, 0, 0);
+        MKV_PV(A1[0], ha)
+        MKV_PV(A2[0], ha)
+        MKV_PV(A1[0], la)
+        MKV_PV(A1[1], hb)
+        MKV_PV(A2[1], hb)
+        MKV_PV(A1[1], lb)
+        MKV_PV(Az, z)
+#undef MKV_PV
       }
     };
-    // O^T += V^T P^T for the FP8 page in ring slot ra (weights hi + lo, the
-    // page's V scale already folded in): lane-chunks (rrow, lg) and (rrow,
-    // lg + 2) of V, dword m = tokens 4 g' .. 4 g' + 3 of channel CL rrow + m
-    auto fp8_pv = [&](const uint8_t* ra, const TqW& w) {
+    // O^T += V^T P^T for the FP8 page of stage j in ring slot ra (weights hi +
+    // lo, the page's V scale already folded in): lane-chunks (rrow, lg) and
+    // (rrow, lg + 2) of V, dword m = tokens 4 g' .. 4 g' + 3 of channel CL
+    // rrow + m
+    auto fp8_pv = [&](const uint8_t* ra, int j) {
       const int rrow = li & 15, hh = li >> 4;
-      const uint2* pv = reinterpret_cast<const uint2*>(ra + PAGE * D);
+      const uint2* pvp = reinterpret_cast<const uint2*>(ra + PAGE * D);
+      half8 Av[NBW];
 #pragma unroll
-      for (int mb = 0; mb < NMB; ++mb) {
+      for (int b = 0; b < NBW; ++b) {
+        const int mb = NBW * pv + b;
         const int blk = 64 * (mb / 2);
-        const uint2 v0 = pv[2 * (blk + 16 * lg + rrow) + (mb & 1)];
-        const uint2 v2 = pv[2 * (blk + 16 * (lg + 2) + rrow) + (mb & 1)];
+        const uint2 v0 = pvp[2 * (blk + 16 * lg + rrow) + (mb & 1)];
+        const uint2 v2 = pvp[2 * (blk + 16 * (lg + 2) + rrow) + (mb & 1)];
         const uint32_t w0 = hh ? v0.y : v0.x, w2 = hh ? v2.y : v2.x;
-        const half8 Av = h8(cvt_lo(w0), cvt_hi(w0), cvt_lo(w2), cvt_hi(w2));
-        acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(Av, w.ha, acc[mb], 0, 0, 0);
-        acc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_f16(Av, w.la, acc[mb], 0, 0, 0);
+        Av[b] = h8(cvt_lo(w0), cvt_hi(w0), cvt_lo(w2), cvt_hi(w2));
+      }
+      rescale(j);
+#pragma unroll
+      for (int g = 0; g < NSW; ++g) {
+        const uint8_t* ws = wsl(j, g);
+        const half8 ha = *reinterpret_cast<const half8*>(ws + 0 * 1024 + 16 * lane);
+        const half8 la = *reinterpret_cast<const half8*>(ws + 1 * 1024 + 16 * lane);
+#pragma unroll
+        for (int b = 0; b < NBW; ++b) acc[b][g] = __builtin_amdgcn_mfma_f32_32x32x16_f16(Av[b], ha, acc[b][g], 0, 0, 0);
+#pragma unroll
+        for (int b = 0; b < NBW; ++b) acc[b][g] = __builtin_amdgcn_mfma_f32_32x32x16_f16(Av[b], la, acc[b][g], 0, 0, 0);
       }
     };
-    barrier();  // the score waves' first unpacking
-    barrier();  // pass 0: the weights of stage 0
-    for (int j = 0; j < st3; ++j) {  // pass j + 1
+    barrier();  // the score waves' first key unpacking
+    barrier();  // pass 0: the score product of stage 0
+    barrier();  // pass 1: the weights of stage 0
+    for (int j = 0; j < st3; ++j) {  // pass j + 2
       barrier();
-      TqW w;
-      get_weights(j, w);
-      tq3_pv(vbuf + (j % 3) * LY::VB, w);
+      tq3_pv(j);
     }
     for (int j = st3; j < n_st; ++j) {
       barrier();
-      TqW w;
-      get_weights(j, w);
-      fp8_pv(smem + (j % CSLOTS) * STAGE, w);
+      fp8_pv(smem + (j % CSLOTS) * STAGE, j);
     }
     barrier();  // the rows' denominators
     // ---- normalize and store: tile row rr = 8 kk + 4 lg + u (kk, u: the
     // lane's elements 4 kk + u and 8 + 4 kk + u) is chunk row rr % 16 = rr
-    // for both halves hh = 0, 1 of every block, so channels CL rr .. CL rr +
-    // CL - 1 are contiguous: channel CL rr + 2 mb + hh <- acc[mb][4 kk + 8
-    // hh + u]
-    if (rho_l < rows_r) {
-      const float L = lbuf[sw * 32 + li];
-      const float inv = L > 0.0f ? 1.0f / L : 0.0f;
-      float* o = a.out + ((int64_t)(q0 + rho_l / G) * Hq + h * G + rho_l % G) * D;
+    // for both halves hh = 0, 1 of every block, so this wave's channels
+    // CL rr + 2 NBW pv .. + 2 NBW - 1 are contiguous: channel CL rr + 2 mb +
+    // hh <- acc[mb - NBW pv][g][4 kk + 8 hh + u]
 #pragma unroll
-      for (int kk = 0; kk < 2; ++kk)
+    for (int g = 0; g < NSW; ++g) {
+      const int rho = xb * (NSW * 32) + g * 32 + li;
+      if (rho < rows_r) {
+        const float L = lbuf[g * 32 + li];
+        const float inv = L > 0.0f ? 1.0f / L : 0.0f;
+        float* o = a.out + ((int64_t)(q0 + rho / G) * Hq + h * G + rho % G) * D + 2 * NBW * pv;
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const int rr = 8 * kk + 4 * lg + u;
+        for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-          for (int v = 0; v < NMB / 2; ++v)
-            *reinterpret_cast<float4*>(o + CL * rr + 4 * v) =
-                make_float4(acc[2 * v][4 * kk + u] * inv, acc[2 * v][4 * kk + 8 + u] * inv,
-                            acc[2 * v + 1][4 * kk + u] * inv, acc[2 * v + 1][4 * kk + 8 + u] * inv);
-        }
+          for (int u = 0; u < 4; ++u) {
+            const int rr = 8 * kk + 4 * lg + u;
+            if constexpr (NBW == 2)
+              *reinterpret_cast<float4*>(o + CL * rr) =
+                  make_float4(acc[0][g][4 * kk + u] * inv, acc[0][g][4 * kk + 8 + u] * inv,
+                              acc[1][g][4 * kk + u] * inv, acc[1][g][4 * kk + 8 + u] * inv);
+            else
+              *reinterpret_cast<float2*>(o + CL * rr) =
+                  make_float2(acc[0][g][4 * kk + u] * inv, acc[0][g][4 * kk + 8 + u] * inv);
+          }
+      }
     }
   }
+}
+
+// Row blocks of a chunk call: request r gets ceil(n_r G / 128) blocks of 128
+// rows (at least one, and one for a request whose query range is invalid, so
+// that its error is reported); rbo[r] = the blocks before request r,
+// rbo[n_req] = all of them.  Query ranges that do not overlap need at most
+// `grid` blocks (the launch's width); ranges that overlap and need more set
+// the range error bit and rbo[n_req] = 0: the call writes nothing.  One
+// workgroup.
+__global__ __launch_bounds__(256) void chunk_rows_kernel(int n_req, const int32_t* cu_q, int n_q_total,
+                                                         int group, int grid, int32_t* rbo,
+                                                         int32_t* err) {
+  __shared__ int part[256];
+  const int t = threadIdx.x;
+  const int per = (n_req + 255) / 256;
+  const int r0 = min(n_req, t * per), r1 = min(n_req, r0 + per);
+  auto blocks = [&](int r) {
+    const int q0 = cu_q[r], q1 = cu_q[r + 1];
+    const bool ok = q0 >= 0 && q1 >= q0 && q1 <= n_q_total;
+    return ok ? max(1, (int)(((int64_t)(q1 - q0) * group + NSW * 32 - 1) / (NSW * 32))) : 1;
+  };
+  int sum = 0;
+  for (int r = r0; r < r1; ++r) sum += blocks(r);
+  part[t] = sum;
+  __syncthreads();
+  for (int o = 1; o < 256; o <<= 1) {  // inclusive scan of the thread sums
+    const int v = t >= o ? part[t - o] : 0;
+    __syncthreads();
+    part[t] += v;
+    __syncthreads();
+  }
+  int base = part[t] - sum;
+  for (int r = r0; r < r1; ++r) {
+    rbo[r] = base;
+    base += blocks(r);
+  }
+  if (t == 255) {
+    const bool fits = part[255] <= grid;
+    rbo[n_req] = fits ? part[255] : 0;
+    if (!fits) atomicOr(err, (int)MKV_DEVERR_RANGE);
+  }
+}
+
+// Grid (row block over all requests, KV head): workgroup x takes global row
+// block x and finds its request in the row-block table (workgroups past the
+// last block return at once).
+template <int D>
+__global__ __launch_bounds__(64 * CW, 1) void chunk_kernel(ChunkArgs a) {
+  extern __shared__ __align__(16) uint8_t smem[];
+  const int gb = blockIdx.x;
+  if (gb >= a.rbo[a.n_req]) return;
+  int lo = 0, hi = a.n_req - 1;  // the last request whose first block is <= gb
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (a.rbo[mid] <= gb)
+      lo = mid;
+    else
+      hi = mid - 1;
+  }
+  chunk_block<D>(a, lo, blockIdx.y, gb - a.rbo[lo], smem);
 }
 
 hipError_t launch_chunk(const PoolView& P, int layer, int n_req, const uint16_t* q,
@@ -927,10 +1121,12 @@ hipError_t launch_chunk(const PoolView& P, int layer, int n_req, const uint16_t*
   int32_t* list3 = reinterpret_cast<int32_t*>(w + wl.list3);
   int32_t* counts = reinterpret_cast<int32_t*>(w + wl.counts);
   int4* stages = reinterpret_cast<int4*>(w + wl.stages);
+  int32_t* rbo = reinterpret_cast<int32_t*>(w + wl.rbo);
   a.list8 = list8;
   a.list3 = list3;
   a.counts = counts;
   a.stages = stages;
+  a.rbo = rbo;
   a.sm_log2 = 1.4426950408889634f / sqrtf((float)P.d);
   hipError_t e = launch_partition(n_req, bt, tags, max_pages, seq_lens, list8, list3, counts,
                                   P.ctrl + CTRL_ERR, s);
@@ -939,15 +1135,20 @@ hipError_t launch_chunk(const PoolView& P, int layer, int n_req, const uint16_t*
                      max_pages, P.n_tq3, P.n_fp8, list8, list3, counts, stages, P.ctrl + CTRL_ERR);
   e = hipGetLastError();
   if (e != hipSuccess) return e;
+  // row blocks of all requests: at most ceil(n_q_total G / 128) + n_req when
+  // the query ranges do not overlap
+  const int64_t rows = (int64_t)n_q_total * P.group;
+  const int wg_rows = NSW * 32;
+  const int blocks = (int)((rows + wg_rows - 1) / wg_rows) + n_req;
+  hipLaunchKernelGGL(chunk_rows_kernel, dim3(1), dim3(256), 0, s, n_req, cu_q, n_q_total, P.group, blocks,
+                     rbo, P.ctrl + CTRL_ERR);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
   const size_t lds = P.d == 256 ? (size_t)ChunkLds<256>::TOTAL : (size_t)ChunkLds<128>::TOTAL;
   const void* kern = P.d == 256 ? (const void*)chunk_kernel<256> : (const void*)chunk_kernel<128>;
   e = hipFuncSetAttribute(kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  // rows of one request: at most n_q_total queries x group heads
-  const int64_t rows = (int64_t)n_q_total * P.group;
-  const int wg_rows = NSW * 32;
-  const int blocks = (int)((rows + wg_rows - 1) / wg_rows);
-  dim3 grid(blocks, P.n_kv_heads, n_req);
+  dim3 grid(blocks, P.n_kv_heads);
   void* args[] = {&a};
   e = hipLaunchKernel(kern, grid, dim3(64 * CW), args, lds, s);
   if (e != hipSuccess) return e;

@@ -551,6 +551,49 @@ def test_chunk_group12_d256(torch_cuda):
     _run_chunk_case(w, list(w.ctx), [70, 21], recent=48)
 
 
+def test_chunk_invalid_requests(torch_cuda):
+    """Error paths of the chunk call.  A request whose length is shorter than
+    its chunk gets zero rows and the range bit, while the other requests'
+    rows equal those of the valid call bit for bit (each 128-row block is
+    computed on its own).  Query ranges that overlap so that their row blocks
+    exceed the launch set the range bit and leave the output untouched."""
+    from _harness import Twin
+    import paper_2608_23834_amd as mk
+    torch = torch_cuda
+    w = wl.scaled(wl.workload(5), (700, 300, 500), n_layers=1, name="chunk-errors")
+    n_q = [40, 21, 33]
+    tw = Twin(w, lens=list(w.ctx), with_oracle=False, recent=64)
+    tw.fill_to([l - n for l, n in zip(w.ctx, n_q)])
+    tw.migrate()
+    tw.append(n_q)
+    res = tw.chunk(n_q)
+    assert mk.kv_pool_check_errors(tw.gpu, clear=True) == 0
+    good, cu = res["out"], res["cu"]
+    q = torch.from_numpy(res["q"].view(np.int16)).cuda()
+    ws = mk.workspace(tw.gpu, tw.n_req, tw.max_pages, res["q"].shape[0])
+
+    def call(cu_np, sl_np, n_rows):
+        out = torch.full((n_rows, w.n_q_heads, w.head_dim), float("nan"), device="cuda")
+        mk.paged_attn_chunk(tw.gpu, 0, q[:n_rows].contiguous(), torch.from_numpy(cu_np).cuda(), tw.bt,
+                            tw.tags, torch.from_numpy(sl_np).cuda(), out, ws)
+        torch.cuda.synchronize()
+        return out.cpu().numpy()
+
+    sl = res["seq_lens"].copy()
+    sl[1] = 10  # below its 21 queries
+    o = call(cu, sl, res["q"].shape[0])
+    assert mk.kv_pool_check_errors(tw.gpu, clear=True) & mk.DEVERR["RANGE"]
+    assert np.all(o[cu[1]:cu[2]] == 0.0)
+    assert np.array_equal(o[:cu[1]], good[:cu[1]]) and np.array_equal(o[cu[2]:], good[cu[2]:])
+    # requests 0 and 2 both claim queries 0..93 (request 1's range is
+    # reversed): 5 + 1 + 5 row blocks against a launch of ceil(94 * 6 / 128)
+    # + 3 = 8
+    o = call(np.array([0, 94, 0, 94], np.int32), res["seq_lens"], 94)
+    assert mk.kv_pool_check_errors(tw.gpu, clear=True) & mk.DEVERR["RANGE"]
+    assert np.all(np.isnan(o))
+    print("\n  invalid length: zero rows, others bit-identical; overlap: untouched", flush=True)
+
+
 def test_chunk_last_query_matches_decode(torch_cuda):
     """Property that holds at any size, checked without the oracle: the last
     query of each request's chunk sees the whole context, so the chunk kernel's
