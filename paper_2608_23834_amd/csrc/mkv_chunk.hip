@@ -135,10 +135,12 @@ __device__ __forceinline__ half2v bcast(_Float16 x) { return half2v{x, x}; }
 // (a, b) as fp16 pairs hi = (a, b) rounded to nearest, lo = the rounded
 // remainders: together 22 significant bits.  (The round-toward-zero packed
 // conversion flushes fp16 subnormals, so the low part of every weight below
-// 2^-4 vanished and chunk outputs moved by up to 1.3e-3.)
-__device__ __forceinline__ void split2(float a, float b, uint32_t& hi, uint32_t& lo) {
+// 2^-4 vanished and chunk outputs moved by up to 1.3e-3.)  The remainders
+// a - hi are single mixed-precision FMAs (hi read as fp16) with neg1 = -1
+// held in a register.
+__device__ __forceinline__ void split2(float a, float b, float neg1, uint32_t& hi, uint32_t& lo) {
   const half2v h = {(_Float16)a, (_Float16)b};
-  const half2v l = {(_Float16)(a - (float)h[0]), (_Float16)(b - (float)h[1])};
+  const half2v l = {(_Float16)__builtin_fmaf((float)h[0], neg1, a), (_Float16)__builtin_fmaf((float)h[1], neg1, b)};
   hi = __builtin_bit_cast(uint32_t, h);
   lo = __builtin_bit_cast(uint32_t, l);
 }
@@ -262,6 +264,8 @@ __device__ __forceinline__ void chunk_block(const ChunkArgs& a, int r, int h, in
     // feed the next one; the PV waves have slack): the SIMD's arbiter takes
     // their instructions first and fills the gaps with the PV waves'.
     __builtin_amdgcn_s_setprio(2);
+    float neg1 = -1.0f;  // kept in a register (see split2)
+    __asm__ __volatile__("" : "+v"(neg1));
     const int rho_c = min(rho_l, rows_r - 1);  // a valid row to load for masked lanes
     const uint16_t* qrow_ptr = a.q + ((int64_t)(q0 + rho_c / G) * Hq + h * G + rho_c % G) * D;
     const uint8_t* stab = reinterpret_cast<const uint8_t*>(a.stages + (int64_t)r * mp);
@@ -458,7 +462,7 @@ __device__ __forceinline__ void chunk_block(const ChunkArgs& a, int r, int h, in
       (void)frexpf(amax, &ex);  // amax in [2^(ex-1), 2^ex)
       const bool ok = rho_l < rows_r && amax > 0.0f;
       const float qsc = ok ? ldexpf(1.0f, 8 - ex) : 0.0f;
-      qinv = ok ? ldexpf(1.0f, ex - 8) : 0.0f;
+      qinv = ok ? ldexpf(1.0f, ex - 8) : 1.0f;  // (the terms of such a row are all zero)
 #pragma unroll
       for (int s = 0; s < NK8; ++s)
 #pragma unroll
@@ -513,7 +517,7 @@ __device__ __forceinline__ void chunk_block(const ChunkArgs& a, int r, int h, in
     auto split8 = [&](const float* p, half8& hi, half8& lo) {
       uint32_t hh4[4], ll4[4];
 #pragma unroll
-      for (int k = 0; k < 4; ++k) split2(p[2 * k], p[2 * k + 1], hh4[k], ll4[k]);
+      for (int k = 0; k < 4; ++k) split2(p[2 * k], p[2 * k + 1], neg1, hh4[k], ll4[k]);
       hi = h8u(hh4[0], hh4[1], hh4[2], hh4[3]);
       lo = h8u(ll4[0], ll4[1], ll4[2], ll4[3]);
     };
@@ -629,7 +633,7 @@ __device__ __forceinline__ void chunk_block(const ChunkArgs& a, int r, int h, in
       const float ra_ = ((sc[0] + sc[1]) + (sc[2] + sc[3])) + ((sc[4] + sc[5]) + (sc[6] + sc[7]));
       const float rb_ = ((sc[8] + sc[9]) + (sc[10] + sc[11])) + ((sc[12] + sc[13]) + (sc[14] + sc[15]));
       uint32_t zh, zl;
-      split2(ra_, rb_, zh, zl);
+      split2(ra_, rb_, neg1, zh, zl);
       w.z = h8u(zh, zl, 0u, 0u);  // (R_a, R_b) hi, then lo
     };
     // a pair whose pages both end before the chunk's first query needs no mask
@@ -680,7 +684,9 @@ __device__ __forceinline__ void chunk_block(const ChunkArgs& a, int r, int h, in
         const int t0 = (e4 < 2 ? e_prev.x : e_prev.z) * PAGE + 8 * (e4 & 1) + 4 * lg;
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          const float v = st_prev[4 * e4 + u] * qinv * (float)reinterpret_cast<const _Float16*>(&gw[e4])[u];
+          // st * gamma as one mixed-precision FMA; the power-of-two row
+          // factor qinv enters with the max and the exponent (exact)
+          const float v = __builtin_fmaf((float)reinterpret_cast<const _Float16*>(&gw[e4])[u], st_prev[4 * e4 + u], 0.0f);
           if constexpr (decltype(masked)::value)
             sc[4 * e4 + u] = t0 + u <= lim ? v : -INFINITY;
           else
@@ -691,7 +697,7 @@ __device__ __forceinline__ void chunk_block(const ChunkArgs& a, int r, int h, in
       auto ex = [&](int k0, int k1) {
 #pragma unroll
         for (int k = k0; k < k1; ++k) {
-          sc[k] = __builtin_amdgcn_exp2f(sc[k] - m_new);  // -inf -> 0
+          sc[k] = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[k], qinv, -m_new));  // -inf -> 0
           lsum += sc[k];
         }
       };
@@ -709,7 +715,7 @@ __device__ __forceinline__ void chunk_block(const ChunkArgs& a, int r, int h, in
         float mx = sc[0];
 #pragma unroll
         for (int k = 1; k < 16; ++k) mx = fmaxf(mx, sc[k]);
-        mx = fmaxf(mx, lane_xor<32>(mx, lane));
+        mx = fmaxf(mx, lane_xor<32>(mx, lane)) * qinv;
         m_new = mx > m_run + 8.0f ? mx : m_run;
         alpha = __builtin_amdgcn_exp2f(m_run - m_new);
         m_run = m_new;
@@ -736,7 +742,7 @@ __device__ __forceinline__ void chunk_block(const ChunkArgs& a, int r, int h, in
         const float ra_ = ((sc[0] + sc[1]) + (sc[2] + sc[3])) + ((sc[4] + sc[5]) + (sc[6] + sc[7]));
         const float rb_ = ((sc[8] + sc[9]) + (sc[10] + sc[11])) + ((sc[12] + sc[13]) + (sc[14] + sc[15]));
         uint32_t zh, zl;
-        split2(ra_, rb_, zh, zl);
+        split2(ra_, rb_, neg1, zh, zl);
         w.z = h8u(zh, zl, 0u, 0u);  // (R_a, R_b) hi, then lo
       }
       put_weights(p - 1, w, alpha);
