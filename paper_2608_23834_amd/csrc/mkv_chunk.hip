@@ -6,35 +6,38 @@
 // plain queries against FP8 keys, one online softmax per query row.
 //
 // Launch: the partition kernel (compact per-format lists, Sec. 4.1), a stage
-// table kernel (per request: the TQ3 pages in pairs, then the FP8 pages) and
-// the attention kernel.  Grid (row block, KV head, request); 512 threads =
-// 8 waves, one workgroup per CU, two waves per SIMD.  A query row is a
-// (query token, head of the GQA group) pair; a workgroup owns 128 rows, and
-// its waves come in pairs over 32 rows each:
-//  * a score wave holds its rows' rotated queries as three E4M3 terms in
-//    registers, copies its share of every stage (direct HBM -> LDS copies
-//    into a ring of eight stages) and of the stage table, unpacks its share
-//    of the next TQ3 pair into MFMA operand layouts in LDS (key codes ->
-//    E4M3 codebook bytes, value codes as bytes, the V scale split for exact
-//    fp16 products), and computes S^T = K Q^T on
+// table kernel (per request: the TQ3 pages in pairs, then the FP8 pages), a
+// row-block table kernel (first 128-row block of each request) and the
+// attention kernel.  Grid (row block over all requests, KV head); 512
+// threads = 8 waves, one workgroup per CU, two waves per SIMD.  A query row
+// is a (query token, head of the GQA group) pair; a workgroup owns 128 rows:
+//  * four score waves of 32 rows each hold their rows' rotated queries as
+//    three E4M3 terms in registers, copy their share of every stage (direct
+//    HBM -> LDS copies into a ring of eight stages) and of the stage table,
+//    unpack TQ3 pairs into MFMA operand layouts in LDS (key codes -> E4M3
+//    codebook bytes, value codes as bytes, the V scale split for exact fp16
+//    products).  Pass p issues S^T = K Q^T of pair p on
 //    v_mfma_f32_32x32x64_f8f6f4 (M = the pair's 32 tokens, N = the 32 rows,
-//    K = 64 channels; three MFMAs per k-step, one per query term), the
-//    causal mask, the online softmax in base 2 (lazy rescale, threshold 2^8)
-//    and the weights as fp16 hi + lo pairs, which it hands over in LDS;
-//  * a PV wave holds the rows' O^T accumulators (32 channels x 32 rows per
-//    block) and computes O^T += V^T P^T on v_mfma_f32_32x32x16_f16 (M = 32
-//    channels, N = the 32 rows, K = the 16 tokens of one page; a lane's
-//    score outputs are exactly the 8 tokens per page its weight operand
-//    holds): values as exact fp16 operands (scale_hi * code, scale_lo *
-//    code), the zero term as one rank-2 product of the pages' zeros and
-//    weight sums, applying the rescale the score wave passed along first.
-// Pass i (one barrier): the score waves take stage i while the PV waves take
-// stage i - 1.  FP8 pages: the score wave scores them on the f16 MFMA against
-// the plain query (the fp8 MFMA keeps too few bits where FP8 keys carry
-// large norms) with one zero-padded half of the tile, and folds the page's V
-// scale into the weights; the PV wave reads the page's values from the ring.
-// The workgroups of one (request, KV head) read the same pages at about the
-// same time, so the page bytes come from L2 after the first reader.
+//    K = 64 channels; three MFMAs per k-step, one per query term) and,
+//    between those MFMAs, finishes pair p - 1: the causal mask, the online
+//    softmax in base 2 (lazy rescale, threshold 2^8) and the weights as fp16
+//    hi + lo pairs, handed over in LDS;
+//  * four PV waves, wave v owning the 32-channel blocks 2v, 2v + 1 of all
+//    128 rows, hold O^T accumulators (32 channels x 32 rows per block and
+//    score wave) and compute O^T += V^T P^T on v_mfma_f32_32x32x16_f16 (M =
+//    32 channels, N = 32 rows, K = the 16 tokens of one page; a lane's score
+//    outputs are exactly the 8 tokens per page its weight operand holds):
+//    values as exact fp16 operands (scale_hi * code, scale_lo * code), the
+//    zero term as one rank-2 product of the pages' zeros and weight sums,
+//    applying the rescale the score waves passed along first.
+// Pass p (one barrier): the score waves issue pair p's product and finish
+// pair p - 1 while the PV waves take pair p - 2.  FP8 pages: the score waves
+// score them on the f16 MFMA against the plain query (the fp8 MFMA keeps too
+// few bits where FP8 keys carry large norms) with one zero-padded half of
+// the tile, and fold the page's V scale into the weights; the PV waves read
+// the page's values from the ring.  The workgroups of one (request, KV head)
+// read the same pages at about the same time, so the page bytes come from
+// L2 after the first reader.
 #include <hip/hip_runtime.h>
 
 #include <type_traits>
@@ -202,7 +205,7 @@ __device__ __forceinline__ void chunk_block(const ChunkArgs& a, int r, int h, in
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const bool score_wave = wid < NSW;
-  const int sw = wid % NSW;  // the score wave (and its rows) this wave belongs to
+  const int sw = wid % NSW;  // score wave: its rows (PV waves: unused)
   // MFMA lane roles: li = lane % 32 (row of A, column of B and of the
   // output), lg = lane / 32 (k-slot group)
   const int li = lane & 31, lg = lane >> 5;
@@ -228,7 +231,7 @@ __device__ __forceinline__ void chunk_block(const ChunkArgs& a, int r, int h, in
     return;
   }
   if (xb * (NSW * 32) >= rows_r) return;  // whole workgroup past the rows (not with the row-block table)
-  // Wave pairs whose rows all lie past the request's rows still take part
+  // Score waves whose rows all lie past the request's rows still take part
   // in the copies, the unpacking and the barriers; their scores are all
   // masked.
   const int P0 = S - nq;  // position of the chunk's first query
@@ -254,15 +257,14 @@ __device__ __forceinline__ void chunk_block(const ChunkArgs& a, int r, int h, in
   auto wslot = [&](int j) { return wbuf + ((j & 1) * NSW + sw) * LY::WPW; };
 
   // Stage j of the loops below is a TQ3 pair for j < st3, else an FP8 page.
-  // Pass i (one barrier each, i = 0 .. n_st): the score waves take stage i
-  // (scores, softmax, weights into LDS; for a TQ3 pair also the unpacking
-  // of pair i + 1) while the PV waves take stage i - 1 with the weights
-  // handed over in pass i - 1.
+  // Pass p (one barrier each, p = 0 .. n_st): the score waves issue stage
+  // p's score product and finish stage p - 1 (scores, softmax, weights into
+  // LDS) while the PV waves take stage p - 2 with the weights handed over in
+  // pass p - 1.
   if (score_wave) {
     // ======================= score waves =======================
-    // The score waves are the critical path of every pass (their weights
-    // feed the next one; the PV waves have slack): the SIMD's arbiter takes
-    // their instructions first and fills the gaps with the PV waves'.
+    // The score waves' instructions go first on the SIMD (their weights gate
+    // the next pass); the PV waves fill the gaps.
     __builtin_amdgcn_s_setprio(2);
     float neg1 = -1.0f;  // kept in a register (see split2)
     __asm__ __volatile__("" : "+v"(neg1));
@@ -644,8 +646,9 @@ __device__ __forceinline__ void chunk_block(const ChunkArgs& a, int r, int h, in
     // the matrix unit works on it, finishes pair p - 1 (scores from the
     // product issued in pass p - 1, softmax, weights into LDS) and unpacks
     // the keys of pair p + 1 and the values of pair p - 1; the PV waves take
-    // pair p - 2.  One straight block per wave kind, so that the VALU and LDS
-    // work fills the MFMA latencies.
+    // pair p - 2.  One straight block per wave kind; scheduling fences place
+    // the twelve MFMAs between segments of the VALU and LDS work (left to
+    // itself the compiler issued all twelve first).
     float16v st_prev = {};                // score product of stage p - 1
     int4 e_prev = make_int4(0, 0, 0, 0);  // entries of stage p - 1
     auto tq3_pass = [&](int p, float16v& st, auto masked, auto key_kind) {
