@@ -233,7 +233,7 @@ def chunk_bench(mk, torch, reps=5):
             "mfma_frac_of_fp8_peak": round(tf * 1e12 / MFMA_FP8_PEAK, 4),
             "mfma_dtypes": "TQ3 scores on fp8 MFMA (3-term E4M3 query), PV and FP8-page scores "
                            "on f16 MFMA (hi + lo operands), fp32 accumulate",
-            "kernel": "chunk_kernel<256> (+ partition_kernel, chunk_stages_kernel)"}
+            "kernel": "chunk_kernel<256> (+ partition_kernel, chunk_stages_kernel, chunk_rows_kernel)"}
 
 
 class DenseControls:
