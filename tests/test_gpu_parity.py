@@ -551,6 +551,34 @@ def test_chunk_group12_d256(torch_cuda):
     _run_chunk_case(w, list(w.ctx), [70, 21], recent=48)
 
 
+def test_chunk_over_tq3_chunk_pages(torch_cuda):
+    """The chunk's own pages already re-encoded to TQ3 (the migration ran
+    after the chunk was appended, with a 32-token Recent window): TQ3 pairs
+    now hold tokens past some queries, so the causal mask applies to TQ3
+    pages too (the masked score passes, including the pass that finishes the
+    last pair), every query row against the oracle."""
+    from _harness import Twin, max_abs
+    w = wl.scaled(wl.workload(5), (900, 467), n_layers=1, name="chunk-tq3-masked")
+    n_q = [200, 150]
+    print(f"\n[chunk case] {w.name} lens={list(w.ctx)} n_q={n_q} W=32, migrated after the append",
+          flush=True)
+    tw = Twin(w, lens=list(w.ctx), recent=32)
+    tw.fill_to([l - n for l, n in zip(w.ctx, n_q)])
+    tw.append(n_q)
+    tw.migrate()
+    tw.check_tables()
+    tw.check_pages()
+    tags = tw.otags
+    for r, (L, n) in enumerate(zip(w.ctx, n_q)):
+        first, last = (L - n) // 16, (L - 1) // 16
+        assert (tags[r, first:last + 1] == 2).sum() >= (last - first + 1) // 2  # mostly TQ3
+    res = tw.chunk(n_q)
+    err = max_abs(res["out"], res["ref_out"])
+    print(f"  every row: max|dO| {err:.3e}", flush=True)
+    assert np.all(np.isfinite(res["out"]))
+    assert err <= TOL, err
+
+
 def test_chunk_invalid_requests(torch_cuda):
     """Error paths of the chunk call.  A request whose length is shorter than
     its chunk gets zero rows and the range bit, while the other requests'
