@@ -291,6 +291,10 @@ mkv_status paged_attn_decode_noalloc(mkv_pool* pool, int32_t layer, int32_t n_re
  * (it holds the compact per-format page lists).  q, out and ws must be
  * 16-byte aligned (MKV_EINVAL otherwise).  A request whose query range or
  * length is invalid sets the error word and its locatable rows get zeros.
+ * Query ranges are expected not to overlap (cu_q nondecreasing); ranges that
+ * overlap so much that their 128-row blocks (ceil(n_r * group / 128) per
+ * request) exceed ceil(n_q_total * group / 128) + n_req set the error word
+ * and the call writes nothing to out.
  * (The paper runs prefill on a generic dense path, Sec. 4.1; this variant
  * keeps the mixed pages and uses MFMA for the dense contraction.) */
 mkv_status paged_attn_chunk(mkv_pool* pool, int32_t layer, int32_t n_req, const uint16_t* q,
