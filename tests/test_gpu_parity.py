@@ -622,6 +622,19 @@ def test_chunk_invalid_requests(torch_cuda):
     print("\n  invalid length: zero rows, others bit-identical; overlap: untouched", flush=True)
 
 
+@pytest.mark.parametrize("n_q_heads,n_kv_heads", [(4, 4), (32, 2)])
+def test_chunk_group_extremes(torch_cuda, n_q_heads, n_kv_heads):
+    """The smallest and the largest GQA group (1 and 16 query heads per KV
+    head): a 128-row block then holds 128 or 8 queries, so the row-block
+    table and the row -> (query, head) mapping meet their edge cases; three
+    requests with chunks of 129, 8 and 1 queries, every row."""
+    import dataclasses
+    w = dataclasses.replace(wl.scaled(wl.workload(5), (1100, 500, 260), n_layers=1,
+                                      name=f"chunk-g{n_q_heads // n_kv_heads}"),
+                            n_q_heads=n_q_heads, n_kv_heads=n_kv_heads)
+    _run_chunk_case(w, list(w.ctx), [129, 8, 1], recent=48)
+
+
 def test_chunk_last_query_matches_decode(torch_cuda):
     """Property that holds at any size, checked without the oracle: the last
     query of each request's chunk sees the whole context, so the chunk kernel's
