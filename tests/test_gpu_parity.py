@@ -635,6 +635,42 @@ def test_chunk_group_extremes(torch_cuda, n_q_heads, n_kv_heads):
     _run_chunk_case(w, list(w.ctx), [129, 8, 1], recent=48)
 
 
+def test_chunk_random_shapes(torch_cuda):
+    """Seeded random chunk calls: head dim 128 or 256, 1-4 KV heads, GQA
+    groups 1-16, 1-4 requests of up to 2,500 tokens with chunks of 1-300
+    queries, Recent windows of 16-256 tokens, the migration before or after
+    the chunk's append (so TQ3 pairs with masked tokens appear); every row
+    against the oracle, no error bits."""
+    import dataclasses
+    from _harness import Twin, max_abs
+    import paper_2608_23834_amd as mk
+    rng = np.random.default_rng(2608)
+    for c in range(6):
+        d = int(rng.choice([128, 256]))
+        H, G = int(rng.choice([1, 2, 4])), int(rng.choice([1, 2, 3, 4, 6, 8, 12, 16]))
+        lens = [int(rng.integers(1, 2500)) for _ in range(int(rng.integers(1, 5)))]
+        n_q = [int(rng.integers(1, min(L, 300) + 1)) for L in lens]
+        recent = int(rng.choice([16, 32, 48, 64, 256]))
+        after = bool(rng.integers(0, 2))
+        w = dataclasses.replace(wl.scaled(wl.workload(1 if d == 128 else 5), tuple(lens), n_layers=1,
+                                          name=f"chunk-random-{c}"), n_q_heads=H * G, n_kv_heads=H)
+        print(f"\n[chunk case] d {d} H {H} G {G} lens {lens} n_q {n_q} W {recent} "
+              f"migrated {'after' if after else 'before'} the append", flush=True)
+        tw = Twin(w, lens=lens, recent=recent)
+        tw.fill_to([L - n for L, n in zip(lens, n_q)])
+        if not after:
+            tw.migrate()
+        tw.append(n_q)
+        if after:
+            tw.migrate()
+        res = tw.chunk(n_q)
+        err = max_abs(res["out"], res["ref_out"])
+        print(f"  every row: max|dO| {err:.3e}", flush=True)
+        assert np.all(np.isfinite(res["out"]))
+        assert err <= TOL, (c, err)
+        assert mk.kv_pool_check_errors(tw.gpu) == 0
+
+
 def test_chunk_last_query_matches_decode(torch_cuda):
     """Property that holds at any size, checked without the oracle: the last
     query of each request's chunk sees the whole context, so the chunk kernel's
