@@ -635,6 +635,43 @@ def test_chunk_group_extremes(torch_cuda, n_q_heads, n_kv_heads):
     _run_chunk_case(w, list(w.ctx), [129, 8, 1], recent=48)
 
 
+def test_decode_random_shapes(torch_cuda):
+    """Seeded random decode calls: head dim 128 or 256, 1-8 KV heads, GQA
+    groups 1-16, 1-8 requests of 0-3,000 tokens (empty ones included),
+    Recent windows of 16-1,024 tokens, the stage schedule deterministic or
+    claimed at run time; a plain decode, then a fused decode step, each
+    against the oracle (outputs and lse), tables bit-exact, no error bits."""
+    import dataclasses
+    from _harness import Twin, max_abs
+    import paper_2608_23834_amd as mk
+    rng = np.random.default_rng(59008)
+    for c in range(6):
+        d = int(rng.choice([128, 256]))
+        H, G = int(rng.choice([1, 2, 4, 8])), int(rng.choice([1, 2, 3, 4, 6, 8, 12, 16]))
+        lens = [int(rng.integers(0, 3000)) for _ in range(int(rng.integers(1, 9)))]
+        lens[0] = max(lens[0], 1)
+        recent = int(rng.choice([16, 32, 64, 256, 1024]))
+        det = bool(rng.integers(0, 2))
+        w = dataclasses.replace(wl.scaled(wl.workload(1 if d == 128 else 5), tuple(max(L, 1) for L in lens),
+                                          n_layers=1, name=f"decode-random-{c}"),
+                                n_q_heads=H * G, n_kv_heads=H)
+        print(f"\n[case] d {d} H {H} G {G} lens {lens} W {recent} deterministic {det}", flush=True)
+        tw = Twin(w, lens=[max(L, 1) for L in lens], recent=recent, headroom=16)
+        tw.fill_to(lens)
+        tw.migrate()
+        mk.paged_attn_set_deterministic(tw.gpu, det)
+        r1 = tw.decode()
+        e1 = max(max_abs(r1["out"], r1["ref_out"]), max_abs(r1["lse"], r1["ref_lse"]))
+        r2 = tw.decode_append()
+        tw.advance()
+        e2 = max(max_abs(r2["out"], r2["ref_out"]), max_abs(r2["lse"], r2["ref_lse"]))
+        tw.check_tables()
+        print(f"  decode max|d| {e1:.3e}, fused step {e2:.3e}", flush=True)
+        assert np.all(np.isfinite(r1["out"])) and np.all(np.isfinite(r2["out"]))
+        assert e1 <= TOL and e2 <= TOL, (c, e1, e2)
+        assert mk.kv_pool_check_errors(tw.gpu) == 0
+
+
 def test_chunk_random_shapes(torch_cuda):
     """Seeded random chunk calls: head dim 128 or 256, 1-4 KV heads, GQA
     groups 1-16, 1-4 requests of up to 2,500 tokens with chunks of 1-300
