@@ -635,6 +635,57 @@ def test_chunk_group_extremes(torch_cuda, n_q_heads, n_kv_heads):
     _run_chunk_case(w, list(w.ctx), [129, 8, 1], recent=48)
 
 
+def test_pool_random_lifecycles(torch_cuda):
+    """Seeded random sequences of pool calls on two layers — appends of up
+    to 200 tokens per request, Retier with random anchor masks, Promote of a
+    random third of the Stale pages, fused decode steps, Finish of random
+    requests (which later append from zero again) — with tables, tags, free
+    lists, reference counts and every page compared bit for bit after each
+    call, decode outputs within 1e-3, and no error bits."""
+    import dataclasses
+    from _harness import Twin, max_abs
+    import paper_2608_23834_amd as mk
+    rng = np.random.default_rng(16)
+    for sq in range(4):
+        d = int(rng.choice([128, 256]))
+        H, G = int(rng.choice([1, 2, 4])), int(rng.choice([1, 2, 6, 8]))
+        n_req = int(rng.integers(1, 5))
+        cap = [int(rng.integers(64, 1500)) for _ in range(n_req)]
+        recent = int(rng.choice([16, 32, 64, 256]))
+        w = dataclasses.replace(wl.scaled(wl.workload(1 if d == 128 else 5), tuple(cap), n_layers=2,
+                                          name=f"lifecycle-{sq}"), n_q_heads=H * G, n_kv_heads=H)
+        print(f"\n[lifecycle {sq}] d {d} H {H} G {G} capacity {cap} W {recent}", flush=True)
+        tw = Twin(w, n_layers=2, lens=cap, recent=recent, headroom=64)
+        done = []
+        for step in range(12):
+            op = str(rng.choice(["append", "migrate", "promote", "step", "finish"],
+                                p=[0.35, 0.25, 0.15, 0.15, 0.10]))
+            if op == "append":
+                cnt = [int(max(0, min(rng.integers(0, 200), c - cur))) for c, cur in zip(cap, tw.cur)]
+                if sum(cnt) == 0:
+                    continue
+                tw.append(cnt)
+            elif op == "migrate":
+                tw.migrate(anchor=(rng.random((n_req, tw.max_pages)) < 0.1).astype(np.uint8))
+            elif op == "promote":
+                tw.promote(((tw.otags == 2) & (rng.random(tw.otags.shape) < 0.3)).astype(np.uint8))
+            elif op == "step":
+                if min(tw.cur) < 1 or any(c >= cp + 32 for c, cp in zip(tw.cur, cap)):
+                    continue
+                res = tw.decode_append(layer=int(rng.integers(0, 2)))
+                tw.advance()
+                err = max(max_abs(res["out"], res["ref_out"]), max_abs(res["lse"], res["ref_lse"]))
+                assert err <= TOL, (sq, step, err)
+            else:
+                tw.finish(sorted(set(int(x) for x in rng.integers(0, n_req, size=int(rng.integers(1, n_req + 1))))))
+            tw.check_tables()
+            tw.check_refcounts()
+            tw.check_pages()
+            assert mk.kv_pool_check_errors(tw.gpu, clear=True) == 0, (sq, step, op)
+            done.append(op)
+        print(f"  bit-exact after: {' '.join(done)}", flush=True)
+
+
 def test_decode_random_shapes(torch_cuda):
     """Seeded random decode calls: head dim 128 or 256, 1-8 KV heads, GQA
     groups 1-16, 1-8 requests of 0-3,000 tokens (empty ones included),
